@@ -1,0 +1,103 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and check that a pin fails.
+
+Each mutant replaces one oracle function for the duration of a test; the
+check that follows is the same comparison a pin in test_oracle_pins makes.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import oracle.commitkv_oracle as OM
+from tests.test_oracle_pins import _random_case, _two_small_pages
+
+
+def _closed_no_renorm(a, o, v, delete, vis):
+    """Mutant: forgets the 1/(1 - A) of Eq. (6)."""
+    sel = vis & delete[None, :]
+    a_e = np.where(sel, a, 0.0)
+    A = a_e.sum(axis=1)
+    u = a_e @ v
+    return np.linalg.norm(u - A[:, None] * o, axis=1) / np.linalg.norm(o, axis=1)
+
+
+def _closed_sign_flip(a, o, v, delete, vis):
+    """Mutant: u + A o instead of u - A o."""
+    sel = vis & delete[None, :]
+    a_e = np.where(sel, a, 0.0)
+    A = a_e.sum(axis=1)
+    u = a_e @ v
+    return np.linalg.norm(u + A[:, None] * o, axis=1) / ((1 - A) * np.linalg.norm(o, axis=1))
+
+
+@pytest.mark.parametrize("mutant", [_closed_no_renorm, _closed_sign_flip])
+def test_closed_form_mutants_are_caught(monkeypatch, mutant):
+    K, V, Q, pos, qpos, pages = _random_case(0)
+    Rb, _ = O.page_effects(K, V, pos, Q, qpos, pages, method="bruteforce")
+    monkeypatch.setattr(OM, "deletion_ratio_closed_form", mutant)
+    with np.errstate(all="ignore"):
+        Rc, _ = OM.page_effects(K, V, pos, Q, qpos, pages, method="closed")
+    fin = np.isfinite(Rb) & np.isfinite(Rc)
+    assert not np.allclose(Rc[fin], Rb[fin], rtol=1e-10)
+
+
+def test_visibility_off_by_one_is_caught(monkeypatch):
+    """Mutant: strict p_i < p drops the window row's own token."""
+    monkeypatch.setattr(OM, "visibility",
+                        lambda pos, qpos: np.asarray(pos)[None, :] < np.asarray(qpos)[:, None])
+    K = np.array([[[0.0, 0.0], [math.log(3.0), 0.0]]])
+    V = np.array([[[1.0, 0.0], [0.0, 1.0]]])
+    Q = np.array([[[1.0, 0.0]]])
+    R, _ = OM.page_effects(K, V, np.array([0, 1]), Q, np.array([1]), [(1, 1)], scale=1.0)
+    assert R[0] != pytest.approx(3 / math.sqrt(5))
+
+
+def test_percentile_non_strict_is_caught(monkeypatch):
+    def mutant(R):
+        R = np.asarray(R, float)
+        n = R.size
+        return np.array([((R <= R[j]).sum() - 1) / (n - 1) for j in range(n)])
+    monkeypatch.setattr(OM, "percentile_ranks", mutant)
+    assert not np.array_equal(OM.percentile_ranks([0.1, 0.1, 0.2]), [0.0, 0.0, 1.0])
+
+
+def test_lifecycle_swap_is_caught(monkeypatch):
+    """Mutant: candidate defined as L- and H+ (the transition reversed)."""
+    def mutant(H_pre, L_pre, H_post, L_post):
+        lam = np.full(len(H_pre), O.UNCERTAIN, np.uint8)
+        lam[L_pre & H_post] = O.CANDIDATE
+        lam[L_pre & L_post] = O.DORMANT
+        lam[H_pre & L_post] = O.NEWLY_ACTIVE
+        lam[H_pre & H_post] = O.STILL_ACTIVE
+        return lam
+    monkeypatch.setattr(OM, "lifecycle", mutant)
+    lam, *_ = OM.classify([0.9, 0.05, 0.001, 0.01, 0.03], [0.05, 0.01, 0.002, 0.5, 0.04],
+                          starts=[0, 16, 32, 48, 64])
+    assert lam[1] != O.CANDIDATE
+
+
+def test_joint_without_union_is_caught(monkeypatch):
+    """Mutant: tests each candidate alone instead of A u {E} (Eq. (11))."""
+    K, V, Q, pos, qpos, pages = _two_small_pages()
+    real = OM.union_effect
+    monkeypatch.setattr(OM, "union_effect",
+                        lambda K, V, pos, Q, qpos, pages, members, scale=None, method="bruteforce":
+                        real(K, V, pos, Q, qpos, pages, members[-1:], scale, method))
+    acc, _ = OM.joint_test(K, V, pos, Q, qpos, pages, [0, 1, 2], tau_joint=0.01)
+    assert not np.array_equal(acc, [True, False, True])
+
+
+def test_protect_skip_instead_of_stop_is_caught(monkeypatch):
+    def mutant(starts, lens, R_pre, B, eta=0.125, max_pages=16):
+        BN = int(math.floor(eta * B))
+        order = sorted(range(len(starts)), key=lambda j: (-R_pre[j], starts[j]))
+        taken, tok = [], 0
+        for j in order:
+            if len(taken) < max_pages and tok + lens[j] <= BN:
+                taken.append(j)
+                tok += lens[j]
+        return np.array(taken)
+    monkeypatch.setattr(OM, "protect_pending", mutant)
+    got = OM.protect_pending([0, 4, 8, 10, 14], [4, 4, 2, 4, 1], [0.5, 0.9, 0.7, 0.7, 0.1], 64)
+    assert not np.array_equal(got, [1, 2])
