@@ -1,0 +1,120 @@
+"""ctypes declarations of include/commitkv.h and the library loader.
+
+The library is the in-tree ``libcommitkv.so`` built by
+``python -m paper_2608_07855_amd.build``.  There is no fallback: if the
+library is missing, loading raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcommitkv.so")
+
+CKV_OK = 0
+CKV_ERR_ARG = -1
+CKV_ERR_SHAPE = -2
+CKV_ERR_BUDGET = -3
+CKV_ERR_UNSUPPORTED = -4
+CKV_ERR_NOMEM = -5
+CKV_ERR_HIP = -6
+CKV_ERR_NONFINITE = -7
+STATUS_NAMES = {0: "CKV_OK", -1: "CKV_ERR_ARG", -2: "CKV_ERR_SHAPE", -3: "CKV_ERR_BUDGET",
+                -4: "CKV_ERR_UNSUPPORTED", -5: "CKV_ERR_NOMEM", -6: "CKV_ERR_HIP",
+                -7: "CKV_ERR_NONFINITE"}
+MAX_PAGE_LEN = 64
+
+c_i32p = ctypes.POINTER(ctypes.c_int32)
+c_f32p = ctypes.POINTER(ctypes.c_float)
+c_u8p = ctypes.POINTER(ctypes.c_uint8)
+c_u16p = ctypes.POINTER(ctypes.c_uint16)
+
+
+class KVView(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("head_stride", ctypes.c_int64), ("tok_stride", ctypes.c_int64),
+                ("pos", ctypes.c_void_p), ("n_tokens", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32)]
+
+
+class WindowView(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("head_stride", ctypes.c_int64),
+                ("row_stride", ctypes.c_int64), ("qpos", ctypes.c_void_p),
+                ("n_q_heads", ctypes.c_int32), ("n_rows", ctypes.c_int32),
+                ("scale", ctypes.c_float)]
+
+
+class PageList(ctypes.Structure):
+    _fields_ = [("start", c_i32p), ("len", c_i32p), ("n_pages", ctypes.c_int32)]
+
+
+class Thresholds(ctypes.Structure):
+    _fields_ = [("tau_use", ctypes.c_float), ("tau_dead", ctypes.c_float),
+                ("rho_use", ctypes.c_float), ("rho_dead", ctypes.c_float),
+                ("tau_joint", ctypes.c_float)]
+
+
+class Budget(ctypes.Structure):
+    _fields_ = [("budget", ctypes.c_int32), ("eta", ctypes.c_float),
+                ("max_pending_pages", ctypes.c_int32), ("keep_recent", ctypes.c_int32)]
+
+
+class CacheView(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("seq_stride", ctypes.c_int64), ("layer_stride", ctypes.c_int64),
+                ("head_stride", ctypes.c_int64), ("tok_stride", ctypes.c_int64),
+                ("pos", ctypes.c_void_p), ("pos_seq_stride", ctypes.c_int64),
+                ("n_seq", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("capacity", ctypes.c_int32)]
+
+
+# name -> (restype, argtypes): every entry point of include/commitkv.h
+SIGNATURES = {
+    "ckv_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int, ctypes.c_void_p]),
+    "ckv_destroy": (ctypes.c_int, [ctypes.c_void_p]),
+    "ckv_set_stream": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
+    "ckv_sync": (ctypes.c_int, [ctypes.c_void_p]),
+    "ckv_last_error": (ctypes.c_char_p, [ctypes.c_void_p]),
+    "ckv_version": (ctypes.c_uint32, []),
+    "ckv_set_workspace_limit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t]),
+    "ckv_workspace_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
+    "ckv_measure_page_effects": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.POINTER(KVView), ctypes.POINTER(WindowView),
+        ctypes.POINTER(PageList), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p]),
+    "ckv_classify_pages": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.POINTER(Thresholds), ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "ckv_joint_test": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.POINTER(KVView), ctypes.POINTER(WindowView),
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(PageList), ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p]),
+    "ckv_select_and_compact": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.POINTER(CacheView), c_i32p, ctypes.c_void_p,
+        ctypes.c_int64, ctypes.POINTER(PageList), ctypes.POINTER(PageList),
+        ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(Budget),
+        ctypes.POINTER(CacheView), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+}
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libcommitkv.so and declare its entry points (raises if absent)."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise OSError(f"{path} not found: build it with `python -m paper_2608_07855_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    if path == LIB_PATH:
+        _lib = lib
+    return lib

@@ -1,0 +1,250 @@
+"""Thin Python binding of the CommitKV C ABI (include/commitkv.h).
+
+Argument marshalling only: torch tensors supply device pointers, strides and
+the current HIP stream; NumPy arrays supply the host page lists.  Every step
+of the hot path runs in the HIP kernels of libcommitkv.so; there is no other
+code path.  Each ``ckv_*`` function mirrors the C entry point of the same
+name and returns the output tensors (allocating those the caller omits).
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import _abi
+from ._abi import Budget, CacheView, KVView, PageList, Thresholds, WindowView
+
+PAPER_THRESHOLDS = dict(tau_use=0.05, tau_dead=0.01, rho_use=0.75, rho_dead=0.25, tau_joint=0.01)
+
+
+class CKVError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{_abi.STATUS_NAMES.get(code, code)}: {message}")
+        self.code = code
+
+
+def lib():
+    return _abi.load()
+
+
+def version() -> int:
+    return int(lib().ckv_version())
+
+
+class Context:
+    """A ckv_ctx bound to one device and one HIP stream (default: torch's current)."""
+
+    def __init__(self, device: int = 0, stream=None):
+        self._lib = lib()
+        if stream is None:
+            stream = torch.cuda.current_stream(device).cuda_stream
+        elif isinstance(stream, torch.cuda.Stream):
+            stream = stream.cuda_stream
+        self.device = device
+        h = ctypes.c_void_p()
+        rc = self._lib.ckv_create(ctypes.byref(h), device, ctypes.c_void_p(stream))
+        if rc != 0:
+            raise CKVError(rc, "ckv_create failed")
+        self.handle = h
+
+    def check(self, rc: int):
+        if rc != 0:
+            msg = self._lib.ckv_last_error(self.handle)
+            raise CKVError(rc, msg.decode() if msg else "")
+
+    def sync(self):
+        self.check(self._lib.ckv_sync(self.handle))
+
+    def set_stream(self, stream):
+        s = stream.cuda_stream if isinstance(stream, torch.cuda.Stream) else stream
+        self.check(self._lib.ckv_set_stream(self.handle, ctypes.c_void_p(s)))
+
+    def set_workspace_limit(self, nbytes: int):
+        self.check(self._lib.ckv_set_workspace_limit(self.handle, nbytes))
+
+    def workspace_bytes(self) -> int:
+        return int(self._lib.ckv_workspace_bytes(self.handle))
+
+    def last_error(self) -> str:
+        return self._lib.ckv_last_error(self.handle).decode()
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self._lib.ckv_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---------------------------------------------------------------- views
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _check_bf16(t, name, ndim):
+    if t.dtype != torch.bfloat16 or not t.is_cuda or t.dim() != ndim or t.stride(-1) != 1:
+        raise ValueError(f"{name}: expected a cuda bfloat16 tensor of {ndim} dims with a contiguous last axis")
+
+
+def kv_view(k, v, pos, n_tokens: int | None = None) -> KVView:
+    """k, v: [Hkv, S_cap, d] bf16 (same strides); pos: int32 [>= n_tokens]."""
+    _check_bf16(k, "k", 3)
+    _check_bf16(v, "v", 3)
+    if k.shape != v.shape or k.stride() != v.stride():
+        raise ValueError("k and v must have the same shape and strides")
+    if pos.dtype != torch.int32 or not pos.is_cuda:
+        raise ValueError("pos must be a cuda int32 tensor")
+    S = k.shape[1] if n_tokens is None else int(n_tokens)
+    return KVView(k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1), pos.data_ptr(), S,
+                  k.shape[0], k.shape[2])
+
+
+def window_view(q, qpos, scale: float = 0.0) -> WindowView:
+    """q: [Hq, W, d] bf16; qpos: int32 [W]."""
+    _check_bf16(q, "q", 3)
+    if qpos.dtype != torch.int32 or not qpos.is_cuda:
+        raise ValueError("qpos must be a cuda int32 tensor")
+    return WindowView(q.data_ptr(), q.stride(0), q.stride(1), qpos.data_ptr(), q.shape[0],
+                      q.shape[1], float(scale))
+
+
+@dataclass
+class Pages:
+    """Host page list (kept alive alongside its ctypes view)."""
+    start: np.ndarray
+    len: np.ndarray
+
+    def __post_init__(self):
+        self.start = np.ascontiguousarray(self.start, dtype=np.int32)
+        self.len = np.ascontiguousarray(self.len, dtype=np.int32)
+
+    @property
+    def n(self):
+        return int(self.start.size)
+
+    def view(self) -> PageList:
+        return PageList(self.start.ctypes.data_as(_abi.c_i32p), self.len.ctypes.data_as(_abi.c_i32p),
+                        self.n)
+
+
+def cache_view(k, v, pos) -> CacheView:
+    """k, v: [n_seq, n_layers, Hkv, capacity, d] bf16; pos: int32 [n_seq, >= capacity]."""
+    _check_bf16(k, "k", 5)
+    _check_bf16(v, "v", 5)
+    if k.shape != v.shape or k.stride() != v.stride():
+        raise ValueError("k and v must have the same shape and strides")
+    if pos.dtype != torch.int32 or pos.dim() != 2 or pos.stride(1) != 1:
+        raise ValueError("pos must be int32 [n_seq, capacity] with a contiguous last axis")
+    s = k.stride()
+    return CacheView(k.data_ptr(), v.data_ptr(), s[0], s[1], s[2], s[3], pos.data_ptr(),
+                     pos.stride(0), k.shape[0], k.shape[1], k.shape[2], k.shape[4], k.shape[3])
+
+
+def _f32(n, device, fill=None):
+    t = torch.empty(n, dtype=torch.float32, device=device)
+    if fill is not None:
+        t.fill_(fill)
+    return t
+
+
+# ---------------------------------------------------------------- calls
+
+def ckv_measure_page_effects(ctx: Context, kv: KVView, win: WindowView, pages: Pages, *,
+                             R=None, R_head=None, o=None, lse=None, token_mass=None,
+                             want=("R",)):
+    """Window deletion effect of every page.  ``want`` names the optional
+    outputs to allocate when not given: "R_head", "o", "lse", "token_mass"."""
+    dev = torch.device("cuda", ctx.device)
+    Hq, W, d = win.n_q_heads, win.n_rows, kv.head_dim
+    if R is None:
+        R = _f32(max(pages.n, 1), dev)
+    if R_head is None and "R_head" in want:
+        R_head = _f32(max(pages.n * Hq, 1), dev)
+    if o is None and "o" in want:
+        o = _f32(Hq * W * d, dev)
+    if lse is None and "lse" in want:
+        lse = _f32(Hq * W, dev)
+    if token_mass is None and "token_mass" in want:
+        token_mass = _f32(kv.n_tokens, dev)
+    pl = pages.view()
+    ctx.check(lib().ckv_measure_page_effects(
+        ctx.handle, ctypes.byref(kv), ctypes.byref(win), ctypes.byref(pl), _ptr(R),
+        _ptr(R_head), _ptr(o), _ptr(lse), _ptr(token_mass)))
+    return dict(R=R[:pages.n], R_head=None if R_head is None else R_head[:pages.n * Hq].view(pages.n, Hq),
+                o=None if o is None else o.view(Hq, W, d),
+                lse=None if lse is None else lse.view(Hq, W), token_mass=token_mass)
+
+
+def ckv_classify_pages(ctx: Context, R_pre, R_post, thresholds: dict | None = None, *,
+                       force=None, max_cand: int = 0):
+    n = int(R_pre.numel())
+    dev = R_pre.device
+    th = dict(PAPER_THRESHOLDS)
+    th.update(thresholds or {})
+    t = Thresholds(th["tau_use"], th["tau_dead"], th["rho_use"], th["rho_dead"], th["tau_joint"])
+    lam = torch.empty(max(n, 1), dtype=torch.uint8, device=dev)
+    P_pre = _f32(max(n, 1), dev)
+    P_post = _f32(max(n, 1), dev)
+    cand = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+    n_cand = torch.zeros(1, dtype=torch.int32, device=dev)
+    ctx.check(lib().ckv_classify_pages(ctx.handle, n, _ptr(R_pre), _ptr(R_post), ctypes.byref(t),
+                                       _ptr(force), int(max_cand), _ptr(lam), _ptr(P_pre),
+                                       _ptr(P_post), _ptr(cand), _ptr(n_cand)))
+    return dict(lam=lam[:n], P_pre=P_pre[:n], P_post=P_post[:n], cand=cand[:n], n_cand=n_cand)
+
+
+def ckv_joint_test(ctx: Context, kv: KVView, win: WindowView, o, lse, pages: Pages, cand, n_cand,
+                   max_cand: int, tau_joint: float = 0.01):
+    dev = o.device
+    accepted = torch.empty(max_cand, dtype=torch.uint8, device=dev)
+    union_R = _f32(max_cand, dev)
+    n_acc = torch.zeros(1, dtype=torch.int32, device=dev)
+    pl = pages.view()
+    ctx.check(lib().ckv_joint_test(ctx.handle, ctypes.byref(kv), ctypes.byref(win), _ptr(o),
+                                   _ptr(lse), ctypes.byref(pl), _ptr(cand), _ptr(n_cand),
+                                   int(max_cand), float(tau_joint), _ptr(accepted), _ptr(union_R),
+                                   _ptr(n_acc)))
+    return dict(accepted=accepted, union_R=union_R, n_accepted=n_acc)
+
+
+def ckv_select_and_compact(ctx: Context, k_in, v_in, pos_in, n_tokens, score, retired, pending,
+                           pending_r_pre, *, budget: int, eta: float = 0.125,
+                           max_pending_pages: int = 16, keep_recent: int = 0,
+                           k_out=None, v_out=None, pos_out=None, token_state=None):
+    """k_in, v_in: [n_seq, n_layers, Hkv, capacity, d] bf16; pos_in: [n_seq, capacity] int32;
+    n_tokens: host ints [n_seq]; score: [n_seq, stride] fp32; retired, pending: lists of
+    Pages (one per sequence); pending_r_pre: list of fp32 device tensors (or None)."""
+    ns, L, H, cap, d = k_in.shape
+    dev = k_in.device
+    if k_out is None:
+        k_out = torch.empty((ns, L, H, budget, d), dtype=torch.bfloat16, device=dev)
+        v_out = torch.empty_like(k_out)
+    if pos_out is None:
+        pos_out = torch.empty((ns, budget), dtype=torch.int32, device=dev)
+    kept = torch.empty((ns, budget), dtype=torch.int32, device=dev)
+    n_kept = torch.zeros(ns, dtype=torch.int32, device=dev)
+    cin, cout = cache_view(k_in, v_in, pos_in), cache_view(k_out, v_out, pos_out)
+    nt = np.ascontiguousarray(n_tokens, dtype=np.int32)
+    ret = (PageList * ns)(*[p.view() for p in retired])
+    pen = (PageList * ns)(*[p.view() for p in pending])
+    rptr = (ctypes.c_void_p * ns)(*[(r.data_ptr() if r is not None else 0) for r in pending_r_pre])
+    b = Budget(int(budget), float(eta), int(max_pending_pages), int(keep_recent))
+    ctx.check(lib().ckv_select_and_compact(
+        ctx.handle, ctypes.byref(cin), nt.ctypes.data_as(_abi.c_i32p), _ptr(score),
+        int(score.stride(0)), ret, pen, rptr, ctypes.byref(b), ctypes.byref(cout), _ptr(kept),
+        _ptr(n_kept), _ptr(token_state)))
+    return dict(k=k_out, v=v_out, pos=pos_out, kept=kept, n_kept=n_kept)

@@ -1,0 +1,683 @@
+// Host runtime behind the C ABI of include/commitkv.h: context, workspace
+// arena, pinned upload ring, page-table cache, argument validation and the
+// launch sequence of each call.  Every argument error is caught here, before
+// anything is enqueued, so no kernel ever sees an out-of-range page or a
+// misaligned row.
+#include "commitkv.h"
+#include "ckv_kernels.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+using namespace ckv;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kPinnedSlots = 4;
+constexpr int kPageCacheEntries = 8;
+constexpr int kJointWindow = 32;       // candidates tested per joint round
+constexpr int kJointRowsPerBlock = 64;
+constexpr int kTargetBlocks = 512;     // about two blocks per compute unit
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+struct PageEntry {
+  std::vector<int32_t> key;   // start[0..n) then len[0..n)
+  int32_t* dev = nullptr;
+  size_t cap = 0;
+  uint64_t used = 0;
+};
+
+struct PinnedSlot {
+  char* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+
+struct Plan {
+  struct Item { void** dst; size_t bytes; };
+  std::vector<Item> items;
+  size_t total = 0;
+  template <class T>
+  void add(T** dst, size_t n) {
+    items.push_back({reinterpret_cast<void**>(dst), n * sizeof(T)});
+    total += round_up(std::max<size_t>(n * sizeof(T), 1), kAlign);
+  }
+};
+
+}  // namespace
+
+struct ckv_ctx {
+  int device = 0;
+  hipStream_t stream = nullptr;
+  char* ws = nullptr;
+  size_t ws_cap = 0;
+  size_t ws_limit = 0;
+  std::string err;
+  PinnedSlot slots[kPinnedSlots];
+  int next_slot = 0;
+  std::vector<PageEntry> pages;
+  uint64_t tick = 0;
+};
+
+namespace {
+
+int fail(ckv_ctx* c, int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c) c->err = buf;
+  return code;
+}
+
+int hip_fail(ckv_ctx* c, hipError_t e, const char* what) {
+  return fail(c, CKV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define CKV_HIP(ctx, expr)                                  \
+  do {                                                      \
+    hipError_t e_ = (expr);                                 \
+    if (e_ != hipSuccess) return hip_fail(ctx, e_, #expr);  \
+  } while (0)
+
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int ensure_ws(ckv_ctx* c, size_t need) {
+  if (need <= c->ws_cap) return CKV_OK;
+  if (c->ws_limit && need > c->ws_limit)
+    return fail(c, CKV_ERR_NOMEM, "workspace of %zu bytes exceeds the limit of %zu", need, c->ws_limit);
+  size_t want = std::max(need, c->ws_cap + c->ws_cap / 2);
+  if (c->ws_limit) want = std::min(want, c->ws_limit);
+  CKV_HIP(c, hipStreamSynchronize(c->stream));   // in-flight work may still use the old arena
+  if (c->ws) {
+    (void)hipFree(c->ws);
+    c->ws = nullptr;
+    c->ws_cap = 0;
+  }
+  void* p = nullptr;
+  if (hipMalloc(&p, want) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(c, CKV_ERR_NOMEM, "hipMalloc of %zu workspace bytes failed", want);
+  }
+  c->ws = static_cast<char*>(p);
+  c->ws_cap = want;
+  return CKV_OK;
+}
+
+int realize(ckv_ctx* c, Plan& plan) {
+  int rc = ensure_ws(c, plan.total);
+  if (rc) return rc;
+  size_t off = 0;
+  for (auto& it : plan.items) {
+    *it.dst = c->ws + off;
+    off += round_up(std::max<size_t>(it.bytes, 1), kAlign);
+  }
+  return CKV_OK;
+}
+
+// copy host bytes to device memory on the context stream via a pinned slot
+int upload(ckv_ctx* c, const void* src, size_t bytes, void* dst) {
+  if (bytes == 0) return CKV_OK;
+  PinnedSlot& s = c->slots[c->next_slot];
+  c->next_slot = (c->next_slot + 1) % kPinnedSlots;
+  if (s.pending) {
+    CKV_HIP(c, hipEventSynchronize(s.ev));
+    s.pending = false;
+  }
+  if (s.cap < bytes) {
+    if (s.host) (void)hipHostFree(s.host);
+    s.host = nullptr;
+    s.cap = 0;
+    void* p = nullptr;
+    const size_t want = std::max<size_t>(round_up(bytes, 4096), 1 << 16);
+    CKV_HIP(c, hipHostMalloc(&p, want, hipHostMallocDefault));
+    s.host = static_cast<char*>(p);
+    s.cap = want;
+  }
+  if (!s.ev) CKV_HIP(c, hipEventCreateWithFlags(&s.ev, hipEventDisableTiming));
+  std::memcpy(s.host, src, bytes);
+  CKV_HIP(c, hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, c->stream));
+  CKV_HIP(c, hipEventRecord(s.ev, c->stream));
+  s.pending = true;
+  return CKV_OK;
+}
+
+// device copy of a (validated) page list, cached by content
+int page_table(ckv_ctx* c, const ckv_page_list* pl, const int32_t** dstart, const int32_t** dlen) {
+  const int n = pl->n_pages;
+  *dstart = *dlen = nullptr;
+  if (n == 0) return CKV_OK;
+  std::vector<int32_t> key(2 * (size_t)n);
+  std::memcpy(key.data(), pl->start, n * sizeof(int32_t));
+  std::memcpy(key.data() + n, pl->len, n * sizeof(int32_t));
+  ++c->tick;
+  for (auto& e : c->pages) {
+    if (e.key == key) {
+      e.used = c->tick;
+      *dstart = e.dev;
+      *dlen = e.dev + n;
+      return CKV_OK;
+    }
+  }
+  PageEntry* e = nullptr;
+  if ((int)c->pages.size() < kPageCacheEntries) {
+    c->pages.emplace_back();
+    e = &c->pages.back();
+  } else {
+    e = &*std::min_element(c->pages.begin(), c->pages.end(),
+                           [](const PageEntry& a, const PageEntry& b) { return a.used < b.used; });
+  }
+  const size_t bytes = key.size() * sizeof(int32_t);
+  if (e->cap < bytes) {
+    if (e->dev) {
+      CKV_HIP(c, hipStreamSynchronize(c->stream));
+      (void)hipFree(e->dev);
+      e->dev = nullptr;
+      e->cap = 0;
+    }
+    void* p = nullptr;
+    if (hipMalloc(&p, round_up(bytes, 4096)) != hipSuccess) {
+      (void)hipGetLastError();
+      e->key.clear();
+      return fail(c, CKV_ERR_NOMEM, "page table allocation of %zu bytes failed", bytes);
+    }
+    e->dev = static_cast<int32_t*>(p);
+    e->cap = round_up(bytes, 4096);
+  }
+  e->key.clear();
+  int rc = upload(c, key.data(), bytes, e->dev);
+  if (rc) return rc;
+  e->key = std::move(key);
+  e->used = c->tick;
+  *dstart = e->dev;
+  *dlen = e->dev + n;
+  return CKV_OK;
+}
+
+int check_kv(ckv_ctx* c, const ckv_kv_view* kv) {
+  if (!kv || !kv->k || !kv->v || !kv->pos) return fail(c, CKV_ERR_ARG, "kv view or one of its pointers is NULL");
+  if (kv->head_dim != 64 && kv->head_dim != 128)
+    return fail(c, CKV_ERR_SHAPE, "head_dim %d unsupported (64 or 128)", kv->head_dim);
+  if (kv->n_tokens < 1 || kv->n_tokens > INT_MAX - 1024) return fail(c, CKV_ERR_SHAPE, "n_tokens %d out of range", kv->n_tokens);
+  if (kv->n_kv_heads < 1) return fail(c, CKV_ERR_SHAPE, "n_kv_heads must be >= 1");
+  if (!aligned16(kv->k) || !aligned16(kv->v) || kv->tok_stride % 8 || kv->head_stride % 8)
+    return fail(c, CKV_ERR_ARG, "K/V rows must be 16-byte aligned (strides multiples of 8)");
+  if (kv->tok_stride < kv->head_dim || kv->head_stride < 0)
+    return fail(c, CKV_ERR_SHAPE, "K/V strides too small");
+  return CKV_OK;
+}
+
+int check_win(ckv_ctx* c, const ckv_window_view* w, const ckv_kv_view* kv) {
+  if (!w || !w->q || !w->qpos) return fail(c, CKV_ERR_ARG, "window view or one of its pointers is NULL");
+  if (w->n_q_heads < 1 || w->n_q_heads % kv->n_kv_heads)
+    return fail(c, CKV_ERR_SHAPE, "n_q_heads %d is not a multiple of n_kv_heads %d", w->n_q_heads, kv->n_kv_heads);
+  if (w->n_rows < 1 || (int64_t)w->n_rows * w->n_q_heads > (1 << 20))
+    return fail(c, CKV_ERR_SHAPE, "window rows %d out of range", w->n_rows);
+  if (!aligned16(w->q) || w->row_stride % 8 || w->head_stride % 8)
+    return fail(c, CKV_ERR_ARG, "query rows must be 16-byte aligned (strides multiples of 8)");
+  if (w->row_stride < kv->head_dim) return fail(c, CKV_ERR_SHAPE, "query row stride too small");
+  if (!(std::isfinite(w->scale))) return fail(c, CKV_ERR_ARG, "scale must be finite");
+  return CKV_OK;
+}
+
+int check_pages(ckv_ctx* c, const ckv_page_list* pl, int n_tokens, const char* what) {
+  if (!pl) return fail(c, CKV_ERR_ARG, "%s page list is NULL", what);
+  if (pl->n_pages < 0) return fail(c, CKV_ERR_SHAPE, "%s: n_pages < 0", what);
+  if (pl->n_pages == 0) return CKV_OK;
+  if (!pl->start || !pl->len) return fail(c, CKV_ERR_ARG, "%s page arrays are NULL", what);
+  int64_t prev_end = 0;
+  for (int i = 0; i < pl->n_pages; ++i) {
+    const int64_t s = pl->start[i], l = pl->len[i];
+    if (l < 1 || l > CKV_MAX_PAGE_LEN) return fail(c, CKV_ERR_SHAPE, "%s page %d: length %lld not in [1, %d]", what, i, (long long)l, CKV_MAX_PAGE_LEN);
+    if (s < 0 || s + l > n_tokens) return fail(c, CKV_ERR_SHAPE, "%s page %d: [%lld, %lld) outside [0, %d)", what, i, (long long)s, (long long)(s + l), n_tokens);
+    if (s < prev_end) return fail(c, CKV_ERR_SHAPE, "%s page %d: pages must be sorted and disjoint", what, i);
+    prev_end = s + l;
+  }
+  return CKV_OK;
+}
+
+AttnGeom make_geom(const ckv_kv_view* kv, const ckv_window_view* w) {
+  AttnGeom a;
+  a.k = kv->k;
+  a.v = kv->v;
+  a.kv_head_stride = kv->head_stride;
+  a.kv_tok_stride = kv->tok_stride;
+  a.pos = kv->pos;
+  a.S = kv->n_tokens;
+  a.Hkv = kv->n_kv_heads;
+  a.D = kv->head_dim;
+  a.q = w->q;
+  a.q_head_stride = w->head_stride;
+  a.q_row_stride = w->row_stride;
+  a.qpos = w->qpos;
+  a.Hq = w->n_q_heads;
+  a.W = w->n_rows;
+  a.group = w->n_q_heads / kv->n_kv_heads;
+  a.rows = a.group * a.W;
+  const float scale = w->scale > 0.f ? w->scale : 1.0f / std::sqrt((float)kv->head_dim);
+  a.sl2 = scale * 1.4426950408889634f;
+  return a;
+}
+
+int items_per_block(int n_items, int other_blocks) {
+  const int per = ceil_div(n_items * std::max(other_blocks, 1), kTargetBlocks);
+  return std::max(1, per);
+}
+
+}  // namespace
+
+// ----------------------------------------------------------------- context
+
+extern "C" int ckv_create(ckv_ctx** out, int device, void* hip_stream) {
+  if (!out) return CKV_ERR_ARG;
+  *out = nullptr;
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || device < 0 || device >= n) {
+    (void)hipGetLastError();
+    return CKV_ERR_HIP;
+  }
+  ckv_ctx* c = new (std::nothrow) ckv_ctx();
+  if (!c) return CKV_ERR_NOMEM;
+  c->device = device;
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  *out = c;
+  return CKV_OK;
+}
+
+extern "C" int ckv_destroy(ckv_ctx* c) {
+  if (!c) return CKV_ERR_ARG;
+  {
+    DeviceGuard g(c->device);
+    (void)hipStreamSynchronize(c->stream);
+    if (c->ws) (void)hipFree(c->ws);
+    for (auto& e : c->pages)
+      if (e.dev) (void)hipFree(e.dev);
+    for (auto& s : c->slots) {
+      if (s.ev) (void)hipEventDestroy(s.ev);
+      if (s.host) (void)hipHostFree(s.host);
+    }
+  }
+  delete c;
+  return CKV_OK;
+}
+
+extern "C" int ckv_set_stream(ckv_ctx* c, void* hip_stream) {
+  if (!c) return CKV_ERR_ARG;
+  DeviceGuard g(c->device);
+  CKV_HIP(c, hipStreamSynchronize(c->stream));
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  return CKV_OK;
+}
+
+extern "C" int ckv_sync(ckv_ctx* c) {
+  if (!c) return CKV_ERR_ARG;
+  DeviceGuard g(c->device);
+  CKV_HIP(c, hipStreamSynchronize(c->stream));
+  return CKV_OK;
+}
+
+extern "C" const char* ckv_last_error(const ckv_ctx* c) { return c ? c->err.c_str() : "NULL context"; }
+
+extern "C" uint32_t ckv_version(void) {
+  return (CKV_VERSION_MAJOR << 16) | (CKV_VERSION_MINOR << 8) | CKV_VERSION_PATCH;
+}
+
+extern "C" int ckv_set_workspace_limit(ckv_ctx* c, size_t bytes) {
+  if (!c) return CKV_ERR_ARG;
+  c->ws_limit = bytes;
+  return CKV_OK;
+}
+
+extern "C" size_t ckv_workspace_bytes(const ckv_ctx* c) { return c ? c->ws_cap : 0; }
+
+// ------------------------------------------------------------- the calls
+
+extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win,
+                                        const ckv_page_list* pages, float* R, float* R_head, float* o,
+                                        float* lse, float* token_mass) {
+  if (!c) return CKV_ERR_ARG;
+  c->err.clear();
+  int rc;
+  if ((rc = check_kv(c, kv)) || (rc = check_win(c, win, kv)) || (rc = check_pages(c, pages, kv->n_tokens, "measured")))
+    return rc;
+  if (pages->n_pages > 0 && !R) return fail(c, CKV_ERR_ARG, "R is NULL");
+  DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
+
+  const AttnGeom a = make_geom(kv, win);
+  const int D = a.D, n = pages->n_pages, total_rows = a.Hq * a.W;
+  const int rpb = rows_per_block_attention();
+  const int nrb = ceil_div(a.rows, rpb);
+  int n_splits = std::max(1, std::min(ceil_div(a.S, 64), ceil_div(kTargetBlocks, a.Hkv * nrb)));
+  const int chunk = (int)round_up(ceil_div(a.S, n_splits), 64);
+  n_splits = ceil_div(a.S, chunk);
+
+  AttnSplit sp{chunk, n_splits, nrb * rpb, nullptr, nullptr, nullptr, nullptr};
+  RowStats rs{o, nullptr, nullptr, nullptr};
+  Plan plan;
+  const size_t nsr = (size_t)a.Hkv * n_splits * sp.rows_pad;
+  plan.add(&sp.part_o, nsr * D);
+  plan.add(&sp.part_m, nsr);
+  plan.add(&sp.part_l, nsr);
+  plan.add(&sp.part_c, nsr);
+  if (!o) plan.add(&rs.o, (size_t)total_rows * D);
+  plan.add(&rs.lse2, total_rows);
+  plan.add(&rs.onorm, total_rows);
+  plan.add(&rs.nvis, total_rows);
+  const int32_t *dstart = nullptr, *dlen = nullptr;
+  if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
+  if ((rc = realize(c, plan))) return rc;
+
+  CKV_HIP(c, launch_window_attention(a, sp, c->stream));
+  ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
+              token_mass ? (size_t)a.S : 0};
+  CKV_HIP(c, launch_combine(a, sp, rs, lse, zl, c->stream));
+  if (n > 0) {
+    PageWork pw{};
+    pw.start = dstart;
+    pw.len = dlen;
+    pw.n_items = n;
+    pw.n_pages = n;
+    pw.items_per_block = items_per_block(n, a.Hkv * ceil_div(a.rows, rows_per_block_page()));
+    pw.R = R;
+    pw.R_head = R_head;
+    pw.Hq = a.Hq;
+    pw.total_rows = total_rows;
+    CKV_HIP(c, launch_page_kernel(a, pw, rs, 0, c->stream));
+  }
+  if (token_mass) {
+    const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kTargetBlocks / a.Hkv)), 64);
+    CKV_HIP(c, launch_token_mass(a, rs, token_mass, mchunk, c->stream));
+  }
+  return CKV_OK;
+}
+
+extern "C" int ckv_classify_pages(ckv_ctx* c, int32_t n, const float* R_pre, const float* R_post,
+                                  const ckv_thresholds* th, const uint8_t* force, int32_t max_cand,
+                                  uint8_t* lambda, float* P_pre, float* P_post, int32_t* cand,
+                                  int32_t* n_cand) {
+  if (!c) return CKV_ERR_ARG;
+  c->err.clear();
+  if (n < 0) return fail(c, CKV_ERR_SHAPE, "n < 0");
+  if (!n_cand) return fail(c, CKV_ERR_ARG, "n_cand is NULL");
+  if (n > 0 && (!R_pre || !R_post || !lambda || !cand)) return fail(c, CKV_ERR_ARG, "NULL input or output array");
+  ckv_thresholds t = th ? *th : ckv_thresholds{0.05f, 0.01f, 0.75f, 0.25f, 0.01f};
+  if (!(t.tau_dead <= t.tau_use) || !(t.rho_dead <= t.rho_use))
+    return fail(c, CKV_ERR_ARG, "thresholds must satisfy tau_dead <= tau_use and rho_dead <= rho_use");
+  DeviceGuard g(c->device);
+  ClassifyArgs a{};
+  a.n = n;
+  a.R_pre = R_pre;
+  a.R_post = R_post;
+  a.tau_use = t.tau_use;
+  a.tau_dead = t.tau_dead;
+  a.rho_use = t.rho_use;
+  a.rho_dead = t.rho_dead;
+  a.force = force;
+  a.max_cand = max_cand;
+  a.lambda = lambda;
+  a.P_pre = P_pre;
+  a.P_post = P_post;
+  a.cand = cand;
+  a.n_cand = n_cand;
+  Plan plan;
+  plan.add(&a.is_cand, std::max(n, 1));
+  if (!P_pre) plan.add(&a.P_pre, std::max(n, 1));
+  if (!P_post) plan.add(&a.P_post, std::max(n, 1));
+  int rc = realize(c, plan);
+  if (rc) return rc;
+  CKV_HIP(c, launch_classify(a, c->stream));
+  return CKV_OK;
+}
+
+extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win, const float* o,
+                              const float* lse, const ckv_page_list* pages, const int32_t* cand,
+                              const int32_t* n_cand, int32_t max_cand, float tau_joint, uint8_t* accepted,
+                              float* union_R, int32_t* n_accepted) {
+  if (!c) return CKV_ERR_ARG;
+  c->err.clear();
+  int rc;
+  if ((rc = check_kv(c, kv)) || (rc = check_win(c, win, kv)) || (rc = check_pages(c, pages, kv->n_tokens, "joint")))
+    return rc;
+  if (!o || !lse || !cand || !n_cand || !accepted || !n_accepted)
+    return fail(c, CKV_ERR_ARG, "NULL input or output array");
+  if (max_cand < 1) return fail(c, CKV_ERR_SHAPE, "max_cand must be >= 1");
+  if (!std::isfinite(tau_joint)) return fail(c, CKV_ERR_ARG, "tau_joint must be finite");
+  DeviceGuard g(c->device);
+  const AttnGeom a = make_geom(kv, win);
+  const int total_rows = a.Hq * a.W, D = a.D;
+  RowStats rs{const_cast<float*>(o), nullptr, nullptr, nullptr};
+  JointArgs j{};
+  j.total_rows = total_rows;
+  j.D = D;
+  j.max_cand = max_cand;
+  j.W = a.W;
+  j.n_cand = n_cand;
+  j.window = kJointWindow;
+  j.rows_per_block = kJointRowsPerBlock;
+  j.tau = tau_joint;
+  j.accepted = accepted;
+  j.union_R = union_R;
+  j.n_accepted = n_accepted;
+  float *resid, *resA, *Dst, *Ast;
+  int *resC, *Cst;
+  Plan plan;
+  plan.add(&rs.lse2, total_rows);
+  plan.add(&rs.onorm, total_rows);
+  plan.add(&rs.nvis, total_rows);
+  plan.add(&resid, (size_t)max_cand * total_rows * D);
+  plan.add(&resA, (size_t)max_cand * total_rows);
+  plan.add(&resC, (size_t)max_cand * total_rows);
+  plan.add(&Dst, 2 * (size_t)total_rows * D);
+  plan.add(&Ast, 2 * (size_t)total_rows);
+  plan.add(&Cst, 2 * (size_t)total_rows);
+  plan.add(&j.ctrl, 8);
+  plan.add(&j.rbuf, kJointWindow);
+  const int32_t *dstart = nullptr, *dlen = nullptr;
+  if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
+  if ((rc = realize(c, plan))) return rc;
+  j.resid = resid;
+  j.resA = resA;
+  j.resC = resC;
+  j.Dstate = Dst;
+  j.Astate = Ast;
+  j.Cstate = Cst;
+  j.onorm = rs.onorm;
+  j.nvis = rs.nvis;
+
+  CKV_HIP(c, launch_joint_prepare(a, o, lse, rs, j, c->stream));
+  if (pages->n_pages > 0) {
+    PageWork pw{};
+    pw.start = dstart;
+    pw.len = dlen;
+    pw.n_items = max_cand;
+    pw.n_pages = pages->n_pages;
+    pw.items_per_block = items_per_block(max_cand, a.Hkv * ceil_div(a.rows, rows_per_block_page()));
+    pw.cand = cand;
+    pw.n_cand = n_cand;
+    pw.Hq = a.Hq;
+    pw.resid = resid;
+    pw.resA = resA;
+    pw.resC = resC;
+    pw.total_rows = total_rows;
+    CKV_HIP(c, launch_page_kernel(a, pw, rs, 1, c->stream));
+    for (int r = 0; r < max_cand; ++r) CKV_HIP(c, launch_joint_round(j, c->stream));
+  }
+  return CKV_OK;
+}
+
+extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, const int32_t* n_tokens,
+                                      const float* score, int64_t score_seq_stride,
+                                      const ckv_page_list* retired, const ckv_page_list* pending,
+                                      const float* const* pending_r_pre, const ckv_budget* budget,
+                                      const ckv_cache_view* out, int32_t* kept_idx, int32_t* n_kept,
+                                      uint8_t* token_state) {
+  if (!c) return CKV_ERR_ARG;
+  c->err.clear();
+  if (!in || !out || !n_tokens || !score || !retired || !pending || !budget || !kept_idx || !n_kept)
+    return fail(c, CKV_ERR_ARG, "NULL argument");
+  if (!in->k || !in->v || !in->pos || !out->k || !out->v || !out->pos) return fail(c, CKV_ERR_ARG, "NULL cache pointer");
+  if (in->n_seq < 1 || in->n_layers < 1 || in->n_kv_heads < 1) return fail(c, CKV_ERR_SHAPE, "empty cache shape");
+  if (in->head_dim != 64 && in->head_dim != 128) return fail(c, CKV_ERR_SHAPE, "head_dim %d unsupported", in->head_dim);
+  if (out->n_seq != in->n_seq || out->n_layers != in->n_layers || out->n_kv_heads != in->n_kv_heads ||
+      out->head_dim != in->head_dim)
+    return fail(c, CKV_ERR_SHAPE, "input and output caches differ in shape");
+  const ckv_cache_view* vv[2] = {in, out};
+  for (const ckv_cache_view* v : vv) {
+    if (!aligned16(v->k) || !aligned16(v->v) || v->tok_stride % 8 || v->head_stride % 8 || v->layer_stride % 8 ||
+        v->seq_stride % 8)
+      return fail(c, CKV_ERR_ARG, "cache rows must be 16-byte aligned (strides multiples of 8)");
+    if (v->tok_stride < v->head_dim || v->capacity < 1) return fail(c, CKV_ERR_SHAPE, "cache strides or capacity");
+  }
+  const int B = budget->budget;
+  if (B < 1 || !(budget->eta >= 0.f && budget->eta <= 1.f) || budget->max_pending_pages < 0 || budget->keep_recent < 0)
+    return fail(c, CKV_ERR_ARG, "invalid budget parameters");
+  const int bn = (int)std::floor((double)budget->eta * (double)B);
+  if ((int64_t)budget->keep_recent + bn > B)
+    return fail(c, CKV_ERR_BUDGET, "keep_recent (%d) + B_N (%d) exceeds the budget %d", budget->keep_recent, bn, B);
+  if (out->capacity < B) return fail(c, CKV_ERR_SHAPE, "output capacity %d < budget %d", out->capacity, B);
+  const int ns = in->n_seq;
+  for (int s = 0; s < ns; ++s) {
+    if (n_tokens[s] < 1 || n_tokens[s] > in->capacity || n_tokens[s] > score_seq_stride)
+      return fail(c, CKV_ERR_SHAPE, "sequence %d: n_tokens %d out of range", s, n_tokens[s]);
+    int rc;
+    if ((rc = check_pages(c, &retired[s], n_tokens[s], "retired")) ||
+        (rc = check_pages(c, &pending[s], n_tokens[s], "pending")))
+      return rc;
+    if (pending[s].n_pages > 0 && (!pending_r_pre || !pending_r_pre[s]))
+      return fail(c, CKV_ERR_ARG, "sequence %d: pending R_pre is NULL", s);
+  }
+  // the output must not overlap the input (bytes of K, V and positions)
+  auto extent = [](const ckv_cache_view* v) {
+    return ((int64_t)(v->n_seq - 1) * v->seq_stride + (int64_t)(v->n_layers - 1) * v->layer_stride +
+            (int64_t)(v->n_kv_heads - 1) * v->head_stride + (int64_t)(v->capacity - 1) * v->tok_stride +
+            v->head_dim) * 2;
+  };
+  auto overlap = [](const void* a, int64_t na, const void* b, int64_t nb) {
+    const char* x = static_cast<const char*>(a);
+    const char* y = static_cast<const char*>(b);
+    return x < y + nb && y < x + na;
+  };
+  const int64_t ei = extent(in), eo = extent(out);
+  const int64_t pi = ((int64_t)(ns - 1) * in->pos_seq_stride + in->capacity) * 4;
+  const int64_t po = ((int64_t)(ns - 1) * out->pos_seq_stride + out->capacity) * 4;
+  const void* ins[3] = {in->k, in->v, in->pos};
+  const int64_t inb[3] = {ei, ei, pi};
+  const void* outs[3] = {out->k, out->v, out->pos};
+  const int64_t outb[3] = {eo, eo, po};
+  for (int x = 0; x < 3; ++x)
+    for (int y = 0; y < 3; ++y)
+      if (overlap(ins[x], inb[x], outs[y], outb[y])) return fail(c, CKV_ERR_ARG, "output cache overlaps the input");
+  if (overlap(out->k, eo, out->v, eo)) return fail(c, CKV_ERR_ARG, "output K and V overlap");
+  DeviceGuard g(c->device);
+
+  // pack every host-side list into one blob: [pend_r ptrs][n_tokens][ret_off][pend_off][ret start,len][pend start,len]
+  int tot_r = 0, tot_p = 0;
+  for (int s = 0; s < ns; ++s) {
+    tot_r += retired[s].n_pages;
+    tot_p += pending[s].n_pages;
+  }
+  std::vector<uint64_t> blob64(ns);
+  for (int s = 0; s < ns; ++s)
+    blob64[s] = pending[s].n_pages > 0 ? reinterpret_cast<uint64_t>(pending_r_pre[s]) : 0;
+  std::vector<int32_t> blob32;
+  blob32.reserve(ns + 2 * (ns + 1) + 2 * (tot_r + tot_p));
+  blob32.insert(blob32.end(), n_tokens, n_tokens + ns);
+  int run = 0;
+  for (int s = 0; s <= ns; ++s) { blob32.push_back(run); if (s < ns) run += retired[s].n_pages; }
+  run = 0;
+  for (int s = 0; s <= ns; ++s) { blob32.push_back(run); if (s < ns) run += pending[s].n_pages; }
+  for (int s = 0; s < ns; ++s) blob32.insert(blob32.end(), retired[s].start, retired[s].start + retired[s].n_pages);
+  for (int s = 0; s < ns; ++s) blob32.insert(blob32.end(), retired[s].len, retired[s].len + retired[s].n_pages);
+  for (int s = 0; s < ns; ++s) blob32.insert(blob32.end(), pending[s].start, pending[s].start + pending[s].n_pages);
+  for (int s = 0; s < ns; ++s) blob32.insert(blob32.end(), pending[s].len, pending[s].len + pending[s].n_pages);
+  std::vector<char> blob(blob64.size() * 8 + blob32.size() * 4);
+  std::memcpy(blob.data(), blob64.data(), blob64.size() * 8);
+  std::memcpy(blob.data() + blob64.size() * 8, blob32.data(), blob32.size() * 4);
+
+  char* dblob = nullptr;
+  SelectArgs sa{};
+  Plan plan;
+  plan.add(&dblob, blob.size());
+  plan.add(&sa.pend_prot, std::max(tot_p, 1));
+  plan.add(&sa.pend_ord, std::max(tot_p, 1));
+  uint8_t* state_ws = nullptr;
+  if (!token_state) plan.add(&state_ws, (size_t)ns * score_seq_stride);
+  int rc = realize(c, plan);
+  if (rc) return rc;
+  if ((rc = upload(c, blob.data(), blob.size(), dblob))) return rc;
+  const int32_t* d32 = reinterpret_cast<const int32_t*>(dblob + blob64.size() * 8);
+  sa.n_seq = ns;
+  sa.pend_r = reinterpret_cast<const uint64_t*>(dblob);
+  sa.n_tokens = d32;
+  sa.ret_off = d32 + ns;
+  sa.pend_off = d32 + ns + (ns + 1);
+  sa.ret_start = d32 + ns + 2 * (ns + 1);
+  sa.ret_len = sa.ret_start + tot_r;
+  sa.pend_start = sa.ret_len + tot_r;
+  sa.pend_len = sa.pend_start + tot_p;
+  sa.score = score;
+  sa.score_seq_stride = score_seq_stride;
+  sa.budget = B;
+  sa.bn = bn;
+  sa.max_pages = budget->max_pending_pages;
+  sa.keep_recent = budget->keep_recent;
+  sa.state = token_state ? token_state : state_ws;
+  sa.kept = kept_idx;
+  sa.n_kept = n_kept;
+  CKV_HIP(c, launch_protect(sa, c->stream));
+  CKV_HIP(c, launch_select(sa, c->stream));
+
+  GatherArgs ga{};
+  ga.k_in = in->k;
+  ga.v_in = in->v;
+  ga.in_seq = in->seq_stride;
+  ga.in_layer = in->layer_stride;
+  ga.in_head = in->head_stride;
+  ga.in_tok = in->tok_stride;
+  ga.k_out = out->k;
+  ga.v_out = out->v;
+  ga.out_seq = out->seq_stride;
+  ga.out_layer = out->layer_stride;
+  ga.out_head = out->head_stride;
+  ga.out_tok = out->tok_stride;
+  ga.pos_in = in->pos;
+  ga.pos_in_seq = in->pos_seq_stride;
+  ga.pos_out = out->pos;
+  ga.pos_out_seq = out->pos_seq_stride;
+  ga.n_seq = ns;
+  ga.n_layers = in->n_layers;
+  ga.Hkv = in->n_kv_heads;
+  ga.D = in->head_dim;
+  ga.kept = kept_idx;
+  ga.n_kept = n_kept;
+  ga.budget = B;
+  CKV_HIP(c, launch_gather(ga, c->stream));
+  return CKV_OK;
+}

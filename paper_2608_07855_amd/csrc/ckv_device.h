@@ -1,0 +1,82 @@
+// Device-side building blocks shared by the CommitKV kernels (gfx950 only).
+//
+// MFMA fragment layouts used throughout (v_mfma_f32_32x32x16_{bf16,f16},
+// one wave of 64 lanes, lane l, half h = l / 32, column c = l % 32):
+//   A operand (32 x 16): lane holds A[c][8h .. 8h+7]
+//   B operand (16 x 32): lane holds B[8h .. 8h+7][c]
+//   C/D (32 x 32), 16 floats: register r holds C[8(r/4) + 4h + r%4][c]
+//
+// The attention kernels compute the TRANSPOSED scores S^T = K Q^T so that a
+// window row sits on a lane column: per-row max/sum/norm reductions are then
+// lane-local plus one exchange with the partner lane (l ^ 32), and the
+// per-row rescaling of the output accumulator is a per-lane scalar.  The
+// value-weighted sum O^T = V^T P^T takes P^T straight from the score
+// accumulator: registers 8u .. 8u+7 of a 32-token score block are the B
+// operand of the u-th 16-token step, provided V^T is staged in LDS with the
+// token order inside each 16-token group permuted by swapping bits 2 and 3.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ckv {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kTile = 64;            // tokens per staged tile / max page length
+constexpr int kMaxPage = 64;
+
+__device__ __forceinline__ f32x16 mfma_bf16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mfma_f16(f16x8 a, f16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+__device__ __forceinline__ float bf16_bits_to_float(uint32_t b) {
+  return __uint_as_float(b << 16);
+}
+
+// 8 bf16 (one 16-byte chunk) -> 8 fp16, exact inside the fp16 normal range.
+__device__ __forceinline__ f16x4 bf16x4_to_f16(uint32_t lo, uint32_t hi) {
+  f16x4 r;
+  r[0] = (_Float16)bf16_bits_to_float(lo & 0xFFFFu);
+  r[1] = (_Float16)bf16_bits_to_float(lo >> 16);
+  r[2] = (_Float16)bf16_bits_to_float(hi & 0xFFFFu);
+  r[3] = (_Float16)bf16_bits_to_float(hi >> 16);
+  return r;
+}
+
+// bf16 element j (0..7) of a 16-byte chunk
+__device__ __forceinline__ uint32_t chunk_elem(const uint4& c, int j) {
+  uint32_t w = (j < 2) ? c.x : (j < 4) ? c.y : (j < 6) ? c.z : c.w;
+  return (j & 1) ? (w >> 16) : (w & 0xFFFFu);
+}
+
+// slot of token t (0..63) in the V^T tile: swap bits 2 and 3
+__device__ __forceinline__ int vt_slot(int t) {
+  return (t & ~0xC) | ((t & 4) << 1) | ((t & 8) >> 1);
+}
+
+__device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, 64); }
+__device__ __forceinline__ int xor32i(int v) { return __shfl_xor(v, 32, 64); }
+
+// bit pattern of a non-negative float (including +inf) keeps its order as uint
+__device__ __forceinline__ void atomic_max_nonneg(float* addr, float v) {
+  atomicMax(reinterpret_cast<unsigned int*>(addr), __float_as_uint(v));
+}
+
+}  // namespace ckv

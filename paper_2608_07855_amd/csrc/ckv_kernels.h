@@ -1,0 +1,162 @@
+// Launch interface between the host runtime (api.cpp) and the HIP kernels.
+// Plain structs of device pointers and sizes; no torch types anywhere.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ckv {
+
+// one layer of one sequence and one query window
+struct AttnGeom {
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t kv_head_stride, kv_tok_stride;   // elements
+  const int32_t* pos;
+  int S, Hkv, D;
+  const uint16_t* q;
+  int64_t q_head_stride, q_row_stride;     // elements
+  const int32_t* qpos;
+  int Hq, W, group;                        // group = Hq / Hkv
+  int rows;                                // window rows per KV head = group * W
+  float sl2;                               // softmax scale * log2(e)
+};
+
+// split-sequence partials of pass A
+struct AttnSplit {
+  int chunk, n_splits, rows_pad;
+  float* part_o;   // [Hkv][n_splits][rows_pad][D]
+  float* part_m;   // [Hkv][n_splits][rows_pad]  (log2 units)
+  float* part_l;
+  int* part_c;     // visible-token counts
+};
+
+// per window row (global row h*W + p): o [rows][D], lse2 (log2 units), ||o||, n_vis
+struct RowStats {
+  float* o;
+  float* lse2;
+  float* onorm;
+  int* nvis;
+};
+
+// pages processed by pass B (MODE 0: item = page; MODE 1: item t = page cand[t])
+struct PageWork {
+  const int32_t* start;
+  const int32_t* len;
+  int n_items;            // MODE 0: pages; MODE 1: max_cand (capped by *n_cand)
+  int n_pages;            // entries of start/len (MODE 1 ignores candidates outside)
+  int items_per_block;
+  const int32_t* cand;    // MODE 1
+  const int32_t* n_cand;  // MODE 1 (device)
+  float* R;               // MODE 0: [n_pages], zeroed before
+  float* R_head;          // MODE 0: [n_pages][Hq] or null, zeroed before
+  int Hq;
+  float* resid;           // MODE 1: [max_cand][total_rows][D]
+  float* resA;            // MODE 1: [max_cand][total_rows]
+  int* resC;              // MODE 1: [max_cand][total_rows]
+  int total_rows;         // Hq * W
+};
+
+struct ZeroList {
+  float* p0; size_t n0;
+  float* p1; size_t n1;
+  float* p2; size_t n2;
+};
+
+int rows_per_block_attention();
+int rows_per_block_page();
+
+hipError_t launch_window_attention(const AttnGeom& a, const AttnSplit& sp, hipStream_t s);
+hipError_t launch_combine(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs, float* lse_out,
+                          const ZeroList& zl, hipStream_t s);
+hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowStats& rs, int mode,
+                              hipStream_t s);
+hipError_t launch_token_mass(const AttnGeom& a, const RowStats& rs, float* mass, int chunk,
+                             hipStream_t s);
+
+// classification (Eq. (8)-(10)) and candidate order
+struct ClassifyArgs {
+  int n;
+  const float* R_pre;
+  const float* R_post;
+  float tau_use, tau_dead, rho_use, rho_dead;
+  const uint8_t* force;   // optional
+  int max_cand;           // <= 0: no cap
+  uint8_t* lambda;
+  float* P_pre;           // required (workspace if the caller passes none)
+  float* P_post;
+  uint8_t* is_cand;       // workspace [n]
+  int32_t* cand;
+  int32_t* n_cand;
+};
+hipError_t launch_classify(const ClassifyArgs& c, hipStream_t s);
+
+// joint test (Eq. (11))
+struct JointArgs {
+  int total_rows, D, max_cand, W;
+  const int32_t* n_cand;
+  const float* resid;     // [max_cand][rows][D]
+  const float* resA;      // [max_cand][rows]
+  const int* resC;
+  const float* onorm;     // [rows]
+  const int* nvis;        // [rows]
+  float* Dstate;          // [rows][D] accumulated residual of accepted pages
+  float* Astate;          // [rows]
+  int* Cstate;            // [rows]
+  int* ctrl;              // [4]: cursor, pending accepted item (-1), done, block counter
+  unsigned int* rbuf;     // [window] per-candidate max ratio bits
+  int window;             // candidates evaluated per round
+  int rows_per_block;
+  float tau;
+  uint8_t* accepted;
+  float* union_R;
+  int32_t* n_accepted;
+};
+hipError_t launch_joint_prepare(const AttnGeom& a, const float* o, const float* lse, RowStats rs,
+                                const JointArgs& j, hipStream_t s);
+hipError_t launch_joint_round(const JointArgs& j, hipStream_t s);
+hipError_t launch_joint_finish(const JointArgs& j, hipStream_t s);
+
+// checkpoint: protection, selection, compaction (Eq. (12)-(13), Eq. (4))
+struct SelectArgs {
+  int n_seq;
+  const int32_t* n_tokens;       // [n_seq]
+  const float* score;
+  int64_t score_seq_stride;
+  const int32_t* ret_off;        // [n_seq+1] offsets into ret_start/ret_len
+  const int32_t* ret_start;
+  const int32_t* ret_len;
+  const int32_t* pend_off;       // [n_seq+1]
+  const int32_t* pend_start;
+  const int32_t* pend_len;
+  const uint64_t* pend_r;        // [n_seq] device pointers to R_pre arrays
+  uint8_t* pend_prot;            // [total pending] workspace
+  int32_t* pend_ord;             // [total pending] workspace
+  int budget, bn, max_pages, keep_recent;
+  uint8_t* state;                // [n_seq][score_seq_stride]
+  int32_t* kept;                 // [n_seq][budget]
+  int32_t* n_kept;               // [n_seq]
+};
+hipError_t launch_protect(const SelectArgs& a, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+
+struct GatherArgs {
+  const uint16_t* k_in;
+  const uint16_t* v_in;
+  int64_t in_seq, in_layer, in_head, in_tok;
+  uint16_t* k_out;
+  uint16_t* v_out;
+  int64_t out_seq, out_layer, out_head, out_tok;
+  const int32_t* pos_in;
+  int64_t pos_in_seq;
+  int32_t* pos_out;
+  int64_t pos_out_seq;
+  int n_seq, n_layers, Hkv, D;
+  const int32_t* kept;           // [n_seq][budget]
+  const int32_t* n_kept;
+  int budget;
+};
+hipError_t launch_gather(const GatherArgs& g, hipStream_t s);
+
+}  // namespace ckv

@@ -1,0 +1,106 @@
+// Lifecycle classification of event pages (CommitKV, Sec. 3.2, Eq. (8)-(10))
+// and the candidate order of Sec. 3.3.
+//
+// rank_kernel: one thread per page.  Percentile P(E) = (number of other pages
+// with a strictly smaller effect) / (n - 1), 0.5 for n = 1; counted exactly
+// against every page (values staged through LDS), so ties share the lower
+// rank.  The comparison P >= rho is made in double precision on the integer
+// count.  Then H/L of Eq. (9) and the state of Eq. (10).
+// order_kernel: one thread per page.  A candidate's slot in the ordered list
+// is the number of candidates that precede it under (R+ ascending, R-
+// descending, index ascending); the keys are unique so the slots form a
+// permutation without any sort.
+#include "ckv_device.h"
+#include "ckv_kernels.h"
+
+namespace ckv {
+
+namespace {
+constexpr int kCT = 256;
+}
+
+__global__ __launch_bounds__(kCT) void rank_kernel(ClassifyArgs c) {
+  __shared__ float s_pre[kCT], s_post[kCT];
+  const int i = blockIdx.x * kCT + threadIdx.x;
+  const bool act = i < c.n;
+  const float rp = act ? c.R_pre[i] : 0.f;
+  const float rq = act ? c.R_post[i] : 0.f;
+  int less_pre = 0, less_post = 0;
+  for (int j0 = 0; j0 < c.n; j0 += kCT) {
+    const int j = j0 + threadIdx.x;
+    __syncthreads();
+    s_pre[threadIdx.x] = j < c.n ? c.R_pre[j] : 0.f;
+    s_post[threadIdx.x] = j < c.n ? c.R_post[j] : 0.f;
+    __syncthreads();
+    const int m = min(kCT, c.n - j0);
+    for (int t = 0; t < m; ++t) {
+      less_pre += s_pre[t] < rp ? 1 : 0;
+      less_post += s_post[t] < rq ? 1 : 0;
+    }
+  }
+  if (!act) return;
+  const double den = c.n > 1 ? (double)(c.n - 1) : 1.0;
+  const double Pm = c.n > 1 ? less_pre / den : 0.5;
+  const double Pp = c.n > 1 ? less_post / den : 0.5;
+  // Eq. (9), inclusive comparisons
+  const bool H_pre = rp >= c.tau_use && Pm >= (double)c.rho_use;
+  const bool L_pre = rp <= c.tau_dead && Pm <= (double)c.rho_dead;
+  const bool H_post = rq >= c.tau_use && Pp >= (double)c.rho_use;
+  const bool L_post = rq <= c.tau_dead && Pp <= (double)c.rho_dead;
+  // Eq. (10)
+  uint8_t lam = 0;
+  if (H_pre && L_post) lam = 1;
+  else if (L_pre && L_post) lam = 2;
+  else if (L_pre && H_post) lam = 3;
+  else if (H_pre && H_post) lam = 4;
+  c.lambda[i] = lam;
+  c.P_pre[i] = (float)Pm;
+  c.P_post[i] = (float)Pp;
+  c.is_cand[i] = (lam == 1 || (c.force && c.force[i])) ? 1 : 0;
+  c.cand[i] = -1;
+}
+
+__device__ __forceinline__ bool precedes(float qj, float pj, int j, float qi, float pi, int i) {
+  if (qj != qi) return qj < qi;          // R+ ascending
+  if (pj != pi) return pj > pi;          // then R- descending
+  return j < i;                          // then page order
+}
+
+__global__ __launch_bounds__(kCT) void order_kernel(ClassifyArgs c) {
+  __shared__ float s_pre[kCT], s_post[kCT];
+  __shared__ uint8_t s_c[kCT];
+  const int i = blockIdx.x * kCT + threadIdx.x;
+  const bool act = i < c.n;
+  const bool me = act && c.is_cand[i];
+  const float rp = act ? c.R_pre[i] : 0.f;
+  const float rq = act ? c.R_post[i] : 0.f;
+  int before = 0, total = 0;
+  for (int j0 = 0; j0 < c.n; j0 += kCT) {
+    const int j = j0 + threadIdx.x;
+    __syncthreads();
+    s_pre[threadIdx.x] = j < c.n ? c.R_pre[j] : 0.f;
+    s_post[threadIdx.x] = j < c.n ? c.R_post[j] : 0.f;
+    s_c[threadIdx.x] = j < c.n ? c.is_cand[j] : 0;
+    __syncthreads();
+    const int m = min(kCT, c.n - j0);
+    for (int t = 0; t < m; ++t) {
+      if (!s_c[t]) continue;
+      ++total;
+      before += precedes(s_post[t], s_pre[t], j0 + t, rq, rp, i) ? 1 : 0;
+    }
+  }
+  const int cap = c.max_cand > 0 ? min(c.max_cand, c.n) : c.n;
+  if (me && before < cap) c.cand[before] = i;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *c.n_cand = min(total, cap);
+}
+
+hipError_t launch_classify(const ClassifyArgs& c, hipStream_t s) {
+  const int nb = c.n > 0 ? (c.n + kCT - 1) / kCT : 1;
+  hipLaunchKernelGGL(rank_kernel, dim3(nb), dim3(kCT), 0, s, c);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(order_kernel, dim3(nb), dim3(kCT), 0, s, c);
+  return hipGetLastError();
+}
+
+}  // namespace ckv

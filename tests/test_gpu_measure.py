@@ -1,0 +1,130 @@
+"""GPU parity of ckv_measure_page_effects against the fp64 oracle (Sec. 3.2).
+
+Bar: R and R_head within 2e-3 relative (floor 1e-6) of the oracle, +inf in
+the same places; window outputs, log-sum-exp and token mass to fp32/fp16
+accuracy.  Every call goes through the C ABI.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from synth import WORKLOADS, make_layer, scaled
+from tests.gpu_util import LayerOnDevice, assert_scores_close, oracle_pass
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ckv():
+    import paper_2608_07855_amd as P
+    ctx = P.Context(0)
+    yield P, ctx
+    ctx.close()
+
+
+def _measure(P, ctx, dl, which, want=("R", "R_head", "o", "lse")):
+    L = dl.L
+    if which == "pre":
+        kv = P.kv_view(dl.k, dl.v, dl.pos, n_tokens=L.layout.s_pre)
+        win = P.window_view(dl.q_pre, dl.qpos_pre)
+    else:
+        kv = P.kv_view(dl.k, dl.v, dl.pos)
+        win = P.window_view(dl.q_post, dl.qpos_post)
+    pages = P.Pages(L.layout.page_start, L.layout.page_len)
+    out = P.ckv_measure_page_effects(ctx, kv, win, pages, want=want)
+    torch.cuda.synchronize()
+    return {k: (v.cpu().numpy() if torch.is_tensor(v) else v) for k, v in out.items()}
+
+
+CASES = {
+    "tiny": WORKLOADS["tiny"],
+    "tiny_gapped": scaled("tiny", gapped_positions=True),
+    "d128_ragged": scaled("q8b", n_tokens=3000, n_q_heads=8, n_kv_heads=2, event_lo=40, event_hi=300),
+    "g64_w128": scaled("q32b", n_tokens=2500, n_q_heads=8, n_kv_heads=1, window=128, event_lo=64,
+                       event_hi=400),
+    "w8_mha": scaled("tiny", n_tokens=1200, n_q_heads=3, n_kv_heads=3, window=8, event_lo=20,
+                     event_hi=90),
+    "w40_d128": scaled("q8b", n_tokens=1500, n_q_heads=6, n_kv_heads=2, window=40, page_size=24,
+                       event_lo=41, event_hi=200),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+@pytest.mark.parametrize("which", ["pre", "post"])
+def test_page_effects_match_oracle(ckv, case, which):
+    P, ctx = ckv
+    L = make_layer(CASES[case], seed=1)
+    print(f"[measure] case={case} pass={which} S={L.w.n_tokens} pages={len(L.pages)}", flush=True)
+    dl = LayerOnDevice(L)
+    got = _measure(P, ctx, dl, which)
+    R, Rh = oracle_pass(L, which)
+    assert_scores_close(got["R"], R, "R")
+    assert_scores_close(got["R_head"], Rh, "R_head")
+    # window outputs and lse against the oracle's full attention
+    S = L.layout.s_pre if which == "pre" else L.w.n_tokens
+    q = L.q_pre if which == "pre" else L.q_post
+    qpos = L.qpos_pre if which == "pre" else L.qpos_post
+    Ow, lse, _ = O.window_outputs(L.k[:, :S], L.v[:, :S], L.pos[:S], q, qpos)
+    np.testing.assert_allclose(got["lse"], lse, rtol=0, atol=2e-4)
+    scale = np.abs(Ow).max()
+    np.testing.assert_allclose(got["o"], Ow, rtol=0, atol=2e-3 * scale)
+
+
+def test_bruteforce_subsample_tiny(ckv):
+    """The same GPU scores against the brute-force definition (masked re-run)."""
+    P, ctx = ckv
+    L = make_layer(WORKLOADS["tiny"], seed=2)
+    dl = LayerOnDevice(L)
+    got = _measure(P, ctx, dl, "post")
+    sub = list(range(0, len(L.pages), 3))
+    R, _ = O.page_effects(L.k, L.v, L.pos, L.q_post, L.qpos_post, [L.pages[j] for j in sub])
+    assert_scores_close(got["R"][sub], R, "R (brute force)")
+
+
+def test_token_mass(ckv):
+    P, ctx = ckv
+    L = make_layer(CASES["d128_ragged"], seed=3)
+    dl = LayerOnDevice(L)
+    got = _measure(P, ctx, dl, "post", want=("R", "token_mass"))
+    want = O.token_mass(L.k, L.v, L.pos, L.q_post, L.qpos_post)
+    np.testing.assert_allclose(got["token_mass"], want, rtol=3e-3, atol=1e-6)
+
+
+def test_edge_pages(ckv):
+    """Hand-placed pages: a page holding every token a row sees (+inf), pages
+    past every window position (0), single-token pages, a 64-token page."""
+    P, ctx = ckv
+    w = scaled("tiny", n_tokens=600, n_q_heads=2, n_kv_heads=1, window=4)
+    L = make_layer(w, seed=4)
+    L.qpos_post[:] = np.array([3, 100, 300, 599], np.int32)
+    pages = [(0, 4), (4, 1), (10, 64), (200, 1), (400, 33), (560, 40)]
+    L.layout.page_start = np.array([p[0] for p in pages], np.int32)
+    L.layout.page_len = np.array([p[1] for p in pages], np.int32)
+    dl = LayerOnDevice(L)
+    got = _measure(P, ctx, dl, "post")
+    R, Rh = O.page_effects(L.k, L.v, L.pos, L.q_post, L.qpos_post, pages, method="bruteforce")
+    assert np.isinf(R[0])
+    assert_scores_close(got["R"], R, "R")
+    assert_scores_close(got["R_head"], Rh, "R_head")
+
+
+def test_no_pages(ckv):
+    P, ctx = ckv
+    L = make_layer(WORKLOADS["tiny"], seed=5)
+    dl = LayerOnDevice(L)
+    kv = P.kv_view(dl.k, dl.v, dl.pos)
+    win = P.window_view(dl.q_post, dl.qpos_post)
+    out = P.ckv_measure_page_effects(ctx, kv, win, P.Pages([], []), want=("R", "lse"))
+    torch.cuda.synchronize()
+    _, lse, _ = O.window_outputs(L.k, L.v, L.pos, L.q_post, L.qpos_post)
+    np.testing.assert_allclose(out["lse"].cpu().numpy(), lse, atol=2e-4, rtol=0)
+
+
+def test_deterministic(ckv):
+    P, ctx = ckv
+    L = make_layer(WORKLOADS["tiny"], seed=6)
+    dl = LayerOnDevice(L)
+    a = _measure(P, ctx, dl, "post")
+    b = _measure(P, ctx, dl, "post")
+    assert np.array_equal(a["R"], b["R"]) and np.array_equal(a["o"], b["o"])
