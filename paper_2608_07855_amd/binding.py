@@ -109,8 +109,12 @@ def kv_view(k, v, pos, n_tokens: int | None = None) -> KVView:
     if pos.dtype != torch.int32 or not pos.is_cuda:
         raise ValueError("pos must be a cuda int32 tensor")
     S = k.shape[1] if n_tokens is None else int(n_tokens)
-    return KVView(k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1), pos.data_ptr(), S,
+    if not 1 <= S <= k.shape[1] or pos.numel() < S:
+        raise ValueError("n_tokens out of range")
+    view = KVView(k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1), pos.data_ptr(), S,
                   k.shape[0], k.shape[2])
+    view._keep = (k, v, pos)      # the struct holds raw pointers: keep the tensors alive
+    return view
 
 
 def window_view(q, qpos, scale: float = 0.0) -> WindowView:
@@ -118,8 +122,12 @@ def window_view(q, qpos, scale: float = 0.0) -> WindowView:
     _check_bf16(q, "q", 3)
     if qpos.dtype != torch.int32 or not qpos.is_cuda:
         raise ValueError("qpos must be a cuda int32 tensor")
-    return WindowView(q.data_ptr(), q.stride(0), q.stride(1), qpos.data_ptr(), q.shape[0],
+    if qpos.numel() < q.shape[1]:
+        raise ValueError("qpos shorter than the window")
+    view = WindowView(q.data_ptr(), q.stride(0), q.stride(1), qpos.data_ptr(), q.shape[0],
                       q.shape[1], float(scale))
+    view._keep = (q, qpos)
+    return view
 
 
 @dataclass
@@ -150,8 +158,10 @@ def cache_view(k, v, pos) -> CacheView:
     if pos.dtype != torch.int32 or pos.dim() != 2 or pos.stride(1) != 1:
         raise ValueError("pos must be int32 [n_seq, capacity] with a contiguous last axis")
     s = k.stride()
-    return CacheView(k.data_ptr(), v.data_ptr(), s[0], s[1], s[2], s[3], pos.data_ptr(),
+    view = CacheView(k.data_ptr(), v.data_ptr(), s[0], s[1], s[2], s[3], pos.data_ptr(),
                      pos.stride(0), k.shape[0], k.shape[1], k.shape[2], k.shape[4], k.shape[3])
+    view._keep = (k, v, pos)
+    return view
 
 
 def _f32(n, device, fill=None):

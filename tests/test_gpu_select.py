@@ -1,0 +1,142 @@
+"""GPU parity of ckv_select_and_compact (Sec. 3.3, Eq. (12)-(13); Sec. 3.1, Eq. (4)).
+
+Bit-exact bar: given the same float32 scores, pending effects and page lists,
+the kept index set must equal the oracle's, and the compacted K, V and
+positions must equal fancy indexing of the inputs byte for byte.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from synth import make_scores
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ckv():
+    import paper_2608_07855_amd as P
+    ctx = P.Context(0)
+    yield P, ctx
+    ctx.close()
+
+
+def _pages(rng, S, n, maxlen=64):
+    starts = np.sort(rng.choice(S - maxlen, n, replace=False))
+    out = []
+    prev = 0
+    for s in starts:
+        s = max(int(s), prev)
+        ln = int(rng.integers(1, maxlen + 1))
+        if s + ln > S:
+            break
+        out.append((s, ln))
+        prev = s + ln
+    return out
+
+
+def _oracle_keep(S, score, retired, pending, r_pre, B, eta, max_pages, keep_recent):
+    prot_idx = O.protect_pending([p[0] for p in pending], [p[1] for p in pending], r_pre, B, eta, max_pages)
+    prot = [pending[i] for i in prot_idx]
+    st = O.token_states(S, retired, prot, keep_recent)
+    return O.select_tokens(score, st, B), st
+
+
+def _run(P, ctx, n_seq, n_layers, H, d, cap, n_tokens, B, seed, keep_recent=0, eta=0.125,
+         max_pages=16, ties=False, nan=False):
+    rng = np.random.default_rng(seed)
+    k = torch.randint(-32768, 32767, (n_seq, n_layers, H, cap, d), dtype=torch.int16).view(torch.bfloat16).cuda()
+    v = torch.randint(-32768, 32767, (n_seq, n_layers, H, cap, d), dtype=torch.int16).view(torch.bfloat16).cuda()
+    pos = torch.from_numpy(np.cumsum(rng.integers(1, 3, (n_seq, cap)), axis=1).astype(np.int32)).cuda()
+    stride = cap + 16
+    score = np.stack([make_scores(stride, seed=seed * 10 + s, ties=ties) for s in range(n_seq)])
+    if nan:
+        score[:, ::97] = np.nan
+        score[:, 5::101] = -0.0
+    retired, pending, rpre = [], [], []
+    for s in range(n_seq):
+        S = n_tokens[s]
+        allp = _pages(rng, S, max(4, S // 80))
+        rng.shuffle(allp)
+        ret = sorted(allp[: len(allp) // 3])
+        pen = sorted(allp[len(allp) // 3: len(allp) // 3 + 40])
+        if s == 0 and ret and pen:
+            pen = sorted(set(pen) | {ret[0]})     # a page both retired and pending
+        retired.append(ret)
+        pending.append(pen)
+        r = rng.uniform(0, 1, len(pen)).astype(np.float32)
+        if len(r) > 3:
+            r[1] = r[2]                            # tie in R-
+        rpre.append(r)
+    out = P.ckv_select_and_compact(
+        ctx, k, v, pos, n_tokens, torch.from_numpy(score).cuda(),
+        [P.Pages([p[0] for p in r], [p[1] for p in r]) for r in retired],
+        [P.Pages([p[0] for p in r], [p[1] for p in r]) for r in pending],
+        [torch.from_numpy(r).cuda() if len(r) else None for r in rpre],
+        budget=B, eta=eta, max_pending_pages=max_pages, keep_recent=keep_recent)
+    torch.cuda.synchronize()
+    kept = out["kept"].cpu().numpy()
+    nk = out["n_kept"].cpu().numpy()
+    kn, vn = k.view(torch.int16).cpu().numpy(), v.view(torch.int16).cpu().numpy()
+    ko, vo = out["k"].view(torch.int16).cpu().numpy(), out["v"].view(torch.int16).cpu().numpy()
+    pn, po = pos.cpu().numpy(), out["pos"].cpu().numpy()
+    for s in range(n_seq):
+        S = n_tokens[s]
+        want, _ = _oracle_keep(S, score[s, :S], retired[s], pending[s], rpre[s], B, eta, max_pages,
+                               keep_recent)
+        assert nk[s] == len(want), (s, nk[s], len(want))
+        np.testing.assert_array_equal(kept[s, :nk[s]], want)
+        assert np.all(kept[s, nk[s]:] == -1)
+        np.testing.assert_array_equal(ko[s, :, :, :nk[s]], kn[s][:, :, want])
+        np.testing.assert_array_equal(vo[s, :, :, :nk[s]], vn[s][:, :, want])
+        np.testing.assert_array_equal(po[s, :nk[s]], pn[s, want])
+    return out
+
+
+def test_single_layer_d128(ckv):
+    P, ctx = ckv
+    _run(P, ctx, 1, 1, 8, 128, 5000, [5000], 1500, seed=1)
+
+
+def test_batched_stack_d64_ties_nan(ckv):
+    P, ctx = ckv
+    _run(P, ctx, 3, 4, 2, 64, 3000, [3000, 2100, 777], 640, seed=2, ties=True, nan=True, keep_recent=32)
+
+
+def test_budget_exceeds_cache(ckv):
+    """Budget larger than the non-retired cache: every non-retired token is kept."""
+    P, ctx = ckv
+    _run(P, ctx, 1, 2, 2, 128, 900, [900], 1024, seed=3, eta=0.5)
+
+
+def test_protection_fills_pending_budget(ckv):
+    P, ctx = ckv
+    _run(P, ctx, 2, 1, 1, 64, 4000, [4000, 3999], 256, seed=4, eta=1.0, max_pages=100)
+
+
+def test_long_cache_q32b_shape(ckv):
+    """131072 tokens, budget 32768 (the long-context layer shape)."""
+    P, ctx = ckv
+    _run(P, ctx, 1, 1, 8, 128, 131072, [131072], 32768, seed=5)
+
+
+def test_host_errors(ckv):
+    P, ctx = ckv
+    k = torch.zeros((1, 1, 1, 64, 64), dtype=torch.bfloat16, device="cuda")
+    pos = torch.zeros((1, 64), dtype=torch.int32, device="cuda")
+    sc = torch.zeros((1, 64), device="cuda")
+    E = P.Pages([], [])
+    with pytest.raises(P.CKVError) as e:
+        P.ckv_select_and_compact(ctx, k, k.clone(), pos, [64], sc, [E], [E], [None], budget=16,
+                                 eta=0.5, keep_recent=9)
+    assert e.value.code == -3
+    with pytest.raises(P.CKVError) as e:        # output aliases the input
+        P.ckv_select_and_compact(ctx, k, k.clone(), pos, [64], sc, [E], [E], [None], budget=16,
+                                 k_out=k[:, :, :, :16], v_out=k[:, :, :, 16:32],
+                                 pos_out=pos[:, :16].clone())
+    assert e.value.code == -1
+    with pytest.raises(P.CKVError) as e:        # page outside the cache
+        P.ckv_select_and_compact(ctx, k, k.clone(), pos, [64], sc, [P.Pages([60], [8])], [E], [None],
+                                 budget=16)
+    assert e.value.code == -2
