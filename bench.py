@@ -1,0 +1,305 @@
+#!/usr/bin/env python3
+"""Benchmark of the CommitKV hot path on one MI355X.
+
+One step is one pass of the whole path over one commit of the synthetic
+Qwen3-8B-shaped layer (32 query heads, 8 KV heads, head width 128, 32768
+cached tokens, 32-token pages, 64-row windows, budget 8192):
+
+  1. page deletion effects in the pre-commit window (cache prefix),
+  2. page deletion effects in the post-commit window (full cache), with the
+     window outputs and the token window-mass used as the base score,
+  3. lifecycle classification and the ordered candidate list,
+  4. the greedy joint test on the candidates,
+  5. pending protection, budgeted selection and compaction of K, V and
+     positions with one index set.
+
+Inputs are resident in HBM before timing starts.  The key/value cache is
+held in four copies and consecutive measurement calls read different copies,
+so no call finds its keys and values still in the 256 MB Infinity Cache (a
+real agent decodes many tokens over the whole cache between the two windows).
+
+Prints one JSON line.  ``value`` = cached tokens scored per second per layer,
+(S_pre + S_post) / step time.  Extra fields give the measurement-only rate,
+the compaction bandwidth and per-kernel times (HIP events recorded by the
+library on its stream).  ``roofline`` is for the kernel with the largest
+total time; ``cpu_baseline`` times the fp64 oracle on a bounded sample on the
+host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "cached tokens scored/sec per layer (pre+post commit) at 32K ctx; compaction GB/s"
+PEAK_HBM = 8.0e12          # bytes/s
+PEAK_MFMA = 2.5e15         # dense bf16/fp16 FLOP/s
+RIDGE = PEAK_MFMA / PEAK_HBM
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="q8b")
+    ap.add_argument("--copies", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+class Setup:
+    def __init__(self, w, copies):
+        import torch
+
+        import paper_2608_07855_amd as P
+        from synth import make_layer
+
+        self.P, self.w = P, w
+        t0 = time.time()
+        L = make_layer(w, seed=0)
+        self.L = L
+        log(f"[bench] generated {w.name}: S={w.n_tokens} S_pre={L.layout.s_pre} pages={len(L.pages)} "
+            f"({time.time() - t0:.1f}s)")
+
+        def dev16(a):
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+        k0, v0 = dev16(L.k), dev16(L.v)
+        self.k = [k0] + [k0.clone() for _ in range(copies - 1)]
+        self.v = [v0] + [v0.clone() for _ in range(copies - 1)]
+        self.pos = torch.from_numpy(L.pos).cuda()
+        self.pos2 = self.pos[None]
+        qpre, qpost = dev16(L.q_pre), dev16(L.q_post)
+        qp_pre, qp_post = torch.from_numpy(L.qpos_pre).cuda(), torch.from_numpy(L.qpos_post).cuda()
+        self.kv_pre = [P.kv_view(k, v, self.pos, L.layout.s_pre) for k, v in zip(self.k, self.v)]
+        self.kv_post = [P.kv_view(k, v, self.pos) for k, v in zip(self.k, self.v)]
+        self.win_pre = P.window_view(qpre, qp_pre)
+        self.win_post = P.window_view(qpost, qp_post)
+        self.pages = P.Pages(L.layout.page_start, L.layout.page_len)
+        n = len(L.pages)
+        self.n_pages = n
+        pend = L.layout.pending_idx
+        assert np.array_equal(pend, np.arange(pend[0], pend[-1] + 1))
+        self.pend_slice = slice(int(pend[0]), int(pend[-1]) + 1)
+        self.pending = P.Pages(L.layout.page_start[pend], L.layout.page_len[pend])
+        self.force = torch.from_numpy(L.forced.astype(np.uint8)).cuda() if L.forced.any() else None
+        self.max_cand = w.max_cand if w.max_cand > 0 else 256
+        Hq, W, d, S = w.n_q_heads, w.window, w.head_dim, w.n_tokens
+        f32 = dict(dtype=torch.float32, device="cuda")
+        self.R_pre = torch.empty(n, **f32)
+        self.R_post = torch.empty(n, **f32)
+        self.o = torch.empty(Hq * W * d, **f32)
+        self.lse = torch.empty(Hq * W, **f32)
+        self.mass = torch.empty(S, **f32)
+        B = w.budget
+        self.k_out = torch.empty((1, 1, w.n_kv_heads, B, d), dtype=torch.bfloat16, device="cuda")
+        self.v_out = torch.empty_like(self.k_out)
+        self.pos_out = torch.empty((1, B), dtype=torch.int32, device="cuda")
+        self.k5 = [k[None, None] for k in self.k]
+        self.v5 = [v[None, None] for v in self.v]
+        self.acc_host = torch.empty(self.max_cand, dtype=torch.uint8, pin_memory=True)
+        self.cand_host = torch.empty(max(n, 1), dtype=torch.int32, pin_memory=True)
+        self.ctx = P.Context(0)
+        self.last = {}
+
+    def step(self, i):
+        import torch
+        P, w = self.P, self.w
+        c_pre, c_post = (2 * i) % len(self.k), (2 * i + 1) % len(self.k)
+        P.ckv_measure_page_effects(self.ctx, self.kv_pre[c_pre], self.win_pre, self.pages, R=self.R_pre)
+        P.ckv_measure_page_effects(self.ctx, self.kv_post[c_post], self.win_post, self.pages,
+                                   R=self.R_post, o=self.o, lse=self.lse, token_mass=self.mass)
+        cl = P.ckv_classify_pages(self.ctx, self.R_pre, self.R_post, force=self.force,
+                                  max_cand=self.max_cand)
+        jt = P.ckv_joint_test(self.ctx, self.kv_post[c_post], self.win_post, self.o, self.lse,
+                              self.pages, cl["cand"], cl["n_cand"], self.max_cand, 0.01)
+        # the accepted pages join the retirement set on the host (Algorithm 1)
+        self.acc_host.copy_(jt["accepted"], non_blocking=True)
+        self.cand_host[:self.n_pages].copy_(cl["cand"], non_blocking=True)
+        torch.cuda.current_stream().synchronize()
+        acc = self.acc_host.numpy()
+        cand = self.cand_host.numpy()[:self.max_cand]
+        sel = np.sort(cand[(acc[:len(cand)] == 1) & (cand >= 0)])
+        retired = P.Pages(self.L.layout.page_start[sel], self.L.layout.page_len[sel])
+        out = P.ckv_select_and_compact(
+            self.ctx, self.k5[c_post], self.v5[c_post], self.pos2, [w.n_tokens], self.mass[None],
+            [retired], [self.pending], [self.R_pre[self.pend_slice]], budget=w.budget, eta=w.eta,
+            max_pending_pages=w.max_pending_pages, keep_recent=w.window,
+            k_out=self.k_out, v_out=self.v_out, pos_out=self.pos_out)
+        self.last = dict(cl=cl, jt=jt, sel=out, n_retired=len(sel))
+
+
+def kernel_work(w, L, name, launches_per_step):
+    """Algorithmic bytes and FLOPs per launch of a library kernel."""
+    Hq, Hkv, W, d, S, Sp = w.n_q_heads, w.n_kv_heads, w.window, w.head_dim, w.n_tokens, L.layout.s_pre
+    rows = Hq * W
+    n_elig = int(L.layout.page_len.sum())
+    if name == "window_attention":      # one launch per pass: pre over S_pre, post over S
+        toks = (Sp + S) / 2
+        byt = toks * (Hkv * d * 2 * 2 + 4) + rows * d * 2 + rows * (d + 1) * 4
+        flop = 4.0 * rows * toks * d
+    elif name == "page_effect":         # eligible tokens, twice per step
+        byt = n_elig * (Hkv * d * 2 * 2 + 4) + rows * d * (2 + 4) + len(L.pages) * 4
+        flop = 4.0 * rows * n_elig * d
+    elif name == "token_mass":
+        byt = S * (Hkv * d * 2 + 4 + 4) + rows * d * 2
+        flop = 2.0 * rows * S * d
+    elif name == "gather":
+        B = w.budget
+        byt = B * Hkv * d * 2 * 2 * 2 + B * 4 * 3
+        flop = 0.0
+    else:
+        return None
+    return byt, flop
+
+
+def source_sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def traffic_for(kernel, workload):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, if they
+    still match the kernel source; else None."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        rec = json.load(open(p))
+        src = os.path.join(ROOT, rec["source"])
+        if source_sha(src) != rec["source_sha256"]:
+            return None
+        return float(rec["bytes_per_launch"])
+    except Exception:
+        return None
+
+
+def cpu_baseline(w, L, budget_s):
+    """Closed-form fp64 oracle (pre + post pass) on a sample of query heads,
+    scaled to all heads; returns tokens per second."""
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:
+        threadpool_limits = None
+    cores = len(os.sched_getaffinity(0))
+    ctx = threadpool_limits(cores) if threadpool_limits else None
+    Sp, S, Hq = L.layout.s_pre, w.n_tokens, w.n_q_heads
+    heads, spent = [], 0.0
+    t_all = time.time()
+    for h in range(Hq):
+        t0 = time.time()
+        O.page_effects(L.k[:, :Sp], L.v[:, :Sp], L.pos[:Sp], L.q_pre, L.qpos_pre, L.pages,
+                       method="closed", heads=[h])
+        O.page_effects(L.k, L.v, L.pos, L.q_post, L.qpos_post, L.pages, method="closed", heads=[h])
+        spent += time.time() - t0
+        heads.append(h)
+        if spent > budget_s:
+            break
+    if ctx is not None:
+        ctx.unregister() if hasattr(ctx, "unregister") else None
+    per_step = spent * Hq / len(heads)
+    log(f"[bench] cpu oracle: {len(heads)} of {Hq} query heads in {spent:.1f}s "
+        f"(wall {time.time() - t_all:.1f}s) -> {per_step:.1f}s per full pre+post pass")
+    return dict(value=(Sp + S) / per_step, unit="tokens/s", cores=cores, kind="oracle",
+                sample=f"closed-form fp64 oracle, pre+post deletion effects of all {len(L.pages)} pages "
+                       f"for query heads 0..{len(heads) - 1} of {Hq}, time scaled by {Hq}/{len(heads)}")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}), flush=True)
+        log("[bench] this build measures one GPU; multi-GPU runs are not part of it")
+        sys.exit(2)
+    import torch
+    from synth import WORKLOADS
+
+    w = WORKLOADS[args.workload]
+    st = Setup(w, args.copies)
+    ctx = st.ctx
+    for i in range(args.warmup):
+        st.step(i)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({args.warmup} steps)")
+    ctx.reset_kernel_stats()
+    ctx.set_kernel_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        st.step(args.warmup + i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ctx.set_kernel_timing(False)
+    stats = ctx.kernel_stats()
+    ms = (t1 - t0) * 1e3 / args.steps
+    L = st.L
+    tokens = L.layout.s_pre + w.n_tokens
+    value = tokens / (ms / 1e3)
+    log(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step")
+    per_kernel = {k: dict(ms_per_step=v[0] / args.steps, launches_per_step=v[1] / args.steps)
+                  for k, v in stats.items()}
+    meas = sum(per_kernel.get(k, {}).get("ms_per_step", 0.0)
+               for k in ("window_attention", "combine", "page_effect", "token_mass"))
+    sel_ms = sum(per_kernel.get(k, {}).get("ms_per_step", 0.0) for k in ("protect", "select", "gather"))
+    g_ms = per_kernel.get("gather", {}).get("ms_per_step", 0.0)
+    n_kept = int(st.last["sel"]["n_kept"][0].item())
+    comp_bytes = 2 * n_kept * w.n_layers * w.n_kv_heads * w.head_dim * 2 * 2 + n_kept * 4 * 2
+    # roofline of the kernel with the largest total time
+    dom = max(per_kernel, key=lambda k: per_kernel[k]["ms_per_step"])
+    work = kernel_work(w, L, dom, per_kernel[dom]["launches_per_step"])
+    roof = None
+    if work:
+        byt, flop = work
+        avg_s = per_kernel[dom]["ms_per_step"] / per_kernel[dom]["launches_per_step"] / 1e3
+        if flop / max(byt, 1) < RIDGE:
+            roof = dict(bound="hbm", achieved=byt / avg_s / 1e9, peak=PEAK_HBM / 1e9, unit="GB/s")
+        else:
+            roof = dict(bound="mfma", achieved=flop / avg_s / 1e12, peak=PEAK_MFMA / 1e12, unit="TFLOP/s")
+        roof["frac"] = roof["achieved"] / roof["peak"]
+        tb = traffic_for(dom, w.name)
+        roof["traffic"] = tb
+        roof["kernel"] = dom
+        roof["algorithmic_bytes_per_launch"] = byt
+        roof["algorithmic_flop_per_launch"] = flop
+        roof["avg_launch_us"] = avg_s * 1e6
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, L, args.cpu_seconds)
+    res = dict(
+        metric=METRIC, value=value, unit="tokens/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
+        ms_per_step=ms, higher_is_better=True, scaling="weak", vs_baseline=None, dtype="bf16",
+        data="synthetic",
+        config=dict(workload="qwen3-8b-shaped layer, 32768 cached tokens (Hq 32, Hkv 8, d 128, "
+                             "32-token pages, 64-row windows, budget 8192)" if w.name == "q8b" else w.name,
+                    name=w.name, n_tokens=w.n_tokens, s_pre=int(L.layout.s_pre), pages=len(L.pages),
+                    parallelism="single GPU"),
+        measure_only_tokens_per_s=tokens / (meas / 1e3) if meas > 0 else None,
+        compaction_GBps=comp_bytes / (sel_ms / 1e3) / 1e9 if sel_ms > 0 else None,
+        gather_GBps=comp_bytes / (g_ms / 1e3) / 1e9 if g_ms > 0 else None,
+        kernels=per_kernel,
+        n_candidates=int(st.last["cl"]["n_cand"].item()),
+        n_accepted=int(st.last["jt"]["n_accepted"].item()),
+        n_kept=n_kept,
+        roofline=roof,
+        cpu_baseline=cpu,
+    )
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

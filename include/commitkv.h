@@ -114,6 +114,18 @@ int ckv_set_workspace_limit(ckv_ctx* ctx, size_t bytes);
 /* Bytes of device workspace currently held by the context. */
 size_t ckv_workspace_bytes(const ckv_ctx* ctx);
 
+/* Kernel timing.  While enabled, every kernel the library launches is
+ * bracketed by a pair of HIP events recorded on the context's stream, and
+ * the elapsed times are summed per kernel name.  ckv_kernel_stats waits for
+ * the recorded events, then reports kernel number idx (0-based, in order of
+ * first launch): its name (owned by the context), total milliseconds and
+ * launch count; idx past the last kernel returns CKV_ERR_ARG.
+ * ckv_reset_kernel_stats zeroes the totals. */
+int ckv_set_kernel_timing(ckv_ctx* ctx, int enable);
+int ckv_kernel_stats(ckv_ctx* ctx, int32_t idx, const char** name,
+                     double* total_ms, int64_t* launches);
+int ckv_reset_kernel_stats(ckv_ctx* ctx);
+
 /* ------------------------------------------------------------------ views */
 
 /* Resident KV cache of ONE layer of ONE sequence (Sec. 3.1, Eq. (3)):
@@ -252,6 +264,10 @@ int ckv_classify_pages(ckv_ctx* ctx, int32_t n, const float* R_pre,
  * float32[max_cand] (optional): R^+(A u {E}) evaluated at step t;
  * n_accepted int32[1].  Entries at t >= *n_cand are 0 / NaN.
  * max_cand must be >= 1.
+ * Unlike the other calls this one waits for the stream: it reads *n_cand
+ * back to size the work, and reads a progress flag between batches of
+ * rounds (the greedy test is sequential; each round decides at least one
+ * candidate).
  */
 int ckv_joint_test(ckv_ctx* ctx, const ckv_kv_view* kv,
                    const ckv_window_view* win, const float* o,

@@ -80,6 +80,12 @@ SIGNATURES = {
     "ckv_version": (ctypes.c_uint32, []),
     "ckv_set_workspace_limit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t]),
     "ckv_workspace_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
+    "ckv_set_kernel_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
+    "ckv_kernel_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32,
+                                        ctypes.POINTER(ctypes.c_char_p),
+                                        ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_int64)]),
+    "ckv_reset_kernel_stats": (ctypes.c_int, [ctypes.c_void_p]),
     "ckv_measure_page_effects": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.POINTER(KVView), ctypes.POINTER(WindowView),
         ctypes.POINTER(PageList), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,

@@ -68,6 +68,22 @@ class Context:
     def workspace_bytes(self) -> int:
         return int(self._lib.ckv_workspace_bytes(self.handle))
 
+    def set_kernel_timing(self, enable: bool):
+        self.check(self._lib.ckv_set_kernel_timing(self.handle, int(bool(enable))))
+
+    def kernel_stats(self) -> dict:
+        """{kernel name: (total ms, launches)} of the launches timed so far."""
+        out, i = {}, 0
+        name, ms, n = ctypes.c_char_p(), ctypes.c_double(), ctypes.c_int64()
+        while self._lib.ckv_kernel_stats(self.handle, i, ctypes.byref(name), ctypes.byref(ms),
+                                         ctypes.byref(n)) == 0:
+            out[name.value.decode()] = (ms.value, n.value)
+            i += 1
+        return out
+
+    def reset_kernel_stats(self):
+        self.check(self._lib.ckv_reset_kernel_stats(self.handle))
+
     def last_error(self) -> str:
         return self._lib.ckv_last_error(self.handle).decode()
 

@@ -27,6 +27,7 @@ constexpr int kPinnedSlots = 4;
 constexpr int kPageCacheEntries = 8;
 constexpr int kJointWindow = 32;       // candidates tested per joint round
 constexpr int kJointRowsPerBlock = 64;
+constexpr int kJointChunk = 4;         // joint rounds launched between progress checks
 constexpr int kTargetBlocks = 512;     // about two blocks per compute unit
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -70,6 +71,17 @@ struct ckv_ctx {
   int next_slot = 0;
   std::vector<PageEntry> pages;
   uint64_t tick = 0;
+  // small pinned buffer for device-to-host reads of counters and flags
+  int32_t* pinned_small = nullptr;
+  hipEvent_t small_ev[2] = {nullptr, nullptr};
+  // kernel timing (events around every launch when enabled)
+  bool timing = false;
+  struct Timed { int kid; hipEvent_t a, b; };
+  std::vector<Timed> timed;
+  std::vector<hipEvent_t> event_pool;
+  std::vector<std::string> knames;
+  std::vector<double> ktotal;
+  std::vector<int64_t> kcount;
 };
 
 namespace {
@@ -138,6 +150,79 @@ int realize(ckv_ctx* c, Plan& plan) {
     *it.dst = c->ws + off;
     off += round_up(std::max<size_t>(it.bytes, 1), kAlign);
   }
+  return CKV_OK;
+}
+
+int kernel_id(ckv_ctx* c, const char* name) {
+  for (size_t i = 0; i < c->knames.size(); ++i)
+    if (c->knames[i] == name) return (int)i;
+  c->knames.push_back(name);
+  c->ktotal.push_back(0.0);
+  c->kcount.push_back(0);
+  return (int)c->knames.size() - 1;
+}
+
+hipError_t pooled_event(ckv_ctx* c, hipEvent_t* ev) {
+  if (!c->event_pool.empty()) {
+    *ev = c->event_pool.back();
+    c->event_pool.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(ev);
+}
+
+// resolve recorded kernel timings (waits for the last recorded event)
+int resolve_timings(ckv_ctx* c) {
+  if (c->timed.empty()) return CKV_OK;
+  CKV_HIP(c, hipEventSynchronize(c->timed.back().b));
+  for (auto& t : c->timed) {
+    float ms = 0.f;
+    CKV_HIP(c, hipEventElapsedTime(&ms, t.a, t.b));
+    c->ktotal[t.kid] += ms;
+    c->kcount[t.kid] += 1;
+    c->event_pool.push_back(t.a);
+    c->event_pool.push_back(t.b);
+  }
+  c->timed.clear();
+  return CKV_OK;
+}
+
+// launch a kernel (launcher expression), bracketed by events when timing is on
+#define CKV_LAUNCH(ctx, name, expr)                                   \
+  do {                                                                \
+    hipEvent_t ea_ = nullptr, eb_ = nullptr;                          \
+    if ((ctx)->timing) {                                              \
+      CKV_HIP(ctx, pooled_event(ctx, &ea_));                          \
+      CKV_HIP(ctx, pooled_event(ctx, &eb_));                          \
+      CKV_HIP(ctx, hipEventRecord(ea_, (ctx)->stream));               \
+    }                                                                 \
+    CKV_HIP(ctx, (expr));                                             \
+    if ((ctx)->timing) {                                              \
+      CKV_HIP(ctx, hipEventRecord(eb_, (ctx)->stream));               \
+      (ctx)->timed.push_back({kernel_id(ctx, name), ea_, eb_});       \
+    }                                                                 \
+  } while (0)
+
+// read one int32 from device memory (waits for the stream up to this point)
+int read_device_int(ckv_ctx* c, const int32_t* src, int slot, int32_t* out, bool wait) {
+  if (!c->pinned_small) {
+    void* p = nullptr;
+    CKV_HIP(c, hipHostMalloc(&p, 64, hipHostMallocDefault));
+    c->pinned_small = static_cast<int32_t*>(p);
+  }
+  if (!c->small_ev[slot]) CKV_HIP(c, hipEventCreateWithFlags(&c->small_ev[slot], hipEventDisableTiming));
+  CKV_HIP(c, hipMemcpyAsync(c->pinned_small + slot, src, sizeof(int32_t), hipMemcpyDeviceToHost, c->stream));
+  CKV_HIP(c, hipEventRecord(c->small_ev[slot], c->stream));
+  if (wait) {
+    CKV_HIP(c, hipEventSynchronize(c->small_ev[slot]));
+    *out = c->pinned_small[slot];
+  }
+  return CKV_OK;
+}
+
+int wait_device_int(ckv_ctx* c, int slot, int32_t* out) {
+  CKV_HIP(c, hipEventSynchronize(c->small_ev[slot]));
+  *out = c->pinned_small[slot];
   return CKV_OK;
 }
 
@@ -322,6 +407,14 @@ extern "C" int ckv_destroy(ckv_ctx* c) {
       if (s.ev) (void)hipEventDestroy(s.ev);
       if (s.host) (void)hipHostFree(s.host);
     }
+    for (auto& t : c->timed) {
+      (void)hipEventDestroy(t.a);
+      (void)hipEventDestroy(t.b);
+    }
+    for (auto e : c->event_pool) (void)hipEventDestroy(e);
+    for (auto e : c->small_ev)
+      if (e) (void)hipEventDestroy(e);
+    if (c->pinned_small) (void)hipHostFree(c->pinned_small);
   }
   delete c;
   return CKV_OK;
@@ -355,6 +448,38 @@ extern "C" int ckv_set_workspace_limit(ckv_ctx* c, size_t bytes) {
 }
 
 extern "C" size_t ckv_workspace_bytes(const ckv_ctx* c) { return c ? c->ws_cap : 0; }
+
+extern "C" int ckv_set_kernel_timing(ckv_ctx* c, int enable) {
+  if (!c) return CKV_ERR_ARG;
+  DeviceGuard g(c->device);
+  int rc = resolve_timings(c);
+  if (rc) return rc;
+  c->timing = enable != 0;
+  return CKV_OK;
+}
+
+extern "C" int ckv_kernel_stats(ckv_ctx* c, int32_t idx, const char** name, double* total_ms,
+                                int64_t* launches) {
+  if (!c) return CKV_ERR_ARG;
+  DeviceGuard g(c->device);
+  int rc = resolve_timings(c);
+  if (rc) return rc;
+  if (idx < 0 || idx >= (int32_t)c->knames.size()) return CKV_ERR_ARG;
+  if (name) *name = c->knames[idx].c_str();
+  if (total_ms) *total_ms = c->ktotal[idx];
+  if (launches) *launches = c->kcount[idx];
+  return CKV_OK;
+}
+
+extern "C" int ckv_reset_kernel_stats(ckv_ctx* c) {
+  if (!c) return CKV_ERR_ARG;
+  DeviceGuard g(c->device);
+  int rc = resolve_timings(c);
+  if (rc) return rc;
+  std::fill(c->ktotal.begin(), c->ktotal.end(), 0.0);
+  std::fill(c->kcount.begin(), c->kcount.end(), 0);
+  return CKV_OK;
+}
 
 // ------------------------------------------------------------- the calls
 
@@ -394,10 +519,10 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
   if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
   if ((rc = realize(c, plan))) return rc;
 
-  CKV_HIP(c, launch_window_attention(a, sp, c->stream));
+  CKV_LAUNCH(c, "window_attention", launch_window_attention(a, sp, c->stream));
   ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
               token_mass ? (size_t)a.S : 0};
-  CKV_HIP(c, launch_combine(a, sp, rs, lse, zl, c->stream));
+  CKV_LAUNCH(c, "combine", launch_combine(a, sp, rs, lse, zl, c->stream));
   if (n > 0) {
     PageWork pw{};
     pw.start = dstart;
@@ -409,11 +534,11 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
     pw.R_head = R_head;
     pw.Hq = a.Hq;
     pw.total_rows = total_rows;
-    CKV_HIP(c, launch_page_kernel(a, pw, rs, 0, c->stream));
+    CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, rs, 0, c->stream));
   }
   if (token_mass) {
     const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kTargetBlocks / a.Hkv)), 64);
-    CKV_HIP(c, launch_token_mass(a, rs, token_mass, mchunk, c->stream));
+    CKV_LAUNCH(c, "token_mass", launch_token_mass(a, rs, token_mass, mchunk, c->stream));
   }
   return CKV_OK;
 }
@@ -452,7 +577,7 @@ extern "C" int ckv_classify_pages(ckv_ctx* c, int32_t n, const float* R_pre, con
   if (!P_post) plan.add(&a.P_post, std::max(n, 1));
   int rc = realize(c, plan);
   if (rc) return rc;
-  CKV_HIP(c, launch_classify(a, c->stream));
+  CKV_LAUNCH(c, "classify", launch_classify(a, c->stream));
   return CKV_OK;
 }
 
@@ -511,14 +636,20 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   j.onorm = rs.onorm;
   j.nvis = rs.nvis;
 
-  CKV_HIP(c, launch_joint_prepare(a, o, lse, rs, j, c->stream));
+  CKV_LAUNCH(c, "joint_prepare", launch_joint_prepare(a, o, lse, rs, j, c->stream));
+  // the number of candidates bounds the rounds: read it once
+  int32_t n_eff = 0;
   if (pages->n_pages > 0) {
+    if ((rc = read_device_int(c, n_cand, 0, &n_eff, true))) return rc;
+    n_eff = std::max(0, std::min(n_eff, max_cand));
+  }
+  if (n_eff > 0) {
     PageWork pw{};
     pw.start = dstart;
     pw.len = dlen;
-    pw.n_items = max_cand;
+    pw.n_items = n_eff;
     pw.n_pages = pages->n_pages;
-    pw.items_per_block = items_per_block(max_cand, a.Hkv * ceil_div(a.rows, rows_per_block_page()));
+    pw.items_per_block = items_per_block(n_eff, a.Hkv * ceil_div(a.rows, rows_per_block_page()));
     pw.cand = cand;
     pw.n_cand = n_cand;
     pw.Hq = a.Hq;
@@ -526,8 +657,23 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
     pw.resA = resA;
     pw.resC = resC;
     pw.total_rows = total_rows;
-    CKV_HIP(c, launch_page_kernel(a, pw, rs, 1, c->stream));
-    for (int r = 0; r < max_cand; ++r) CKV_HIP(c, launch_joint_round(j, c->stream));
+    CKV_LAUNCH(c, "joint_residual", launch_page_kernel(a, pw, rs, 1, c->stream));
+    // Each round decides at least one candidate, so n_eff rounds always
+    // suffice.  Rounds go out in chunks; the done flag of chunk k-2 is read
+    // before chunk k is launched, so at most two chunks run past the end.
+    int launched = 0;
+    for (int k = 0; launched < n_eff; ++k) {
+      if (k >= 2) {
+        int32_t done = 0;
+        if ((rc = wait_device_int(c, k & 1, &done))) return rc;
+        if (done) break;
+      }
+      const int m = std::min(kJointChunk, n_eff - launched);
+      for (int r = 0; r < m; ++r) CKV_LAUNCH(c, "joint_round", launch_joint_round(j, c->stream));
+      launched += m;
+      int32_t unused;
+      if ((rc = read_device_int(c, j.ctrl + 2, k & 1, &unused, false))) return rc;
+    }
   }
   return CKV_OK;
 }
@@ -651,8 +797,8 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   sa.state = token_state ? token_state : state_ws;
   sa.kept = kept_idx;
   sa.n_kept = n_kept;
-  CKV_HIP(c, launch_protect(sa, c->stream));
-  CKV_HIP(c, launch_select(sa, c->stream));
+  CKV_LAUNCH(c, "protect", launch_protect(sa, c->stream));
+  CKV_LAUNCH(c, "select", launch_select(sa, c->stream));
 
   GatherArgs ga{};
   ga.k_in = in->k;
@@ -678,6 +824,6 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   ga.kept = kept_idx;
   ga.n_kept = n_kept;
   ga.budget = B;
-  CKV_HIP(c, launch_gather(ga, c->stream));
+  CKV_LAUNCH(c, "gather", launch_gather(ga, c->stream));
   return CKV_OK;
 }
