@@ -28,7 +28,7 @@ constexpr int kPageCacheEntries = 8;
 constexpr int kJointWindow = 32;       // candidates tested per joint round
 constexpr int kJointRowsPerBlock = 64;
 constexpr int kJointChunk = 4;         // joint rounds launched between progress checks
-constexpr int kTargetBlocks = 512;     // about two blocks per compute unit
+constexpr int kTargetBlocks = 256;     // one 8-wave workgroup per compute unit
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
@@ -492,6 +492,9 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
   if ((rc = check_kv(c, kv)) || (rc = check_win(c, win, kv)) || (rc = check_pages(c, pages, kv->n_tokens, "measured")))
     return rc;
   if (pages->n_pages > 0 && !R) return fail(c, CKV_ERR_ARG, "R is NULL");
+  if (token_mass && (win->n_q_heads / kv->n_kv_heads) * win->n_rows > token_mass_max_rows())
+    return fail(c, CKV_ERR_UNSUPPORTED, "token_mass supports at most %d window rows per KV head",
+                token_mass_max_rows());
   DeviceGuard g(c->device);
   if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
 
@@ -515,13 +518,19 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
   plan.add(&rs.lse2, total_rows);
   plan.add(&rs.onorm, total_rows);
   plan.add(&rs.nvis, total_rows);
+  int *fix_list = nullptr, *fix_count = nullptr, *fix_done = nullptr;
+  float* fix_part = nullptr;
+  plan.add(&fix_list, 2 * (size_t)total_rows);
+  plan.add(&fix_count, 1);
+  plan.add(&fix_part, (size_t)total_rows * fixup_parts() * (D + 1));
+  plan.add(&fix_done, total_rows);
   const int32_t *dstart = nullptr, *dlen = nullptr;
   if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
   if ((rc = realize(c, plan))) return rc;
 
   CKV_LAUNCH(c, "window_attention", launch_window_attention(a, sp, c->stream));
   ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
-              token_mass ? (size_t)a.S : 0};
+              token_mass ? (size_t)a.S : 0, fix_count, fix_done, (size_t)total_rows};
   CKV_LAUNCH(c, "combine", launch_combine(a, sp, rs, lse, zl, c->stream));
   if (n > 0) {
     PageWork pw{};
@@ -534,7 +543,13 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
     pw.R_head = R_head;
     pw.Hq = a.Hq;
     pw.total_rows = total_rows;
+    pw.fix_list = fix_list;
+    pw.fix_count = fix_count;
+    pw.fix_cap = total_rows;
+    pw.fix_part = fix_part;
+    pw.fix_done = fix_done;
     CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, rs, 0, c->stream));
+    CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, sp, rs, pw, c->stream));
   }
   if (token_mass) {
     const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kTargetBlocks / a.Hkv)), 64);

@@ -61,14 +61,27 @@ __device__ __forceinline__ f16x4 bf16x4_to_f16(uint32_t lo, uint32_t hi) {
 }
 
 // bf16 element j (0..7) of a 16-byte chunk
-__device__ __forceinline__ uint32_t chunk_elem(const uint4& c, int j) {
-  uint32_t w = (j < 2) ? c.x : (j < 4) ? c.y : (j < 6) ? c.z : c.w;
+template <class V4>
+__device__ __forceinline__ uint32_t chunk_elem(const V4& c, int j) {
+  const uint32_t w = c[j >> 1];
   return (j & 1) ? (w >> 16) : (w & 0xFFFFu);
 }
 
 // slot of token t (0..63) in the V^T tile: swap bits 2 and 3
 __device__ __forceinline__ int vt_slot(int t) {
   return (t & ~0xC) | ((t & 4) << 1) | ((t & 8) >> 1);
+}
+
+// loads through the global address space (pointers inside by-value argument
+// structs otherwise compile to flat accesses)
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x4 ldg_u4(const void* p) {
+  typedef const __attribute__((address_space(1))) u32x4* gptr;
+  return *(gptr)(p);
+}
+__device__ __forceinline__ int ldg_i32(const void* p) {
+  typedef const __attribute__((address_space(1))) int* gptr;
+  return *(gptr)(p);
 }
 
 __device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, 64); }

@@ -52,6 +52,11 @@ struct PageWork {
   float* R;               // MODE 0: [n_pages], zeroed before
   float* R_head;          // MODE 0: [n_pages][Hq] or null, zeroed before
   int Hq;
+  int* fix_list;          // MODE 0: (page, global row) pairs left to the fix-up kernel
+  int* fix_count;         // MODE 0: entries in fix_list (zeroed before)
+  int fix_cap;            // MODE 0: capacity of fix_list (window rows)
+  float* fix_part;        // fix-up partial sums [fix_cap][parts][D + 1]
+  int* fix_done;          // fix-up part counters [fix_cap], zero between calls
   float* resid;           // MODE 1: [max_cand][total_rows][D]
   float* resA;            // MODE 1: [max_cand][total_rows]
   int* resC;              // MODE 1: [max_cand][total_rows]
@@ -62,10 +67,14 @@ struct ZeroList {
   float* p0; size_t n0;
   float* p1; size_t n1;
   float* p2; size_t n2;
+  int* i0;               // one int set to zero (or null)
+  int* i1; size_t n1i;   // ints set to zero
 };
 
 int rows_per_block_attention();
 int rows_per_block_page();
+int token_mass_max_rows();
+int fixup_parts();
 
 hipError_t launch_window_attention(const AttnGeom& a, const AttnSplit& sp, hipStream_t s);
 hipError_t launch_combine(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs, float* lse_out,
@@ -74,6 +83,8 @@ hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowSt
                               hipStream_t s);
 hipError_t launch_token_mass(const AttnGeom& a, const RowStats& rs, float* mass, int chunk,
                              hipStream_t s);
+hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
+                             const PageWork& pw, hipStream_t s);
 
 // classification (Eq. (8)-(10)) and candidate order
 struct ClassifyArgs {

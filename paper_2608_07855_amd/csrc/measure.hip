@@ -6,7 +6,8 @@
 //      (query head h, row p) the full attention output o_p, its log-sum-exp
 //      and the number of visible tokens.  Split over the token axis, partial
 //      (max, sum, unnormalised output) merged by the combine kernel.
-//   B. page_kernel: for every page E and row p, with a page-local max m_E:
+//   B. page_kernel: for every page E and row p, with the page-local max
+//      m_E = max_{i in E} x_i:
 //        l^ = sum_{i in E} 2^(x_i - m_E),  U^ = sum_{i in E} 2^(x_i - m_E) v_i,
 //        f  = 2^(m_E - lse_p),  A = f l^,
 //        ||o_p - o_p^{\E}|| / ||o_p|| = f ||U^ - l^ o_p|| / ((1 - A) ||o_p||)
@@ -16,85 +17,130 @@
 //      A and the visible count for the joint test.
 //   C. token_mass_kernel: max_h sum_p a_hpi for every token.
 // Logits are carried in log2 units: x = scale * log2(e) * q.k.
+//
+// Every kernel runs 8 waves of 32 window rows each (256 rows per workgroup),
+// so a wave's registers (queries, one output block, one score block) fit in
+// the 256 architectural VGPRs and two waves share each SIMD: one wave's
+// softmax overlaps the other's MFMA.
 #include "ckv_device.h"
 #include "ckv_kernels.h"
 
+#include <algorithm>
 #include <climits>
 
 namespace ckv {
 
+constexpr int kNW = 8;               // waves per workgroup
+constexpr int kRowsWG = 32 * kNW;    // window rows per workgroup
+// The running output is rescaled whenever a row's max grows (the wave skips
+// the rescale when no row's max grew), so the dominant token's float16 weight
+// is exactly 1 in both passes.
+//
+// A page that holds nearly all of a row's mass (A -> 1) is ill-conditioned
+// for Eq. (6): o - u = (1 - A) o' keeps only the digits of o' that survive
+// float32 accumulation of o.  Rows where a page has A > kFixA are therefore
+// left out of the page kernel's maximum and listed; the fix-up kernel
+// recomputes the output without the page, o', directly (all other splits'
+// partial sums as they are, the page's own split again with the page
+// excluded) and takes ||o - o'|| / ||o|| by definition.  At most one page
+// per row can exceed kFixA, so the list never holds more than one entry per
+// window row.
+constexpr float kFixA = 0.9f;
+
 // ---------------------------------------------------------------------------
-// staging of a 64-token tile: K as [token][width] bf16, V^T as
-// [width][slot] fp16 (slot = vt_slot(token)), positions as int32.
+// staging of a 64-token tile made of two 32-token segments (slot 0: offsets
+// 0..31, slot 1: offsets 32..63): K as [token][width] bf16, V^T as
+// [width][slot] fp16 (slot = vt_slot(offset)), positions as int32 (INT_MAX
+// for offsets past a segment's length, whose K and V rows are zero).
 // ---------------------------------------------------------------------------
 template <int D, int NT>
 struct Stager {
-  static constexpr int KP = D + 8;          // K tile row stride (elements)
-  static constexpr int VP = kTile + 8;      // V^T tile row stride (halves)
-  static constexpr int CPR = D / 8;         // 16-byte chunks per row
-  static constexpr int KCH = kTile * CPR;   // chunks per K tile
+  static constexpr int KP = D + 8;              // K tile row stride (elements)
+  static constexpr int VP = kTile + 8;          // V^T tile row stride (halves)
+  static constexpr int CPR = D / 8;             // 16-byte chunks per row
+  static constexpr int KCH = kTile * CPR;       // chunks per K tile
   static constexpr int KPT = (KCH + NT - 1) / NT;
-  static constexpr int VQ = (kTile / 4) * CPR;   // (4 tokens x 8 widths) quads
-  static constexpr int VPT = (VQ + NT - 1) / NT;
+  static constexpr int VU = (kTile / 2) * CPR;  // (2 tokens x 8 widths) units of V
+  static constexpr int VPT = (VU + NT - 1) / NT;
 
-  uint4 kr[KPT];
-  uint4 vr[VPT][4];
+  u32x4 kr[KPT];
+  u32x4 vr[VPT][2];
   int pr;
 
-  // load tokens t0 .. t0+63 of one head; tokens at offset >= n_valid are zero
-  __device__ __forceinline__ void issue(const uint16_t* kh, const uint16_t* vh,
-                                        int64_t ts, const int32_t* pos, int t0,
-                                        int n_valid, int tid) {
-    const uint4 z = make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int c = tid + i * NT;
-      const int tr = c / CPR, cc = c % CPR;
-      kr[i] = (c < KCH && tr < n_valid)
-                  ? *reinterpret_cast<const uint4*>(kh + (int64_t)(t0 + tr) * ts + cc * 8)
-                  : z;
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int qd = tid + i * NT;
-      const int tq = qd / CPR, cg = qd % CPR;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int tr = 4 * tq + j;
-        vr[i][j] = (qd < VQ && tr < n_valid)
-                       ? *reinterpret_cast<const uint4*>(vh + (int64_t)(t0 + tr) * ts + cg * 8)
-                       : z;
-      }
-    }
-    pr = (tid < kTile && tid < n_valid) ? pos[t0 + tid] : INT_MAX;
+  __device__ __forceinline__ static int tok(int off, int s0, int n0, int s1, int n1, bool& ok) {
+    if (off < 32) { ok = off < n0; return s0 + off; }
+    ok = off - 32 < n1;
+    return s1 + off - 32;
   }
 
-  __device__ __forceinline__ void commit(uint16_t* sK, _Float16* sV, int* sP, int tid) const {
+  // Loads are unconditional (a token outside the segments reads token 0,
+  // which always exists) and the unwanted values are replaced by zero, so
+  // the staging registers never need a branch.
+  __device__ __forceinline__ void issue(const uint16_t* kh, const uint16_t* vh, int64_t ts,
+                                        const int32_t* pos, int s0, int n0, int s1, int n1,
+                                        int tid) {
+    const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * NT;
-      if (c < KCH) {
-        const int tr = c / CPR, cc = c % CPR;
-        *reinterpret_cast<uint4*>(sK + tr * KP + cc * 8) = kr[i];
-      }
+      bool ok = false;
+      int t = tok((c / CPR) & (kTile - 1), s0, n0, s1, n1, ok);
+      ok = ok && c < KCH;
+      t = ok ? t : 0;
+      const u32x4 v = ldg_u4(kh + (int64_t)t * ts + (c % CPR) * 8);
+      kr[i] = ok ? v : z;
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
-      const int qd = tid + i * NT;
-      if (qd < VQ) {
-        const int tq = qd / CPR, cg = qd % CPR;
-        const int slot = vt_slot(4 * tq);
+      const int u = tid + i * NT;
+      const int tp = (u / CPR) & (kTile / 2 - 1), cg = u % CPR;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        bool ok = false;
+        int t = tok(2 * tp + j, s0, n0, s1, n1, ok);
+        ok = ok && u < VU;
+        t = ok ? t : 0;
+        const u32x4 v = ldg_u4(vh + (int64_t)t * ts + cg * 8);
+        vr[i][j] = ok ? v : z;
+      }
+    }
+    bool ok = false;
+    int t = tok(tid & 63, s0, n0, s1, n1, ok);
+    ok = ok && tid < kTile;
+    t = ok ? t : 0;
+    const int pv = ldg_i32(pos + t);
+    pr = ok ? pv : INT_MAX;
+  }
+
+  // writes the tile; wave 0 also flags whether every position is <= minq
+  __device__ __forceinline__ void commit(uint16_t* sK, _Float16* sV, int* sP, int* sFull, int minq,
+                                         int tid) const {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + i * NT;
+      if (c < KCH) *reinterpret_cast<u32x4*>(sK + (c / CPR) * KP + (c % CPR) * 8) = kr[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int u = tid + i * NT;
+      if (u < VU) {
+        const int tp = u / CPR, cg = u % CPR;
+        const int slot = vt_slot(2 * tp);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          f16x4 w;
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            w[j] = (_Float16)bf16_bits_to_float(chunk_elem(vr[i][j], e));
-          *reinterpret_cast<f16x4*>(sV + (cg * 8 + e) * VP + slot) = w;
+          typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+          f16x2 w;
+          w[0] = (_Float16)bf16_bits_to_float(chunk_elem(vr[i][0], e));
+          w[1] = (_Float16)bf16_bits_to_float(chunk_elem(vr[i][1], e));
+          *reinterpret_cast<f16x2*>(sV + (cg * 8 + e) * VP + slot) = w;
         }
       }
     }
-    if (tid < kTile) sP[tid] = pr;
+    if (tid < kTile) {
+      sP[tid] = pr;
+      const unsigned long long late = __ballot(pr > minq);
+      if (tid == 0) *sFull = late == 0ull;
+    }
   }
 };
 
@@ -105,9 +151,9 @@ __device__ __forceinline__ bf16x8 zero_bf16x8() {
   return __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
 }
 
-// rows of KV head g handled by lane: row = base + rb*32 + col
+// the window row a lane handles inside KV head g
 struct RowInfo {
-  int row;     // row inside the KV head (0 .. rows-1), or >= rows if padding
+  int row;     // row inside the KV head (0 .. rows-1); padding rows are >= rows
   bool ok;
   int qp;      // absolute position of the window row
   int rg;      // global row index h*W + p
@@ -123,30 +169,87 @@ __device__ __forceinline__ RowInfo row_info(const AttnGeom& a, int g, int row) {
   return r;
 }
 
-template <int D, int RB>
-__device__ __forceinline__ void load_q(const AttnGeom& a, int g, const RowInfo (&ri)[RB],
-                                       int half, bf16x8 (&qf)[RB][D / 16]) {
+template <int D>
+__device__ __forceinline__ void load_q(const AttnGeom& a, int g, const RowInfo& ri, int half,
+                                       bf16x8 (&qf)[D / 16]) {
+  const int h = g * a.group + (ri.ok ? ri.row / a.W : 0);
+  const int p = ri.ok ? ri.row % a.W : 0;
+  const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)p * a.q_row_stride;
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int h = g * a.group + (ri[rb].ok ? ri[rb].row / a.W : 0);
-    const int p = ri[rb].ok ? ri[rb].row % a.W : 0;
-    const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)p * a.q_row_stride;
+  for (int ks = 0; ks < D / 16; ++ks)
+    qf[ks] = ri.ok ? load_bf16x8(qrow + 16 * ks + 8 * half) : zero_bf16x8();
+}
+
+// smallest window position among the valid rows of the workgroup
+__device__ __forceinline__ int block_min_qpos(const RowInfo& ri, int* sMin) {
+  if (threadIdx.x == 0) *sMin = INT_MAX;
+  __syncthreads();
+  int q = ri.ok ? ri.qp : INT_MAX;
 #pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks)
-      qf[rb][ks] = ri[rb].ok ? load_bf16x8(qrow + 16 * ks + 8 * half) : zero_bf16x8();
+  for (int off = 32; off >= 1; off >>= 1) q = min(q, __shfl_xor(q, off, 64));
+  if ((threadIdx.x & 63) == 0) atomicMin(sMin, q);
+  __syncthreads();
+  return *sMin;
+}
+
+// S^T block (32 tokens x 32 rows) of tile slot tb: K from LDS, Q^T in registers
+template <int D, int KP>
+__device__ __forceinline__ f32x16 scores(const uint16_t* sK, int tb, int col, int half,
+                                         const bf16x8 (&qf)[D / 16]) {
+  f32x16 acc = zero16();
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks)
+    acc = mfma_bf16(load_bf16x8(sK + (32 * tb + col) * KP + 16 * ks + 8 * half), qf[ks], acc);
+  return acc;
+}
+
+// Rounds the 16 weights of a score block to float16 (the B operands of the
+// two 16-token steps of O^T += V^T P^T) and adds the ROUNDED weights to sum.
+// Normalising by the sum of exactly the weights that multiply V keeps the
+// output a true weighted average; with unrounded sums, a page that carries
+// nearly all of a row's mass would see its rounding error amplified by
+// 1/(1 - A) in the residual u - A o.
+__device__ __forceinline__ void to_f16(const f32x16& p, f16x8 (&h)[2], float& sum) {
+  typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+  const f16x2 one = {(_Float16)1.f, (_Float16)1.f};
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[u][e] = (_Float16)p[8 * u + e];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const f16x2 pr = {h[u][2 * e], h[u][2 * e + 1]};
+      sum = __builtin_amdgcn_fdot2(pr, one, sum, false);
+    }
+  }
+}
+
+// O^T (+)= V^T P^T for one 32-token slot, P^T given as float16 operands
+template <int D, int VP>
+__device__ __forceinline__ void pv_slot(const _Float16* sV, int tb, int col, int half, const f16x8 (&h)[2],
+                                        f32x16 (&acc)[D / 32]) {
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const f16x8 af = *reinterpret_cast<const f16x8*>(sV + (32 * db + col) * VP + 32 * tb + 16 * u + 8 * half);
+      acc[db] = mfma_f16(af, h[u], acc[db]);
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
 // A. split window attention
 // ---------------------------------------------------------------------------
-template <int D, int RB, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void window_attention_kernel(AttnGeom a, AttnSplit sp) {
-  constexpr int NT = NW * 64, KS = D / 16, DB = D / 32;
+template <int D>
+__global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom a, AttnSplit sp) {
+  constexpr int NT = kNW * 64, KS = D / 16, DB = D / 32;
   using St = Stager<D, NT>;
   __shared__ __align__(16) uint16_t sK[2][kTile * St::KP];
   __shared__ __align__(16) _Float16 sV[2][D * St::VP];
   __shared__ __align__(16) int sP[2][kTile];
+  __shared__ int sFull[2];
+  __shared__ int sMin;
 
   const int g = blockIdx.z, split = blockIdx.x, rblk = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -156,136 +259,114 @@ __global__ __launch_bounds__(NW * 64, 1) void window_attention_kernel(AttnGeom a
   const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
   const uint16_t* vh = a.v + (int64_t)g * a.kv_head_stride;
 
-  RowInfo ri[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
-    ri[rb] = row_info(a, g, (rblk * NW + wave) * (32 * RB) + rb * 32 + col);
-  bf16x8 qf[RB][KS];
-  load_q<D, RB>(a, g, ri, half, qf);
+  const RowInfo ri = row_info(a, g, rblk * kRowsWG + wave * 32 + col);
+  const bool wave_on = __ballot(ri.ok) != 0ull;
+  const int minq = block_min_qpos(ri, &sMin);
+  bf16x8 qf[KS];
+  load_q<D>(a, g, ri, half, qf);
 
-  f32x16 oacc[RB][DB];
-  float m[RB], l[RB];
-  int cnt[RB];
+  f32x16 oacc[DB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    m[rb] = -INFINITY;
-    l[rb] = 0.f;
-    cnt[rb] = 0;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) oacc[rb][db] = zero16();
-  }
+  for (int db = 0; db < DB; ++db) oacc[db] = zero16();
+  float mref = -INFINITY, l = 0.f;
+  int cnt = 0;
 
   const int n_tiles = t_end > t_begin ? (t_end - t_begin + kTile - 1) / kTile : 0;
+  auto seg = [&](int t0, int& s0, int& n0, int& s1, int& n1) {
+    const int n = min(kTile, t_end - t0);
+    s0 = t0; n0 = min(32, n); s1 = t0 + 32; n1 = max(0, n - 32);
+  };
   St st;
   if (n_tiles > 0) {
-    st.issue(kh, vh, a.kv_tok_stride, a.pos, t_begin, min(kTile, t_end - t_begin), tid);
-    st.commit(sK[0], sV[0], sP[0], tid);
+    int s0, n0, s1, n1;
+    seg(t_begin, s0, n0, s1, n1);
+    st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, n0, s1, n1, tid);
+    st.commit(sK[0], sV[0], sP[0], &sFull[0], minq, tid);
   }
   __syncthreads();
 
   for (int it = 0; it < n_tiles; ++it) {
     const int b = it & 1;
-    const int tn = t_begin + (it + 1) * kTile;
-    if (it + 1 < n_tiles) st.issue(kh, vh, a.kv_tok_stride, a.pos, tn, min(kTile, t_end - tn), tid);
-
-    // S^T = K Q^T for 64 tokens (two 32-token blocks)
-    f32x16 sacc[RB][2];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) sacc[rb][0] = sacc[rb][1] = zero16();
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-      for (int tb = 0; tb < 2; ++tb) {
-        const bf16x8 af = load_bf16x8(&sK[b][(32 * tb + col) * St::KP + 16 * ks + 8 * half]);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) sacc[rb][tb] = mfma_bf16(af, qf[rb][ks], sacc[rb][tb]);
-      }
+    if (it + 1 < n_tiles) {
+      int s0, n0, s1, n1;
+      seg(t_begin + (it + 1) * kTile, s0, n0, s1, n1);
+      st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, n0, s1, n1, tid);
     }
-    // causal mask by absolute position, online softmax (log2 units)
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
+    if (wave_on) {
+      f32x16 s[2];
+      s[0] = scores<D, St::KP>(sK[b], 0, col, half, qf);
+      s[1] = scores<D, St::KP>(sK[b], 1, col, half, qf);
       float mx = -INFINITY;
+      if (sFull[b]) {
+        // every token of the tile is visible to every row of the workgroup
 #pragma unroll
-      for (int tb = 0; tb < 2; ++tb) {
+        for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int4 pq = *reinterpret_cast<const int4*>(&sP[b][32 * tb + 8 * i + 4 * half]);
-          const int pv[4] = {pq.x, pq.y, pq.z, pq.w};
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[tb][r]);
+        cnt += 32;
+      } else {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const bool vis = ri[rb].ok && pv[j] <= ri[rb].qp;
-            const float x = vis ? sacc[rb][tb][4 * i + j] * a.sl2 : -INFINITY;
-            cnt[rb] += vis ? 1 : 0;
-            sacc[rb][tb][4 * i + j] = x;
-            mx = fmaxf(mx, x);
+        for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int4 pq = *reinterpret_cast<const int4*>(&sP[b][32 * tb + 8 * i + 4 * half]);
+            const int pv[4] = {pq.x, pq.y, pq.z, pq.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const bool vis = ri.ok && pv[j] <= ri.qp;
+              const float x = vis ? s[tb][4 * i + j] : -INFINITY;
+              cnt += vis ? 1 : 0;
+              s[tb][4 * i + j] = x;
+              mx = fmaxf(mx, x);
+            }
           }
-        }
       }
-      mx = fmaxf(mx, xor32(mx));
-      const float mn = fmaxf(m[rb], mx);
-      const float base = (mn == -INFINITY) ? 0.f : mn;
-      const float alpha = __builtin_amdgcn_exp2f(m[rb] - base);
-      float ls = 0.f;
+      mx = fmaxf(mx, xor32(mx)) * a.sl2;
+      // rescale the running output when a row max grew
+      const bool need = mx > mref;
+      if (__ballot(need) != 0ull) {
+        const float nref = need ? mx : mref;
+        const float alpha = need ? __builtin_amdgcn_exp2f(mref - nref) : 1.f;
+        l *= alpha;
 #pragma unroll
-      for (int tb = 0; tb < 2; ++tb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(sacc[rb][tb][r] - base);
-          sacc[rb][tb][r] = p;
-          ls += p;
-        }
+        for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+        mref = nref;
       }
-      l[rb] = l[rb] * alpha + ls;
-      m[rb] = mn;
+      const float base = mref == -INFINITY ? 0.f : mref;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) oacc[rb][db] *= alpha;
+      for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[tb][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[tb][r], a.sl2, -base));
+      f16x8 h[2][2];
+      to_f16(s[0], h[0], l);
+      to_f16(s[1], h[1], l);
+      pv_slot<D, St::VP>(sV[b], 0, col, half, h[0], oacc);
+      pv_slot<D, St::VP>(sV[b], 1, col, half, h[1], oacc);
     }
-    // O^T += V^T P^T (fp16 weights and values, fp32 accumulation)
-#pragma unroll
-    for (int tb = 0; tb < 2; ++tb) {
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        f16x8 bfr[RB];
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) bfr[rb][e] = (_Float16)sacc[rb][tb][8 * u + e];
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const f16x8 af = *reinterpret_cast<const f16x8*>(
-              &sV[b][(32 * db + col) * St::VP + 32 * tb + 16 * u + 8 * half]);
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) oacc[rb][db] = mfma_f16(af, bfr[rb], oacc[rb][db]);
-        }
-      }
-    }
-    if (it + 1 < n_tiles) st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], tid);
+    if (it + 1 < n_tiles) st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], &sFull[b ^ 1], minq, tid);
     __syncthreads();
   }
 
-  // partial results of this split
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const float lt = l[rb] + xor32(l[rb]);
-    const int ct = cnt[rb] + xor32i(cnt[rb]);
-    if (!ri[rb].ok) continue;
-    const size_t idx = ((size_t)(g * sp.n_splits + split) * sp.rows_pad + ri[rb].row);
-    if (half == 0) {
-      sp.part_m[idx] = m[rb];
-      sp.part_l[idx] = lt;
-      sp.part_c[idx] = ct;
-    }
-    float* po = sp.part_o + idx * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f32x4 v4;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) v4[j] = oacc[rb][db][4 * i + j];
-        *reinterpret_cast<f32x4*>(po + 32 * db + 8 * i + 4 * half) = v4;
-      }
+  // partial results of this split (m in log2 units, output relative to it)
+  const float lt = l + xor32(l);
+  const int ct = cnt + xor32i(cnt);
+  if (!ri.ok) return;
+  const size_t idx = ((size_t)(g * sp.n_splits + split) * sp.rows_pad + ri.row);
+  if (half == 0) {
+    sp.part_m[idx] = mref;
+    sp.part_l[idx] = lt;
+    sp.part_c[idx] = ct;
   }
+  float* po = sp.part_o + idx * D;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f32x4 v4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v4[j] = oacc[db][4 * i + j];
+      *reinterpret_cast<f32x4*>(po + 32 * db + 8 * i + 4 * half) = v4;
+    }
 }
 
 // one wave per window row: merge the splits, write o, lse, ||o||, n_vis
@@ -295,21 +376,27 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
   const int lane = threadIdx.x & 63;
   const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
   // zero the outputs that later kernels reduce into with atomic max
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < zl.n0; i += (size_t)gridDim.x * blockDim.x)
-    zl.p0[i] = 0.f;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < zl.n1; i += (size_t)gridDim.x * blockDim.x)
-    zl.p1[i] = 0.f;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < zl.n2; i += (size_t)gridDim.x * blockDim.x)
-    zl.p2[i] = 0.f;
+  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t gsz = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = gid; i < zl.n0; i += gsz) zl.p0[i] = 0.f;
+  for (size_t i = gid; i < zl.n1; i += gsz) zl.p1[i] = 0.f;
+  for (size_t i = gid; i < zl.n2; i += gsz) zl.p2[i] = 0.f;
+  if (zl.i0 && gid == 0) *zl.i0 = 0;
+  for (size_t i = gid; i < zl.n1i; i += gsz) zl.i1[i] = 0;
   if (wid >= a.Hkv * a.rows) return;
   const int g = wid / a.rows, row = wid % a.rows;
   const int rg = g * a.rows + row;
   float M = -INFINITY;
   int nv = 0;
-  for (int s = 0; s < sp.n_splits; ++s) {
+  for (int s = lane; s < sp.n_splits; s += 64) {
     const size_t idx = (size_t)(g * sp.n_splits + s) * sp.rows_pad + row;
     M = fmaxf(M, sp.part_m[idx]);
     nv += sp.part_c[idx];
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    M = fmaxf(M, __shfl_xor(M, off, 64));
+    nv += __shfl_xor(nv, off, 64);
   }
   float wsum = 0.f;
   float acc[D / 64];
@@ -347,15 +434,21 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
 
 // ---------------------------------------------------------------------------
 // B. per-page deletion effect (MODE 0) or per-candidate residual (MODE 1)
+//
+// A staged 64-token tile holds either two pages of at most 32 tokens (one per
+// 32-token slot) or one page of 33..64 tokens (both slots).  Every thread
+// derives the same tile sequence from the page lengths.
 // ---------------------------------------------------------------------------
-template <int D, int RB, int NW, int MODE>
-__global__ __launch_bounds__(NW * 64, 1) void page_kernel(AttnGeom a, PageWork pw, RowStats rs) {
-  constexpr int NT = NW * 64, KS = D / 16, DB = D / 32, RWG = 32 * RB * NW;
+template <int D, int MODE>
+__global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork pw, RowStats rs) {
+  constexpr int NT = kNW * 64, KS = D / 16, DB = D / 32;
+  constexpr int NH = kRowsWG + 2;     // bound on the heads touched by one workgroup
   using St = Stager<D, NT>;
   __shared__ __align__(16) uint16_t sK[2][kTile * St::KP];
   __shared__ __align__(16) _Float16 sV[2][D * St::VP];
   __shared__ __align__(16) int sP[2][kTile];
-  __shared__ unsigned int sMax[2][RWG + 2];
+  __shared__ int sFull[2];
+  __shared__ unsigned int sMax[2][2][NH];   // [buffer][page of the tile][local head]
 
   const int g = blockIdx.z, rblk = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -368,221 +461,411 @@ __global__ __launch_bounds__(NW * 64, 1) void page_kernel(AttnGeom a, PageWork p
   const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
   const uint16_t* vh = a.v + (int64_t)g * a.kv_head_stride;
 
-  RowInfo ri[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
-    ri[rb] = row_info(a, g, (rblk * NW + wave) * (32 * RB) + rb * 32 + col);
-  bf16x8 qf[RB][KS];
-  load_q<D, RB>(a, g, ri, half, qf);
+  const RowInfo ri = row_info(a, g, rblk * kRowsWG + wave * 32 + col);
+  const bool wave_on = __ballot(ri.ok) != 0ull;
+  bf16x8 qf[KS];
+  load_q<D>(a, g, ri, half, qf);
   // o_p in accumulator layout: register r of block db holds width 32db + 8(r/4) + 4h + r%4
-  f32x16 of[RB][DB];
-  float lse2[RB], onorm[RB];
-  int nvis[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const float* orow = rs.o + (size_t)ri[rb].rg * D;
+  f32x16 of[DB];
+  {
+    const float* orow = rs.o + (size_t)ri.rg * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const f32x4 v4 = ri[rb].ok ? *reinterpret_cast<const f32x4*>(orow + 32 * db + 8 * i + 4 * half)
-                                   : f32x4{0.f, 0.f, 0.f, 0.f};
+        const f32x4 v4 = ri.ok ? *reinterpret_cast<const f32x4*>(orow + 32 * db + 8 * i + 4 * half)
+                               : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) of[rb][db][4 * i + j] = v4[j];
+        for (int j = 0; j < 4; ++j) of[db][4 * i + j] = v4[j];
       }
-    lse2[rb] = ri[rb].ok ? rs.lse2[ri[rb].rg] : -INFINITY;
-    onorm[rb] = ri[rb].ok ? rs.onorm[ri[rb].rg] : 0.f;
-    nvis[rb] = ri[rb].ok ? rs.nvis[ri[rb].rg] : 0;
   }
-  const int row0 = rblk * RWG;                 // first row of this block
-  const int head0 = row0 / a.W;                // first local head touched
-  const int n_heads_blk = min(a.group, (min(a.rows, row0 + RWG) - 1) / a.W + 1) - head0;
-  if (MODE == 0) {
-    for (int i = tid; i < 2 * (RWG + 2); i += NT) (&sMax[0][0])[i] = 0u;
-  }
+  const float lse2 = ri.ok ? rs.lse2[ri.rg] : -INFINITY;
+  const float onorm = ri.ok ? rs.onorm[ri.rg] : 0.f;
+  const int nvis = ri.ok ? rs.nvis[ri.rg] : 0;
+  const int row0 = rblk * kRowsWG;
+  const int head0 = row0 / a.W;
+  const int n_heads_blk = min(a.group, (min(a.rows, row0 + kRowsWG) - 1) / a.W + 1) - head0;
+  const bool wave_one_head = (a.W % 32) == 0;   // the 32 rows of a wave share one head
+  if (MODE == 0)
+    for (int i = tid; i < 2 * 2 * NH; i += NT) (&sMax[0][0][0])[i] = 0u;
 
-  // page of an item; a candidate index outside the page list is an empty page
   auto page_of = [&](int item) { return MODE == 0 ? item : pw.cand[item]; };
   auto page_ok = [&](int pg) { return pg >= 0 && pg < pw.n_pages; };
   auto pstart = [&](int item) { const int pg = page_of(item); return page_ok(pg) ? pw.start[pg] : 0; };
   auto plen = [&](int item) { const int pg = page_of(item); return page_ok(pg) ? pw.len[pg] : 0; };
+  // pages in the tile that starts at item `it`: two short pages share a tile
+  auto tile_items = [&](int it) {
+    return (it + 1 < i_end && plen(it) <= 32 && plen(it + 1) <= 32) ? 2 : 1;
+  };
   St st;
-  st.issue(kh, vh, a.kv_tok_stride, a.pos, pstart(i_begin), plen(i_begin), tid);
-  st.commit(sK[0], sV[0], sP[0], tid);
+  auto issue_tile = [&](int it) {
+    const int s0 = pstart(it), l0 = plen(it);
+    if (tile_items(it) == 2)
+      st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, l0, pstart(it + 1), plen(it + 1), tid);
+    else
+      st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, min(l0, 32), s0 + 32, max(0, l0 - 32), tid);
+  };
+  issue_tile(i_begin);
+  st.commit(sK[0], sV[0], sP[0], &sFull[0], INT_MIN, tid);
   __syncthreads();
 
-  for (int it = i_begin; it < i_end; ++it) {
-    const int b = (it - i_begin) & 1;
-    if (it + 1 < i_end) st.issue(kh, vh, a.kv_tok_stride, a.pos, pstart(it + 1), plen(it + 1), tid);
-    // flush the previous item's per-head maxima (its LDS slots are final)
-    if (MODE == 0 && it > i_begin && tid < n_heads_blk) {
-      const int pb = b ^ 1;
-      const float v = __uint_as_float(sMax[pb][tid]);
-      const int page = it - 1;
-      const int h = g * a.group + head0 + tid;
-      if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], v);
-      atomic_max_nonneg(&pw.R[page], v);
-      sMax[pb][tid] = 0u;
-    }
-
-    const int len = plen(it);
-    const int nblk = len > 32 ? 2 : 1;
-    f32x16 sacc[RB][2];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) sacc[rb][0] = sacc[rb][1] = zero16();
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-      for (int tb = 0; tb < 2; ++tb) {
-        if (tb < nblk) {
-          const bf16x8 af = load_bf16x8(&sK[b][(32 * tb + col) * St::KP + 16 * ks + 8 * half]);
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) sacc[rb][tb] = mfma_bf16(af, qf[rb][ks], sacc[rb][tb]);
-        }
+  int prev_it = -1, prev_m = 0, k = 0;
+  for (int it = i_begin; it < i_end; ++k) {
+    const int b = k & 1;
+    const int m = tile_items(it);
+    const int next = it + m;
+    if (next < i_end) issue_tile(next);
+    // flush the previous tile's per-head maxima (final since the last barrier)
+    if (MODE == 0 && prev_it >= 0 && tid < 2 * n_heads_blk) {
+      const int ps = tid / n_heads_blk, hl = tid % n_heads_blk;
+      if (ps < prev_m) {
+        const float v = __uint_as_float(sMax[b ^ 1][ps][hl]);
+        const int page = prev_it + ps;
+        const int h = g * a.group + head0 + hl;
+        if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], v);
+        atomic_max_nonneg(&pw.R[page], v);
       }
+      sMax[b ^ 1][ps][hl] = 0u;
     }
-    float lhat[RB], mE[RB];
-    int cE[RB];
+    if (wave_on) {
+      for (int ps = 0; ps < m; ++ps) {
+        const int item = it + ps;
+        const int len = plen(item);
+        // a short page occupies slot ps; a long one both slots from slot 0
+        const int nblk = (m == 2) ? 1 : (len > 32 ? 2 : 1);
+        const int slot0 = ps;
+        f32x16 s[2];
+        s[0] = scores<D, St::KP>(sK[b], slot0, col, half, qf);
+        s[1] = nblk == 2 ? scores<D, St::KP>(sK[b], 1, col, half, qf) : zero16();
+        float mx = -INFINITY;
+        int c = 0;
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      float mx = -INFINITY;
-      int c = 0;
+        for (int tb = 0; tb < 2; ++tb) {
+          if (tb < nblk) {
 #pragma unroll
-      for (int tb = 0; tb < 2; ++tb) {
+            for (int i = 0; i < 4; ++i) {
+              const int o0 = 8 * i + 4 * half;          // offset inside the 32-token slot
+              const int4 pq = *reinterpret_cast<const int4*>(&sP[b][32 * (slot0 + tb) + o0]);
+              const int pv[4] = {pq.x, pq.y, pq.z, pq.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int t0 = 32 * tb + 8 * i + 4 * half;
-          const int4 pq = *reinterpret_cast<const int4*>(&sP[b][t0]);
-          const int pv[4] = {pq.x, pq.y, pq.z, pq.w};
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const bool vis = ri[rb].ok && (t0 + j) < len && pv[j] <= ri[rb].qp;
-            const float x = vis ? sacc[rb][tb][4 * i + j] * a.sl2 : -INFINITY;
-            c += vis ? 1 : 0;
-            sacc[rb][tb][4 * i + j] = x;
-            mx = fmaxf(mx, x);
+              for (int j = 0; j < 4; ++j) {
+                const bool vis = ri.ok && (32 * tb + o0 + j) < len && pv[j] <= ri.qp;
+                const float x = vis ? s[tb][4 * i + j] : -INFINITY;
+                c += vis ? 1 : 0;
+                s[tb][4 * i + j] = x;
+                mx = fmaxf(mx, x);
+              }
+            }
           }
         }
-      }
-      mx = fmaxf(mx, xor32(mx));
-      c += xor32i(c);
-      const float base = (mx == -INFINITY) ? 0.f : mx;
-      float ls = 0.f;
+        mx = fmaxf(mx, xor32(mx));
+        c += xor32i(c);
+        const float base = mx == -INFINITY ? 0.f : mx * a.sl2;
 #pragma unroll
-      for (int tb = 0; tb < 2; ++tb)
+        for (int r = 0; r < 16; ++r) s[0][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0][r], a.sl2, -base));
+        float ls = 0.f;
+        f16x8 h0[2], h1[2];
+        to_f16(s[0], h0, ls);
+        if (nblk == 2) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(sacc[rb][tb][r] - base);
-          sacc[rb][tb][r] = p;
-          ls += p;
+          for (int r = 0; r < 16; ++r) s[1][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1][r], a.sl2, -base));
+          to_f16(s[1], h1, ls);
         }
-      lhat[rb] = ls + xor32(ls);
-      mE[rb] = mx;
-      cE[rb] = c;
-    }
-    // U^T = V_E^T P^T
-    f32x16 uacc[RB][DB];
+        const float lhat = ls + xor32(ls);
+        f32x16 u[DB];
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
+        for (int db = 0; db < DB; ++db) u[db] = zero16();
+        pv_slot<D, St::VP>(sV[b], slot0, col, half, h0, u);
+        if (nblk == 2) pv_slot<D, St::VP>(sV[b], 1, col, half, h1, u);
+        // residual r^ = U^ - l^ o, its norm, and the ratio of Eq. (6)-(7)
+        float n2 = 0.f;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) uacc[rb][db] = zero16();
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int tb = 0; tb < 2; ++tb) {
-      if (tb < nblk) {
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          f16x8 bfr[RB];
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) bfr[rb][e] = (_Float16)sacc[rb][tb][8 * u + e];
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const f16x8 af = *reinterpret_cast<const f16x8*>(
-                &sV[b][(32 * db + col) * St::VP + 32 * tb + 16 * u + 8 * half]);
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) uacc[rb][db] = mfma_f16(af, bfr[rb], uacc[rb][db]);
+          for (int r = 0; r < 16; ++r) {
+            const float rv = __builtin_fmaf(-lhat, of[db][r], u[db][r]);
+            u[db][r] = rv;
+            n2 = __builtin_fmaf(rv, rv, n2);
           }
-        }
-      }
-    }
-    // residual r^ = U^ - l^ o, its norm, and the ratio of Eq. (6)-(7)
+        n2 += xor32(n2);
+        const bool touched = c > 0;
+        const float f = touched ? __builtin_amdgcn_exp2f(base - lse2) : 0.f;
+        const float A = f * lhat;
+        if (MODE == 0) {
+          float ratio = 0.f;
+          if (touched) {
+            const float keep = 1.f - A;
+            if (c >= nvis) {
+              ratio = INFINITY;                 // the page holds every visible token
+            } else if (A > kFixA || !(keep > 0.f)) {
+              if (ri.ok && half == 0) {         // ill-conditioned: recomputed by the fix-up
+                const int slot = atomicAdd(pw.fix_count, 1);
+                if (slot < pw.fix_cap) {
+                  pw.fix_list[2 * slot] = item;
+                  pw.fix_list[2 * slot + 1] = ri.rg;
+                }
+              }
+            } else if (onorm > 0.f) {
+              ratio = f * sqrtf(n2) / (keep * onorm);
+            } else {
+              ratio = n2 > 0.f ? INFINITY : 0.f;
+            }
+          }
+          if (!ri.ok) ratio = 0.f;
+          if (wave_one_head) {
+            float wm = ratio;
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      float n2 = 0.f;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float rv = uacc[rb][db][r] - lhat[rb] * of[rb][db][r];
-          uacc[rb][db][r] = rv;
-          n2 += rv * rv;
-        }
-      n2 += xor32(n2);
-      const bool touched = cE[rb] > 0;
-      const float f = touched ? __builtin_amdgcn_exp2f(mE[rb] - lse2[rb]) : 0.f;
-      const float A = f * lhat[rb];
-      if (MODE == 0) {
-        float ratio = 0.f;
-        if (touched) {
-          const float keep = 1.f - A;
-          if (cE[rb] >= nvis[rb] || !(keep > 0.f)) ratio = INFINITY;
-          else if (onorm[rb] > 0.f) ratio = f * sqrtf(n2) / (keep * onorm[rb]);
-          else ratio = n2 > 0.f ? INFINITY : 0.f;
-        }
-        if (ri[rb].ok && half == 0)
-          atomicMax(&sMax[b][ri[rb].row / a.W - head0], __float_as_uint(ratio));
-      } else {
-        if (ri[rb].ok) {
-          const size_t base = (size_t)it * pw.total_rows + ri[rb].rg;
-          float* rrow = pw.resid + base * D;
+            for (int off = 16; off >= 1; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off, 64));
+            if (lane == 0 && ri.ok) atomicMax(&sMax[b][ps][ri.row / a.W - head0], __float_as_uint(wm));
+          } else if (ri.ok && half == 0) {
+            atomicMax(&sMax[b][ps][ri.row / a.W - head0], __float_as_uint(ratio));
+          }
+        } else if (ri.ok) {
+          const size_t base_i = (size_t)item * pw.total_rows + ri.rg;
+          float* rrow = pw.resid + base_i * D;
 #pragma unroll
           for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               f32x4 v4;
 #pragma unroll
-              for (int j = 0; j < 4; ++j) v4[j] = f * uacc[rb][db][4 * i + j];
+              for (int j = 0; j < 4; ++j) v4[j] = f * u[db][4 * i + j];
               *reinterpret_cast<f32x4*>(rrow + 32 * db + 8 * i + 4 * half) = v4;
             }
           if (half == 0) {
-            pw.resA[base] = A;
-            pw.resC[base] = cE[rb];
+            pw.resA[base_i] = A;
+            pw.resC[base_i] = c;
           }
         }
       }
     }
-    if (it + 1 < i_end) st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], tid);
+    if (next < i_end) st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], &sFull[b ^ 1], INT_MIN, tid);
     __syncthreads();
+    prev_it = it;
+    prev_m = m;
+    it = next;
   }
-  if (MODE == 0 && tid < n_heads_blk) {
-    const int pb = (i_end - 1 - i_begin) & 1;
-    const float v = __uint_as_float(sMax[pb][tid]);
-    const int page = i_end - 1;
-    const int h = g * a.group + head0 + tid;
-    if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], v);
-    atomic_max_nonneg(&pw.R[page], v);
+  if (MODE == 0 && tid < 2 * n_heads_blk) {
+    const int b = (k - 1) & 1;
+    const int ps = tid / n_heads_blk, hl = tid % n_heads_blk;
+    if (ps < prev_m) {
+      const float v = __uint_as_float(sMax[b][ps][hl]);
+      const int page = prev_it + ps;
+      const int h = g * a.group + head0 + hl;
+      if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], v);
+      atomic_max_nonneg(&pw.R[page], v);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// B'. fix-up of ill-conditioned (page, row) pairs: o' = output without the
+// page from the other splits' partial sums plus the page's own split(s)
+// recomputed in float32 with the page excluded; ratio = ||o - o'|| / ||o||.
+// One workgroup per listed pair (grid-stride over the list).
+// ---------------------------------------------------------------------------
+constexpr int kFixParts = 8;      // workgroups sharing one listed pair
+constexpr int kFixChunk = 1024;   // tokens whose weights are staged at once
+
+// Workgroup (pair slot e, part kp): kp == 0 also adds the other splits'
+// partial sums; every part recomputes a slice of the page's split(s) with
+// the page excluded.  Parts write (sum over width, weight) to fix_part; the
+// last part to finish merges them in part order and writes the ratio.
+template <int D>
+__global__ __launch_bounds__(256) void page_fixup_kernel(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw) {
+  constexpr int TPR = D / 8;                  // threads per token row (16 bytes each)
+  constexpr int RPR = 256 / TPR;              // token rows per round
+  __shared__ float sw[kFixChunk];
+  __shared__ float sacc[RPR][D];
+  __shared__ float sl[RPR];
+  __shared__ float sred[2][4];
+  __shared__ int s_last;
+  const int tid = threadIdx.x, c = tid % TPR, r = tid / TPR;
+  const int kp = blockIdx.y;
+  const int n = min(*pw.fix_count, pw.fix_cap);
+  for (int e = blockIdx.x; e < n; e += gridDim.x) {
+    const int page = pw.fix_list[2 * e], rg = pw.fix_list[2 * e + 1];
+    const int h = rg / a.W, p = rg % a.W, g = h / a.group, row = rg - g * a.rows;
+    const int st = pw.start[page], ln = pw.len[page];
+    const int qp = a.qpos[p];
+    float qv[8];
+    {
+      const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)p * a.q_row_stride;
+      const u32x4 qc = ldg_u4(qrow + 8 * c);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) qv[j] = bf16_bits_to_float(chunk_elem(qc, j));
+    }
+    // the row's reference: max over the splits' maxima
+    float M = -INFINITY;
+    for (int s = tid; s < sp.n_splits; s += 256)
+      M = fmaxf(M, sp.part_m[(size_t)(g * sp.n_splits + s) * sp.rows_pad + row]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+    __syncthreads();
+    if ((tid & 63) == 0) sred[0][tid >> 6] = M;
+    __syncthreads();
+    M = fmaxf(fmaxf(sred[0][0], sred[0][1]), fmaxf(sred[0][2], sred[0][3]));
+    const int s0 = st / sp.chunk, s1 = (st + ln - 1) / sp.chunk;
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    float lacc = 0.f;
+    if (kp == 0) {
+      // other splits' partial sums as they are (row group r takes splits r, r+RPR, ...)
+      for (int s = r; s < sp.n_splits; s += RPR) {
+        if (s >= s0 && s <= s1) continue;
+        const size_t idx = (size_t)(g * sp.n_splits + s) * sp.rows_pad + row;
+        const float ms = sp.part_m[idx];
+        if (ms == -INFINITY) continue;
+        const float w = __builtin_amdgcn_exp2f(ms - M);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = __builtin_fmaf(w, sp.part_o[idx * D + 8 * c + j], acc[j]);
+        if (c == 0) lacc = __builtin_fmaf(w, sp.part_l[idx], lacc);
+      }
+    }
+    // this part's slice of the page's split(s), without the page, in float32
+    const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
+    const uint16_t* vh = a.v + (int64_t)g * a.kv_head_stride;
+    const int r_lo = s0 * sp.chunk, r_hi = min(a.S, (s1 + 1) * sp.chunk);
+    const int per = (r_hi - r_lo + kFixParts - 1) / kFixParts;
+    const int t_lo = min(r_hi, r_lo + kp * per), t_hi = min(r_hi, t_lo + per);
+    for (int sub = t_lo; sub < t_hi; sub += kFixChunk) {
+      const int n_sub = min(kFixChunk, t_hi - sub);
+      __syncthreads();
+      // scores and weights, 8 token rows per thread in flight
+      for (int i0 = r; i0 < n_sub; i0 += 8 * RPR) {
+        u32x4 kc[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = min(i0 + u * RPR, n_sub - 1);
+          kc[u] = ldg_u4(kh + (int64_t)(sub + i) * a.kv_tok_stride + 8 * c);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = i0 + u * RPR;
+          float x = 0.f;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) x = __builtin_fmaf(qv[j], bf16_bits_to_float(chunk_elem(kc[u], j)), x);
+#pragma unroll
+          for (int off = TPR / 2; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+          if (c == 0 && i < n_sub) {
+            const int t = sub + i;
+            const bool keep = ldg_i32(a.pos + t) <= qp && !(t >= st && t < st + ln);
+            sw[i] = keep ? __builtin_amdgcn_exp2f(__builtin_fmaf(x, a.sl2, -M)) : 0.f;
+          }
+        }
+      }
+      __syncthreads();
+      for (int i0 = r; i0 < n_sub; i0 += 8 * RPR) {
+        u32x4 vc[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = min(i0 + u * RPR, n_sub - 1);
+          vc[u] = ldg_u4(vh + (int64_t)(sub + i) * a.kv_tok_stride + 8 * c);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = i0 + u * RPR;
+          const float w = i < n_sub ? sw[i] : 0.f;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) acc[j] = __builtin_fmaf(w, bf16_bits_to_float(chunk_elem(vc[u], j)), acc[j]);
+          if (c == 0) lacc += w;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sacc[r][8 * c + j] = acc[j];
+    if (c == 0) sl[r] = lacc;
+    __syncthreads();
+    // this part's (sum, weight) -> fix_part[e][kp]
+    float* part = pw.fix_part + ((size_t)e * kFixParts + kp) * (D + 1);
+    if (tid < D) {
+      float num = 0.f;
+      for (int i = 0; i < RPR; ++i) num += sacc[i][tid];
+      part[tid] = num;
+    }
+    if (tid == 0) {
+      float den = 0.f;
+      for (int i = 0; i < RPR; ++i) den += sl[i];
+      part[D] = den;
+      __threadfence();
+      s_last = atomicAdd(&pw.fix_done[e], 1) == kFixParts - 1;
+    }
+    __syncthreads();
+    if (!s_last) continue;
+    // last part: merge in part order, o' = sum / weight, ratio = ||o - o'|| / ||o||
+    __threadfence();
+    float dd = 0.f, oo = 0.f;
+    const float* parts = pw.fix_part + (size_t)e * kFixParts * (D + 1);
+    if (tid < D) {
+      float num = 0.f, den = 0.f;
+      for (int k = 0; k < kFixParts; ++k) {
+        num += __hip_atomic_load(&parts[k * (D + 1) + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        den += __hip_atomic_load(&parts[k * (D + 1) + D], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      const float ov = rs.o[(size_t)rg * D + tid];
+      const float od = den > 0.f ? num / den : 0.f;
+      dd = (ov - od) * (ov - od);
+      oo = ov * ov;
+      if (tid == 0) sred[1][0] = den;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      dd += __shfl_xor(dd, off, 64);
+      oo += __shfl_xor(oo, off, 64);
+    }
+    __syncthreads();
+    if ((tid & 63) == 0 && tid < D) { sred[0][tid >> 6] = dd; sred[0][2 + (tid >> 6)] = oo; }
+    __syncthreads();
+    if (tid == 0) {
+      const float D2 = sred[0][0] + (D > 64 ? sred[0][1] : 0.f);
+      const float O2 = sred[0][2] + (D > 64 ? sred[0][3] : 0.f);
+      const float den = sred[1][0];
+      float ratio;
+      if (!(den > 0.f)) ratio = INFINITY;
+      else if (O2 > 0.f) ratio = sqrtf(D2) / sqrtf(O2);
+      else ratio = D2 > 0.f ? INFINITY : 0.f;
+      if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], ratio);
+      atomic_max_nonneg(&pw.R[page], ratio);
+      pw.fix_done[e] = 0;       // ready for the next call
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
 // C. window-attention mass of every token: max_h sum_p a_hpi
+//
+// Workgroup (token chunk, KV head g); wave w handles the query heads
+// w, w + 8, ... of the group, each over all its window rows, so a head's sum
+// is accumulated in one wave in a fixed order (deterministic).  The scores
+// use the C = Q K^T orientation (tokens on lanes, rows in registers), so the
+// sum over rows is lane-local.
 // ---------------------------------------------------------------------------
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void token_mass_kernel(AttnGeom a, RowStats rs, float* mass,
-                                                             int chunk) {
-  constexpr int NT = NW * 64, KS = D / 16;
+constexpr int kMassMaxRows = 2048;   // window rows per KV head the mass kernel supports
+
+template <int D>
+__global__ __launch_bounds__(kNW * 64) void token_mass_kernel(AttnGeom a, RowStats rs, float* mass,
+                                                              int chunk) {
+  constexpr int NT = kNW * 64, KS = D / 16;
   constexpr int KP = D + 8, CPR = D / 8, KCH = kTile * CPR;
   __shared__ __align__(16) uint16_t sK[kTile * KP];
   __shared__ int sP[kTile];
   __shared__ unsigned int sM[kTile];
+  __shared__ float sL2[kMassMaxRows];
+  __shared__ int sQP[kMassMaxRows];
   const int g = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int t_begin = blockIdx.x * chunk;
   const int t_end = min(a.S, t_begin + chunk);
+  if (t_begin >= t_end) return;
   const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
   const int nrb = (a.W + 31) / 32;
+  // per-row log-sum-exp and window position of this KV head's rows
+  for (int r = tid; r < a.rows; r += NT) {
+    sL2[r] = rs.lse2[g * a.rows + r];
+    sQP[r] = a.qpos[r % a.W];
+  }
   for (int t0 = t_begin; t0 < t_end; t0 += kTile) {
     const int nv = min(kTile, t_end - t0);
     for (int c = tid; c < KCH; c += NT) {
@@ -596,7 +879,7 @@ __global__ __launch_bounds__(NW * 64) void token_mass_kernel(AttnGeom a, RowStat
       sM[tid] = 0u;
     }
     __syncthreads();
-    for (int hl = wave; hl < a.group; hl += NW) {
+    for (int hl = wave; hl < a.group; hl += kNW) {
       const int h = g * a.group + hl;
       float msum[2] = {0.f, 0.f};
       for (int rb = 0; rb < nrb; ++rb) {
@@ -606,28 +889,21 @@ __global__ __launch_bounds__(NW * 64) void token_mass_kernel(AttnGeom a, RowStat
         bf16x8 qa[KS];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) qa[ks] = aok ? load_bf16x8(qrow + 16 * ks + 8 * half) : zero_bf16x8();
-        // rows of the C layout held by this lane
-        int qpr[16];
-        float l2r[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int p = 32 * rb + 8 * (r >> 2) + 4 * half + (r & 3);
-          qpr[r] = p < a.W ? a.qpos[p] : INT_MIN;
-          l2r[r] = p < a.W ? rs.lse2[h * a.W + p] : 0.f;
-        }
 #pragma unroll
         for (int tb = 0; tb < 2; ++tb) {
           f32x16 acc = zero16();
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8 kb = load_bf16x8(&sK[(32 * tb + col) * KP + 16 * ks + 8 * half]);
-            acc = mfma_bf16(qa[ks], kb, acc);
-          }
+          for (int ks = 0; ks < KS; ++ks)
+            acc = mfma_bf16(qa[ks], load_bf16x8(&sK[(32 * tb + col) * KP + 16 * ks + 8 * half]), acc);
           const int pt = sP[32 * tb + col];
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const bool vis = qpr[r] != INT_MIN && pt <= qpr[r];
-            msum[tb] += vis ? __builtin_amdgcn_exp2f(acc[r] * a.sl2 - l2r[r]) : 0.f;
+            const int p = 32 * rb + 8 * (r >> 2) + 4 * half + (r & 3);
+            if (p < a.W) {
+              const int row = hl * a.W + p;
+              const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[r], a.sl2, -sL2[row]));
+              msum[tb] += pt <= sQP[row] ? e : 0.f;
+            }
           }
         }
       }
@@ -646,22 +922,16 @@ __global__ __launch_bounds__(NW * 64) void token_mass_kernel(AttnGeom a, RowStat
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
-namespace {
-constexpr int kNW = 4;
-constexpr int kRBA = 2;     // row blocks per wave in pass A
-constexpr int kRBB = 2;     // row blocks per wave in pass B
-}  // namespace
-
-int rows_per_block_attention() { return 32 * kRBA * kNW; }
-int rows_per_block_page() { return 32 * kRBB * kNW; }
+int rows_per_block_attention() { return kRowsWG; }
+int rows_per_block_page() { return kRowsWG; }
+int token_mass_max_rows() { return kMassMaxRows; }
+int fixup_parts() { return kFixParts; }
 
 hipError_t launch_window_attention(const AttnGeom& a, const AttnSplit& sp, hipStream_t s) {
-  const int nrb = (a.rows + rows_per_block_attention() - 1) / rows_per_block_attention();
+  const int nrb = (a.rows + kRowsWG - 1) / kRowsWG;
   dim3 grid(sp.n_splits, nrb, a.Hkv), block(kNW * 64);
-  if (a.D == 128)
-    hipLaunchKernelGGL((window_attention_kernel<128, kRBA, kNW>), grid, block, 0, s, a, sp);
-  else
-    hipLaunchKernelGGL((window_attention_kernel<64, kRBA, kNW>), grid, block, 0, s, a, sp);
+  if (a.D == 128) hipLaunchKernelGGL((window_attention_kernel<128>), grid, block, 0, s, a, sp);
+  else hipLaunchKernelGGL((window_attention_kernel<64>), grid, block, 0, s, a, sp);
   return hipGetLastError();
 }
 
@@ -669,36 +939,40 @@ hipError_t launch_combine(const AttnGeom& a, const AttnSplit& sp, const RowStats
                           const ZeroList& zl, hipStream_t s) {
   const int waves = a.Hkv * a.rows;
   dim3 grid((waves + 3) / 4), block(256);
-  if (a.D == 128)
-    hipLaunchKernelGGL((combine_kernel<128>), grid, block, 0, s, a, sp, rs, lse_out, zl);
-  else
-    hipLaunchKernelGGL((combine_kernel<64>), grid, block, 0, s, a, sp, rs, lse_out, zl);
+  if (a.D == 128) hipLaunchKernelGGL((combine_kernel<128>), grid, block, 0, s, a, sp, rs, lse_out, zl);
+  else hipLaunchKernelGGL((combine_kernel<64>), grid, block, 0, s, a, sp, rs, lse_out, zl);
   return hipGetLastError();
 }
 
 hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowStats& rs, int mode,
                               hipStream_t s) {
-  const int nrb = (a.rows + rows_per_block_page() - 1) / rows_per_block_page();
+  const int nrb = (a.rows + kRowsWG - 1) / kRowsWG;
   const int nblk = (pw.n_items + pw.items_per_block - 1) / pw.items_per_block;
   if (nblk == 0) return hipSuccess;
   dim3 grid(nblk, nrb, a.Hkv), block(kNW * 64);
   if (a.D == 128) {
-    if (mode == 0) hipLaunchKernelGGL((page_kernel<128, kRBB, kNW, 0>), grid, block, 0, s, a, pw, rs);
-    else hipLaunchKernelGGL((page_kernel<128, kRBB, kNW, 1>), grid, block, 0, s, a, pw, rs);
+    if (mode == 0) hipLaunchKernelGGL((page_kernel<128, 0>), grid, block, 0, s, a, pw, rs);
+    else hipLaunchKernelGGL((page_kernel<128, 1>), grid, block, 0, s, a, pw, rs);
   } else {
-    if (mode == 0) hipLaunchKernelGGL((page_kernel<64, kRBB, kNW, 0>), grid, block, 0, s, a, pw, rs);
-    else hipLaunchKernelGGL((page_kernel<64, kRBB, kNW, 1>), grid, block, 0, s, a, pw, rs);
+    if (mode == 0) hipLaunchKernelGGL((page_kernel<64, 0>), grid, block, 0, s, a, pw, rs);
+    else hipLaunchKernelGGL((page_kernel<64, 1>), grid, block, 0, s, a, pw, rs);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
+                             const PageWork& pw, hipStream_t s) {
+  dim3 grid(std::min(pw.fix_cap, 256), kFixParts), block(256);
+  if (a.D == 128) hipLaunchKernelGGL((page_fixup_kernel<128>), grid, block, 0, s, a, sp, rs, pw);
+  else hipLaunchKernelGGL((page_fixup_kernel<64>), grid, block, 0, s, a, sp, rs, pw);
   return hipGetLastError();
 }
 
 hipError_t launch_token_mass(const AttnGeom& a, const RowStats& rs, float* mass, int chunk,
                              hipStream_t s) {
   dim3 grid((a.S + chunk - 1) / chunk, a.Hkv), block(kNW * 64);
-  if (a.D == 128)
-    hipLaunchKernelGGL((token_mass_kernel<128, kNW>), grid, block, 0, s, a, rs, mass, chunk);
-  else
-    hipLaunchKernelGGL((token_mass_kernel<64, kNW>), grid, block, 0, s, a, rs, mass, chunk);
+  if (a.D == 128) hipLaunchKernelGGL((token_mass_kernel<128>), grid, block, 0, s, a, rs, mass, chunk);
+  else hipLaunchKernelGGL((token_mass_kernel<64>), grid, block, 0, s, a, rs, mass, chunk);
   return hipGetLastError();
 }
 

@@ -128,3 +128,41 @@ def test_deterministic(ckv):
     a = _measure(P, ctx, dl, "post")
     b = _measure(P, ctx, dl, "post")
     assert np.array_equal(a["R"], b["R"]) and np.array_equal(a["o"], b["o"])
+
+
+@pytest.mark.parametrize("which", ["single_heavy", "two_heavy_straddling"])
+def test_dominant_page(ckv, which):
+    """Pages that hold nearly all of a row's attention mass (A -> 1): the
+    closed form of Eq. (6) cancels there; the library recomputes such rows
+    without the page and must still meet the score tolerance."""
+    P, ctx = ckv
+    w = scaled("tiny", n_tokens=2048, n_q_heads=4, n_kv_heads=1)
+    L = make_layer(w, seed=7)
+    from synth import bf16_bits, bf16_bits_to_f32
+    k = bf16_bits_to_f32(L.k).copy()
+    q = bf16_bits_to_f32(L.q_post)
+    qdir = q[:, :, :].mean(axis=(0, 1))
+    qdir /= np.linalg.norm(qdir)
+    if which == "single_heavy":
+        st = int(L.layout.page_start[len(L.pages) // 2])
+        k[0, st + 3] = qdir * 60.0          # logit ~ 60/8 * |q| per row: dominant
+    else:
+        # page straddling a 64-token boundary, two heavy tokens inside it
+        j = int(np.argmin(np.abs((L.layout.page_start % 64) - 56)))
+        st = int(L.layout.page_start[j])
+        k[0, st + 2] = qdir * 55.0
+        k[0, st + 9] = qdir * 52.0
+    L.k = bf16_bits(k)
+    dl = LayerOnDevice(L)
+    got = _measure(P, ctx, dl, "post")
+    R, Rh = O.page_effects(L.k, L.v, L.pos, L.q_post, L.qpos_post, L.pages, method="closed")
+    # the oracle confirms the page is dominant for some rows
+    import math
+    K, V, Q = O.as_f64(L.k), O.as_f64(L.v), O.as_f64(L.q_post)
+    s = O.head_logits(Q[0], K[0], 1 / math.sqrt(64))
+    a, _ = O.attend(s, O.visibility(L.pos, L.qpos_post), V[0])
+    page = [p for p in L.pages if p[0] <= st < p[0] + p[1]][0]
+    A = a[:, page[0]:page[0] + page[1]].sum(1)
+    assert A.max() > 0.999
+    assert_scores_close(got["R"], R, "R")
+    assert_scores_close(got["R_head"], Rh, "R_head")
