@@ -630,7 +630,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   Plan plan;
   plan.add(&rs.lse2, total_rows);
   plan.add(&rs.onorm, total_rows);
-  plan.add(&rs.nvis, total_rows);
+  plan.add(&rs.nvis, a.W);
   plan.add(&resid, (size_t)max_cand * total_rows * D);
   plan.add(&resA, (size_t)max_cand * total_rows);
   plan.add(&resC, (size_t)max_cand * total_rows);
@@ -651,14 +651,18 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   j.onorm = rs.onorm;
   j.nvis = rs.nvis;
 
-  CKV_LAUNCH(c, "joint_prepare", launch_joint_prepare(a, o, lse, rs, j, c->stream));
   // the number of candidates bounds the rounds: read it once
   int32_t n_eff = 0;
   if (pages->n_pages > 0) {
     if ((rc = read_device_int(c, n_cand, 0, &n_eff, true))) return rc;
     n_eff = std::max(0, std::min(n_eff, max_cand));
   }
-  if (n_eff > 0) {
+  if (n_eff == 0) {
+    CKV_LAUNCH(c, "joint_prepare", launch_joint_init(j, c->stream));
+    return CKV_OK;
+  }
+  CKV_LAUNCH(c, "joint_prepare", launch_joint_prepare(a, o, lse, rs, j, c->stream));
+  {
     PageWork pw{};
     pw.start = dstart;
     pw.len = dlen;

@@ -111,7 +111,7 @@ struct JointArgs {
   const float* resA;      // [max_cand][rows]
   const int* resC;
   const float* onorm;     // [rows]
-  const int* nvis;        // [rows]
+  const int* nvis;        // [W]: visible tokens of window row p
   float* Dstate;          // [rows][D] accumulated residual of accepted pages
   float* Astate;          // [rows]
   int* Cstate;            // [rows]
@@ -127,7 +127,7 @@ struct JointArgs {
 hipError_t launch_joint_prepare(const AttnGeom& a, const float* o, const float* lse, RowStats rs,
                                 const JointArgs& j, hipStream_t s);
 hipError_t launch_joint_round(const JointArgs& j, hipStream_t s);
-hipError_t launch_joint_finish(const JointArgs& j, hipStream_t s);
+hipError_t launch_joint_init(const JointArgs& j, hipStream_t s);
 
 // checkpoint: protection, selection, compaction (Eq. (12)-(13), Eq. (4))
 struct SelectArgs {

@@ -19,26 +19,28 @@ namespace {
 constexpr int kCT = 256;
 }
 
+// 16 lanes cooperate on one page: lane j of the group compares against pages
+// j, j + 16, ...; the counts are summed with shuffles.
+constexpr int kLanes = 16;
+constexpr int kPagesPerBlock = kCT / kLanes;
+
 __global__ __launch_bounds__(kCT) void rank_kernel(ClassifyArgs c) {
-  __shared__ float s_pre[kCT], s_post[kCT];
-  const int i = blockIdx.x * kCT + threadIdx.x;
+  const int i = blockIdx.x * kPagesPerBlock + threadIdx.x / kLanes;
+  const int sub = threadIdx.x % kLanes;
   const bool act = i < c.n;
   const float rp = act ? c.R_pre[i] : 0.f;
   const float rq = act ? c.R_post[i] : 0.f;
   int less_pre = 0, less_post = 0;
-  for (int j0 = 0; j0 < c.n; j0 += kCT) {
-    const int j = j0 + threadIdx.x;
-    __syncthreads();
-    s_pre[threadIdx.x] = j < c.n ? c.R_pre[j] : 0.f;
-    s_post[threadIdx.x] = j < c.n ? c.R_post[j] : 0.f;
-    __syncthreads();
-    const int m = min(kCT, c.n - j0);
-    for (int t = 0; t < m; ++t) {
-      less_pre += s_pre[t] < rp ? 1 : 0;
-      less_post += s_post[t] < rq ? 1 : 0;
-    }
+  for (int j = sub; j < c.n; j += kLanes) {
+    less_pre += c.R_pre[j] < rp ? 1 : 0;
+    less_post += c.R_post[j] < rq ? 1 : 0;
   }
-  if (!act) return;
+#pragma unroll
+  for (int off = kLanes / 2; off >= 1; off >>= 1) {
+    less_pre += __shfl_xor(less_pre, off, 64);
+    less_post += __shfl_xor(less_post, off, 64);
+  }
+  if (!act || sub != 0) return;
   const double den = c.n > 1 ? (double)(c.n - 1) : 1.0;
   const double Pm = c.n > 1 ? less_pre / den : 0.5;
   const double Pp = c.n > 1 ? less_post / den : 0.5;
@@ -67,35 +69,30 @@ __device__ __forceinline__ bool precedes(float qj, float pj, int j, float qi, fl
 }
 
 __global__ __launch_bounds__(kCT) void order_kernel(ClassifyArgs c) {
-  __shared__ float s_pre[kCT], s_post[kCT];
-  __shared__ uint8_t s_c[kCT];
-  const int i = blockIdx.x * kCT + threadIdx.x;
+  const int i = blockIdx.x * kPagesPerBlock + threadIdx.x / kLanes;
+  const int sub = threadIdx.x % kLanes;
   const bool act = i < c.n;
   const bool me = act && c.is_cand[i];
   const float rp = act ? c.R_pre[i] : 0.f;
   const float rq = act ? c.R_post[i] : 0.f;
   int before = 0, total = 0;
-  for (int j0 = 0; j0 < c.n; j0 += kCT) {
-    const int j = j0 + threadIdx.x;
-    __syncthreads();
-    s_pre[threadIdx.x] = j < c.n ? c.R_pre[j] : 0.f;
-    s_post[threadIdx.x] = j < c.n ? c.R_post[j] : 0.f;
-    s_c[threadIdx.x] = j < c.n ? c.is_cand[j] : 0;
-    __syncthreads();
-    const int m = min(kCT, c.n - j0);
-    for (int t = 0; t < m; ++t) {
-      if (!s_c[t]) continue;
-      ++total;
-      before += precedes(s_post[t], s_pre[t], j0 + t, rq, rp, i) ? 1 : 0;
-    }
+  for (int j = sub; j < c.n; j += kLanes) {
+    if (!c.is_cand[j]) continue;
+    ++total;
+    before += precedes(c.R_post[j], c.R_pre[j], j, rq, rp, i) ? 1 : 0;
+  }
+#pragma unroll
+  for (int off = kLanes / 2; off >= 1; off >>= 1) {
+    before += __shfl_xor(before, off, 64);
+    total += __shfl_xor(total, off, 64);
   }
   const int cap = c.max_cand > 0 ? min(c.max_cand, c.n) : c.n;
-  if (me && before < cap) c.cand[before] = i;
+  if (me && sub == 0 && before < cap) c.cand[before] = i;
   if (blockIdx.x == 0 && threadIdx.x == 0) *c.n_cand = min(total, cap);
 }
 
 hipError_t launch_classify(const ClassifyArgs& c, hipStream_t s) {
-  const int nb = c.n > 0 ? (c.n + kCT - 1) / kCT : 1;
+  const int nb = c.n > 0 ? (c.n + kPagesPerBlock - 1) / kPagesPerBlock : 1;
   hipLaunchKernelGGL(rank_kernel, dim3(nb), dim3(kCT), 0, s, c);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -39,6 +39,7 @@ __global__ __launch_bounds__(256) void joint_prep_rows(AttnGeom a, const float* 
     if (j.union_R) j.union_R[i] = __builtin_nanf("");
   }
   for (size_t i = gid; i < (size_t)j.window; i += gsz) j.rbuf[i] = 0u;
+  for (size_t i = gid; i < (size_t)j.W; i += gsz) rs.nvis[i] = 0;
   if (gid == 0) {
     j.ctrl[kCursor] = 0;
     j.ctrl[kPending] = -1;
@@ -62,21 +63,32 @@ __global__ __launch_bounds__(256) void joint_prep_rows(AttnGeom a, const float* 
   }
 }
 
-// n_vis of window row p (shared by every query head): #{i : pos[i] <= qpos[p]}
+// n_vis of window row p (shared by every query head): #{i : pos[i] <= qpos[p]},
+// counted over a (row, token slice) grid; rs.nvis holds one count per row p
+// and is zeroed by joint_prep_rows.
+constexpr int kVisSlice = 8192;
+
 __global__ __launch_bounds__(256) void joint_prep_vis(AttnGeom a, RowStats rs) {
   __shared__ int part[4];
   const int p = blockIdx.x;
   const int qp = a.qpos[p];
+  const int t0 = blockIdx.y * kVisSlice, t1 = min(a.S, t0 + kVisSlice);
   int c = 0;
-  for (int i = threadIdx.x; i < a.S; i += 256) c += a.pos[i] <= qp ? 1 : 0;
+  for (int i = t0 + threadIdx.x; i < t1; i += 256) c += a.pos[i] <= qp ? 1 : 0;
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off, 64);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = c;
   __syncthreads();
-  if (threadIdx.x < a.Hq) {
-    const int tot = part[0] + part[1] + part[2] + part[3];
-    for (int h = threadIdx.x; h < a.Hq; h += 256) rs.nvis[h * a.W + p] = tot;
+  if (threadIdx.x == 0) atomicAdd(&rs.nvis[p], part[0] + part[1] + part[2] + part[3]);
+}
+
+// outputs when there is no candidate to test
+__global__ __launch_bounds__(256) void joint_init_outputs(JointArgs j) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < j.max_cand; i += gridDim.x * 256) {
+    j.accepted[i] = 0;
+    if (j.union_R) j.union_R[i] = __builtin_nanf("");
   }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *j.n_accepted = 0;
 }
 
 hipError_t launch_joint_prepare(const AttnGeom& a, const float* o, const float* lse, RowStats rs,
@@ -84,7 +96,12 @@ hipError_t launch_joint_prepare(const AttnGeom& a, const float* o, const float* 
   hipLaunchKernelGGL(joint_prep_rows, dim3((j.total_rows + 3) / 4), dim3(256), 0, s, a, o, lse, rs, j);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(joint_prep_vis, dim3(a.W), dim3(256), 0, s, a, rs);
+  hipLaunchKernelGGL(joint_prep_vis, dim3(a.W, (a.S + kVisSlice - 1) / kVisSlice), dim3(256), 0, s, a, rs);
+  return hipGetLastError();
+}
+
+hipError_t launch_joint_init(const JointArgs& j, hipStream_t s) {
+  hipLaunchKernelGGL(joint_init_outputs, dim3((j.max_cand + 255) / 256), dim3(256), 0, s, j);
   return hipGetLastError();
 }
 
@@ -151,7 +168,7 @@ __global__ __launch_bounds__(256) void joint_round_kernel(JointArgs j, RowStats 
     if (Ct > 0) {
       const float keep = 1.f - At;
       const float on = rs.onorm[row];
-      if (Ct >= rs.nvis[row] || !(keep > 0.f)) ratio = INFINITY;
+      if (Ct >= rs.nvis[row % j.W] || !(keep > 0.f)) ratio = INFINITY;
       else if (on > 0.f) ratio = sqrtf(n2) / (keep * on);
       else ratio = n2 > 0.f ? INFINITY : 0.f;
     }
@@ -201,6 +218,5 @@ hipError_t launch_joint_round(const JointArgs& j, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_joint_finish(const JointArgs&, hipStream_t) { return hipSuccess; }
 
 }  // namespace ckv

@@ -403,14 +403,25 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
 #pragma unroll
   for (int j = 0; j < D / 64; ++j) acc[j] = 0.f;
   if (M != -INFINITY) {
-    for (int s = 0; s < sp.n_splits; ++s) {
-      const size_t idx = (size_t)(g * sp.n_splits + s) * sp.rows_pad + row;
-      const float ms = sp.part_m[idx];
-      if (ms == -INFINITY) continue;
-      const float w = __builtin_amdgcn_exp2f(ms - M);
-      wsum += sp.part_l[idx] * w;
+    // eight splits' loads in flight at a time
+    for (int s0 = 0; s0 < sp.n_splits; s0 += 8) {
+      float ms[8], ls[8], os[8][D / 64];
 #pragma unroll
-      for (int j = 0; j < D / 64; ++j) acc[j] += sp.part_o[idx * D + lane + 64 * j] * w;
+      for (int u = 0; u < 8; ++u) {
+        const int s = min(s0 + u, sp.n_splits - 1);
+        const size_t idx = (size_t)(g * sp.n_splits + s) * sp.rows_pad + row;
+        ms[u] = s0 + u < sp.n_splits ? sp.part_m[idx] : -INFINITY;
+        ls[u] = sp.part_l[idx];
+#pragma unroll
+        for (int j = 0; j < D / 64; ++j) os[u][j] = sp.part_o[idx * D + lane + 64 * j];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float w = ms[u] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms[u] - M);
+        wsum += ls[u] * w;
+#pragma unroll
+        for (int j = 0; j < D / 64; ++j) acc[j] += os[u][j] * w;
+      }
     }
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
@@ -481,7 +492,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   }
   const float lse2 = ri.ok ? rs.lse2[ri.rg] : -INFINITY;
   const float onorm = ri.ok ? rs.onorm[ri.rg] : 0.f;
-  const int nvis = ri.ok ? rs.nvis[ri.rg] : 0;
+  const int nvis = (MODE == 0 && ri.ok) ? rs.nvis[ri.rg] : 0;   // read by MODE 0 only
   const int row0 = rblk * kRowsWG;
   const int head0 = row0 / a.W;
   const int n_heads_blk = min(a.group, (min(a.rows, row0 + kRowsWG) - 1) / a.W + 1) - head0;
@@ -835,22 +846,23 @@ __global__ __launch_bounds__(256) void page_fixup_kernel(AttnGeom a, AttnSplit s
 // ---------------------------------------------------------------------------
 // C. window-attention mass of every token: max_h sum_p a_hpi
 //
-// Workgroup (token chunk, KV head g); wave w handles the query heads
-// w, w + 8, ... of the group, each over all its window rows, so a head's sum
-// is accumulated in one wave in a fixed order (deterministic).  The scores
-// use the C = Q K^T orientation (tokens on lanes, rows in registers), so the
-// sum over rows is lane-local.
+// Workgroup (token chunk, KV head g).  A (query head, 32-row block) pair is
+// one wave's unit of work: its scores use the C = Q K^T orientation (tokens
+// on lanes, rows in registers), so the sum over the block's rows is
+// lane-local.  Pair sums go to LDS; a query head's rows are then added in a
+// fixed block order (deterministic) and the max over heads is taken.
 // ---------------------------------------------------------------------------
 constexpr int kMassMaxRows = 2048;   // window rows per KV head the mass kernel supports
+constexpr int kMassMaxPairs = kMassMaxRows / 32;
 
 template <int D>
 __global__ __launch_bounds__(kNW * 64) void token_mass_kernel(AttnGeom a, RowStats rs, float* mass,
                                                               int chunk) {
   constexpr int NT = kNW * 64, KS = D / 16;
-  constexpr int KP = D + 8, CPR = D / 8, KCH = kTile * CPR;
-  __shared__ __align__(16) uint16_t sK[kTile * KP];
-  __shared__ int sP[kTile];
-  __shared__ unsigned int sM[kTile];
+  constexpr int KP = D + 8, CPR = D / 8, KCH = kTile * CPR, KPT = (KCH + NT - 1) / NT;
+  __shared__ __align__(16) uint16_t sK[2][kTile * KP];
+  __shared__ int sP[2][kTile];
+  __shared__ float sPart[kMassMaxPairs][kTile];
   __shared__ float sL2[kMassMaxRows];
   __shared__ int sQP[kMassMaxRows];
   const int g = blockIdx.y;
@@ -861,60 +873,84 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_kernel(AttnGeom a, RowSta
   if (t_begin >= t_end) return;
   const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
   const int nrb = (a.W + 31) / 32;
-  // per-row log-sum-exp and window position of this KV head's rows
+  const int n_pairs = a.group * nrb;
   for (int r = tid; r < a.rows; r += NT) {
     sL2[r] = rs.lse2[g * a.rows + r];
     sQP[r] = a.qpos[r % a.W];
   }
-  for (int t0 = t_begin; t0 < t_end; t0 += kTile) {
+  u32x4 kr[KPT];
+  int pr = INT_MAX;
+  auto issue = [&](int t0) {
     const int nv = min(kTile, t_end - t0);
-    for (int c = tid; c < KCH; c += NT) {
-      const int tr = c / CPR, cc = c % CPR;
-      *reinterpret_cast<uint4*>(&sK[tr * KP + cc * 8]) =
-          tr < nv ? *reinterpret_cast<const uint4*>(kh + (int64_t)(t0 + tr) * a.kv_tok_stride + cc * 8)
-                  : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + i * NT;
+      const int tr = (c / CPR) & (kTile - 1);
+      const bool ok = c < KCH && tr < nv;
+      const u32x4 v = ldg_u4(kh + (int64_t)(ok ? t0 + tr : 0) * a.kv_tok_stride + (c % CPR) * 8);
+      kr[i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
     }
-    if (tid < kTile) {
-      sP[tid] = tid < nv ? a.pos[t0 + tid] : INT_MAX;
-      sM[tid] = 0u;
+    const bool okp = tid < nv;
+    const int pv = ldg_i32(a.pos + (okp ? t0 + tid : 0));
+    pr = okp ? pv : INT_MAX;
+  };
+  auto commit = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + i * NT;
+      if (c < KCH) *reinterpret_cast<u32x4*>(&sK[b][(c / CPR) * KP + (c % CPR) * 8]) = kr[i];
     }
-    __syncthreads();
-    for (int hl = wave; hl < a.group; hl += kNW) {
+    if (tid < kTile) sP[b][tid] = pr;
+  };
+  const int n_tiles = (t_end - t_begin + kTile - 1) / kTile;
+  issue(t_begin);
+  commit(0);
+  __syncthreads();
+  for (int it = 0; it < n_tiles; ++it) {
+    const int b = it & 1;
+    const int t0 = t_begin + it * kTile;
+    if (it + 1 < n_tiles) issue(t0 + kTile);
+    for (int pi = wave; pi < n_pairs; pi += kNW) {
+      const int hl = pi / nrb, rb = pi % nrb;
       const int h = g * a.group + hl;
-      float msum[2] = {0.f, 0.f};
-      for (int rb = 0; rb < nrb; ++rb) {
-        const int prow = 32 * rb + col;          // A operand row of this lane
-        const bool aok = prow < a.W;
-        const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)(aok ? prow : 0) * a.q_row_stride;
-        bf16x8 qa[KS];
+      const int prow = 32 * rb + col;          // A operand row of this lane
+      const bool aok = prow < a.W;
+      const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)(aok ? prow : 0) * a.q_row_stride;
+      bf16x8 qa[KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) qa[ks] = aok ? load_bf16x8(qrow + 16 * ks + 8 * half) : zero_bf16x8();
-#pragma unroll
-        for (int tb = 0; tb < 2; ++tb) {
-          f32x16 acc = zero16();
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks)
-            acc = mfma_bf16(qa[ks], load_bf16x8(&sK[(32 * tb + col) * KP + 16 * ks + 8 * half]), acc);
-          const int pt = sP[32 * tb + col];
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int p = 32 * rb + 8 * (r >> 2) + 4 * half + (r & 3);
-            if (p < a.W) {
-              const int row = hl * a.W + p;
-              const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[r], a.sl2, -sL2[row]));
-              msum[tb] += pt <= sQP[row] ? e : 0.f;
-            }
-          }
-        }
-      }
+      for (int ks = 0; ks < KS; ++ks) qa[ks] = aok ? load_bf16x8(qrow + 16 * ks + 8 * half) : zero_bf16x8();
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb) {
-        const float s = msum[tb] + xor32(msum[tb]);
-        if (half == 0) atomicMax(&sM[32 * tb + col], __float_as_uint(s));
+        f32x16 acc = zero16();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          acc = mfma_bf16(qa[ks], load_bf16x8(&sK[b][(32 * tb + col) * KP + 16 * ks + 8 * half]), acc);
+        const int pt = sP[b][32 * tb + col];
+        float msum = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int p = 32 * rb + 8 * (r >> 2) + 4 * half + (r & 3);
+          if (p < a.W) {
+            const int row = hl * a.W + p;
+            const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[r], a.sl2, -sL2[row]));
+            msum += pt <= sQP[row] ? e : 0.f;
+          }
+        }
+        msum += xor32(msum);
+        if (half == 0) sPart[pi][32 * tb + col] = msum;
       }
     }
+    if (it + 1 < n_tiles) commit(b ^ 1);
     __syncthreads();
-    if (tid < nv) atomic_max_nonneg(&mass[t0 + tid], __uint_as_float(sM[tid]));
+    if (tid < kTile && t0 + tid < t_end) {
+      float best = 0.f;
+      for (int hl = 0; hl < a.group; ++hl) {
+        float sum = 0.f;
+        for (int rb = 0; rb < nrb; ++rb) sum += sPart[hl * nrb + rb][tid];
+        best = fmaxf(best, sum);
+      }
+      atomic_max_nonneg(&mass[t0 + tid], best);
+    }
     __syncthreads();
   }
 }

@@ -62,6 +62,26 @@ __global__ __launch_bounds__(256) void protect_kernel(SelectArgs a) {
   }
 }
 
+// Histogram increment with lanes of a wave that share a bin combined into
+// one atomic: the leading key bytes of float scores take few values, and
+// plain LDS atomics on one address serialise.  After a few combining rounds
+// the remaining (spread) bins use plain atomics.
+__device__ __forceinline__ void hist_add(unsigned int* hist, uint32_t bin, bool act) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int round = 0; round < 4; ++round) {
+    const unsigned long long m = __ballot(act);
+    if (m == 0ull) return;
+    const int leader = __ffsll((long long)m) - 1;
+    const uint32_t lb = __shfl((int)bin, leader, 64);
+    const bool same = act && bin == lb;
+    const unsigned long long sm = __ballot(same);
+    if (lane == leader) atomicAdd(&hist[lb], (unsigned int)__popcll(sm));
+    if (same) act = false;
+  }
+  if (act) atomicAdd(&hist[bin], 1u);
+}
+
 // block-wide exclusive scan of one int per thread (kST threads)
 __device__ int block_exclusive_scan(int v, int* tmp, int& total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -142,10 +162,16 @@ __global__ __launch_bounds__(kST) void select_kernel(SelectArgs a) {
       for (int i = tid; i < 256; i += kST) hist[i] = 0u;
       __syncthreads();
       const unsigned int prefix = s_prefix, mask = s_mask;
-      for (int t = tid; t < S; t += kST) {
-        if (st[t] != kFree) continue;
-        const uint32_t key = score_key(sc[t]);
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      for (int t0 = 0; t0 < S; t0 += kST) {
+        const int t = t0 + tid;
+        bool act = false;
+        uint32_t bin = 0;
+        if (t < S && st[t] == kFree) {
+          const uint32_t key = score_key(sc[t]);
+          act = (key & mask) == prefix;
+          bin = (key >> shift) & 255u;
+        }
+        hist_add(hist, bin, act);
       }
       __syncthreads();
       if (tid == 0) {
@@ -165,52 +191,58 @@ __global__ __launch_bounds__(kST) void select_kernel(SelectArgs a) {
   const uint32_t T = s_prefix;
   const int need_eq = s_need;     // how many tokens with key == T to keep
 
-  // contiguous chunk per thread for the ordered passes
-  const int C = (S + kST - 1) / kST;
-  const int c0 = min(S, tid * C), c1 = min(S, c0 + C);
-  int eq = 0;
-  if (k > 0 && !take_all)
-    for (int t = c0; t < c1; ++t) eq += (st[t] == kFree && score_key(sc[t]) == T) ? 1 : 0;
-  int eq_tot;
-  int eq_before = block_exclusive_scan(eq, tmp, eq_tot);
-  int keepc = 0;
-  {
-    int e = eq_before;
-    for (int t = c0; t < c1; ++t) {
-      const uint8_t x = st[t];
-      bool keep = x == kProt;
-      if (x == kFree && k > 0) {
-        if (take_all) keep = true;
-        else {
-          const uint32_t key = score_key(sc[t]);
-          if (key > T) keep = true;
-          else if (key == T) { keep = e < need_eq; ++e; }
-        }
-      }
-      keepc += keep ? 1 : 0;
-    }
-  }
-  int n_keep;
-  int out = block_exclusive_scan(keepc, tmp, n_keep);
+  // One ordered sweep in blocks of kST tokens (one per thread, coalesced):
+  // a free token with key == T is kept while fewer than need_eq such tokens
+  // precede it; kept tokens are written in ascending order.  Prefix counts
+  // inside a wave come from ballots, across the 16 waves from LDS.
   int32_t* kept = a.kept + (size_t)s * a.budget;
-  {
-    int e = eq_before;
-    for (int t = c0; t < c1; ++t) {
+  const int lane = tid & 63, w = tid >> 6;
+  const unsigned long long lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int eq_run = 0, out_run = 0;
+  for (int t0 = 0; t0 < S; t0 += kST) {
+    const int t = t0 + tid;
+    bool prot = false, free_gt = false, free_eq = false;
+    if (t < S) {
       const uint8_t x = st[t];
-      bool keep = x == kProt;
+      prot = x == kProt;
       if (x == kFree && k > 0) {
-        if (take_all) keep = true;
+        if (take_all) free_gt = true;
         else {
           const uint32_t key = score_key(sc[t]);
-          if (key > T) keep = true;
-          else if (key == T) { keep = e < need_eq; ++e; }
+          free_gt = key > T;
+          free_eq = key == T;
         }
       }
-      if (keep) kept[out++] = t;
     }
+    // rank of this token among the block's key == T tokens
+    const unsigned long long me = __ballot(free_eq);
+    if (lane == 0) tmp[w] = __popcll(me);
+    __syncthreads();
+    int wbase = 0, btot = 0;
+    for (int i = 0; i < kST / 64; ++i) {
+      const int c = tmp[i];
+      wbase += i < w ? c : 0;
+      btot += c;
+    }
+    const int eq_rank = eq_run + wbase + __popcll(me & lt_mask);
+    eq_run += btot;
+    const bool keep = prot || free_gt || (free_eq && eq_rank < need_eq);
+    __syncthreads();
+    const unsigned long long km = __ballot(keep);
+    if (lane == 0) tmp[w] = __popcll(km);
+    __syncthreads();
+    int kbase = 0, ktot = 0;
+    for (int i = 0; i < kST / 64; ++i) {
+      const int c = tmp[i];
+      kbase += i < w ? c : 0;
+      ktot += c;
+    }
+    if (keep) kept[out_run + kbase + __popcll(km & lt_mask)] = t;
+    out_run += ktot;
+    __syncthreads();
   }
-  for (int j = n_keep + tid; j < a.budget; j += kST) kept[j] = -1;
-  if (tid == 0) a.n_kept[s] = n_keep;
+  for (int j = out_run + tid; j < a.budget; j += kST) kept[j] = -1;
+  if (tid == 0) a.n_kept[s] = out_run;
 }
 
 hipError_t launch_protect(const SelectArgs& a, hipStream_t s) {
