@@ -22,7 +22,7 @@ The deletion effect is defined by brute force (``page_effects_bruteforce``):
 attention is run again with the page masked out.  ``page_effects_closed_form``
 evaluates Eq. (6) instead; both are kept so that one pins the other.
 
-Readings taken where the paper is silent (each also listed in the design doc):
+Readings taken where the paper is silent:
 
 * R1  softmax scale 1/sqrt(d); inputs are post-RoPE keys and queries.
 * R2  grouped-query attention: query head h reads KV head h // (Hq/Hkv);

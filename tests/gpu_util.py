@@ -39,8 +39,10 @@ def assert_scores_close(got, want, what="R", rel=REL_TOL, floor=ABS_FLOOR):
     err = np.abs(got[fin] - want[fin])
     lim = rel * np.maximum(want[fin], floor)
     bad = np.flatnonzero(err > lim)
+    rel_err = err / np.maximum(want[fin], floor)
+    if rel_err.size:
+        print(f"[parity] {what}: worst relative error {rel_err.max():.3g} over {rel_err.size} values", flush=True)
     if bad.size:
-        rel_err = err / np.maximum(want[fin], floor)
         i = int(np.argmax(rel_err))
         raise AssertionError(f"{what}: {bad.size}/{fin.sum()} outside {rel} relative; worst got "
                              f"{got[fin][i]!r} want {want[fin][i]!r} (rel {rel_err[i]:.3g})")
