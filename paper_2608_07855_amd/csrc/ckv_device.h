@@ -72,6 +72,15 @@ __device__ __forceinline__ int vt_slot(int t) {
   return (t & ~0xC) | ((t & 4) << 1) | ((t & 8) >> 1);
 }
 
+// Stored column of slot s in row r of the V^T tile: the 8-slot (16-byte)
+// group index is XOR-ed with bits 3..5 of the row.  A 16-byte read of eight
+// consecutive rows at one group then still covers all 32 banks, and the
+// transposing 4-byte writes of sixteen rows 8 apart (one 16-byte chunk of V
+// per lane) land in distinct groups instead of one bank.
+__device__ __forceinline__ int vt_col(int r, int s) {
+  return (((s >> 3) ^ (r >> 3)) & 7) << 3 | (s & 7);
+}
+
 // loads through the global address space (pointers inside by-value argument
 // structs otherwise compile to flat accesses)
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -86,6 +95,30 @@ __device__ __forceinline__ int ldg_i32(const void* p) {
 
 __device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, 64); }
 __device__ __forceinline__ int xor32i(int v) { return __shfl_xor(v, 32, 64); }
+
+// Both halves of a wave combined lane by lane (lane l with lane l ^ 32) in
+// one VALU op: v_permlane32_swap hands lanes 0-31 the upper half and lanes
+// 32-63 the lower half, so {lo, hi} below is {v[l % 32], v[l % 32 + 32]} in
+// every lane and the result is bit-identical in both halves.
+__device__ __forceinline__ void halves(float v, float& lo, float& hi) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  lo = __uint_as_float(r[0]);
+  hi = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum32(float v) {
+  float lo, hi;
+  halves(v, lo, hi);
+  return lo + hi;
+}
+__device__ __forceinline__ float max32(float v) {
+  float lo, hi;
+  halves(v, lo, hi);
+  return fmaxf(lo, hi);
+}
+__device__ __forceinline__ int sum32i(int v) {
+  const auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+  return (int)(r[0] + r[1]);
+}
 
 // bit pattern of a non-negative float (including +inf) keeps its order as uint
 __device__ __forceinline__ void atomic_max_nonneg(float* addr, float v) {

@@ -73,13 +73,13 @@ struct Stager {
     return s1 + off - 32;
   }
 
-  // Loads are unconditional (a token outside the segments reads token 0,
-  // which always exists) and the unwanted values are replaced by zero, so
-  // the staging registers never need a branch.
+  // Loads are unconditional: a token outside the segments reads token 0,
+  // which always exists.  Its key and value land in the tile as they are;
+  // the offset's position is INT_MAX, so every row masks its score to -inf
+  // and its weight is exactly 0 (values are finite).
   __device__ __forceinline__ void issue(const uint16_t* kh, const uint16_t* vh, int64_t ts,
                                         const int32_t* pos, int s0, int n0, int s1, int n1,
                                         int tid) {
-    const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * NT;
@@ -87,8 +87,7 @@ struct Stager {
       int t = tok((c / CPR) & (kTile - 1), s0, n0, s1, n1, ok);
       ok = ok && c < KCH;
       t = ok ? t : 0;
-      const u32x4 v = ldg_u4(kh + (int64_t)t * ts + (c % CPR) * 8);
-      kr[i] = ok ? v : z;
+      kr[i] = ldg_u4(kh + (int64_t)t * ts + (c % CPR) * 8);
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
@@ -100,8 +99,7 @@ struct Stager {
         int t = tok(2 * tp + j, s0, n0, s1, n1, ok);
         ok = ok && u < VU;
         t = ok ? t : 0;
-        const u32x4 v = ldg_u4(vh + (int64_t)t * ts + cg * 8);
-        vr[i][j] = ok ? v : z;
+        vr[i][j] = ldg_u4(vh + (int64_t)t * ts + cg * 8);
       }
     }
     bool ok = false;
@@ -112,7 +110,8 @@ struct Stager {
     pr = ok ? pv : INT_MAX;
   }
 
-  // writes the tile; wave 0 also flags whether every position is <= minq
+  // writes the tile; wave 0 also flags, per 32-token slot, whether every
+  // position is <= minq (sFull[0], sFull[1])
   __device__ __forceinline__ void commit(uint16_t* sK, _Float16* sV, int* sP, int* sFull, int minq,
                                          int tid) const {
 #pragma unroll
@@ -125,21 +124,25 @@ struct Stager {
       const int u = tid + i * NT;
       if (u < VU) {
         const int tp = u / CPR, cg = u % CPR;
-        const int slot = vt_slot(2 * tp);
+        // rows cg*8 .. cg*8+7 share bits 3..5, hence one stored column
+        const int col = vt_col(cg * 8, vt_slot(2 * tp));
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-          f16x2 w;
-          w[0] = (_Float16)bf16_bits_to_float(chunk_elem(vr[i][0], e));
-          w[1] = (_Float16)bf16_bits_to_float(chunk_elem(vr[i][1], e));
-          *reinterpret_cast<f16x2*>(sV + (cg * 8 + e) * VP + slot) = w;
+          typedef float f32x2 __attribute__((ext_vector_type(2)));
+          const f32x2 w = {bf16_bits_to_float(chunk_elem(vr[i][0], e)),
+                           bf16_bits_to_float(chunk_elem(vr[i][1], e))};
+          *reinterpret_cast<f16x2*>(sV + (cg * 8 + e) * VP + col) = __builtin_convertvector(w, f16x2);
         }
       }
     }
     if (tid < kTile) {
       sP[tid] = pr;
       const unsigned long long late = __ballot(pr > minq);
-      if (tid == 0) *sFull = late == 0ull;
+      if (tid == 0) {
+        sFull[0] = (late & 0xFFFFFFFFull) == 0ull;
+        sFull[1] = (late >> 32) == 0ull;
+      }
     }
   }
 };
@@ -232,8 +235,24 @@ __device__ __forceinline__ void pv_slot(const _Float16* sV, int tb, int col, int
   for (int u = 0; u < 2; ++u) {
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
-      const f16x8 af = *reinterpret_cast<const f16x8*>(sV + (32 * db + col) * VP + 32 * tb + 16 * u + 8 * half);
+      const int r = 32 * db + col;
+      const f16x8 af = *reinterpret_cast<const f16x8*>(sV + r * VP + vt_col(r, 32 * tb + 16 * u + 8 * half));
       acc[db] = mfma_f16(af, h[u], acc[db]);
+    }
+  }
+}
+
+// the same for the two width blocks db0, db0 + 1 only
+template <int D, int VP>
+__device__ __forceinline__ void pv_half(const _Float16* sV, int tb, int col, int half, const f16x8 (&h)[2],
+                                        int db0, f32x16 (&acc)[2]) {
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int r = 32 * (db0 + j) + col;
+      const f16x8 af = *reinterpret_cast<const f16x8*>(sV + r * VP + vt_col(r, 32 * tb + 16 * u + 8 * half));
+      acc[j] = mfma_f16(af, h[u], acc[j]);
     }
   }
 }
@@ -248,7 +267,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
   __shared__ __align__(16) uint16_t sK[2][kTile * St::KP];
   __shared__ __align__(16) _Float16 sV[2][D * St::VP];
   __shared__ __align__(16) int sP[2][kTile];
-  __shared__ int sFull[2];
+  __shared__ int sFull[2][2];
   __shared__ int sMin;
 
   const int g = blockIdx.z, split = blockIdx.x, rblk = blockIdx.y;
@@ -272,32 +291,20 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
   int cnt = 0;
 
   const int n_tiles = t_end > t_begin ? (t_end - t_begin + kTile - 1) / kTile : 0;
-  auto seg = [&](int t0, int& s0, int& n0, int& s1, int& n1) {
-    const int n = min(kTile, t_end - t0);
-    s0 = t0; n0 = min(32, n); s1 = t0 + 32; n1 = max(0, n - 32);
+  // Loads run two tiles ahead of the math: stager A holds even tiles, B odd
+  // ones; a tile past the end is an empty segment (its loads read token 0).
+  auto issue = [&](St& st, int it) {
+    const int t0 = t_begin + it * kTile;
+    const int n = it < n_tiles ? min(kTile, t_end - t0) : 0;
+    st.issue(kh, vh, a.kv_tok_stride, a.pos, t0, min(32, n), t0 + 32, max(0, n - 32), tid);
   };
-  St st;
-  if (n_tiles > 0) {
-    int s0, n0, s1, n1;
-    seg(t_begin, s0, n0, s1, n1);
-    st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, n0, s1, n1, tid);
-    st.commit(sK[0], sV[0], sP[0], &sFull[0], minq, tid);
-  }
-  __syncthreads();
-
-  for (int it = 0; it < n_tiles; ++it) {
-    const int b = it & 1;
-    if (it + 1 < n_tiles) {
-      int s0, n0, s1, n1;
-      seg(t_begin + (it + 1) * kTile, s0, n0, s1, n1);
-      st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, n0, s1, n1, tid);
-    }
+  auto compute = [&](int b) {
     if (wave_on) {
       f32x16 s[2];
       s[0] = scores<D, St::KP>(sK[b], 0, col, half, qf);
       s[1] = scores<D, St::KP>(sK[b], 1, col, half, qf);
       float mx = -INFINITY;
-      if (sFull[b]) {
+      if (sFull[b][0] && sFull[b][1]) {
         // every token of the tile is visible to every row of the workgroup
 #pragma unroll
         for (int tb = 0; tb < 2; ++tb)
@@ -321,7 +328,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
             }
           }
       }
-      mx = fmaxf(mx, xor32(mx)) * a.sl2;
+      mx = max32(mx) * a.sl2;
       // rescale the running output when a row max grew
       const bool need = mx > mref;
       if (__ballot(need) != 0ull) {
@@ -343,13 +350,27 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
       pv_slot<D, St::VP>(sV[b], 0, col, half, h[0], oacc);
       pv_slot<D, St::VP>(sV[b], 1, col, half, h[1], oacc);
     }
-    if (it + 1 < n_tiles) st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], &sFull[b ^ 1], minq, tid);
+  };
+  St stA, stB;
+  issue(stA, 0);
+  issue(stB, 1);
+  if (n_tiles > 0) stA.commit(sK[0], sV[0], sP[0], sFull[0], minq, tid);
+  __syncthreads();
+  for (int it = 0; it < n_tiles; it += 2) {
+    issue(stA, it + 2);
+    compute(0);
+    if (it + 1 < n_tiles) stB.commit(sK[1], sV[1], sP[1], sFull[1], minq, tid);
+    __syncthreads();
+    if (it + 1 >= n_tiles) break;
+    issue(stB, it + 3);
+    compute(1);
+    if (it + 2 < n_tiles) stA.commit(sK[0], sV[0], sP[0], sFull[0], minq, tid);
     __syncthreads();
   }
 
   // partial results of this split (m in log2 units, output relative to it)
-  const float lt = l + xor32(l);
-  const int ct = cnt + xor32i(cnt);
+  const float lt = sum32(l);
+  const int ct = sum32i(cnt);
   if (!ri.ok) return;
   const size_t idx = ((size_t)(g * sp.n_splits + split) * sp.rows_pad + ri.row);
   if (half == 0) {
@@ -458,8 +479,9 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   __shared__ __align__(16) uint16_t sK[2][kTile * St::KP];
   __shared__ __align__(16) _Float16 sV[2][D * St::VP];
   __shared__ __align__(16) int sP[2][kTile];
-  __shared__ int sFull[2];
+  __shared__ int sFull[2][2];
   __shared__ unsigned int sMax[2][2][NH];   // [buffer][page of the tile][local head]
+  __shared__ int sMin;
 
   const int g = blockIdx.z, rblk = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -474,6 +496,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
 
   const RowInfo ri = row_info(a, g, rblk * kRowsWG + wave * 32 + col);
   const bool wave_on = __ballot(ri.ok) != 0ull;
+  const int minq = block_min_qpos(ri, &sMin);
   bf16x8 qf[KS];
   load_q<D>(a, g, ri, half, qf);
   // o_p in accumulator layout: register r of block db holds width 32db + 8(r/4) + 4h + r%4
@@ -497,6 +520,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   const int head0 = row0 / a.W;
   const int n_heads_blk = min(a.group, (min(a.rows, row0 + kRowsWG) - 1) / a.W + 1) - head0;
   const bool wave_one_head = (a.W % 32) == 0;   // the 32 rows of a wave share one head
+  const int my_hl = ri.ok ? ri.row / a.W - head0 : 0;   // this row's head inside the block
   if (MODE == 0)
     for (int i = tid; i < 2 * 2 * NH; i += NT) (&sMax[0][0][0])[i] = 0u;
 
@@ -508,165 +532,189 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   auto tile_items = [&](int it) {
     return (it + 1 < i_end && plen(it) <= 32 && plen(it + 1) <= 32) ? 2 : 1;
   };
-  St st;
-  auto issue_tile = [&](int it) {
+  // Loads run two tiles ahead of the math (stager A: even tiles, B: odd);
+  // a tile that starts at or past i_end is an empty segment.
+  auto issue_tile = [&](St& st, int it) {
+    if (it >= i_end) {
+      st.issue(kh, vh, a.kv_tok_stride, a.pos, 0, 0, 0, 0, tid);
+      return;
+    }
     const int s0 = pstart(it), l0 = plen(it);
     if (tile_items(it) == 2)
       st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, l0, pstart(it + 1), plen(it + 1), tid);
     else
       st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, min(l0, 32), s0 + 32, max(0, l0 - 32), tid);
   };
-  issue_tile(i_begin);
-  st.commit(sK[0], sV[0], sP[0], &sFull[0], INT_MIN, tid);
-  __syncthreads();
+  auto next_tile = [&](int it) { return it < i_end ? it + tile_items(it) : i_end; };
+  // A row sees at least nvis tokens; a page (at most kMaxPage tokens) can
+  // hold all of them only if nvis <= kMaxPage, so most waves skip the count.
+  const bool need_count = MODE == 1 || __ballot(ri.ok && nvis <= kMaxPage) != 0ull;
 
-  int prev_it = -1, prev_m = 0, k = 0;
-  for (int it = i_begin; it < i_end; ++k) {
-    const int b = k & 1;
-    const int m = tile_items(it);
-    const int next = it + m;
-    if (next < i_end) issue_tile(next);
-    // flush the previous tile's per-head maxima (final since the last barrier)
-    if (MODE == 0 && prev_it >= 0 && tid < 2 * n_heads_blk) {
+  // flush the per-head maxima of the tile in buffer bf (final after a barrier)
+  auto flush = [&](int bf, int t_it, int t_m) {
+    if (MODE == 0 && t_it >= 0 && tid < 2 * n_heads_blk) {
       const int ps = tid / n_heads_blk, hl = tid % n_heads_blk;
-      if (ps < prev_m) {
-        const float v = __uint_as_float(sMax[b ^ 1][ps][hl]);
-        const int page = prev_it + ps;
+      if (ps < t_m) {
+        const float v = __uint_as_float(sMax[bf][ps][hl]);
+        const int page = t_it + ps;
         const int h = g * a.group + head0 + hl;
         if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], v);
         atomic_max_nonneg(&pw.R[page], v);
       }
-      sMax[b ^ 1][ps][hl] = 0u;
+      sMax[bf][ps][hl] = 0u;
     }
-    if (wave_on) {
-      for (int ps = 0; ps < m; ++ps) {
-        const int item = it + ps;
-        const int len = plen(item);
-        // a short page occupies slot ps; a long one both slots from slot 0
-        const int nblk = (m == 2) ? 1 : (len > 32 ? 2 : 1);
-        const int slot0 = ps;
-        f32x16 s[2];
-        s[0] = scores<D, St::KP>(sK[b], slot0, col, half, qf);
-        s[1] = nblk == 2 ? scores<D, St::KP>(sK[b], 1, col, half, qf) : zero16();
-        float mx = -INFINITY;
-        int c = 0;
+  };
+
+  // the pages of the tile in buffer b
+  auto process = [&](int b, int it, int m) {
+    if (!wave_on) return;
+#pragma nounroll
+    for (int ps = 0; ps < m; ++ps) {
+      const int item = it + ps;
+      const int len = plen(item);
+      // a short page occupies slot ps; a long one both slots from slot 0
+      const int nblk = (m == 2) ? 1 : (len > 32 ? 2 : 1);
+      const int slot0 = ps;
+      f32x16 s[2];
+      s[0] = scores<D, St::KP>(sK[b], slot0, col, half, qf);
+      s[1] = nblk == 2 ? scores<D, St::KP>(sK[b], 1, col, half, qf) : zero16();
+      // Offsets past the page's length carry position INT_MAX, so the
+      // position test alone masks them (window positions are < INT_MAX).
+      // A slot whose every position is <= the workgroup's smallest window
+      // position (a whole page, all visible) needs no test at all.
+      float mx = -INFINITY;
+      int c = 0;
+      if (sFull[b][slot0] && (nblk == 1 || sFull[b][1])) {
 #pragma unroll
-        for (int tb = 0; tb < 2; ++tb) {
+        for (int tb = 0; tb < 2; ++tb)
           if (tb < nblk) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int o0 = 8 * i + 4 * half;          // offset inside the 32-token slot
-              const int4 pq = *reinterpret_cast<const int4*>(&sP[b][32 * (slot0 + tb) + o0]);
-              const int pv[4] = {pq.x, pq.y, pq.z, pq.w};
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[tb][r]);
+          }
+        c = 32 * nblk;
+      } else {
 #pragma unroll
-              for (int j = 0; j < 4; ++j) {
-                const bool vis = ri.ok && (32 * tb + o0 + j) < len && pv[j] <= ri.qp;
-                const float x = vis ? s[tb][4 * i + j] : -INFINITY;
-                c += vis ? 1 : 0;
-                s[tb][4 * i + j] = x;
-                mx = fmaxf(mx, x);
-              }
+      for (int tb = 0; tb < 2; ++tb) {
+        if (tb < nblk) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int4 pq = *reinterpret_cast<const int4*>(&sP[b][32 * (slot0 + tb) + 8 * i + 4 * half]);
+            const int pv[4] = {pq.x, pq.y, pq.z, pq.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const bool vis = pv[j] <= ri.qp;
+              const float x = vis ? s[tb][4 * i + j] : -INFINITY;
+              if (need_count) c += vis ? 1 : 0;
+              s[tb][4 * i + j] = x;
+              mx = fmaxf(mx, x);
             }
           }
         }
-        mx = fmaxf(mx, xor32(mx));
-        c += xor32i(c);
-        const float base = mx == -INFINITY ? 0.f : mx * a.sl2;
+      }
+      if (need_count) c = sum32i(c);
+      }
+      mx = max32(mx);
+      const bool touched = mx != -INFINITY;
+      const float base = touched ? mx * a.sl2 : 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s[0][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0][r], a.sl2, -base));
-        float ls = 0.f;
-        f16x8 h0[2], h1[2];
-        to_f16(s[0], h0, ls);
-        if (nblk == 2) {
+      for (int r = 0; r < 16; ++r) s[0][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0][r], a.sl2, -base));
+      float ls = 0.f;
+      f16x8 h0[2], h1[2];
+      to_f16(s[0], h0, ls);
+      if (nblk == 2) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) s[1][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1][r], a.sl2, -base));
-          to_f16(s[1], h1, ls);
-        }
-        const float lhat = ls + xor32(ls);
-        f32x16 u[DB];
+        for (int r = 0; r < 16; ++r) s[1][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1][r], a.sl2, -base));
+        to_f16(s[1], h1, ls);
+      }
+      const float lhat = sum32(ls);
+      const float f = touched ? __builtin_amdgcn_exp2f(base - lse2) : 0.f;
+      const float A = f * lhat;
+      // r^ = U^ - l^ o in two halves of the width (32 accumulator registers
+      // each): the accumulators start at -l^ o, so the MFMAs leave r^.
+      float n2 = 0.f;
 #pragma unroll
-        for (int db = 0; db < DB; ++db) u[db] = zero16();
-        pv_slot<D, St::VP>(sV[b], slot0, col, half, h0, u);
-        if (nblk == 2) pv_slot<D, St::VP>(sV[b], 1, col, half, h1, u);
-        // residual r^ = U^ - l^ o, its norm, and the ratio of Eq. (6)-(7)
-        float n2 = 0.f;
+      for (int hh = 0; hh < DB / 2; ++hh) {
+        f32x16 u[2];
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
+        for (int j = 0; j < 2; ++j) u[j] = of[2 * hh + j] * (-lhat);
+        pv_half<D, St::VP>(sV[b], slot0, col, half, h0, 2 * hh, u);
+        if (nblk == 2) pv_half<D, St::VP>(sV[b], 1, col, half, h1, 2 * hh, u);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float rv = __builtin_fmaf(-lhat, of[db][r], u[db][r]);
-            u[db][r] = rv;
-            n2 = __builtin_fmaf(rv, rv, n2);
-          }
-        n2 += xor32(n2);
-        const bool touched = c > 0;
-        const float f = touched ? __builtin_amdgcn_exp2f(base - lse2) : 0.f;
-        const float A = f * lhat;
-        if (MODE == 0) {
-          float ratio = 0.f;
-          if (touched) {
-            const float keep = 1.f - A;
-            if (c >= nvis) {
-              ratio = INFINITY;                 // the page holds every visible token
-            } else if (A > kFixA || !(keep > 0.f)) {
-              if (ri.ok && half == 0) {         // ill-conditioned: recomputed by the fix-up
-                const int slot = atomicAdd(pw.fix_count, 1);
-                if (slot < pw.fix_cap) {
-                  pw.fix_list[2 * slot] = item;
-                  pw.fix_list[2 * slot + 1] = ri.rg;
-                }
-              }
-            } else if (onorm > 0.f) {
-              ratio = f * sqrtf(n2) / (keep * onorm);
-            } else {
-              ratio = n2 > 0.f ? INFINITY : 0.f;
-            }
-          }
-          if (!ri.ok) ratio = 0.f;
-          if (wave_one_head) {
-            float wm = ratio;
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
-            for (int off = 16; off >= 1; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off, 64));
-            if (lane == 0 && ri.ok) atomicMax(&sMax[b][ps][ri.row / a.W - head0], __float_as_uint(wm));
-          } else if (ri.ok && half == 0) {
-            atomicMax(&sMax[b][ps][ri.row / a.W - head0], __float_as_uint(ratio));
-          }
-        } else if (ri.ok) {
-          const size_t base_i = (size_t)item * pw.total_rows + ri.rg;
-          float* rrow = pw.resid + base_i * D;
+          for (int r = 0; r < 16; ++r) n2 = __builtin_fmaf(u[j][r], u[j][r], n2);
+        if (MODE == 1 && ri.ok) {
+          float* rrow = pw.resid + ((size_t)item * pw.total_rows + ri.rg) * D;
 #pragma unroll
-          for (int db = 0; db < DB; ++db)
+          for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               f32x4 v4;
 #pragma unroll
-              for (int j = 0; j < 4; ++j) v4[j] = f * u[db][4 * i + j];
-              *reinterpret_cast<f32x4*>(rrow + 32 * db + 8 * i + 4 * half) = v4;
+              for (int e = 0; e < 4; ++e) v4[e] = f * u[j][4 * i + e];
+              *reinterpret_cast<f32x4*>(rrow + 32 * (2 * hh + j) + 8 * i + 4 * half) = v4;
             }
-          if (half == 0) {
-            pw.resA[base_i] = A;
-            pw.resC[base_i] = c;
+        }
+      }
+      n2 = sum32(n2);
+      // the ratio of Eq. (6)-(7)
+      if (MODE == 0) {
+        float ratio = 0.f;
+        if (touched) {
+          const float keep = 1.f - A;
+          if (need_count && c >= nvis) {
+            ratio = INFINITY;                 // the page holds every visible token
+          } else if (A > kFixA || !(keep > 0.f)) {
+            if (ri.ok && half == 0) {         // ill-conditioned: recomputed by the fix-up
+              const int slot = atomicAdd(pw.fix_count, 1);
+              if (slot < pw.fix_cap) {
+                pw.fix_list[2 * slot] = item;
+                pw.fix_list[2 * slot + 1] = ri.rg;
+              }
+            }
+          } else if (onorm > 0.f) {
+            ratio = f * sqrtf(n2) / (keep * onorm);
+          } else {
+            ratio = n2 > 0.f ? INFINITY : 0.f;
           }
+        }
+        if (!ri.ok) ratio = 0.f;
+        if (wave_one_head) {
+          float wm = ratio;
+#pragma unroll
+          for (int off = 16; off >= 1; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off, 64));
+          if (lane == 0 && ri.ok) atomicMax(&sMax[b][ps][my_hl], __float_as_uint(wm));
+        } else if (ri.ok && half == 0) {
+          atomicMax(&sMax[b][ps][my_hl], __float_as_uint(ratio));
+        }
+      } else if (ri.ok) {
+        const size_t base_i = (size_t)item * pw.total_rows + ri.rg;
+        if (half == 0) {
+          pw.resA[base_i] = A;
+          pw.resC[base_i] = c;
         }
       }
     }
-    if (next < i_end) st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], &sFull[b ^ 1], INT_MIN, tid);
+  };
+
+  St st;
+  int t_cur = i_begin;
+  issue_tile(st, t_cur);
+  st.commit(sK[0], sV[0], sP[0], sFull[0], minq, tid);
+  __syncthreads();
+  int prev_it = -1, prev_m = 0, k = 0;
+  while (t_cur < i_end) {
+    const int b = k & 1;
+    const int t_n1 = next_tile(t_cur);
+    const int m = t_n1 - t_cur;
+    issue_tile(st, t_n1);
+    flush(b ^ 1, prev_it, prev_m);
+    process(b, t_cur, m);
+    if (t_n1 < i_end) st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], sFull[b ^ 1], minq, tid);
     __syncthreads();
-    prev_it = it;
-    prev_m = m;
-    it = next;
+    prev_it = t_cur; prev_m = m; t_cur = t_n1; ++k;
   }
-  if (MODE == 0 && tid < 2 * n_heads_blk) {
-    const int b = (k - 1) & 1;
-    const int ps = tid / n_heads_blk, hl = tid % n_heads_blk;
-    if (ps < prev_m) {
-      const float v = __uint_as_float(sMax[b][ps][hl]);
-      const int page = prev_it + ps;
-      const int h = g * a.group + head0 + hl;
-      if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], v);
-      atomic_max_nonneg(&pw.R[page], v);
-    }
-  }
+  flush((k - 1) & 1, prev_it, prev_m);
 }
 
 // ---------------------------------------------------------------------------
