@@ -792,8 +792,13 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   plan.add(&dblob, blob.size());
   plan.add(&sa.pend_prot, std::max(tot_p, 1));
   plan.add(&sa.pend_ord, std::max(tot_p, 1));
-  uint8_t* state_ws = nullptr;
-  if (!token_state) plan.add(&state_ws, (size_t)ns * score_seq_stride);
+  int max_s = 0;
+  for (int s = 0; s < ns; ++s) max_s = std::max(max_s, n_tokens[s]);
+  sa.n_chunks = (max_s + ckv::kSelChunk - 1) / ckv::kSelChunk;
+  plan.add(&sa.kv, (size_t)ns * score_seq_stride);
+  plan.add(&sa.ctrl, (size_t)ns * ckv::kSelCtrl);
+  plan.add(&sa.hist, (size_t)ns * 3 * ckv::kSelBins);
+  plan.add(&sa.wcnt, (size_t)ns * sa.n_chunks * 2);
   int rc = realize(c, plan);
   if (rc) return rc;
   if ((rc = upload(c, blob.data(), blob.size(), dblob))) return rc;
@@ -813,7 +818,7 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   sa.bn = bn;
   sa.max_pages = budget->max_pending_pages;
   sa.keep_recent = budget->keep_recent;
-  sa.state = token_state ? token_state : state_ws;
+  sa.state = token_state;
   sa.kept = kept_idx;
   sa.n_kept = n_kept;
   CKV_LAUNCH(c, "protect", launch_protect(sa, c->stream));

@@ -145,10 +145,19 @@ struct SelectArgs {
   uint8_t* pend_prot;            // [total pending] workspace
   int32_t* pend_ord;             // [total pending] workspace
   int budget, bn, max_pages, keep_recent;
-  uint8_t* state;                // [n_seq][score_seq_stride]
+  uint8_t* state;                // [n_seq][score_seq_stride] or nullptr
   int32_t* kept;                 // [n_seq][budget]
   int32_t* n_kept;               // [n_seq]
+  // workspace of the multi-workgroup selection
+  int n_chunks;                  // token chunks of the longest sequence
+  uint32_t* kv;                  // [n_seq][score_seq_stride] state-coded keys
+  int32_t* ctrl;                 // [n_seq][kSelCtrl]
+  uint32_t* hist;                // [n_seq][3][2048] digit histograms
+  int32_t* wcnt;                 // [n_seq][n_chunks][2] per-chunk counts
 };
+constexpr int kSelChunk = 2048;  // tokens per selection workgroup
+constexpr int kSelCtrl = 16;     // ints of per-sequence selection state
+constexpr int kSelBins = 2048;   // radix digit bins (11-bit digits)
 hipError_t launch_protect(const SelectArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 

@@ -4,11 +4,19 @@
 //   (R- descending, page order ascending) by counting, and protected in that
 //   order while fewer than max_pages are taken and the token total stays
 //   within B_N; the first page that does not fit stops the protection.
-// select_kernel (one block per sequence): token states (retired > protected >
-//   free), then the k = min(B - #protected, #free) free tokens with the
-//   largest score are found by a 4-pass 8-bit radix select on an order-
-//   preserving 32-bit image of the score; ties at the threshold go to the
-//   lowest indices.  Kept indices are written in ascending order.
+// Selection, on token chunks of kSelChunk tokens (grid: chunks x sequences):
+//   sel_keys   token states (retired > protected > free) in LDS, one coded
+//              key per token (0 retired, ~0 protected, else the order-
+//              preserving image of the score, NaN as -inf and -0.0 as +0.0),
+//              counts, and the histogram of the first 11-bit digit;
+//   sel_pass   the histograms of digits 2 and 3 among the keys that share
+//              the digits chosen so far (radix select of the k-th largest);
+//   sel_count  per chunk: tokens kept outright, free tokens tied at the
+//              threshold key;
+//   sel_write  kept indices in ascending order; ties at the threshold go to
+//              the lowest indices.
+//   k = min(B - #protected, #free).  The last workgroup of each histogram
+//   launch (atomic arrival counter) chooses the digit for every sequence.
 // gather_kernel: K'[s,l,g,j] = K[s,l,g,I[j]], the same for V, and
 //   pos'[s,j] = pos[s,I[j]], 16-byte vector copies of whole rows.
 #include "ckv_device.h"
@@ -17,7 +25,6 @@
 namespace ckv {
 
 namespace {
-constexpr int kST = 1024;   // threads of the selection block
 constexpr uint8_t kFree = 0, kProt = 1, kRet = 2;
 }  // namespace
 
@@ -39,6 +46,9 @@ __global__ __launch_bounds__(256) void protect_kernel(SelectArgs a) {
   const int32_t* len = a.pend_len + off;
   uint8_t* prot = a.pend_prot + off;
   int32_t* ord = a.pend_ord + off;
+  // clear the selection state of this sequence for the kernels that follow
+  for (int i = threadIdx.x; i < kSelCtrl; i += 256) a.ctrl[(size_t)s * kSelCtrl + i] = 0;
+  for (int i = threadIdx.x; i < 3 * kSelBins; i += 256) a.hist[(size_t)s * 3 * kSelBins + i] = 0u;
   for (int i = threadIdx.x; i < n; i += 256) {
     const float ri = pend_key(R[i]);
     int rank = 0;
@@ -82,8 +92,23 @@ __device__ __forceinline__ void hist_add(unsigned int* hist, uint32_t bin, bool 
   if (act) atomicAdd(&hist[bin], 1u);
 }
 
-// block-wide exclusive scan of one int per thread (kST threads)
-__device__ int block_exclusive_scan(int v, int* tmp, int& total) {
+namespace {
+constexpr int kSelT = 256;                       // threads per selection workgroup
+constexpr int kPerT = kSelChunk / kSelT;         // tokens per thread
+constexpr uint32_t kKeyRet = 0u, kKeyProt = 0xFFFFFFFFu;
+// control block of one sequence
+enum { cNP = 0, cNF = 1, cArr0 = 2, cArr1 = 3, cArr2 = 4, cK = 5, cMode = 6, cPrefix = 7,
+       cMask = 8, cNeed = 9, cT = 10, cNeedEq = 11 };
+enum { kModeRadix = 0, kModeAll = 1, kModeNone = 2 };
+constexpr int kShift[3] = {21, 10, 0};
+constexpr uint32_t kDigit[3] = {0x7FFu, 0x7FFu, 0x3FFu};
+
+__device__ __forceinline__ bool key_free(uint32_t k) { return k != kKeyRet && k != kKeyProt; }
+}  // namespace
+
+// exclusive scan of one int per thread over a block of NT threads
+template <int NT>
+__device__ int block_scan(int v, int* tmp, int& total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int x = v;
 #pragma unroll
@@ -93,156 +118,272 @@ __device__ int block_exclusive_scan(int v, int* tmp, int& total) {
   }
   if (lane == 63) tmp[w] = x;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int run = 0;
-    for (int i = 0; i < kST / 64; ++i) {
-      const int t = tmp[i];
-      tmp[i] = run;
-      run += t;
-    }
-    tmp[kST / 64] = run;
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) {
+    const int t = tmp[i];
+    base += i < w ? t : 0;
+    tot += t;
   }
+  total = tot;
   __syncthreads();
-  const int res = tmp[w] + x - v;
-  total = tmp[kST / 64];
-  __syncthreads();
-  return res;
+  return base + x - v;
 }
 
-__global__ __launch_bounds__(kST) void select_kernel(SelectArgs a) {
-  __shared__ unsigned int hist[256];
-  __shared__ int tmp[kST / 64 + 1];
-  __shared__ unsigned int s_prefix, s_mask;
-  __shared__ int s_need;
-  const int s = blockIdx.x;
-  const int S = a.n_tokens[s];
-  uint8_t* st = a.state + (size_t)s * a.score_seq_stride;
-  const float* sc = a.score + (size_t)s * a.score_seq_stride;
-  const int tid = threadIdx.x;
-
-  // token states: recent -> protected; protected pending pages; retired pages
-  for (int t = tid; t < S; t += kST) st[t] = (t >= S - a.keep_recent) ? kProt : kFree;
+// Last workgroup of a histogram launch, for sequence s: choose the digit of
+// pass p that holds the need-th largest matching key.  Thread i owns bins
+// [8(255-i), 8(255-i)+8), so an exclusive scan in thread order counts the
+// keys in higher bins.
+__device__ void choose_digit(const SelectArgs& a, int s, int p, int* tmp) {
+  int32_t* ctrl = a.ctrl + (size_t)s * kSelCtrl;
+  const uint32_t* hg = a.hist + ((size_t)s * 3 + p) * kSelBins;
+  const int g = kSelT - 1 - (int)threadIdx.x;
+  int h[8], sum = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    h[j] = (int)__hip_atomic_load(&hg[8 * g + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sum += h[j];
+  }
+  int total;
+  int above = block_scan<kSelT>(sum, tmp, total);
+  const int need = ctrl[cNeed];
   __syncthreads();
+#pragma unroll
+  for (int j = 7; j >= 0; --j) {
+    if (above < need && above + h[j] >= need) {
+      const uint32_t d = (uint32_t)(8 * g + j);
+      const uint32_t prefix = (uint32_t)ctrl[cPrefix] | (d << kShift[p]);
+      ctrl[cPrefix] = (int)prefix;
+      ctrl[cMask] = (int)((uint32_t)ctrl[cMask] | (kDigit[p] << kShift[p]));
+      ctrl[cNeed] = need - above;
+      if (p == 2) {
+        ctrl[cT] = (int)prefix;
+        ctrl[cNeedEq] = need - above;
+      }
+    }
+    above += h[j];
+  }
+}
+
+// arrival at the end of a histogram launch; true in the last workgroup of
+// sequence s (all threads)
+__device__ bool arrive_last(int32_t* counter, int n_blocks, int* s_flag) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    *s_flag = atomicAdd(counter, 1) == n_blocks - 1;
+  }
+  __syncthreads();
+  const bool last = *s_flag;
+  if (last) __threadfence();
+  return last;
+}
+
+__device__ __forceinline__ void bins_to_global(uint32_t* hg, const unsigned int* hl) {
+  for (int i = threadIdx.x; i < kSelBins; i += kSelT)
+    if (hl[i]) atomicAdd(&hg[i], hl[i]);
+}
+
+// token states, coded keys, counts and the first digit's histogram
+__global__ __launch_bounds__(kSelT) void sel_keys(SelectArgs a) {
+  __shared__ uint8_t st[kSelChunk];
+  __shared__ unsigned int hl[kSelBins];
+  __shared__ int tmp[kSelT / 64];
+  __shared__ int s_flag;
+  const int s = blockIdx.y;
+  const int S = a.n_tokens[s];
+  const int t0 = blockIdx.x * kSelChunk;
+  if (t0 >= S) return;
+  const int t1 = min(S, t0 + kSelChunk);
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kSelBins; i += kSelT) hl[i] = 0u;
+  for (int i = tid; i < kSelChunk; i += kSelT) st[i] = (t0 + i >= S - a.keep_recent) ? kProt : kFree;
+  __syncthreads();
+  // protected pending pages, then retired pages (retired wins)
   {
     const int off = a.pend_off[s], n = a.pend_off[s + 1] - off;
-    for (int idx = tid; idx < n * kMaxPage; idx += kST) {
+    for (int idx = tid; idx < n * kMaxPage; idx += kSelT) {
       const int i = idx / kMaxPage, e = idx % kMaxPage;
-      if (a.pend_prot[off + i] && e < a.pend_len[off + i]) st[a.pend_start[off + i] + e] = kProt;
+      const int t = a.pend_start[off + i] + e;
+      if (a.pend_prot[off + i] && e < a.pend_len[off + i] && t >= t0 && t < t1) st[t - t0] = kProt;
     }
   }
   __syncthreads();
   {
     const int off = a.ret_off[s], n = a.ret_off[s + 1] - off;
-    for (int idx = tid; idx < n * kMaxPage; idx += kST) {
+    for (int idx = tid; idx < n * kMaxPage; idx += kSelT) {
       const int i = idx / kMaxPage, e = idx % kMaxPage;
-      if (e < a.ret_len[off + i]) st[a.ret_start[off + i] + e] = kRet;
+      const int t = a.ret_start[off + i] + e;
+      if (e < a.ret_len[off + i] && t >= t0 && t < t1) st[t - t0] = kRet;
     }
   }
   __syncthreads();
-
-  // counts
+  const float* sc = a.score + (size_t)s * a.score_seq_stride;
+  uint32_t* kv = a.kv + (size_t)s * a.score_seq_stride;
+  uint8_t* sto = a.state ? a.state + (size_t)s * a.score_seq_stride : nullptr;
+  float f[kPerT];
+#pragma unroll
+  for (int u = 0; u < kPerT; ++u) {
+    const int t = t0 + u * kSelT + tid;
+    f[u] = t < t1 ? sc[t] : 0.f;
+  }
   int np = 0, nf = 0;
-  for (int t = tid; t < S; t += kST) {
-    const uint8_t x = st[t];
-    np += x == kProt;
-    nf += x == kFree;
+#pragma unroll
+  for (int u = 0; u < kPerT; ++u) {
+    const int i = u * kSelT + tid, t = t0 + i;
+    const bool in = t < t1;
+    const uint8_t x = in ? st[i] : kRet;
+    const uint32_t key = x == kProt ? kKeyProt : (x == kRet ? kKeyRet : score_key(f[u]));
+    if (in) {
+      kv[t] = key;
+      if (sto) sto[t] = x;
+    }
+    np += x == kProt && in;
+    nf += x == kFree && in;
+    hist_add(hl, key >> kShift[0], in && x == kFree);
   }
-  int tot_p, tot_f;
-  block_exclusive_scan(np, tmp, tot_p);
-  block_exclusive_scan(nf, tmp, tot_f);
-  const int k = max(0, min(a.budget - tot_p, tot_f));
-
-  // radix select of the k-th largest key among free tokens
-  bool take_all = (k == tot_f);
-  if (tid == 0) { s_prefix = 0u; s_mask = 0u; s_need = k; }
+  int tot;
+  block_scan<kSelT>(np, tmp, tot);
+  np = tot;
+  block_scan<kSelT>(nf, tmp, tot);
+  nf = tot;
+  int32_t* ctrl = a.ctrl + (size_t)s * kSelCtrl;
+  if (tid == 0) {
+    atomicAdd(&ctrl[cNP], np);
+    atomicAdd(&ctrl[cNF], nf);
+  }
+  bins_to_global(a.hist + (size_t)s * 3 * kSelBins, hl);
+  const int nb = (S + kSelChunk - 1) / kSelChunk;
+  if (!arrive_last(&ctrl[cArr0], nb, &s_flag)) return;
+  // last workgroup of the sequence: k, the mode, and the first digit
+  const int NP = __hip_atomic_load(&ctrl[cNP], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int NF = __hip_atomic_load(&ctrl[cNF], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int k = max(0, min(a.budget - NP, NF));
+  const int mode = k == 0 ? kModeNone : (k == NF ? kModeAll : kModeRadix);
   __syncthreads();
-  if (k > 0 && !take_all) {
-    for (int pass = 0; pass < 4; ++pass) {
-      const int shift = 24 - 8 * pass;
-      for (int i = tid; i < 256; i += kST) hist[i] = 0u;
-      __syncthreads();
-      const unsigned int prefix = s_prefix, mask = s_mask;
-      for (int t0 = 0; t0 < S; t0 += kST) {
-        const int t = t0 + tid;
-        bool act = false;
-        uint32_t bin = 0;
-        if (t < S && st[t] == kFree) {
-          const uint32_t key = score_key(sc[t]);
-          act = (key & mask) == prefix;
-          bin = (key >> shift) & 255u;
-        }
-        hist_add(hist, bin, act);
-      }
-      __syncthreads();
-      if (tid == 0) {
-        int need = s_need;
-        int d = 255;
-        for (; d > 0; --d) {
-          if ((int)hist[d] >= need) break;
-          need -= (int)hist[d];
-        }
-        s_prefix = prefix | ((unsigned int)d << shift);
-        s_mask = mask | (255u << shift);
-        s_need = need;
-      }
-      __syncthreads();
-    }
+  if (tid == 0) {
+    ctrl[cK] = k;
+    ctrl[cMode] = mode;
+    ctrl[cPrefix] = 0;
+    ctrl[cMask] = 0;
+    ctrl[cNeed] = k;
+    // all free tokens: every free key is > 0; none: no free key is >= ~0 - 1
+    ctrl[cT] = mode == kModeAll ? 0 : (int)(kKeyProt - 1u);
+    ctrl[cNeedEq] = 0;
   }
-  const uint32_t T = s_prefix;
-  const int need_eq = s_need;     // how many tokens with key == T to keep
+  __syncthreads();
+  if (mode == kModeRadix) choose_digit(a, s, 0, tmp);
+}
 
-  // One ordered sweep in blocks of kST tokens (one per thread, coalesced):
-  // a free token with key == T is kept while fewer than need_eq such tokens
-  // precede it; kept tokens are written in ascending order.  Prefix counts
-  // inside a wave come from ballots, across the 16 waves from LDS.
-  int32_t* kept = a.kept + (size_t)s * a.budget;
-  const int lane = tid & 63, w = tid >> 6;
-  const unsigned long long lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  int eq_run = 0, out_run = 0;
-  for (int t0 = 0; t0 < S; t0 += kST) {
-    const int t = t0 + tid;
-    bool prot = false, free_gt = false, free_eq = false;
-    if (t < S) {
-      const uint8_t x = st[t];
-      prot = x == kProt;
-      if (x == kFree && k > 0) {
-        if (take_all) free_gt = true;
-        else {
-          const uint32_t key = score_key(sc[t]);
-          free_gt = key > T;
-          free_eq = key == T;
-        }
-      }
-    }
-    // rank of this token among the block's key == T tokens
-    const unsigned long long me = __ballot(free_eq);
-    if (lane == 0) tmp[w] = __popcll(me);
-    __syncthreads();
-    int wbase = 0, btot = 0;
-    for (int i = 0; i < kST / 64; ++i) {
-      const int c = tmp[i];
-      wbase += i < w ? c : 0;
-      btot += c;
-    }
-    const int eq_rank = eq_run + wbase + __popcll(me & lt_mask);
-    eq_run += btot;
-    const bool keep = prot || free_gt || (free_eq && eq_rank < need_eq);
-    __syncthreads();
-    const unsigned long long km = __ballot(keep);
-    if (lane == 0) tmp[w] = __popcll(km);
-    __syncthreads();
-    int kbase = 0, ktot = 0;
-    for (int i = 0; i < kST / 64; ++i) {
-      const int c = tmp[i];
-      kbase += i < w ? c : 0;
-      ktot += c;
-    }
-    if (keep) kept[out_run + kbase + __popcll(km & lt_mask)] = t;
-    out_run += ktot;
-    __syncthreads();
+// histogram of digit p (1 or 2) among free keys matching the chosen prefix
+__global__ __launch_bounds__(kSelT) void sel_pass(SelectArgs a, int p) {
+  __shared__ unsigned int hl[kSelBins];
+  __shared__ int tmp[kSelT / 64];
+  __shared__ int s_flag;
+  const int s = blockIdx.y;
+  const int S = a.n_tokens[s];
+  const int t0 = blockIdx.x * kSelChunk;
+  int32_t* ctrl = a.ctrl + (size_t)s * kSelCtrl;
+  if (t0 >= S || ctrl[cMode] != kModeRadix) return;
+  const int t1 = min(S, t0 + kSelChunk);
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kSelBins; i += kSelT) hl[i] = 0u;
+  const uint32_t prefix = (uint32_t)ctrl[cPrefix], mask = (uint32_t)ctrl[cMask];
+  const uint32_t* kv = a.kv + (size_t)s * a.score_seq_stride;
+  uint32_t key[kPerT];
+#pragma unroll
+  for (int u = 0; u < kPerT; ++u) {
+    const int t = t0 + u * kSelT + tid;
+    key[u] = t < t1 ? kv[t] : kKeyRet;
   }
-  for (int j = out_run + tid; j < a.budget; j += kST) kept[j] = -1;
-  if (tid == 0) a.n_kept[s] = out_run;
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < kPerT; ++u) {
+    const bool act = key_free(key[u]) && (key[u] & mask) == prefix;
+    hist_add(hl, (key[u] >> kShift[p]) & kDigit[p], act);
+  }
+  __syncthreads();
+  bins_to_global(a.hist + ((size_t)s * 3 + p) * kSelBins, hl);
+  const int nb = (S + kSelChunk - 1) / kSelChunk;
+  if (!arrive_last(&ctrl[cArr0 + p], nb, &s_flag)) return;
+  choose_digit(a, s, p, tmp);
+}
+
+// per chunk: tokens kept outright (protected, or free above the threshold
+// key T) and free tokens with key == T
+__global__ __launch_bounds__(kSelT) void sel_count(SelectArgs a) {
+  __shared__ int tmp[kSelT / 64];
+  const int s = blockIdx.y;
+  const int S = a.n_tokens[s];
+  const int t0 = blockIdx.x * kSelChunk;
+  if (t0 >= S) return;
+  const int t1 = min(S, t0 + kSelChunk);
+  const int32_t* ctrl = a.ctrl + (size_t)s * kSelCtrl;
+  const uint32_t T = (uint32_t)ctrl[cT];
+  const uint32_t* kv = a.kv + (size_t)s * a.score_seq_stride;
+  int nk = 0, ne = 0;
+#pragma unroll
+  for (int u = 0; u < kPerT; ++u) {
+    const int t = t0 + u * kSelT + threadIdx.x;
+    const uint32_t key = t < t1 ? kv[t] : kKeyRet;
+    nk += (key == kKeyProt || (key_free(key) && key > T)) ? 1 : 0;
+    ne += (key_free(key) && key == T) ? 1 : 0;
+  }
+  int tk, te;
+  block_scan<kSelT>(nk, tmp, tk);
+  block_scan<kSelT>(ne, tmp, te);
+  if (threadIdx.x == 0) {
+    int32_t* w = a.wcnt + ((size_t)s * a.n_chunks + blockIdx.x) * 2;
+    w[0] = tk;
+    w[1] = te;
+  }
+}
+
+// kept indices of the chunk, in order, at the chunk's offset
+__global__ __launch_bounds__(kSelT) void sel_write(SelectArgs a) {
+  __shared__ int tmp[kSelT / 64];
+  const int s = blockIdx.y;
+  const int S = a.n_tokens[s];
+  const int t0 = blockIdx.x * kSelChunk;
+  const int32_t* ctrl = a.ctrl + (size_t)s * kSelCtrl;
+  const int n_kept = ctrl[cNP] + ctrl[cK];
+  int32_t* kept = a.kept + (size_t)s * a.budget;
+  // pad the tail of the index list
+  for (int j = n_kept + blockIdx.x * kSelT + (int)threadIdx.x; j < a.budget; j += gridDim.x * kSelT) kept[j] = -1;
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.n_kept[s] = n_kept;
+  if (t0 >= S) return;
+  const int t1 = min(S, t0 + kSelChunk);
+  const uint32_t T = (uint32_t)ctrl[cT];
+  const int need_eq = ctrl[cNeedEq];
+  // offsets from the chunks before this one
+  int out = 0, eq_before = 0;
+  const int32_t* wc = a.wcnt + (size_t)s * a.n_chunks * 2;
+  for (int w = 0; w < (int)blockIdx.x; ++w) {
+    const int nk = wc[2 * w], ne = wc[2 * w + 1];
+    out += nk + max(0, min(ne, need_eq - eq_before));
+    eq_before += ne;
+  }
+  const uint32_t* kv = a.kv + (size_t)s * a.score_seq_stride;
+  uint32_t key[kPerT];
+#pragma unroll
+  for (int u = 0; u < kPerT; ++u) {
+    const int t = t0 + u * kSelT + threadIdx.x;
+    key[u] = t < t1 ? kv[t] : kKeyRet;
+  }
+  // rounds of kSelT consecutive tokens: ranks from an exclusive scan
+#pragma unroll
+  for (int u = 0; u < kPerT; ++u) {
+    const int t = t0 + u * kSelT + threadIdx.x;
+    const bool eq = key_free(key[u]) && key[u] == T;
+    int te;
+    const int eq_rank = eq_before + block_scan<kSelT>(eq ? 1 : 0, tmp, te);
+    eq_before += te;
+    const bool keep = key[u] == kKeyProt || (key_free(key[u]) && key[u] > T) || (eq && eq_rank < need_eq);
+    int tk;
+    const int pos = out + block_scan<kSelT>(keep ? 1 : 0, tmp, tk);
+    if (keep && pos < a.budget) kept[pos] = t;
+    out += tk;
+  }
 }
 
 hipError_t launch_protect(const SelectArgs& a, hipStream_t s) {
@@ -251,7 +392,17 @@ hipError_t launch_protect(const SelectArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(select_kernel, dim3(a.n_seq), dim3(kST), 0, s, a);
+  const dim3 grid(a.n_chunks, a.n_seq), block(kSelT);
+  hipLaunchKernelGGL(sel_keys, grid, block, 0, s, a);
+  hipError_t e = hipGetLastError();
+  for (int p = 1; p <= 2 && e == hipSuccess; ++p) {
+    hipLaunchKernelGGL(sel_pass, grid, block, 0, s, a, p);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(sel_count, grid, block, 0, s, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(sel_write, grid, block, 0, s, a);
   return hipGetLastError();
 }
 
