@@ -1003,6 +1003,162 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_kernel(AttnGeom a, RowSta
   }
 }
 
+// The same with every (query head, 32-row block) pair of the workgroup owned
+// by one wave for the whole launch (PPW pairs per wave): the wave's query
+// fragments, log-sum-exp and window positions stay in registers, keys are
+// loaded two tiles ahead, and a tile whose positions are all <= the smallest
+// window position skips the visibility test.  Workgroup z takes pairs
+// [8 PPW z, 8 PPW (z+1)), whole heads only (8 PPW is a multiple of the row
+// blocks per head); heads of other z-slices meet in the atomic max.
+template <int D, int PPW>
+__global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats rs, float* mass, int chunk) {
+  constexpr int NT = kNW * 64, KS = D / 16;
+  constexpr int KP = D + 8, CPR = D / 8, KCH = kTile * CPR, KPT = (KCH + NT - 1) / NT;
+  constexpr int NP = kNW * PPW;                 // pairs per workgroup
+  __shared__ __align__(16) uint16_t sK[2][kTile * KP];
+  __shared__ int sP[2][kTile];
+  __shared__ int sFull[2];
+  __shared__ float sPart[2][NP][kTile];
+  __shared__ int sMin;
+  const int g = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, col = lane & 31;
+  const int t_begin = blockIdx.x * chunk;
+  const int t_end = min(a.S, t_begin + chunk);
+  if (t_begin >= t_end) return;
+  const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
+  const int nrb = (a.W + 31) / 32;
+  const int n_pairs = a.group * nrb;
+  const int p0 = blockIdx.z * NP;
+  const int np_blk = min(NP, n_pairs - p0);
+  // smallest window position (every head has the same window rows)
+  if (tid == 0) sMin = INT_MAX;
+  __syncthreads();
+  {
+    int q = INT_MAX;
+    for (int p = tid; p < a.W; p += NT) q = min(q, a.qpos[p]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) q = min(q, __shfl_xor(q, off, 64));
+    if (lane == 0) atomicMin(&sMin, q);
+  }
+  __syncthreads();
+  const int minq = sMin;
+
+  bf16x8 qa[PPW][KS];
+  float l2[PPW][16];
+  int qp[PPW][16];
+  bool pon[PPW];
+#pragma unroll
+  for (int j = 0; j < PPW; ++j) {
+    const int pl = wave + kNW * j;               // pair inside the workgroup
+    const int pi = p0 + pl;
+    pon[j] = pl < np_blk;
+    const int hl = pon[j] ? pi / nrb : 0, rb = pon[j] ? pi % nrb : 0;
+    const int h = g * a.group + hl;
+    const int prow = 32 * rb + col;            // A operand row of this lane
+    const bool aok = pon[j] && prow < a.W;
+    const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)(aok ? prow : 0) * a.q_row_stride;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qa[j][ks] = aok ? load_bf16x8(qrow + 16 * ks + 8 * half) : zero_bf16x8();
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int p = 32 * rb + 8 * (r >> 2) + 4 * half + (r & 3);
+      const bool ok = pon[j] && p < a.W;
+      // rows outside the window get weight 0: -inf log-sum-exp offset
+      l2[j][r] = ok ? rs.lse2[g * a.rows + hl * a.W + p] : INFINITY;
+      qp[j][r] = ok ? a.qpos[p] : INT_MIN;
+    }
+  }
+
+  struct KStage { u32x4 kr[KPT]; int pr; };
+  KStage sa, sb;
+  const int n_tiles = (t_end - t_begin + kTile - 1) / kTile;
+  auto issue = [&](KStage& st, int it) {
+    const int t0 = t_begin + it * kTile;
+    const int nv = it < n_tiles ? min(kTile, t_end - t0) : 0;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + i * NT;
+      const int tr = (c / CPR) & (kTile - 1);
+      const bool ok = c < KCH && tr < nv;
+      st.kr[i] = ldg_u4(kh + (int64_t)(ok ? t0 + tr : 0) * a.kv_tok_stride + (c % CPR) * 8);
+    }
+    const bool okp = tid < nv;
+    const int pv = ldg_i32(a.pos + (okp ? t0 + tid : 0));
+    st.pr = okp ? pv : INT_MAX;
+  };
+  auto commit = [&](const KStage& st, int b) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + i * NT;
+      if (c < KCH) *reinterpret_cast<u32x4*>(&sK[b][(c / CPR) * KP + (c % CPR) * 8]) = st.kr[i];
+    }
+    if (tid < kTile) {
+      sP[b][tid] = st.pr;
+      const unsigned long long late = __ballot(st.pr > minq);
+      if (tid == 0) sFull[b] = late == 0ull;
+    }
+  };
+  auto compute = [&](int b, int it) {
+    const bool full = sFull[b];
+#pragma unroll
+    for (int j = 0; j < PPW; ++j) {
+      if (!pon[j]) continue;
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb) {
+        f32x16 acc = zero16();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          acc = mfma_bf16(qa[j][ks], load_bf16x8(&sK[b][(32 * tb + col) * KP + 16 * ks + 8 * half]), acc);
+        float msum = 0.f;
+        if (full) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) msum += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[r], a.sl2, -l2[j][r]));
+        } else {
+          const int pt = sP[b][32 * tb + col];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[r], a.sl2, -l2[j][r]));
+            msum += pt <= qp[j][r] ? e : 0.f;
+          }
+        }
+        msum = sum32(msum);
+        if (half == 0) sPart[it & 1][wave + kNW * j][32 * tb + col] = msum;
+      }
+    }
+  };
+  // threads 0..63: sum a head's row blocks, max over the heads of the workgroup
+  auto reduce = [&](int it) {
+    const int t0 = t_begin + it * kTile;
+    if (tid < kTile && t0 + tid < t_end) {
+      float best = 0.f;
+      for (int hp = 0; hp < np_blk; hp += nrb) {
+        float sum = 0.f;
+        for (int rb = 0; rb < nrb; ++rb) sum += sPart[it & 1][hp + rb][tid];
+        best = fmaxf(best, sum);
+      }
+      atomic_max_nonneg(&mass[t0 + tid], best);
+    }
+  };
+  issue(sa, 0);
+  issue(sb, 1);
+  commit(sa, 0);
+  __syncthreads();
+  for (int it = 0; it < n_tiles; it += 2) {
+    issue(sa, it + 2);
+    compute(0, it);
+    if (it + 1 < n_tiles) commit(sb, 1);
+    __syncthreads();
+    reduce(it);
+    if (it + 1 >= n_tiles) break;
+    issue(sb, it + 3);
+    compute(1, it + 1);
+    if (it + 2 < n_tiles) commit(sa, 0);
+    __syncthreads();
+    reduce(it + 1);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
@@ -1054,6 +1210,20 @@ hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowSt
 
 hipError_t launch_token_mass(const AttnGeom& a, const RowStats& rs, float* mass, int chunk,
                              hipStream_t s) {
+  const int nrb = (a.W + 31) / 32, n_pairs = a.group * nrb;
+  const int ppw = n_pairs <= kNW ? 1 : 2;
+  if ((kNW * ppw) % nrb == 0) {
+    const int nz = (n_pairs + kNW * ppw - 1) / (kNW * ppw);
+    dim3 grid((a.S + chunk - 1) / chunk, a.Hkv, nz), block(kNW * 64);
+    if (a.D == 128) {
+      if (ppw == 1) hipLaunchKernelGGL((token_mass_fast<128, 1>), grid, block, 0, s, a, rs, mass, chunk);
+      else hipLaunchKernelGGL((token_mass_fast<128, 2>), grid, block, 0, s, a, rs, mass, chunk);
+    } else {
+      if (ppw == 1) hipLaunchKernelGGL((token_mass_fast<64, 1>), grid, block, 0, s, a, rs, mass, chunk);
+      else hipLaunchKernelGGL((token_mass_fast<64, 2>), grid, block, 0, s, a, rs, mass, chunk);
+    }
+    return hipGetLastError();
+  }
   dim3 grid((a.S + chunk - 1) / chunk, a.Hkv), block(kNW * 64);
   if (a.D == 128) hipLaunchKernelGGL((token_mass_kernel<128>), grid, block, 0, s, a, rs, mass, chunk);
   else hipLaunchKernelGGL((token_mass_kernel<64>), grid, block, 0, s, a, rs, mass, chunk);

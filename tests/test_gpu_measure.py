@@ -82,9 +82,13 @@ def test_bruteforce_subsample_tiny(ckv):
     assert_scores_close(got["R"][sub], R, "R (brute force)")
 
 
-def test_token_mass(ckv):
+@pytest.mark.parametrize("case", ["d128_ragged", "g64_w128", "w8_mha", "w40_d128", "tiny_gapped"])
+def test_token_mass(ckv, case):
+    """Window mass max_h sum_p a_hpi of every token (the base score that
+    fills the budget), over several head groupings and window sizes."""
     P, ctx = ckv
-    L = make_layer(CASES["d128_ragged"], seed=3)
+    L = make_layer(CASES[case], seed=3)
+    print(f"[token_mass] case={case}", flush=True)
     dl = LayerOnDevice(L)
     got = _measure(P, ctx, dl, "post", want=("R", "token_mass"))
     want = O.token_mass(L.k, L.v, L.pos, L.q_post, L.qpos_post)
