@@ -518,19 +518,16 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
   plan.add(&rs.lse2, total_rows);
   plan.add(&rs.onorm, total_rows);
   plan.add(&rs.nvis, total_rows);
-  int *fix_list = nullptr, *fix_count = nullptr, *fix_done = nullptr;
-  float* fix_part = nullptr;
-  plan.add(&fix_list, 2 * (size_t)total_rows);
+  int *fix_list = nullptr, *fix_count = nullptr;
+  plan.add(&fix_list, 4 * (size_t)total_rows);
   plan.add(&fix_count, 1);
-  plan.add(&fix_part, (size_t)total_rows * fixup_parts() * (D + 1));
-  plan.add(&fix_done, total_rows);
   const int32_t *dstart = nullptr, *dlen = nullptr;
   if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
   if ((rc = realize(c, plan))) return rc;
 
   CKV_LAUNCH(c, "window_attention", launch_window_attention(a, sp, c->stream));
   ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
-              token_mass ? (size_t)a.S : 0, fix_count, fix_done, (size_t)total_rows};
+              token_mass ? (size_t)a.S : 0, fix_count, nullptr, 0};
   CKV_LAUNCH(c, "combine", launch_combine(a, sp, rs, lse, zl, c->stream));
   if (n > 0) {
     PageWork pw{};
@@ -546,8 +543,6 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
     pw.fix_list = fix_list;
     pw.fix_count = fix_count;
     pw.fix_cap = total_rows;
-    pw.fix_part = fix_part;
-    pw.fix_done = fix_done;
     CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, rs, 0, c->stream));
     CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, sp, rs, pw, c->stream));
   }

@@ -52,11 +52,9 @@ struct PageWork {
   float* R;               // MODE 0: [n_pages], zeroed before
   float* R_head;          // MODE 0: [n_pages][Hq] or null, zeroed before
   int Hq;
-  int* fix_list;          // MODE 0: (page, global row) pairs left to the fix-up kernel
+  int* fix_list;          // MODE 0: (page, global row, start, len) entries left to the fix-up kernel
   int* fix_count;         // MODE 0: entries in fix_list (zeroed before)
   int fix_cap;            // MODE 0: capacity of fix_list (window rows)
-  float* fix_part;        // fix-up partial sums [fix_cap][parts][D + 1]
-  int* fix_done;          // fix-up part counters [fix_cap], zero between calls
   float* resid;           // MODE 1: [max_cand][total_rows][D]
   float* resA;            // MODE 1: [max_cand][total_rows]
   int* resC;              // MODE 1: [max_cand][total_rows]
@@ -74,7 +72,6 @@ struct ZeroList {
 int rows_per_block_attention();
 int rows_per_block_page();
 int token_mass_max_rows();
-int fixup_parts();
 
 hipError_t launch_window_attention(const AttnGeom& a, const AttnSplit& sp, hipStream_t s);
 hipError_t launch_combine(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs, float* lse_out,

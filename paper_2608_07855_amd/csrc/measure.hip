@@ -668,8 +668,12 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
             if (ri.ok && half == 0) {         // ill-conditioned: recomputed by the fix-up
               const int slot = atomicAdd(pw.fix_count, 1);
               if (slot < pw.fix_cap) {
-                pw.fix_list[2 * slot] = item;
-                pw.fix_list[2 * slot + 1] = ri.rg;
+                int4 ent;
+                ent.x = item;
+                ent.y = ri.rg;
+                ent.z = pstart(item);
+                ent.w = len;
+                reinterpret_cast<int4*>(pw.fix_list)[slot] = ent;
               }
             }
           } else if (onorm > 0.f) {
@@ -723,30 +727,51 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
 // recomputed in float32 with the page excluded; ratio = ||o - o'|| / ||o||.
 // One workgroup per listed pair (grid-stride over the list).
 // ---------------------------------------------------------------------------
-constexpr int kFixParts = 8;      // workgroups sharing one listed pair
-constexpr int kFixChunk = 1024;   // tokens whose weights are staged at once
+constexpr int kFixT = 1024;       // threads of a fix-up workgroup
+constexpr int kFixGrid = 128;     // listed pairs in flight
 
-// Workgroup (pair slot e, part kp): kp == 0 also adds the other splits'
-// partial sums; every part recomputes a slice of the page's split(s) with
-// the page excluded.  Parts write (sum over width, weight) to fix_part; the
-// last part to finish merges them in part order and writes the ratio.
+// One workgroup per listed pair (grid-stride over the list), so no
+// workgroup waits for another: the other splits' partial sums as they are,
+// plus the page's own split(s) recomputed in float32 without the page.
+// Weights are taken relative to the row's log-sum-exp (every weight <= 1).
 template <int D>
-__global__ __launch_bounds__(256) void page_fixup_kernel(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw) {
+__global__ __launch_bounds__(kFixT) void page_fixup_kernel(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw) {
   constexpr int TPR = D / 8;                  // threads per token row (16 bytes each)
-  constexpr int RPR = 256 / TPR;              // token rows per round
-  __shared__ float sw[kFixChunk];
-  __shared__ float sacc[RPR][D];
-  __shared__ float sl[RPR];
-  __shared__ float sred[2][4];
-  __shared__ int s_last;
+  constexpr int RPR = kFixT / TPR;            // token rows per round
+  constexpr int UNR = 4;                      // rounds whose loads are in flight together
+  __shared__ float sacc[RPR][D + 1];
+  __shared__ float sred[2][kFixT / 64];
   const int tid = threadIdx.x, c = tid % TPR, r = tid / TPR;
-  const int kp = blockIdx.y;
   const int n = min(*pw.fix_count, pw.fix_cap);
   for (int e = blockIdx.x; e < n; e += gridDim.x) {
-    const int page = pw.fix_list[2 * e], rg = pw.fix_list[2 * e + 1];
+    // entry: page, global row, page start, page length
+    const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
+    const int page = ent.x, rg = ent.y, st = ent.z, ln = ent.w;
     const int h = rg / a.W, p = rg % a.W, g = h / a.group, row = rg - g * a.rows;
-    const int st = pw.start[page], ln = pw.len[page];
+    const float ov = tid < D ? rs.o[(size_t)rg * D + tid] : 0.f;
     const int qp = a.qpos[p];
+    const float ref = rs.lse2[rg];
+    const int s0 = st / sp.chunk, s1 = (st + ln - 1) / sp.chunk;
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    float lacc = 0.f;
+    // other splits' partial sums as they are (row group r takes splits r, r+RPR, ...)
+    for (int s = r; s < sp.n_splits; s += RPR) {
+      if (s >= s0 && s <= s1) continue;
+      const size_t idx = (size_t)(g * sp.n_splits + s) * sp.rows_pad + row;
+      const float ms = sp.part_m[idx];
+      const float w = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - ref);
+      const u32x4 o0 = ldg_u4(sp.part_o + idx * D + 8 * c);
+      const u32x4 o1 = ldg_u4(sp.part_o + idx * D + 8 * c + 4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        acc[j] = __builtin_fmaf(w, __uint_as_float(o0[j]), acc[j]);
+        acc[4 + j] = __builtin_fmaf(w, __uint_as_float(o1[j]), acc[4 + j]);
+      }
+      if (c == 0) lacc = __builtin_fmaf(w, sp.part_l[idx], lacc);
+    }
+    // the page's split(s) without the page, in float32
     float qv[8];
     {
       const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)p * a.q_row_stride;
@@ -754,140 +779,68 @@ __global__ __launch_bounds__(256) void page_fixup_kernel(AttnGeom a, AttnSplit s
 #pragma unroll
       for (int j = 0; j < 8; ++j) qv[j] = bf16_bits_to_float(chunk_elem(qc, j));
     }
-    // the row's reference: max over the splits' maxima
-    float M = -INFINITY;
-    for (int s = tid; s < sp.n_splits; s += 256)
-      M = fmaxf(M, sp.part_m[(size_t)(g * sp.n_splits + s) * sp.rows_pad + row]);
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
-    __syncthreads();
-    if ((tid & 63) == 0) sred[0][tid >> 6] = M;
-    __syncthreads();
-    M = fmaxf(fmaxf(sred[0][0], sred[0][1]), fmaxf(sred[0][2], sred[0][3]));
-    const int s0 = st / sp.chunk, s1 = (st + ln - 1) / sp.chunk;
-    float acc[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-    float lacc = 0.f;
-    if (kp == 0) {
-      // other splits' partial sums as they are (row group r takes splits r, r+RPR, ...)
-      for (int s = r; s < sp.n_splits; s += RPR) {
-        if (s >= s0 && s <= s1) continue;
-        const size_t idx = (size_t)(g * sp.n_splits + s) * sp.rows_pad + row;
-        const float ms = sp.part_m[idx];
-        if (ms == -INFINITY) continue;
-        const float w = __builtin_amdgcn_exp2f(ms - M);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[j] = __builtin_fmaf(w, sp.part_o[idx * D + 8 * c + j], acc[j]);
-        if (c == 0) lacc = __builtin_fmaf(w, sp.part_l[idx], lacc);
-      }
-    }
-    // this part's slice of the page's split(s), without the page, in float32
     const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
     const uint16_t* vh = a.v + (int64_t)g * a.kv_head_stride;
-    const int r_lo = s0 * sp.chunk, r_hi = min(a.S, (s1 + 1) * sp.chunk);
-    const int per = (r_hi - r_lo + kFixParts - 1) / kFixParts;
-    const int t_lo = min(r_hi, r_lo + kp * per), t_hi = min(r_hi, t_lo + per);
-    for (int sub = t_lo; sub < t_hi; sub += kFixChunk) {
-      const int n_sub = min(kFixChunk, t_hi - sub);
-      __syncthreads();
-      // scores and weights, 8 token rows per thread in flight
-      for (int i0 = r; i0 < n_sub; i0 += 8 * RPR) {
-        u32x4 kc[8];
+    const int t_lo = s0 * sp.chunk, t_hi = min(a.S, (s1 + 1) * sp.chunk);
+    for (int b0 = t_lo; b0 < t_hi; b0 += UNR * RPR) {
+      u32x4 kc[UNR], vc[UNR];
+      int pv[UNR];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int i = min(i0 + u * RPR, n_sub - 1);
-          kc[u] = ldg_u4(kh + (int64_t)(sub + i) * a.kv_tok_stride + 8 * c);
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int i = i0 + u * RPR;
-          float x = 0.f;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) x = __builtin_fmaf(qv[j], bf16_bits_to_float(chunk_elem(kc[u], j)), x);
-#pragma unroll
-          for (int off = TPR / 2; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
-          if (c == 0 && i < n_sub) {
-            const int t = sub + i;
-            const bool keep = ldg_i32(a.pos + t) <= qp && !(t >= st && t < st + ln);
-            sw[i] = keep ? __builtin_amdgcn_exp2f(__builtin_fmaf(x, a.sl2, -M)) : 0.f;
-          }
-        }
+      for (int u = 0; u < UNR; ++u) {
+        const int t = min(b0 + u * RPR + r, t_hi - 1);
+        kc[u] = ldg_u4(kh + (int64_t)t * a.kv_tok_stride + 8 * c);
+        vc[u] = ldg_u4(vh + (int64_t)t * a.kv_tok_stride + 8 * c);
+        pv[u] = ldg_i32(a.pos + t);
       }
-      __syncthreads();
-      for (int i0 = r; i0 < n_sub; i0 += 8 * RPR) {
-        u32x4 vc[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int i = min(i0 + u * RPR, n_sub - 1);
-          vc[u] = ldg_u4(vh + (int64_t)(sub + i) * a.kv_tok_stride + 8 * c);
-        }
+      for (int u = 0; u < UNR; ++u) {
+        const int t = b0 + u * RPR + r;
+        float x = 0.f;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int i = i0 + u * RPR;
-          const float w = i < n_sub ? sw[i] : 0.f;
+        for (int j = 0; j < 8; ++j) x = __builtin_fmaf(qv[j], bf16_bits_to_float(chunk_elem(kc[u], j)), x);
 #pragma unroll
-          for (int j = 0; j < 8; ++j) acc[j] = __builtin_fmaf(w, bf16_bits_to_float(chunk_elem(vc[u], j)), acc[j]);
-          if (c == 0) lacc += w;
-        }
+        for (int off = TPR / 2; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+        const bool keep = t < t_hi && pv[u] <= qp && !(t >= st && t < st + ln);
+        const float w = keep ? __builtin_amdgcn_exp2f(__builtin_fmaf(x, a.sl2, -ref)) : 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = __builtin_fmaf(w, bf16_bits_to_float(chunk_elem(vc[u], j)), acc[j]);
+        if (c == 0) lacc += w;
       }
     }
+    __syncthreads();
 #pragma unroll
     for (int j = 0; j < 8; ++j) sacc[r][8 * c + j] = acc[j];
-    if (c == 0) sl[r] = lacc;
+    if (c == 0) sacc[r][D] = lacc;
     __syncthreads();
-    // this part's (sum, weight) -> fix_part[e][kp]
-    float* part = pw.fix_part + ((size_t)e * kFixParts + kp) * (D + 1);
+    // o' = sum / weight, ratio = ||o - o'|| / ||o||
+    float den = 0.f;
+    for (int i = 0; i < RPR; ++i) den += sacc[i][D];
+    float dd = 0.f, oo = 0.f;
     if (tid < D) {
       float num = 0.f;
       for (int i = 0; i < RPR; ++i) num += sacc[i][tid];
-      part[tid] = num;
-    }
-    if (tid == 0) {
-      float den = 0.f;
-      for (int i = 0; i < RPR; ++i) den += sl[i];
-      part[D] = den;
-      __threadfence();
-      s_last = atomicAdd(&pw.fix_done[e], 1) == kFixParts - 1;
-    }
-    __syncthreads();
-    if (!s_last) continue;
-    // last part: merge in part order, o' = sum / weight, ratio = ||o - o'|| / ||o||
-    __threadfence();
-    float dd = 0.f, oo = 0.f;
-    const float* parts = pw.fix_part + (size_t)e * kFixParts * (D + 1);
-    if (tid < D) {
-      float num = 0.f, den = 0.f;
-      for (int k = 0; k < kFixParts; ++k) {
-        num += __hip_atomic_load(&parts[k * (D + 1) + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        den += __hip_atomic_load(&parts[k * (D + 1) + D], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-      const float ov = rs.o[(size_t)rg * D + tid];
       const float od = den > 0.f ? num / den : 0.f;
       dd = (ov - od) * (ov - od);
       oo = ov * ov;
-      if (tid == 0) sred[1][0] = den;
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
       dd += __shfl_xor(dd, off, 64);
       oo += __shfl_xor(oo, off, 64);
     }
-    __syncthreads();
-    if ((tid & 63) == 0 && tid < D) { sred[0][tid >> 6] = dd; sred[0][2 + (tid >> 6)] = oo; }
+    if ((tid & 63) == 0 && tid < D) { sred[0][tid >> 6] = dd; sred[1][tid >> 6] = oo; }
     __syncthreads();
     if (tid == 0) {
       const float D2 = sred[0][0] + (D > 64 ? sred[0][1] : 0.f);
-      const float O2 = sred[0][2] + (D > 64 ? sred[0][3] : 0.f);
-      const float den = sred[1][0];
+      const float O2 = sred[1][0] + (D > 64 ? sred[1][1] : 0.f);
       float ratio;
       if (!(den > 0.f)) ratio = INFINITY;
       else if (O2 > 0.f) ratio = sqrtf(D2) / sqrtf(O2);
       else ratio = D2 > 0.f ? INFINITY : 0.f;
       if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], ratio);
       atomic_max_nonneg(&pw.R[page], ratio);
-      pw.fix_done[e] = 0;       // ready for the next call
     }
+    __syncthreads();
   }
 }
 
@@ -1165,7 +1118,6 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats
 int rows_per_block_attention() { return kRowsWG; }
 int rows_per_block_page() { return kRowsWG; }
 int token_mass_max_rows() { return kMassMaxRows; }
-int fixup_parts() { return kFixParts; }
 
 hipError_t launch_window_attention(const AttnGeom& a, const AttnSplit& sp, hipStream_t s) {
   const int nrb = (a.rows + kRowsWG - 1) / kRowsWG;
@@ -1202,7 +1154,7 @@ hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowSt
 
 hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
                              const PageWork& pw, hipStream_t s) {
-  dim3 grid(std::min(pw.fix_cap, 256), kFixParts), block(256);
+  dim3 grid(std::min(pw.fix_cap, kFixGrid)), block(kFixT);
   if (a.D == 128) hipLaunchKernelGGL((page_fixup_kernel<128>), grid, block, 0, s, a, sp, rs, pw);
   else hipLaunchKernelGGL((page_fixup_kernel<64>), grid, block, 0, s, a, sp, rs, pw);
   return hipGetLastError();
