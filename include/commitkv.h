@@ -122,6 +122,11 @@ size_t ckv_workspace_bytes(const ckv_ctx* ctx);
  * launch count; idx past the last kernel returns CKV_ERR_ARG.
  * ckv_reset_kernel_stats zeroes the totals. */
 int ckv_set_kernel_timing(ckv_ctx* ctx, int enable);
+/* Restrict the timing to the kernel called `name` (as reported by
+ * ckv_kernel_stats); NULL or "" times every kernel again.  Each timed launch
+ * adds two event records to the stream, so a benchmark that times only its
+ * dominant kernel perturbs the rest of the step least. */
+int ckv_set_kernel_timing_only(ckv_ctx* ctx, const char* name);
 int ckv_kernel_stats(ckv_ctx* ctx, int32_t idx, const char** name,
                      double* total_ms, int64_t* launches);
 int ckv_reset_kernel_stats(ckv_ctx* ctx);
@@ -276,6 +281,21 @@ int ckv_joint_test(ckv_ctx* ctx, const ckv_kv_view* kv,
                    int32_t max_cand, float tau_joint, uint8_t* accepted,
                    float* union_R, int32_t* n_accepted);
 
+/* Pages retired by the joint test of the current commit, resolved on the
+ * device so that the checkpoint needs no host round trip (Algorithm 1: the
+ * accepted set joins the retired set before the budget is applied).  Page
+ * pages->start[cand[i]] .. + len[cand[i]] is retired when
+ * i < min(*n_cand, max_cand) and accepted[i] != 0.  `pages` is a host page
+ * list (the one given to ckv_joint_test); cand, n_cand and accepted are
+ * device arrays as produced by ckv_classify_pages and ckv_joint_test. */
+typedef struct ckv_accepted_pages {
+  const ckv_page_list* pages;
+  const int32_t* cand;       /* device int32[max_cand] */
+  const int32_t* n_cand;     /* device int32[1] */
+  const uint8_t* accepted;   /* device uint8[max_cand] */
+  int32_t max_cand;
+} ckv_accepted_pages;
+
 /*
  * Compression checkpoint (Sec. 3.3, Eq. (12)-(13); Sec. 3.1, Eq. (4)) for
  * in->n_seq sequences.  For sequence s:
@@ -284,8 +304,9 @@ int ckv_joint_test(ckv_ctx* ctx, const ckv_kv_view* kv,
  *      ascending, are protected while fewer than max_pending_pages are taken
  *      and their token total stays <= B_N = floor(eta * B); the first page
  *      that does not fit ends the protection.
- *   2. Token state: retired (in a page of retired[s]) > protected (protected
- *      page, or among the last keep_recent of n_tokens[s] tokens) > free.
+ *   2. Token state: retired (in a page of retired[s], or of accepted[s]
+ *      when `accepted` is not NULL) > protected (protected page, or among
+ *      the last keep_recent of n_tokens[s] tokens) > free.
  *   3. Retained set I: every protected token plus the
  *      min(B - #protected, #free) free tokens of highest score (float32
  *      score[s*score_seq_stride + t]; ties to the lower index; NaN ranks as
@@ -295,7 +316,8 @@ int ckv_joint_test(ckv_ctx* ctx, const ckv_kv_view* kv,
  *      Slots j >= |I| of `out` are left untouched.
  * Host arguments: n_tokens int32[n_seq]; retired, pending ckv_page_list[n_seq];
  * pending_r_pre: host array of n_seq device pointers (NULL allowed where
- * pending[s].n_pages == 0).  Device outputs: kept_idx int32[n_seq * B]
+ * pending[s].n_pages == 0); accepted: ckv_accepted_pages[n_seq] or NULL
+ * (an entry with cand == NULL adds nothing).  Device outputs: kept_idx int32[n_seq * B]
  * (row s holds I, entries past n_kept[s] are -1), n_kept int32[n_seq],
  * token_state uint8[n_seq * score_seq_stride] (optional).
  * Errors: CKV_ERR_BUDGET if keep_recent + B_N > B; CKV_ERR_ARG if `out`
@@ -307,6 +329,7 @@ int ckv_select_and_compact(ckv_ctx* ctx, const ckv_cache_view* in,
                            const ckv_page_list* retired,
                            const ckv_page_list* pending,
                            const float* const* pending_r_pre,
+                           const ckv_accepted_pages* accepted,
                            const ckv_budget* budget, const ckv_cache_view* out,
                            int32_t* kept_idx, int32_t* n_kept,
                            uint8_t* token_state);

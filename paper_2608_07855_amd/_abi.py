@@ -70,6 +70,11 @@ class CacheView(ctypes.Structure):
                 ("capacity", ctypes.c_int32)]
 
 
+class AcceptedPages(ctypes.Structure):
+    _fields_ = [("pages", ctypes.c_void_p), ("cand", ctypes.c_void_p), ("n_cand", ctypes.c_void_p),
+                ("accepted", ctypes.c_void_p), ("max_cand", ctypes.c_int32)]
+
+
 # name -> (restype, argtypes): every entry point of include/commitkv.h
 SIGNATURES = {
     "ckv_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int, ctypes.c_void_p]),
@@ -81,6 +86,7 @@ SIGNATURES = {
     "ckv_set_workspace_limit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t]),
     "ckv_workspace_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
     "ckv_set_kernel_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
+    "ckv_set_kernel_timing_only": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_char_p]),
     "ckv_kernel_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32,
                                         ctypes.POINTER(ctypes.c_char_p),
                                         ctypes.POINTER(ctypes.c_double),
@@ -102,7 +108,7 @@ SIGNATURES = {
     "ckv_select_and_compact": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.POINTER(CacheView), c_i32p, ctypes.c_void_p,
         ctypes.c_int64, ctypes.POINTER(PageList), ctypes.POINTER(PageList),
-        ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(Budget),
+        ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(AcceptedPages), ctypes.POINTER(Budget),
         ctypes.POINTER(CacheView), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
 }
 

@@ -15,7 +15,7 @@ import numpy as np
 import torch
 
 from . import _abi
-from ._abi import Budget, CacheView, KVView, PageList, Thresholds, WindowView
+from ._abi import AcceptedPages, Budget, CacheView, KVView, PageList, Thresholds, WindowView
 
 PAPER_THRESHOLDS = dict(tau_use=0.05, tau_dead=0.01, rho_use=0.75, rho_dead=0.25, tau_joint=0.01)
 
@@ -70,6 +70,11 @@ class Context:
 
     def set_kernel_timing(self, enable: bool):
         self.check(self._lib.ckv_set_kernel_timing(self.handle, int(bool(enable))))
+
+    def set_kernel_timing_only(self, name: str | None):
+        """Time only the kernel called ``name`` (None: every kernel)."""
+        self.check(self._lib.ckv_set_kernel_timing_only(
+            self.handle, None if name is None else name.encode()))
 
     def kernel_stats(self) -> dict:
         """{kernel name: (total ms, launches)} of the launches timed so far."""
@@ -226,7 +231,7 @@ def ckv_classify_pages(ctx: Context, R_pre, R_post, thresholds: dict | None = No
     P_pre = _f32(max(n, 1), dev)
     P_post = _f32(max(n, 1), dev)
     cand = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
-    n_cand = torch.zeros(1, dtype=torch.int32, device=dev)
+    n_cand = torch.empty(1, dtype=torch.int32, device=dev)     # written by the call
     ctx.check(lib().ckv_classify_pages(ctx.handle, n, _ptr(R_pre), _ptr(R_post), ctypes.byref(t),
                                        _ptr(force), int(max_cand), _ptr(lam), _ptr(P_pre),
                                        _ptr(P_post), _ptr(cand), _ptr(n_cand)))
@@ -238,7 +243,7 @@ def ckv_joint_test(ctx: Context, kv: KVView, win: WindowView, o, lse, pages: Pag
     dev = o.device
     accepted = torch.empty(max_cand, dtype=torch.uint8, device=dev)
     union_R = _f32(max_cand, dev)
-    n_acc = torch.zeros(1, dtype=torch.int32, device=dev)
+    n_acc = torch.empty(1, dtype=torch.int32, device=dev)      # written by the call
     pl = pages.view()
     ctx.check(lib().ckv_joint_test(ctx.handle, ctypes.byref(kv), ctypes.byref(win), _ptr(o),
                                    _ptr(lse), ctypes.byref(pl), _ptr(cand), _ptr(n_cand),
@@ -250,10 +255,13 @@ def ckv_joint_test(ctx: Context, kv: KVView, win: WindowView, o, lse, pages: Pag
 def ckv_select_and_compact(ctx: Context, k_in, v_in, pos_in, n_tokens, score, retired, pending,
                            pending_r_pre, *, budget: int, eta: float = 0.125,
                            max_pending_pages: int = 16, keep_recent: int = 0,
-                           k_out=None, v_out=None, pos_out=None, token_state=None):
+                           k_out=None, v_out=None, pos_out=None, token_state=None,
+                           accepted=None, kept=None, n_kept=None):
     """k_in, v_in: [n_seq, n_layers, Hkv, capacity, d] bf16; pos_in: [n_seq, capacity] int32;
     n_tokens: host ints [n_seq]; score: [n_seq, stride] fp32; retired, pending: lists of
-    Pages (one per sequence); pending_r_pre: list of fp32 device tensors (or None)."""
+    Pages (one per sequence); pending_r_pre: list of fp32 device tensors (or None).
+    accepted: optional list (one per sequence) of None or (Pages, cand, n_cand,
+    accepted flags, max_cand) -- pages retired on the device by the joint test."""
     ns, L, H, cap, d = k_in.shape
     dev = k_in.device
     if k_out is None:
@@ -261,9 +269,22 @@ def ckv_select_and_compact(ctx: Context, k_in, v_in, pos_in, n_tokens, score, re
         v_out = torch.empty_like(k_out)
     if pos_out is None:
         pos_out = torch.empty((ns, budget), dtype=torch.int32, device=dev)
-    kept = torch.empty((ns, budget), dtype=torch.int32, device=dev)
-    n_kept = torch.zeros(ns, dtype=torch.int32, device=dev)
+    if kept is None:
+        kept = torch.empty((ns, budget), dtype=torch.int32, device=dev)
+    if n_kept is None:
+        n_kept = torch.empty(ns, dtype=torch.int32, device=dev)   # written by the call
     cin, cout = cache_view(k_in, v_in, pos_in), cache_view(k_out, v_out, pos_out)
+    acc_arr, keep = None, []
+    if accepted is not None:
+        acc_arr = (AcceptedPages * ns)()
+        for s_, e in enumerate(accepted):
+            if e is None:
+                continue
+            pg, cand, ncand, flags, mc = e
+            pl = pg.view()
+            keep.append(pl)
+            acc_arr[s_] = AcceptedPages(ctypes.cast(ctypes.pointer(pl), ctypes.c_void_p), _ptr(cand),
+                                        _ptr(ncand), _ptr(flags), int(mc))
     nt = np.ascontiguousarray(n_tokens, dtype=np.int32)
     ret = (PageList * ns)(*[p.view() for p in retired])
     pen = (PageList * ns)(*[p.view() for p in pending])
@@ -271,6 +292,6 @@ def ckv_select_and_compact(ctx: Context, k_in, v_in, pos_in, n_tokens, score, re
     b = Budget(int(budget), float(eta), int(max_pending_pages), int(keep_recent))
     ctx.check(lib().ckv_select_and_compact(
         ctx.handle, ctypes.byref(cin), nt.ctypes.data_as(_abi.c_i32p), _ptr(score),
-        int(score.stride(0)), ret, pen, rptr, ctypes.byref(b), ctypes.byref(cout), _ptr(kept),
+        int(score.stride(0)), ret, pen, rptr, acc_arr, ctypes.byref(b), ctypes.byref(cout), _ptr(kept),
         _ptr(n_kept), _ptr(token_state)))
     return dict(k=k_out, v=v_out, pos=pos_out, kept=kept, n_kept=n_kept)

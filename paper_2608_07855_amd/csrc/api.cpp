@@ -16,6 +16,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <string>
 #include <vector>
 
 using namespace ckv;
@@ -76,6 +77,7 @@ struct ckv_ctx {
   hipEvent_t small_ev[2] = {nullptr, nullptr};
   // kernel timing (events around every launch when enabled)
   bool timing = false;
+  std::string timing_only;   // empty: every kernel
   struct Timed { int kid; hipEvent_t a, b; };
   std::vector<Timed> timed;
   std::vector<hipEvent_t> event_pool;
@@ -191,13 +193,15 @@ int resolve_timings(ckv_ctx* c) {
 #define CKV_LAUNCH(ctx, name, expr)                                   \
   do {                                                                \
     hipEvent_t ea_ = nullptr, eb_ = nullptr;                          \
-    if ((ctx)->timing) {                                              \
+    const bool timed_ = (ctx)->timing &&                              \
+        ((ctx)->timing_only.empty() || (ctx)->timing_only == (name)); \
+    if (timed_) {                                                     \
       CKV_HIP(ctx, pooled_event(ctx, &ea_));                          \
       CKV_HIP(ctx, pooled_event(ctx, &eb_));                          \
       CKV_HIP(ctx, hipEventRecord(ea_, (ctx)->stream));               \
     }                                                                 \
     CKV_HIP(ctx, (expr));                                             \
-    if ((ctx)->timing) {                                              \
+    if (timed_) {                                                     \
       CKV_HIP(ctx, hipEventRecord(eb_, (ctx)->stream));               \
       (ctx)->timed.push_back({kernel_id(ctx, name), ea_, eb_});       \
     }                                                                 \
@@ -449,6 +453,12 @@ extern "C" int ckv_set_workspace_limit(ckv_ctx* c, size_t bytes) {
 
 extern "C" size_t ckv_workspace_bytes(const ckv_ctx* c) { return c ? c->ws_cap : 0; }
 
+extern "C" int ckv_set_kernel_timing_only(ckv_ctx* c, const char* name) {
+  if (!c) return CKV_ERR_ARG;
+  c->timing_only = name ? name : "";
+  return CKV_OK;
+}
+
 extern "C" int ckv_set_kernel_timing(ckv_ctx* c, int enable) {
   if (!c) return CKV_ERR_ARG;
   DeviceGuard g(c->device);
@@ -695,7 +705,8 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
 extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, const int32_t* n_tokens,
                                       const float* score, int64_t score_seq_stride,
                                       const ckv_page_list* retired, const ckv_page_list* pending,
-                                      const float* const* pending_r_pre, const ckv_budget* budget,
+                                      const float* const* pending_r_pre,
+                                      const ckv_accepted_pages* accepted, const ckv_budget* budget,
                                       const ckv_cache_view* out, int32_t* kept_idx, int32_t* n_kept,
                                       uint8_t* token_state) {
   if (!c) return CKV_ERR_ARG;
@@ -732,6 +743,11 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
       return rc;
     if (pending[s].n_pages > 0 && (!pending_r_pre || !pending_r_pre[s]))
       return fail(c, CKV_ERR_ARG, "sequence %d: pending R_pre is NULL", s);
+    if (accepted && accepted[s].cand) {
+      if (!accepted[s].pages || !accepted[s].n_cand || !accepted[s].accepted || accepted[s].max_cand < 1)
+        return fail(c, CKV_ERR_ARG, "sequence %d: incomplete accepted-page arguments", s);
+      if ((rc = check_pages(c, accepted[s].pages, n_tokens[s], "accepted")) != 0) return rc;
+    }
   }
   // the output must not overlap the input (bytes of K, V and positions)
   auto extent = [](const ckv_cache_view* v) {
@@ -757,7 +773,24 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   if (overlap(out->k, eo, out->v, eo)) return fail(c, CKV_ERR_ARG, "output K and V overlap");
   DeviceGuard g(c->device);
 
-  // pack every host-side list into one blob: [pend_r ptrs][n_tokens][ret_off][pend_off][ret start,len][pend start,len]
+  // accepted pages of this commit: device page tables (cached by content)
+  std::vector<AccPages> acc(ns);
+  bool any_acc = false;
+  for (int s = 0; s < ns && accepted; ++s) {
+    if (!accepted[s].cand) continue;
+    AccPages& e = acc[s];
+    int rc2 = page_table(c, accepted[s].pages, &e.start, &e.len);
+    if (rc2) return rc2;
+    e.cand = accepted[s].cand;
+    e.n_cand = accepted[s].n_cand;
+    e.accepted = accepted[s].accepted;
+    e.max_cand = accepted[s].max_cand;
+    e.n_pages = accepted[s].pages->n_pages;
+    if (e.n_pages > 0) any_acc = true;
+    else e.cand = nullptr;
+  }
+
+  // pack every host-side list into one blob: [accepted][pend_r ptrs][n_tokens][ret_off][pend_off][ret start,len][pend start,len]
   int tot_r = 0, tot_p = 0;
   for (int s = 0; s < ns; ++s) {
     tot_r += retired[s].n_pages;
@@ -777,9 +810,11 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   for (int s = 0; s < ns; ++s) blob32.insert(blob32.end(), retired[s].len, retired[s].len + retired[s].n_pages);
   for (int s = 0; s < ns; ++s) blob32.insert(blob32.end(), pending[s].start, pending[s].start + pending[s].n_pages);
   for (int s = 0; s < ns; ++s) blob32.insert(blob32.end(), pending[s].len, pending[s].len + pending[s].n_pages);
-  std::vector<char> blob(blob64.size() * 8 + blob32.size() * 4);
-  std::memcpy(blob.data(), blob64.data(), blob64.size() * 8);
-  std::memcpy(blob.data() + blob64.size() * 8, blob32.data(), blob32.size() * 4);
+  const size_t acc_bytes = any_acc ? acc.size() * sizeof(AccPages) : 0;
+  std::vector<char> blob(acc_bytes + blob64.size() * 8 + blob32.size() * 4);
+  if (acc_bytes) std::memcpy(blob.data(), acc.data(), acc_bytes);
+  std::memcpy(blob.data() + acc_bytes, blob64.data(), blob64.size() * 8);
+  std::memcpy(blob.data() + acc_bytes + blob64.size() * 8, blob32.data(), blob32.size() * 4);
 
   char* dblob = nullptr;
   SelectArgs sa{};
@@ -797,9 +832,10 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   int rc = realize(c, plan);
   if (rc) return rc;
   if ((rc = upload(c, blob.data(), blob.size(), dblob))) return rc;
-  const int32_t* d32 = reinterpret_cast<const int32_t*>(dblob + blob64.size() * 8);
+  const int32_t* d32 = reinterpret_cast<const int32_t*>(dblob + acc_bytes + blob64.size() * 8);
   sa.n_seq = ns;
-  sa.pend_r = reinterpret_cast<const uint64_t*>(dblob);
+  sa.acc = acc_bytes ? reinterpret_cast<const AccPages*>(dblob) : nullptr;
+  sa.pend_r = reinterpret_cast<const uint64_t*>(dblob + acc_bytes);
   sa.n_tokens = d32;
   sa.ret_off = d32 + ns;
   sa.pend_off = d32 + ns + (ns + 1);

@@ -127,8 +127,21 @@ hipError_t launch_joint_round(const JointArgs& j, hipStream_t s);
 hipError_t launch_joint_init(const JointArgs& j, hipStream_t s);
 
 // checkpoint: protection, selection, compaction (Eq. (12)-(13), Eq. (4))
+// pages retired on the device: page cand[i] (i < min(*n_cand, max_cand))
+// of the table (start, len) when accepted[i] != 0
+struct AccPages {
+  const int32_t* cand;
+  const int32_t* n_cand;
+  const uint8_t* accepted;
+  const int32_t* start;
+  const int32_t* len;
+  int32_t max_cand;
+  int32_t n_pages;
+};
+
 struct SelectArgs {
   int n_seq;
+  const AccPages* acc;           // [n_seq] or nullptr
   const int32_t* n_tokens;       // [n_seq]
   const float* score;
   int64_t score_seq_stride;

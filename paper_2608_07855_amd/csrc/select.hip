@@ -216,6 +216,18 @@ __global__ __launch_bounds__(kSelT) void sel_keys(SelectArgs a) {
       const int t = a.ret_start[off + i] + e;
       if (e < a.ret_len[off + i] && t >= t0 && t < t1) st[t - t0] = kRet;
     }
+    if (a.acc && a.acc[s].cand) {
+      const AccPages ap = a.acc[s];
+      const int nc = min(*ap.n_cand, ap.max_cand);
+      for (int idx = tid; idx < nc * kMaxPage; idx += kSelT) {
+        const int i = idx / kMaxPage, e = idx % kMaxPage;
+        if (!ap.accepted[i]) continue;
+        const int pg = ap.cand[i];
+        if (pg < 0 || pg >= ap.n_pages || e >= ap.len[pg]) continue;
+        const int t = ap.start[pg] + e;
+        if (t >= t0 && t < t1) st[t - t0] = kRet;
+      }
+    }
   }
   __syncthreads();
   const float* sc = a.score + (size_t)s * a.score_seq_stride;

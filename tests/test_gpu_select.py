@@ -43,8 +43,27 @@ def _oracle_keep(S, score, retired, pending, r_pre, B, eta, max_pages, keep_rece
     return O.select_tokens(score, st, B), st
 
 
+def _accepted_form(P, rng, allp, retired):
+    """Half of the retired pages as a host list; the other half as accepted
+    flags over a shuffled candidate list of a page table (with rejected
+    decoys, and accepted-looking entries past n_cand that must be ignored)."""
+    table = sorted(set(allp) | set(retired))
+    index = {p: i for i, p in enumerate(table)}
+    dev_ret, host_ret = retired[::2], retired[1::2]
+    decoys = [p for p in table if p not in set(retired)][: max(1, len(dev_ret))]
+    entries = [(index[p], 1) for p in dev_ret] + [(index[p], 0) for p in decoys]
+    rng.shuffle(entries)
+    n = len(entries)
+    pad = [(index[p], 1) for p in decoys[:3]]            # beyond n_cand: ignored
+    cand = torch.tensor([e[0] for e in entries + pad], dtype=torch.int32).cuda()
+    flags = torch.tensor([e[1] for e in entries + pad], dtype=torch.uint8).cuda()
+    n_cand = torch.tensor([n], dtype=torch.int32).cuda()
+    tab = P.Pages([p[0] for p in table], [p[1] for p in table])
+    return host_ret, (tab, cand, n_cand, flags, n + len(pad))
+
+
 def _run(P, ctx, n_seq, n_layers, H, d, cap, n_tokens, B, seed, keep_recent=0, eta=0.125,
-         max_pages=16, ties=False, nan=False):
+         max_pages=16, ties=False, nan=False, accepted=False):
     rng = np.random.default_rng(seed)
     k = torch.randint(-32768, 32767, (n_seq, n_layers, H, cap, d), dtype=torch.int16).view(torch.bfloat16).cuda()
     v = torch.randint(-32768, 32767, (n_seq, n_layers, H, cap, d), dtype=torch.int16).view(torch.bfloat16).cuda()
@@ -54,7 +73,7 @@ def _run(P, ctx, n_seq, n_layers, H, d, cap, n_tokens, B, seed, keep_recent=0, e
     if nan:
         score[:, ::97] = np.nan
         score[:, 5::101] = -0.0
-    retired, pending, rpre = [], [], []
+    retired, pending, rpre, tables = [], [], [], []
     for s in range(n_seq):
         S = n_tokens[s]
         allp = _pages(rng, S, max(4, S // 80))
@@ -64,17 +83,23 @@ def _run(P, ctx, n_seq, n_layers, H, d, cap, n_tokens, B, seed, keep_recent=0, e
         if s == 0 and ret and pen:
             pen = sorted(set(pen) | {ret[0]})     # a page both retired and pending
         retired.append(ret)
+        tables.append(allp)
         pending.append(pen)
         r = rng.uniform(0, 1, len(pen)).astype(np.float32)
         if len(r) > 3:
             r[1] = r[2]                            # tie in R-
         rpre.append(r)
+    host_retired, acc = retired, None
+    if accepted:
+        forms = [_accepted_form(P, rng, tables[s], retired[s]) for s in range(n_seq)]
+        host_retired = [f[0] for f in forms]
+        acc = [f[1] for f in forms]
     out = P.ckv_select_and_compact(
         ctx, k, v, pos, n_tokens, torch.from_numpy(score).cuda(),
-        [P.Pages([p[0] for p in r], [p[1] for p in r]) for r in retired],
+        [P.Pages([p[0] for p in r], [p[1] for p in r]) for r in host_retired],
         [P.Pages([p[0] for p in r], [p[1] for p in r]) for r in pending],
         [torch.from_numpy(r).cuda() if len(r) else None for r in rpre],
-        budget=B, eta=eta, max_pending_pages=max_pages, keep_recent=keep_recent)
+        budget=B, eta=eta, max_pending_pages=max_pages, keep_recent=keep_recent, accepted=acc)
     torch.cuda.synchronize()
     kept = out["kept"].cpu().numpy()
     nk = out["n_kept"].cpu().numpy()
@@ -113,6 +138,13 @@ def test_budget_exceeds_cache(ckv):
 def test_protection_fills_pending_budget(ckv):
     P, ctx = ckv
     _run(P, ctx, 2, 1, 1, 64, 4000, [4000, 3999], 256, seed=4, eta=1.0, max_pages=100)
+
+
+def test_retired_on_device(ckv):
+    """Retired pages given partly as a host list and partly as accepted
+    flags over a device candidate list (the joint test's output)."""
+    P, ctx = ckv
+    _run(P, ctx, 2, 2, 2, 128, 6000, [6000, 4100], 1200, seed=6, keep_recent=64, accepted=True)
 
 
 def test_long_cache_q32b_shape(ckv):
