@@ -374,9 +374,15 @@ AttnGeom make_geom(const ckv_kv_view* kv, const ckv_window_view* w) {
   return a;
 }
 
+int max_page_len(const ckv_page_list* pl) {
+  int m = 0;
+  for (int i = 0; i < pl->n_pages; ++i) m = std::max(m, (int)pl->len[i]);
+  return m;
+}
+
 int items_per_block(int n_items, int other_blocks) {
   const int per = ceil_div(n_items * std::max(other_blocks, 1), kTargetBlocks);
-  return std::max(1, per);
+  return std::min(ckv::kPageItemsMax, std::max(1, per));
 }
 
 }  // namespace
@@ -553,7 +559,7 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
     pw.fix_list = fix_list;
     pw.fix_count = fix_count;
     pw.fix_cap = total_rows;
-    CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, rs, 0, c->stream));
+    CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, rs, 0, max_page_len(pages), c->stream));
     CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, sp, rs, pw, c->stream));
   }
   if (token_mass) {
@@ -681,7 +687,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
     pw.resA = resA;
     pw.resC = resC;
     pw.total_rows = total_rows;
-    CKV_LAUNCH(c, "joint_residual", launch_page_kernel(a, pw, rs, 1, c->stream));
+    CKV_LAUNCH(c, "joint_residual", launch_page_kernel(a, pw, rs, 1, max_page_len(pages), c->stream));
     // Each round decides at least one candidate, so n_eff rounds always
     // suffice.  Rounds go out in chunks; the done flag of chunk k-2 is read
     // before chunk k is launched, so at most two chunks run past the end.

@@ -73,12 +73,13 @@ __device__ __forceinline__ int vt_slot(int t) {
 }
 
 // Stored column of slot s in row r of the V^T tile: the 8-slot (16-byte)
-// group index is XOR-ed with bits 3..5 of the row.  A 16-byte read of eight
-// consecutive rows at one group then still covers all 32 banks, and the
-// transposing 4-byte writes of sixteen rows 8 apart (one 16-byte chunk of V
-// per lane) land in distinct groups instead of one bank.
+// group index is XOR-ed with bits 4..6 of the row.  With the padded row
+// stride (36 dwords) and gfx950's 64 LDS banks, a 16-byte read of sixteen
+// consecutive rows at one group stays conflict-free, and the transposing
+// 4-byte writes of sixteen rows 8 apart (one 16-byte chunk of V per lane)
+// spread over distinct bank groups instead of a few.
 __device__ __forceinline__ int vt_col(int r, int s) {
-  return (((s >> 3) ^ (r >> 3)) & 7) << 3 | (s & 7);
+  return (((s >> 3) ^ (r >> 4)) & 7) << 3 | (s & 7);
 }
 
 // loads through the global address space (pointers inside by-value argument

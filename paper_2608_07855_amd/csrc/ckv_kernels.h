@@ -41,6 +41,8 @@ struct RowStats {
 };
 
 // pages processed by pass B (MODE 0: item = page; MODE 1: item t = page cand[t])
+constexpr int kPageItemsMax = 256;   // pages (or candidates) per page-kernel workgroup
+
 struct PageWork {
   const int32_t* start;
   const int32_t* len;
@@ -77,7 +79,7 @@ hipError_t launch_window_attention(const AttnGeom& a, const AttnSplit& sp, hipSt
 hipError_t launch_combine(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs, float* lse_out,
                           const ZeroList& zl, hipStream_t s);
 hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowStats& rs, int mode,
-                              hipStream_t s);
+                              int max_len, hipStream_t s);
 hipError_t launch_token_mass(const AttnGeom& a, const RowStats& rs, float* mass, int chunk,
                              hipStream_t s);
 hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,

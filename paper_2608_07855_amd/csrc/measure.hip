@@ -124,7 +124,7 @@ struct Stager {
       const int u = tid + i * NT;
       if (u < VU) {
         const int tp = u / CPR, cg = u % CPR;
-        // rows cg*8 .. cg*8+7 share bits 3..5, hence one stored column
+        // rows cg*8 .. cg*8+7 share bits 4..6, hence one stored column
         const int col = vt_col(cg * 8, vt_slot(2 * tp));
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -471,7 +471,8 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
 // 32-token slot) or one page of 33..64 tokens (both slots).  Every thread
 // derives the same tile sequence from the page lengths.
 // ---------------------------------------------------------------------------
-template <int D, int MODE>
+// NB: 32-token slots a page may span (1 when every page has <= 32 tokens).
+template <int D, int MODE, int NB>
 __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork pw, RowStats rs) {
   constexpr int NT = kNW * 64, KS = D / 16, DB = D / 32;
   constexpr int NH = kRowsWG + 2;     // bound on the heads touched by one workgroup
@@ -482,6 +483,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   __shared__ int sFull[2][2];
   __shared__ unsigned int sMax[2][2][NH];   // [buffer][page of the tile][local head]
   __shared__ int sMin;
+  __shared__ int sItStart[kPageItemsMax], sItLen[kPageItemsMax];   // this block's pages
 
   const int g = blockIdx.z, rblk = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -494,9 +496,19 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
   const uint16_t* vh = a.v + (int64_t)g * a.kv_head_stride;
 
+  // the block's page spans go to LDS once, so the tile sequence never waits
+  // on a global load inside the loop (a wait there would also drain the
+  // loads issued ahead); an invalid candidate index is an empty page
+  for (int i = tid; i < i_end - i_begin; i += NT) {
+    const int item = i_begin + i;
+    const int pg = MODE == 0 ? item : pw.cand[item];
+    const bool ok = pg >= 0 && pg < pw.n_pages;
+    sItStart[i] = ok ? pw.start[pg] : 0;
+    sItLen[i] = ok ? pw.len[pg] : 0;
+  }
   const RowInfo ri = row_info(a, g, rblk * kRowsWG + wave * 32 + col);
   const bool wave_on = __ballot(ri.ok) != 0ull;
-  const int minq = block_min_qpos(ri, &sMin);
+  const int minq = block_min_qpos(ri, &sMin);    // its barriers also publish the page spans
   bf16x8 qf[KS];
   load_q<D>(a, g, ri, half, qf);
   // o_p in accumulator layout: register r of block db holds width 32db + 8(r/4) + 4h + r%4
@@ -524,10 +536,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   if (MODE == 0)
     for (int i = tid; i < 2 * 2 * NH; i += NT) (&sMax[0][0][0])[i] = 0u;
 
-  auto page_of = [&](int item) { return MODE == 0 ? item : pw.cand[item]; };
-  auto page_ok = [&](int pg) { return pg >= 0 && pg < pw.n_pages; };
-  auto pstart = [&](int item) { const int pg = page_of(item); return page_ok(pg) ? pw.start[pg] : 0; };
-  auto plen = [&](int item) { const int pg = page_of(item); return page_ok(pg) ? pw.len[pg] : 0; };
+  auto pstart = [&](int item) { return sItStart[item - i_begin]; };
+  auto plen = [&](int item) { return sItLen[item - i_begin]; };
   // pages in the tile that starts at item `it`: two short pages share a tile
   auto tile_items = [&](int it) {
     return (it + 1 < i_end && plen(it) <= 32 && plen(it + 1) <= 32) ? 2 : 1;
@@ -573,11 +583,11 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
       const int item = it + ps;
       const int len = plen(item);
       // a short page occupies slot ps; a long one both slots from slot 0
-      const int nblk = (m == 2) ? 1 : (len > 32 ? 2 : 1);
+      const int nblk = (NB == 1 || m == 2) ? 1 : (len > 32 ? 2 : 1);
       const int slot0 = ps;
       f32x16 s[2];
       s[0] = scores<D, St::KP>(sK[b], slot0, col, half, qf);
-      s[1] = nblk == 2 ? scores<D, St::KP>(sK[b], 1, col, half, qf) : zero16();
+      if (NB == 2) s[1] = nblk == 2 ? scores<D, St::KP>(sK[b], 1, col, half, qf) : zero16();
       // Offsets past the page's length carry position INT_MAX, so the
       // position test alone masks them (window positions are < INT_MAX).
       // A slot whose every position is <= the workgroup's smallest window
@@ -621,7 +631,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
       float ls = 0.f;
       f16x8 h0[2], h1[2];
       to_f16(s[0], h0, ls);
-      if (nblk == 2) {
+      if (NB == 2 && nblk == 2) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[1][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1][r], a.sl2, -base));
         to_f16(s[1], h1, ls);
@@ -638,7 +648,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
 #pragma unroll
         for (int j = 0; j < 2; ++j) u[j] = of[2 * hh + j] * (-lhat);
         pv_half<D, St::VP>(sV[b], slot0, col, half, h0, 2 * hh, u);
-        if (nblk == 2) pv_half<D, St::VP>(sV[b], 1, col, half, h1, 2 * hh, u);
+        if (NB == 2 && nblk == 2) pv_half<D, St::VP>(sV[b], 1, col, half, h1, 2 * hh, u);
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -1137,18 +1147,25 @@ hipError_t launch_combine(const AttnGeom& a, const AttnSplit& sp, const RowStats
 }
 
 hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowStats& rs, int mode,
-                              hipStream_t s) {
+                              int max_len, hipStream_t s) {
   const int nrb = (a.rows + kRowsWG - 1) / kRowsWG;
   const int nblk = (pw.n_items + pw.items_per_block - 1) / pw.items_per_block;
   if (nblk == 0) return hipSuccess;
   dim3 grid(nblk, nrb, a.Hkv), block(kNW * 64);
+  const bool two = max_len > 32;
+#define CKV_PAGE_LAUNCH(DD, MM)                                                                  \
+  do {                                                                                           \
+    if (two) hipLaunchKernelGGL((page_kernel<DD, MM, 2>), grid, block, 0, s, a, pw, rs);         \
+    else hipLaunchKernelGGL((page_kernel<DD, MM, 1>), grid, block, 0, s, a, pw, rs);             \
+  } while (0)
   if (a.D == 128) {
-    if (mode == 0) hipLaunchKernelGGL((page_kernel<128, 0>), grid, block, 0, s, a, pw, rs);
-    else hipLaunchKernelGGL((page_kernel<128, 1>), grid, block, 0, s, a, pw, rs);
+    if (mode == 0) CKV_PAGE_LAUNCH(128, 0);
+    else CKV_PAGE_LAUNCH(128, 1);
   } else {
-    if (mode == 0) hipLaunchKernelGGL((page_kernel<64, 0>), grid, block, 0, s, a, pw, rs);
-    else hipLaunchKernelGGL((page_kernel<64, 1>), grid, block, 0, s, a, pw, rs);
+    if (mode == 0) CKV_PAGE_LAUNCH(64, 0);
+    else CKV_PAGE_LAUNCH(64, 1);
   }
+#undef CKV_PAGE_LAUNCH
   return hipGetLastError();
 }
 
