@@ -32,9 +32,11 @@ namespace ckv {
 
 constexpr int kNW = 8;               // waves per workgroup
 constexpr int kRowsWG = 32 * kNW;    // window rows per workgroup
-// The running output is rescaled whenever a row's max grows (the wave skips
-// the rescale when no row's max grew), so the dominant token's float16 weight
-// is exactly 1 in both passes.
+// The running reference of a row (log2 units) moves only when the row's
+// max exceeds it by more than kLazyRef, so the float16 weights stay in
+// (0, 2^kLazyRef] (well inside float16 range, same relative precision) and
+// the wave rescales its output only on such a jump, not at every new max.
+constexpr float kLazyRef = 8.f;
 //
 // A page that holds nearly all of a row's mass (A -> 1) is ill-conditioned
 // for Eq. (6): o - u = (1 - A) o' keeps only the digits of o' that survive
@@ -65,7 +67,8 @@ struct Stager {
 
   u32x4 kr[KPT];
   u32x4 vr[VPT][2];
-  int pr;
+  int pr;        // loaded position (its use waits for the load: only in commit)
+  bool pok;      // false: offset outside the segments, position INT_MAX
 
   __device__ __forceinline__ static int tok(int off, int s0, int n0, int s1, int n1, bool& ok) {
     if (off < 32) { ok = off < n0; return s0 + off; }
@@ -106,8 +109,8 @@ struct Stager {
     int t = tok(tid & 63, s0, n0, s1, n1, ok);
     ok = ok && tid < kTile;
     t = ok ? t : 0;
-    const int pv = ldg_i32(pos + t);
-    pr = ok ? pv : INT_MAX;
+    pr = ldg_i32(pos + t);
+    pok = ok;
   }
 
   // writes the tile; wave 0 also flags, per 32-token slot, whether every
@@ -137,8 +140,9 @@ struct Stager {
       }
     }
     if (tid < kTile) {
-      sP[tid] = pr;
-      const unsigned long long late = __ballot(pr > minq);
+      const int p = pok ? pr : INT_MAX;
+      sP[tid] = p;
+      const unsigned long long late = __ballot(p > minq);
       if (tid == 0) {
         sFull[0] = (late & 0xFFFFFFFFull) == 0ull;
         sFull[1] = (late >> 32) == 0ull;
@@ -329,8 +333,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
           }
       }
       mx = max32(mx) * a.sl2;
-      // rescale the running output when a row max grew
-      const bool need = mx > mref;
+      // rescale the running output when a row max outgrew the reference
+      const bool need = mx > mref + kLazyRef;
       if (__ballot(need) != 0ull) {
         const float nref = need ? mx : mref;
         const float alpha = need ? __builtin_amdgcn_exp2f(mref - nref) : 1.f;
@@ -542,18 +546,21 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   auto tile_items = [&](int it) {
     return (it + 1 < i_end && plen(it) <= 32 && plen(it + 1) <= 32) ? 2 : 1;
   };
-  // Loads run two tiles ahead of the math (stager A: even tiles, B: odd);
-  // a tile that starts at or past i_end is an empty segment.
+  // The next tile's loads are issued before the current tile's math; a tile
+  // that starts at or past i_end is an empty segment.
   auto issue_tile = [&](St& st, int it) {
-    if (it >= i_end) {
-      st.issue(kh, vh, a.kv_tok_stride, a.pos, 0, 0, 0, 0, tid);
-      return;
-    }
-    const int s0 = pstart(it), l0 = plen(it);
-    if (tile_items(it) == 2)
-      st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, l0, pstart(it + 1), plen(it + 1), tid);
-    else
-      st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, min(l0, 32), s0 + 32, max(0, l0 - 32), tid);
+    // branch-free, so every path leaves the loads in the same registers
+    // and nothing waits for them before the commit
+    const bool any = it < i_end;
+    const int i0 = any ? it : i_begin;
+    const bool two = any && tile_items(i0) == 2;
+    const int l0 = any ? plen(i0) : 0;
+    const int s0 = pstart(i0);
+    const int i1 = min(i0 + 1, i_end - 1);
+    const int s1 = two ? pstart(i1) : s0 + 32;
+    const int n0 = two ? l0 : min(l0, 32);
+    const int n1 = two ? plen(i1) : max(0, l0 - 32);
+    st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, n0, s1, n1, tid);
   };
   auto next_tile = [&](int it) { return it < i_end ? it + tile_items(it) : i_end; };
   // A row sees at least nvis tokens; a page (at most kMaxPage tokens) can
@@ -1033,7 +1040,7 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats
     }
   }
 
-  struct KStage { u32x4 kr[KPT]; int pr; };
+  struct KStage { u32x4 kr[KPT]; int pr; bool pok; };   // position used only in commit
   KStage sa, sb;
   const int n_tiles = (t_end - t_begin + kTile - 1) / kTile;
   auto issue = [&](KStage& st, int it) {
@@ -1046,9 +1053,8 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats
       const bool ok = c < KCH && tr < nv;
       st.kr[i] = ldg_u4(kh + (int64_t)(ok ? t0 + tr : 0) * a.kv_tok_stride + (c % CPR) * 8);
     }
-    const bool okp = tid < nv;
-    const int pv = ldg_i32(a.pos + (okp ? t0 + tid : 0));
-    st.pr = okp ? pv : INT_MAX;
+    st.pok = tid < nv;
+    st.pr = ldg_i32(a.pos + (st.pok ? t0 + tid : 0));
   };
   auto commit = [&](const KStage& st, int b) {
 #pragma unroll
@@ -1057,8 +1063,9 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats
       if (c < KCH) *reinterpret_cast<u32x4*>(&sK[b][(c / CPR) * KP + (c % CPR) * 8]) = st.kr[i];
     }
     if (tid < kTile) {
-      sP[b][tid] = st.pr;
-      const unsigned long long late = __ballot(st.pr > minq);
+      const int p = st.pok ? st.pr : INT_MAX;
+      sP[b][tid] = p;
+      const unsigned long long late = __ballot(p > minq);
       if (tid == 0) sFull[b] = late == 0ull;
     }
   };
