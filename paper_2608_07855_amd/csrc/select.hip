@@ -38,7 +38,11 @@ __device__ __forceinline__ uint32_t score_key(float f) {
 
 __device__ __forceinline__ float pend_key(float f) { return f != f ? -INFINITY : f; }
 
+constexpr int kProtLds = 1024;   // pending pages ranked from LDS (more: from global memory)
+
 __global__ __launch_bounds__(256) void protect_kernel(SelectArgs a) {
+  __shared__ float sR[kProtLds];
+  __shared__ int sLen[kProtLds], sOrd[kProtLds];
   const int s = blockIdx.x;
   const int off = a.pend_off[s];
   const int n = a.pend_off[s + 1] - off;
@@ -46,28 +50,37 @@ __global__ __launch_bounds__(256) void protect_kernel(SelectArgs a) {
   const int32_t* len = a.pend_len + off;
   uint8_t* prot = a.pend_prot + off;
   int32_t* ord = a.pend_ord + off;
+  const bool lds = n <= kProtLds;
   // clear the selection state of this sequence for the kernels that follow
   for (int i = threadIdx.x; i < kSelCtrl; i += 256) a.ctrl[(size_t)s * kSelCtrl + i] = 0;
   for (int i = threadIdx.x; i < 3 * kSelBins; i += 256) a.hist[(size_t)s * 3 * kSelBins + i] = 0u;
+  if (lds)
+    for (int i = threadIdx.x; i < n; i += 256) {
+      sR[i] = pend_key(R[i]);
+      sLen[i] = len[i];
+    }
+  __syncthreads();
   for (int i = threadIdx.x; i < n; i += 256) {
-    const float ri = pend_key(R[i]);
+    const float ri = lds ? sR[i] : pend_key(R[i]);
     int rank = 0;
     for (int j = 0; j < n; ++j) {
-      const float rj = pend_key(R[j]);
+      const float rj = lds ? sR[j] : pend_key(R[j]);
       rank += (rj > ri || (rj == ri && j < i)) ? 1 : 0;
     }
-    ord[rank] = i;
+    if (lds) sOrd[rank] = i;
+    else ord[rank] = i;
     prot[i] = 0;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     int taken = 0, tok = 0;
     for (int r = 0; r < n; ++r) {
-      const int i = ord[r];
-      if (taken >= a.max_pages || tok + len[i] > a.bn) break;
+      const int i = lds ? sOrd[r] : ord[r];
+      const int li = lds ? sLen[i] : len[i];
+      if (taken >= a.max_pages || tok + li > a.bn) break;
       prot[i] = 1;
       ++taken;
-      tok += len[i];
+      tok += li;
     }
   }
 }
