@@ -32,11 +32,14 @@ namespace ckv {
 
 constexpr int kNW = 8;               // waves per workgroup
 constexpr int kRowsWG = 32 * kNW;    // window rows per workgroup
-// The running reference of a row (log2 units) moves only when the row's
-// max exceeds it by more than kLazyRef, so the float16 weights stay in
-// (0, 2^kLazyRef] (well inside float16 range, same relative precision) and
-// the wave rescales its output only on such a jump, not at every new max.
-constexpr float kLazyRef = 8.f;
+// The running output is rescaled whenever a row's max grows (the wave skips
+// the rescale when no row's max grew), so the float16 weight of a row's
+// largest logit is exactly 1, as it is in the per-page pass (whose reference
+// is the page's own max).  A page that carries most of a row's mass then
+// enters o and its own sum with the same weight, which keeps the residual
+// u - A o of Eq. (6) free of that token's rounding; a reference that lags
+// the max (weights above 1) was measured to cost ~10x in score error on
+// such pages.
 //
 // A page that holds nearly all of a row's mass (A -> 1) is ill-conditioned
 // for Eq. (6): o - u = (1 - A) o' keeps only the digits of o' that survive
@@ -333,8 +336,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
           }
       }
       mx = max32(mx) * a.sl2;
-      // rescale the running output when a row max outgrew the reference
-      const bool need = mx > mref + kLazyRef;
+      // rescale the running output when a row max grew
+      const bool need = mx > mref;
       if (__ballot(need) != 0ull) {
         const float nref = need ? mx : mref;
         const float alpha = need ? __builtin_amdgcn_exp2f(mref - nref) : 1.f;
