@@ -319,6 +319,10 @@ int check_kv(ckv_ctx* c, const ckv_kv_view* kv) {
     return fail(c, CKV_ERR_ARG, "K/V rows must be 16-byte aligned (strides multiples of 8)");
   if (kv->tok_stride < kv->head_dim || kv->head_stride < 0)
     return fail(c, CKV_ERR_SHAPE, "K/V strides too small");
+  // the kernels address a token of one head with a 32-bit element offset
+  // (24-bit multiply of token index and stride)
+  if (kv->tok_stride >= (1 << 24) || (int64_t)kv->n_tokens * kv->tok_stride >= ((int64_t)1 << 31))
+    return fail(c, CKV_ERR_UNSUPPORTED, "n_tokens * tok_stride must stay below 2^31 elements");
   return CKV_OK;
 }
 

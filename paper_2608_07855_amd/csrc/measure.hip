@@ -73,27 +73,30 @@ struct Stager {
   int pr;        // loaded position (its use waits for the load: only in commit)
   bool pok;      // false: offset outside the segments, position INT_MAX
 
-  __device__ __forceinline__ static int tok(int off, int s0, int n0, int s1, int n1, bool& ok) {
-    if (off < 32) { ok = off < n0; return s0 + off; }
-    ok = off - 32 < n1;
-    return s1 + off - 32;
+  // element offset of tile row r (0..63) inside the head; rows outside the
+  // segments read token 0.  r depends only on the thread, so the slot test
+  // is a per-thread constant.
+  __device__ __forceinline__ static uint32_t row_off(int r, int s0, int n0, int s1, int n1, uint32_t ts,
+                                                     bool& ok) {
+    const bool hi = r >= 32;
+    const int o = r & 31;
+    ok = o < (hi ? n1 : n0);
+    return ok ? __umul24((uint32_t)((hi ? s1 : s0) + o), ts) : 0u;
   }
 
   // Loads are unconditional: a token outside the segments reads token 0,
   // which always exists.  Its key and value land in the tile as they are;
   // the offset's position is INT_MAX, so every row masks its score to -inf
   // and its weight is exactly 0 (values are finite).
-  __device__ __forceinline__ void issue(const uint16_t* kh, const uint16_t* vh, int64_t ts,
+  __device__ __forceinline__ void issue(const uint16_t* kh, const uint16_t* vh, uint32_t ts,
                                         const int32_t* pos, int s0, int n0, int s1, int n1,
                                         int tid) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * NT;
-      bool ok = false;
-      int t = tok((c / CPR) & (kTile - 1), s0, n0, s1, n1, ok);
-      ok = ok && c < KCH;
-      t = ok ? t : 0;
-      kr[i] = ldg_u4(kh + (int64_t)t * ts + (c % CPR) * 8);
+      bool ok;
+      const uint32_t e = row_off((c / CPR) & (kTile - 1), s0, n0, s1, n1, ts, ok);
+      kr[i] = ldg_u4(kh + ((c < KCH ? e : 0u) + (c % CPR) * 8));
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
@@ -101,18 +104,17 @@ struct Stager {
       const int tp = (u / CPR) & (kTile / 2 - 1), cg = u % CPR;
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        bool ok = false;
-        int t = tok(2 * tp + j, s0, n0, s1, n1, ok);
-        ok = ok && u < VU;
-        t = ok ? t : 0;
-        vr[i][j] = ldg_u4(vh + (int64_t)t * ts + cg * 8);
+        bool ok;
+        const uint32_t e = row_off(2 * tp + j, s0, n0, s1, n1, ts, ok);
+        vr[i][j] = ldg_u4(vh + ((u < VU ? e : 0u) + cg * 8));
       }
     }
-    bool ok = false;
-    int t = tok(tid & 63, s0, n0, s1, n1, ok);
+    bool ok;
+    const int r = tid & 63;
+    const int t = (r >= 32 ? s1 : s0) + (r & 31);
+    row_off(r, s0, n0, s1, n1, ts, ok);
     ok = ok && tid < kTile;
-    t = ok ? t : 0;
-    pr = ldg_i32(pos + t);
+    pr = ldg_i32(pos + (ok ? t : 0));
     pok = ok;
   }
 
@@ -303,7 +305,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
   auto issue = [&](St& st, int it) {
     const int t0 = t_begin + it * kTile;
     const int n = it < n_tiles ? min(kTile, t_end - t0) : 0;
-    st.issue(kh, vh, a.kv_tok_stride, a.pos, t0, min(32, n), t0 + 32, max(0, n - 32), tid);
+    st.issue(kh, vh, (uint32_t)a.kv_tok_stride, a.pos, t0, min(32, n), t0 + 32, max(0, n - 32), tid);
   };
   auto compute = [&](int b) {
     if (wave_on) {
@@ -491,6 +493,9 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   __shared__ unsigned int sMax[2][2][NH];   // [buffer][page of the tile][local head]
   __shared__ int sMin;
   __shared__ int sItStart[kPageItemsMax], sItLen[kPageItemsMax];   // this block's pages
+  __shared__ int4 sTileSeg[kPageItemsMax];    // per tile: segments (s0, n0, s1, n1)
+  __shared__ int sTileIt[kPageItemsMax + 1];  // per tile: first item; entry n_tiles = i_end
+  __shared__ int sNTiles;
 
   const int g = blockIdx.z, rblk = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -549,23 +554,28 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   auto tile_items = [&](int it) {
     return (it + 1 < i_end && plen(it) <= 32 && plen(it + 1) <= 32) ? 2 : 1;
   };
+  // the block's tile sequence, built once (thread 0) into LDS
+  if (tid == 0) {
+    int k = 0;
+    for (int it = i_begin; it < i_end; ++k) {
+      const int m = tile_items(it);
+      const int s0 = pstart(it), l0 = plen(it);
+      sTileIt[k] = it;
+      sTileSeg[k] = m == 2 ? make_int4(s0, l0, pstart(it + 1), plen(it + 1))
+                           : make_int4(s0, min(l0, 32), s0 + 32, max(0, l0 - 32));
+      it += m;
+    }
+    sTileIt[k] = i_end;
+    sNTiles = k;
+  }
+  __syncthreads();
+  const int n_tiles = sNTiles;
   // The next tile's loads are issued before the current tile's math; a tile
-  // that starts at or past i_end is an empty segment.
-  auto issue_tile = [&](St& st, int it) {
-    // branch-free, so every path leaves the loads in the same registers
-    // and nothing waits for them before the commit
-    const bool any = it < i_end;
-    const int i0 = any ? it : i_begin;
-    const bool two = any && tile_items(i0) == 2;
-    const int l0 = any ? plen(i0) : 0;
-    const int s0 = pstart(i0);
-    const int i1 = min(i0 + 1, i_end - 1);
-    const int s1 = two ? pstart(i1) : s0 + 32;
-    const int n0 = two ? l0 : min(l0, 32);
-    const int n1 = two ? plen(i1) : max(0, l0 - 32);
-    st.issue(kh, vh, a.kv_tok_stride, a.pos, s0, n0, s1, n1, tid);
+  // index past the end is an empty segment (its loads read token 0).
+  auto issue_tile = [&](St& st, int k) {
+    const int4 sg = k < n_tiles ? sTileSeg[k] : make_int4(0, 0, 0, 0);
+    st.issue(kh, vh, (uint32_t)a.kv_tok_stride, a.pos, sg.x, sg.y, sg.z, sg.w, tid);
   };
-  auto next_tile = [&](int it) { return it < i_end ? it + tile_items(it) : i_end; };
   // A row sees at least nvis tokens; a page (at most kMaxPage tokens) can
   // hold all of them only if nvis <= kMaxPage, so most waves skip the count.
   const bool need_count = MODE == 1 || __ballot(ri.ok && nvis <= kMaxPage) != 0ull;
@@ -722,23 +732,22 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   };
 
   St st;
-  int t_cur = i_begin;
-  issue_tile(st, t_cur);
+  issue_tile(st, 0);
   st.commit(sK[0], sV[0], sP[0], sFull[0], minq, tid);
   __syncthreads();
-  int prev_it = -1, prev_m = 0, k = 0;
-  while (t_cur < i_end) {
+  int prev_it = -1, prev_m = 0;
+  for (int k = 0; k < n_tiles; ++k) {
     const int b = k & 1;
-    const int t_n1 = next_tile(t_cur);
-    const int m = t_n1 - t_cur;
-    issue_tile(st, t_n1);
+    const int t_cur = sTileIt[k], m = sTileIt[k + 1] - t_cur;
+    issue_tile(st, k + 1);
     flush(b ^ 1, prev_it, prev_m);
     process(b, t_cur, m);
-    if (t_n1 < i_end) st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], sFull[b ^ 1], minq, tid);
+    if (k + 1 < n_tiles) st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], sFull[b ^ 1], minq, tid);
     __syncthreads();
-    prev_it = t_cur; prev_m = m; t_cur = t_n1; ++k;
+    prev_it = t_cur;
+    prev_m = m;
   }
-  flush((k - 1) & 1, prev_it, prev_m);
+  flush((n_tiles - 1) & 1, prev_it, prev_m);
 }
 
 // ---------------------------------------------------------------------------
