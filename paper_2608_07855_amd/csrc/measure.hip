@@ -596,11 +596,10 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   };
 
   // the pages of the tile in buffer b
-  auto process = [&](int b, int it, int m) {
-    if (!wave_on) return;
-#pragma nounroll
-    for (int ps = 0; ps < m; ++ps) {
-      const int item = it + ps;
+  // page `item` of the tile in buffer b, at slot ps (a constant at each call,
+  // so the slot's LDS offsets fold into the instructions)
+  auto page = [&](int b, int item, int m, const int ps) {
+    {
       const int len = plen(item);
       // a short page occupies slot ps; a long one both slots from slot 0
       const int nblk = (NB == 1 || m == 2) ? 1 : (len > 32 ? 2 : 1);
@@ -729,6 +728,11 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
         }
       }
     }
+  };
+  auto process = [&](int b, int it, int m) {
+    if (!wave_on) return;
+    page(b, it, m, 0);
+    if (m == 2) page(b, it + 1, m, 1);
   };
 
   St st;
