@@ -269,10 +269,10 @@ int ckv_classify_pages(ckv_ctx* ctx, int32_t n, const float* R_pre,
  * float32[max_cand] (optional): R^+(A u {E}) evaluated at step t;
  * n_accepted int32[1].  Entries at t >= *n_cand are 0 / NaN.
  * max_cand must be >= 1.
- * Unlike the other calls this one waits for the stream: it reads *n_cand
- * back to size the work, and reads a progress flag between batches of
- * rounds (the greedy test is sequential; each round decides at least one
- * candidate).
+ * Like the other calls it only enqueues work: the kernels read *n_cand on
+ * the device, and the sequential greedy loop runs as speculative rounds
+ * inside one cooperative launch (each round decides at least one
+ * candidate, so at most min(*n_cand, max_cand) rounds run).
  */
 int ckv_joint_test(ckv_ctx* ctx, const ckv_kv_view* kv,
                    const ckv_window_view* win, const float* o,

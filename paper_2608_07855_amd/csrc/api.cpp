@@ -28,7 +28,6 @@ constexpr int kPinnedSlots = 4;
 constexpr int kPageCacheEntries = 8;
 constexpr int kJointWindow = 32;       // candidates tested per joint round
 constexpr int kJointRowsPerBlock = 64;
-constexpr int kJointChunk = 4;         // joint rounds launched between progress checks
 constexpr int kTargetBlocks = 256;     // one 8-wave workgroup per compute unit
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -73,8 +72,6 @@ struct ckv_ctx {
   std::vector<PageEntry> pages;
   uint64_t tick = 0;
   // small pinned buffer for device-to-host reads of counters and flags
-  int32_t* pinned_small = nullptr;
-  hipEvent_t small_ev[2] = {nullptr, nullptr};
   // kernel timing (events around every launch when enabled)
   bool timing = false;
   std::string timing_only;   // empty: every kernel
@@ -206,29 +203,6 @@ int resolve_timings(ckv_ctx* c) {
       (ctx)->timed.push_back({kernel_id(ctx, name), ea_, eb_});       \
     }                                                                 \
   } while (0)
-
-// read one int32 from device memory (waits for the stream up to this point)
-int read_device_int(ckv_ctx* c, const int32_t* src, int slot, int32_t* out, bool wait) {
-  if (!c->pinned_small) {
-    void* p = nullptr;
-    CKV_HIP(c, hipHostMalloc(&p, 64, hipHostMallocDefault));
-    c->pinned_small = static_cast<int32_t*>(p);
-  }
-  if (!c->small_ev[slot]) CKV_HIP(c, hipEventCreateWithFlags(&c->small_ev[slot], hipEventDisableTiming));
-  CKV_HIP(c, hipMemcpyAsync(c->pinned_small + slot, src, sizeof(int32_t), hipMemcpyDeviceToHost, c->stream));
-  CKV_HIP(c, hipEventRecord(c->small_ev[slot], c->stream));
-  if (wait) {
-    CKV_HIP(c, hipEventSynchronize(c->small_ev[slot]));
-    *out = c->pinned_small[slot];
-  }
-  return CKV_OK;
-}
-
-int wait_device_int(ckv_ctx* c, int slot, int32_t* out) {
-  CKV_HIP(c, hipEventSynchronize(c->small_ev[slot]));
-  *out = c->pinned_small[slot];
-  return CKV_OK;
-}
 
 // copy host bytes to device memory on the context stream via a pinned slot
 int upload(ckv_ctx* c, const void* src, size_t bytes, void* dst) {
@@ -426,9 +400,6 @@ extern "C" int ckv_destroy(ckv_ctx* c) {
       (void)hipEventDestroy(t.b);
     }
     for (auto e : c->event_pool) (void)hipEventDestroy(e);
-    for (auto e : c->small_ev)
-      if (e) (void)hipEventDestroy(e);
-    if (c->pinned_small) (void)hipHostFree(c->pinned_small);
   }
   delete c;
   return CKV_OK;
@@ -666,24 +637,17 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   j.onorm = rs.onorm;
   j.nvis = rs.nvis;
 
-  // the number of candidates bounds the rounds: read it once
-  int32_t n_eff = 0;
-  if (pages->n_pages > 0) {
-    if ((rc = read_device_int(c, n_cand, 0, &n_eff, true))) return rc;
-    n_eff = std::max(0, std::min(n_eff, max_cand));
-  }
-  if (n_eff == 0) {
-    CKV_LAUNCH(c, "joint_prepare", launch_joint_init(j, c->stream));
-    return CKV_OK;
-  }
+  // Nothing here reads the candidate count on the host: the kernels read
+  // *n_cand and size their work from it (max_cand bounds the launches).
   CKV_LAUNCH(c, "joint_prepare", launch_joint_prepare(a, o, lse, rs, j, c->stream));
-  {
+  if (pages->n_pages > 0) {
     PageWork pw{};
     pw.start = dstart;
     pw.len = dlen;
-    pw.n_items = n_eff;
+    pw.n_items = max_cand;
     pw.n_pages = pages->n_pages;
-    pw.items_per_block = items_per_block(n_eff, a.Hkv * ceil_div(a.rows, rows_per_block_page()));
+    pw.items_per_block = items_per_block(std::min(max_cand, pages->n_pages),
+                                         a.Hkv * ceil_div(a.rows, rows_per_block_page()));
     pw.cand = cand;
     pw.n_cand = n_cand;
     pw.Hq = a.Hq;
@@ -692,22 +656,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
     pw.resC = resC;
     pw.total_rows = total_rows;
     CKV_LAUNCH(c, "joint_residual", launch_page_kernel(a, pw, rs, 1, max_page_len(pages), c->stream));
-    // Each round decides at least one candidate, so n_eff rounds always
-    // suffice.  Rounds go out in chunks; the done flag of chunk k-2 is read
-    // before chunk k is launched, so at most two chunks run past the end.
-    int launched = 0;
-    for (int k = 0; launched < n_eff; ++k) {
-      if (k >= 2) {
-        int32_t done = 0;
-        if ((rc = wait_device_int(c, k & 1, &done))) return rc;
-        if (done) break;
-      }
-      const int m = std::min(kJointChunk, n_eff - launched);
-      for (int r = 0; r < m; ++r) CKV_LAUNCH(c, "joint_round", launch_joint_round(j, c->stream));
-      launched += m;
-      int32_t unused;
-      if ((rc = read_device_int(c, j.ctrl + 2, k & 1, &unused, false))) return rc;
-    }
+    CKV_LAUNCH(c, "joint_round", launch_joint_persistent(j, kTargetBlocks, c->stream));
   }
   return CKV_OK;
 }

@@ -114,7 +114,7 @@ struct JointArgs {
   float* Dstate;          // [rows][D] accumulated residual of accepted pages
   float* Astate;          // [rows]
   int* Cstate;            // [rows]
-  int* ctrl;              // [4]: cursor, pending accepted item (-1), done, block counter
+  int* ctrl;              // [8]: cursor, pending accepted item (-1), -, -, parity
   unsigned int* rbuf;     // [window] per-candidate max ratio bits
   int window;             // candidates evaluated per round
   int rows_per_block;
@@ -125,8 +125,7 @@ struct JointArgs {
 };
 hipError_t launch_joint_prepare(const AttnGeom& a, const float* o, const float* lse, RowStats rs,
                                 const JointArgs& j, hipStream_t s);
-hipError_t launch_joint_round(const JointArgs& j, hipStream_t s);
-hipError_t launch_joint_init(const JointArgs& j, hipStream_t s);
+hipError_t launch_joint_persistent(const JointArgs& j, int max_blocks, hipStream_t s);
 
 // checkpoint: protection, selection, compaction (Eq. (12)-(13), Eq. (4))
 // pages retired on the device: page cand[i] (i < min(*n_cand, max_cand))

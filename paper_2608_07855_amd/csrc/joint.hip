@@ -11,19 +11,27 @@
 // `window` candidates against the same accepted set (each test is exact,
 // because all earlier candidates are decided); the first one that passes is
 // accepted, the ones before it are rejected, and the ones after it are
-// tested again in the next round.  One launch per round: the last block of a
-// round to finish takes the decision; the accepted candidate's residual is
+// tested again in the next round.  The accepted candidate's residual is
 // folded into the state by the next round while it copies the state into
 // the other buffer (double buffering, so no block reads a row another block
 // is writing).
+//
+// All rounds run in one cooperative launch (every workgroup resident): a
+// grid barrier ends a round's tests, block 0 takes the decision, a second
+// barrier publishes it.  The candidate count is read on the device, so the
+// call needs no host round trip; each round decides at least one candidate,
+// so the loop ends within max_cand rounds.
 #include "ckv_device.h"
 #include "ckv_kernels.h"
 
+#include <hip/hip_cooperative_groups.h>
+
+#include <algorithm>
 #include <climits>
 
 namespace ckv {
 
-enum { kCursor = 0, kPending = 1, kDone = 2, kCounter = 3, kParity = 4 };
+enum { kCursor = 0, kPending = 1, kParity = 4 };
 
 // per row: ||o||, n_vis, lse in log2 units; clear the joint state and outputs
 __global__ __launch_bounds__(256) void joint_prep_rows(AttnGeom a, const float* o, const float* lse,
@@ -32,6 +40,15 @@ __global__ __launch_bounds__(256) void joint_prep_rows(AttnGeom a, const float* 
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const size_t gsz = (size_t)gridDim.x * blockDim.x;
+  const int n_eff = min(*j.n_cand, j.max_cand);
+  if (n_eff <= 0) {       // nothing to test: outputs only
+    for (size_t i = gid; i < (size_t)j.max_cand; i += gsz) {
+      j.accepted[i] = 0;
+      if (j.union_R) j.union_R[i] = __builtin_nanf("");
+    }
+    if (gid == 0) *j.n_accepted = 0;
+    return;
+  }
   for (size_t i = gid; i < (size_t)j.total_rows * j.D; i += gsz) j.Dstate[i] = 0.f;
   for (size_t i = gid; i < (size_t)j.total_rows; i += gsz) { j.Astate[i] = 0.f; j.Cstate[i] = 0; }
   for (size_t i = gid; i < (size_t)j.max_cand; i += gsz) {
@@ -43,8 +60,6 @@ __global__ __launch_bounds__(256) void joint_prep_rows(AttnGeom a, const float* 
   if (gid == 0) {
     j.ctrl[kCursor] = 0;
     j.ctrl[kPending] = -1;
-    j.ctrl[kDone] = 0;
-    j.ctrl[kCounter] = 0;
     j.ctrl[kParity] = 0;
     *j.n_accepted = 0;
   }
@@ -68,8 +83,9 @@ __global__ __launch_bounds__(256) void joint_prep_rows(AttnGeom a, const float* 
 // and is zeroed by joint_prep_rows.
 constexpr int kVisSlice = 8192;
 
-__global__ __launch_bounds__(256) void joint_prep_vis(AttnGeom a, RowStats rs) {
+__global__ __launch_bounds__(256) void joint_prep_vis(AttnGeom a, RowStats rs, const int32_t* n_cand) {
   __shared__ int part[4];
+  if (*n_cand <= 0) return;
   const int p = blockIdx.x;
   const int qp = a.qpos[p];
   const int t0 = blockIdx.y * kVisSlice, t1 = min(a.S, t0 + kVisSlice);
@@ -82,43 +98,25 @@ __global__ __launch_bounds__(256) void joint_prep_vis(AttnGeom a, RowStats rs) {
   if (threadIdx.x == 0) atomicAdd(&rs.nvis[p], part[0] + part[1] + part[2] + part[3]);
 }
 
-// outputs when there is no candidate to test
-__global__ __launch_bounds__(256) void joint_init_outputs(JointArgs j) {
-  for (int i = blockIdx.x * 256 + threadIdx.x; i < j.max_cand; i += gridDim.x * 256) {
-    j.accepted[i] = 0;
-    if (j.union_R) j.union_R[i] = __builtin_nanf("");
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) *j.n_accepted = 0;
-}
-
 hipError_t launch_joint_prepare(const AttnGeom& a, const float* o, const float* lse, RowStats rs,
                                 const JointArgs& j, hipStream_t s) {
   hipLaunchKernelGGL(joint_prep_rows, dim3((j.total_rows + 3) / 4), dim3(256), 0, s, a, o, lse, rs, j);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(joint_prep_vis, dim3(a.W, (a.S + kVisSlice - 1) / kVisSlice), dim3(256), 0, s, a, rs);
+  hipLaunchKernelGGL(joint_prep_vis, dim3(a.W, (a.S + kVisSlice - 1) / kVisSlice), dim3(256), 0, s, a, rs, j.n_cand);
   return hipGetLastError();
 }
 
-hipError_t launch_joint_init(const JointArgs& j, hipStream_t s) {
-  hipLaunchKernelGGL(joint_init_outputs, dim3((j.max_cand + 255) / 256), dim3(256), 0, s, j);
-  return hipGetLastError();
-}
-
-// one round: block (jx, rb) tests candidate cursor + jx on rows of block rb
-__global__ __launch_bounds__(256) void joint_round_kernel(JointArgs j, RowStats rs) {
-  __shared__ unsigned int smax;
-  __shared__ int is_last;
-  if (j.ctrl[kDone]) return;
-  const int cursor = j.ctrl[kCursor];
-  const int pend = j.ctrl[kPending];
-  const int par = j.ctrl[kParity];
-  const int n_eff = min(*j.n_cand, j.max_cand);
-  const int jx = blockIdx.x;
+// One candidate x row-block test item of a round (the body of a round):
+// item (jx, rb) tests candidate cursor + jx on the rows of block rb and
+// raises rbuf[jx] to its largest ratio; items with jx == 0 also copy the
+// state (with the pending accepted residual folded in) into the other buffer.
+__device__ void joint_item(const JointArgs& j, const RowStats& rs, int jx, int rb, int cursor, int pend,
+                           int par, int n_eff, unsigned int* smax) {
   const int t = cursor + jx;
   const bool valid = t < n_eff;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r0 = blockIdx.y * j.rows_per_block;
+  const int r0 = rb * j.rows_per_block;
   const int r1 = min(j.total_rows, r0 + j.rows_per_block);
   const size_t RD = (size_t)j.total_rows * j.D;
   const float* Din = j.Dstate + (size_t)par * RD;
@@ -127,21 +125,18 @@ __global__ __launch_bounds__(256) void joint_round_kernel(JointArgs j, RowStats 
   float* Aout = j.Astate + (size_t)(par ^ 1) * j.total_rows;
   const int* Cin = j.Cstate + (size_t)par * j.total_rows;
   int* Cout = j.Cstate + (size_t)(par ^ 1) * j.total_rows;
-  if (threadIdx.x == 0) smax = 0u;
+  if (threadIdx.x == 0) *smax = 0u;
   __syncthreads();
   float wmax = 0.f;
   for (int row = r0 + wave; row < r1; row += 4) {
-    // current state of this row = stored state + residual of the pending accept
-    float dcur[4];
     float n2 = 0.f;
     const float* rp = pend >= 0 ? j.resid + ((size_t)pend * j.total_rows + row) * j.D : nullptr;
     const float* rt = valid ? j.resid + ((size_t)t * j.total_rows + row) * j.D : nullptr;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int d = lane + 64 * k;
-      float dv = 0.f;
       if (d < j.D) {
-        dv = Din[(size_t)row * j.D + d];
+        float dv = Din[(size_t)row * j.D + d];
         if (rp) dv += rp[d];
         if (jx == 0) Dout[(size_t)row * j.D + d] = dv;
         if (rt) {
@@ -149,9 +144,7 @@ __global__ __launch_bounds__(256) void joint_round_kernel(JointArgs j, RowStats 
           n2 += x * x;
         }
       }
-      dcur[k] = dv;
     }
-    (void)dcur;
     float Acur = Ain[row];
     int Ccur = Cin[row];
     if (pend >= 0) {
@@ -174,49 +167,69 @@ __global__ __launch_bounds__(256) void joint_round_kernel(JointArgs j, RowStats 
     }
     wmax = fmaxf(wmax, ratio);
   }
-  if (valid && lane == 0) atomicMax(&smax, __float_as_uint(wmax));
+  if (valid && lane == 0) atomicMax(smax, __float_as_uint(wmax));
   __syncthreads();
-  if (threadIdx.x == 0) {
-    if (valid) atomicMax(&j.rbuf[jx], smax);
-    __threadfence();
-    const int total = gridDim.x * gridDim.y;
-    const int prev = atomicAdd(&j.ctrl[kCounter], 1);
-    is_last = (prev == total - 1);
-  }
+  if (threadIdx.x == 0 && valid) atomicMax(&j.rbuf[jx], *smax);
   __syncthreads();
-  if (!is_last || threadIdx.x != 0) return;
-  // decision: the first passer in order is accepted, the ones before it rejected
-  __threadfence();
-  int cur = cursor;
-  int acc = -1;
-  for (int k = 0; k < (int)gridDim.x; ++k) {
-    const int tt = cursor + k;
-    if (tt >= n_eff) break;
-    const unsigned int bits = __hip_atomic_load(&j.rbuf[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const float r = __uint_as_float(bits);
-    if (j.union_R) j.union_R[tt] = r;
-    cur = tt + 1;
-    if (r <= j.tau) {
-      j.accepted[tt] = 1;
-      acc = tt;
-      *j.n_accepted += 1;
-      break;
-    }
-  }
-  for (int k = 0; k < (int)gridDim.x; ++k) j.rbuf[k] = 0u;
-  j.ctrl[kCursor] = cur;
-  j.ctrl[kPending] = acc;
-  j.ctrl[kParity] = par ^ 1;
-  j.ctrl[kDone] = cur >= n_eff ? 1 : 0;
-  j.ctrl[kCounter] = 0;
 }
 
-hipError_t launch_joint_round(const JointArgs& j, hipStream_t s) {
-  RowStats rs{nullptr, nullptr, const_cast<float*>(j.onorm), const_cast<int*>(j.nvis)};
-  dim3 grid(j.window, (j.total_rows + j.rows_per_block - 1) / j.rows_per_block);
-  hipLaunchKernelGGL(joint_round_kernel, grid, dim3(256), 0, s, j, rs);
-  return hipGetLastError();
+__global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs) {
+  namespace cg = cooperative_groups;
+  cg::grid_group grid = cg::this_grid();
+  __shared__ unsigned int smax;
+  const int n_eff = min(*j.n_cand, j.max_cand);
+  if (n_eff <= 0) return;
+  const int n_rb = (j.total_rows + j.rows_per_block - 1) / j.rows_per_block;
+  const int items = j.window * n_rb;
+  // every round decides at least one candidate: n_eff rounds suffice
+  for (int round = 0; round < n_eff; ++round) {
+    const int cursor = __hip_atomic_load(&j.ctrl[kCursor], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int pend = __hip_atomic_load(&j.ctrl[kPending], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int par = __hip_atomic_load(&j.ctrl[kParity], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (cursor >= n_eff) break;               // the same decision in every block
+    for (int it = blockIdx.x; it < items; it += gridDim.x)
+      joint_item(j, rs, it / n_rb, it % n_rb, cursor, pend, par, n_eff, &smax);
+    grid.sync();
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      // the first passer in order is accepted, the ones before it rejected
+      int cur = cursor, acc = -1;
+      for (int k = 0; k < j.window; ++k) {
+        const int tt = cursor + k;
+        if (tt >= n_eff) break;
+        const float r = __uint_as_float(__hip_atomic_load(&j.rbuf[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        if (j.union_R) j.union_R[tt] = r;
+        cur = tt + 1;
+        if (r <= j.tau) {
+          j.accepted[tt] = 1;
+          acc = tt;
+          *j.n_accepted += 1;
+          break;
+        }
+      }
+      for (int k = 0; k < j.window; ++k) __hip_atomic_store(&j.rbuf[k], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&j.ctrl[kCursor], cur, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&j.ctrl[kPending], acc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&j.ctrl[kParity], par ^ 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    grid.sync();
+  }
 }
+
+hipError_t launch_joint_persistent(const JointArgs& j, int max_blocks, hipStream_t s) {
+  RowStats rs{nullptr, nullptr, const_cast<float*>(j.onorm), const_cast<int*>(j.nvis)};
+  const int n_rb = (j.total_rows + j.rows_per_block - 1) / j.rows_per_block;
+  int per_cu = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, joint_persistent, 256, 0);
+  if (e != hipSuccess) return e;
+  int dev = 0, cus = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  const int nb = std::max(1, std::min({j.window * n_rb, per_cu * cus, max_blocks}));
+  JointArgs ja = j;
+  void* args[] = {&ja, &rs};
+  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(joint_persistent), dim3(nb), dim3(256), args, 0, s);
+}
+
 
 
 }  // namespace ckv
