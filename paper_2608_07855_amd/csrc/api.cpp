@@ -26,6 +26,7 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int kPinnedSlots = 4;
 constexpr int kPageCacheEntries = 8;
+constexpr float kLog2eHost = 1.4426950408889634f;   // log2(e): natural-log LSE to log2 units
 constexpr int kJointWindow = 32;       // candidates tested per joint round
 constexpr int kJointRowsPerBlock = 64;
 constexpr int kTargetBlocks = 256;     // one 8-wave workgroup per compute unit
@@ -526,9 +527,11 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
     pw.len = dlen;
     pw.n_items = n;
     pw.n_pages = n;
-    pw.items_per_block = items_per_block(n, a.Hkv * ceil_div(a.rows, rows_per_block_page()));
+    pw.items_per_block = std::min(items_per_block(n, a.Hkv * ceil_div(a.rows, rows_per_block_page())),
+                                  ckv::kPageRmaxCap / page_heads_per_block(a.W, a.group));
     pw.R = R;
     pw.R_head = R_head;
+    pw.lse_scale = 1.f;
     pw.Hq = a.Hq;
     pw.total_rows = total_rows;
     pw.fix_list = fix_list;
@@ -598,7 +601,8 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   DeviceGuard g(c->device);
   const AttnGeom a = make_geom(kv, win);
   const int total_rows = a.Hq * a.W, D = a.D;
-  RowStats rs{const_cast<float*>(o), nullptr, nullptr, nullptr};
+  // the residual pass reads the caller's o and natural-log lse directly
+  RowStats rs{const_cast<float*>(o), const_cast<float*>(lse), nullptr, nullptr};
   JointArgs j{};
   j.total_rows = total_rows;
   j.D = D;
@@ -611,12 +615,17 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   j.accepted = accepted;
   j.union_R = union_R;
   j.n_accepted = n_accepted;
+  j.o = o;
+  j.pos = a.pos;
+  j.qpos = a.qpos;
+  j.S = a.S;
+  j.n_vis_slices = joint_vis_slices(a.S);
+  j.test_cap = pages->n_pages > 0 ? max_cand : 0;
   float *resid, *resA, *Dst, *Ast;
   int *resC, *Cst;
   Plan plan;
-  plan.add(&rs.lse2, total_rows);
-  plan.add(&rs.onorm, total_rows);
-  plan.add(&rs.nvis, a.W);
+  plan.add(&j.onorm, total_rows);
+  plan.add(&j.nvis_part, (size_t)a.W * j.n_vis_slices);
   plan.add(&resid, (size_t)max_cand * total_rows * D);
   plan.add(&resA, (size_t)max_cand * total_rows);
   plan.add(&resC, (size_t)max_cand * total_rows);
@@ -634,12 +643,10 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   j.Dstate = Dst;
   j.Astate = Ast;
   j.Cstate = Cst;
-  j.onorm = rs.onorm;
-  j.nvis = rs.nvis;
 
   // Nothing here reads the candidate count on the host: the kernels read
   // *n_cand and size their work from it (max_cand bounds the launches).
-  CKV_LAUNCH(c, "joint_prepare", launch_joint_prepare(a, o, lse, rs, j, c->stream));
+  // The residual pass also clears the joint kernel's control words.
   if (pages->n_pages > 0) {
     PageWork pw{};
     pw.start = dstart;
@@ -655,9 +662,13 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
     pw.resA = resA;
     pw.resC = resC;
     pw.total_rows = total_rows;
+    pw.lse_scale = kLog2eHost;
+    pw.clear = j.ctrl;
+    pw.n_clear = 8;
     CKV_LAUNCH(c, "joint_residual", launch_page_kernel(a, pw, rs, 1, max_page_len(pages), c->stream));
-    CKV_LAUNCH(c, "joint_round", launch_joint_persistent(j, kTargetBlocks, c->stream));
   }
+  // with no pages the joint kernel only writes the outputs
+  CKV_LAUNCH(c, "joint_round", launch_joint_persistent(j, kTargetBlocks, c->stream));
   return CKV_OK;
 }
 

@@ -42,6 +42,7 @@ struct RowStats {
 
 // pages processed by pass B (MODE 0: item = page; MODE 1: item t = page cand[t])
 constexpr int kPageItemsMax = 256;   // pages (or candidates) per page-kernel workgroup
+constexpr int kPageRmaxCap = 4096;   // (page, head) maxima a MODE 0 workgroup keeps in LDS
 
 struct PageWork {
   const int32_t* start;
@@ -61,6 +62,10 @@ struct PageWork {
   float* resA;            // MODE 1: [max_cand][total_rows]
   int* resC;              // MODE 1: [max_cand][total_rows]
   int total_rows;         // Hq * W
+  float lse_scale;        // rs.lse2 x lse_scale = log-sum-exp in log2 units (1, or log2 e
+                          // when rs.lse2 holds natural-log values)
+  int* clear;             // MODE 1: words set to zero by workgroup (0, 0, 0) (or null)
+  int n_clear;
 };
 
 struct ZeroList {
@@ -73,6 +78,7 @@ struct ZeroList {
 
 int rows_per_block_attention();
 int rows_per_block_page();
+int page_heads_per_block(int W, int group);   // bound on the query heads of one workgroup
 int token_mass_max_rows();
 
 hipError_t launch_window_attention(const AttnGeom& a, const AttnSplit& sp, hipStream_t s);
@@ -109,12 +115,19 @@ struct JointArgs {
   const float* resid;     // [max_cand][rows][D]
   const float* resA;      // [max_cand][rows]
   const int* resC;
-  const float* onorm;     // [rows]
-  const int* nvis;        // [W]: visible tokens of window row p
+  float* onorm;           // [rows]: ||o_p|| (phase 0)
+  int* nvis_part;         // [W][n_vis_slices]: visible tokens of window row p per slice (phase 0)
+  int n_vis_slices;
+  const float* o;         // [rows][D] window outputs
+  const int32_t* pos;     // [S] token positions
+  const int32_t* qpos;    // [W] window positions
+  int S;
+  int test_cap;           // candidates tested at most (0: none, e.g. no pages)
   float* Dstate;          // [rows][D] accumulated residual of accepted pages
   float* Astate;          // [rows]
   int* Cstate;            // [rows]
-  int* ctrl;              // [8]: cursor, pending accepted item (-1), -, -, parity
+  int* ctrl;              // [8]: cursor, pending accepted item, barrier arrivals, error, parity
+                          //      (zero before the launch: the residual pass clears them)
   unsigned int* rbuf;     // [window] per-candidate max ratio bits
   int window;             // candidates evaluated per round
   int rows_per_block;
@@ -123,8 +136,7 @@ struct JointArgs {
   float* union_R;
   int32_t* n_accepted;
 };
-hipError_t launch_joint_prepare(const AttnGeom& a, const float* o, const float* lse, RowStats rs,
-                                const JointArgs& j, hipStream_t s);
+int joint_vis_slices(int S);
 hipError_t launch_joint_persistent(const JointArgs& j, int max_blocks, hipStream_t s);
 
 // checkpoint: protection, selection, compaction (Eq. (12)-(13), Eq. (4))

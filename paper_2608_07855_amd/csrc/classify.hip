@@ -1,12 +1,12 @@
 // Lifecycle classification of event pages (CommitKV, Sec. 3.2, Eq. (8)-(10))
 // and the candidate order of Sec. 3.3.
 //
-// rank_kernel: one thread per page.  Percentile P(E) = (number of other pages
+// rank_kernel: 16 lanes per page.  Percentile P(E) = (number of other pages
 // with a strictly smaller effect) / (n - 1), 0.5 for n = 1; counted exactly
-// against every page (values staged through LDS), so ties share the lower
-// rank.  The comparison P >= rho is made in double precision on the integer
+// against every page (values staged through LDS in chunks, so the count loop
+// never waits on a global load), so ties share the lower rank.  The comparison P >= rho is made in double precision on the integer
 // count.  Then H/L of Eq. (9) and the state of Eq. (10).
-// order_kernel: one thread per page.  A candidate's slot in the ordered list
+// order_kernel: 16 lanes per page, the same staging.  A candidate's slot in the ordered list
 // is the number of candidates that precede it under (R+ ascending, R-
 // descending, index ascending); the keys are unique so the slots form a
 // permutation without any sort.
@@ -23,6 +23,7 @@ constexpr int kCT = 256;
 // j, j + 16, ...; the counts are summed with shuffles.
 constexpr int kLanes = 16;
 constexpr int kPagesPerBlock = kCT / kLanes;
+constexpr int kStage = 2048;   // pages staged in LDS per chunk
 
 __global__ __launch_bounds__(kCT) void rank_kernel(ClassifyArgs c) {
   const int i = blockIdx.x * kPagesPerBlock + threadIdx.x / kLanes;
@@ -30,10 +31,20 @@ __global__ __launch_bounds__(kCT) void rank_kernel(ClassifyArgs c) {
   const bool act = i < c.n;
   const float rp = act ? c.R_pre[i] : 0.f;
   const float rq = act ? c.R_post[i] : 0.f;
+  __shared__ float sPre[kStage], sPost[kStage];
   int less_pre = 0, less_post = 0;
-  for (int j = sub; j < c.n; j += kLanes) {
-    less_pre += c.R_pre[j] < rp ? 1 : 0;
-    less_post += c.R_post[j] < rq ? 1 : 0;
+  for (int base = 0; base < c.n; base += kStage) {
+    const int m = min(kStage, c.n - base);
+    __syncthreads();
+    for (int j = threadIdx.x; j < m; j += kCT) {
+      sPre[j] = c.R_pre[base + j];
+      sPost[j] = c.R_post[base + j];
+    }
+    __syncthreads();
+    for (int j = sub; j < m; j += kLanes) {
+      less_pre += sPre[j] < rp ? 1 : 0;
+      less_post += sPost[j] < rq ? 1 : 0;
+    }
   }
 #pragma unroll
   for (int off = kLanes / 2; off >= 1; off >>= 1) {
@@ -75,11 +86,23 @@ __global__ __launch_bounds__(kCT) void order_kernel(ClassifyArgs c) {
   const bool me = act && c.is_cand[i];
   const float rp = act ? c.R_pre[i] : 0.f;
   const float rq = act ? c.R_post[i] : 0.f;
+  __shared__ float sPre[kStage], sPost[kStage];
+  __shared__ uint8_t sCand[kStage];
   int before = 0, total = 0;
-  for (int j = sub; j < c.n; j += kLanes) {
-    if (!c.is_cand[j]) continue;
-    ++total;
-    before += precedes(c.R_post[j], c.R_pre[j], j, rq, rp, i) ? 1 : 0;
+  for (int base = 0; base < c.n; base += kStage) {
+    const int m = min(kStage, c.n - base);
+    __syncthreads();
+    for (int j = threadIdx.x; j < m; j += kCT) {
+      sPre[j] = c.R_pre[base + j];
+      sPost[j] = c.R_post[base + j];
+      sCand[j] = c.is_cand[base + j];
+    }
+    __syncthreads();
+    for (int j = sub; j < m; j += kLanes) {
+      if (!sCand[j]) continue;
+      ++total;
+      before += precedes(sPost[j], sPre[j], base + j, rq, rp, i) ? 1 : 0;
+    }
   }
 #pragma unroll
   for (int off = kLanes / 2; off >= 1; off >>= 1) {

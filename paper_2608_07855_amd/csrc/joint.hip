@@ -16,95 +16,51 @@
 // the other buffer (double buffering, so no block reads a row another block
 // is writing).
 //
-// All rounds run in one cooperative launch (every workgroup resident): a
-// grid barrier ends a round's tests, block 0 takes the decision, a second
-// barrier publishes it.  The candidate count is read on the device, so the
-// call needs no host round trip; each round decides at least one candidate,
-// so the loop ends within max_cand rounds.
+// All rounds run in one launch of at most as many workgroups as the device
+// holds at once: phase 0 clears the state and computes ||o_p|| and the
+// visible-token counts, then a grid barrier ends each round's tests, block 0
+// takes the decision, and a second barrier publishes it.  The candidate count
+// is read on the device, so the call needs no host round trip; each round
+// decides at least one candidate, so the loop ends within max_cand rounds.
+// A barrier wait is bounded: if the workgroups cannot all run at once (a
+// device shared with other work), every block leaves and *n_accepted = -1.
 #include "ckv_device.h"
 #include "ckv_kernels.h"
-
-#include <hip/hip_cooperative_groups.h>
 
 #include <algorithm>
 #include <climits>
 
 namespace ckv {
 
-enum { kCursor = 0, kPending = 1, kParity = 4 };
+// control words (cleared by the residual pass before this kernel starts)
+enum { kCursor = 0, kPending = 1, kBarrier = 2, kError = 3, kParity = 4 };
+constexpr long long kBarrierTimeoutTicks = 1ll << 27;   // ~1.3 s of the 100 MHz wall clock
+constexpr int kVisSlice = 8192;                         // tokens per visible-count item
 
-// per row: ||o||, n_vis, lse in log2 units; clear the joint state and outputs
-__global__ __launch_bounds__(256) void joint_prep_rows(AttnGeom a, const float* o, const float* lse,
-                                                      RowStats rs, JointArgs j) {
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t gsz = (size_t)gridDim.x * blockDim.x;
-  const int n_eff = min(*j.n_cand, j.max_cand);
-  if (n_eff <= 0) {       // nothing to test: outputs only
-    for (size_t i = gid; i < (size_t)j.max_cand; i += gsz) {
-      j.accepted[i] = 0;
-      if (j.union_R) j.union_R[i] = __builtin_nanf("");
-    }
-    if (gid == 0) *j.n_accepted = 0;
-    return;
-  }
-  for (size_t i = gid; i < (size_t)j.total_rows * j.D; i += gsz) j.Dstate[i] = 0.f;
-  for (size_t i = gid; i < (size_t)j.total_rows; i += gsz) { j.Astate[i] = 0.f; j.Cstate[i] = 0; }
-  for (size_t i = gid; i < (size_t)j.max_cand; i += gsz) {
-    j.accepted[i] = 0;
-    if (j.union_R) j.union_R[i] = __builtin_nanf("");
-  }
-  for (size_t i = gid; i < (size_t)j.window; i += gsz) j.rbuf[i] = 0u;
-  for (size_t i = gid; i < (size_t)j.W; i += gsz) rs.nvis[i] = 0;
-  if (gid == 0) {
-    j.ctrl[kCursor] = 0;
-    j.ctrl[kPending] = -1;
-    j.ctrl[kParity] = 0;
-    *j.n_accepted = 0;
-  }
-  if (row >= j.total_rows) return;
-  float n2 = 0.f;
-  for (int d = lane; d < j.D; d += 64) {
-    const float v = o[(size_t)row * j.D + d];
-    n2 += v * v;
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) n2 += __shfl_xor(n2, off, 64);
-  if (lane == 0) {
-    rs.onorm[row] = sqrtf(n2);
-    const float l = lse[row];
-    rs.lse2[row] = l == -INFINITY ? -INFINITY : l * kLog2e;
-  }
-}
-
-// n_vis of window row p (shared by every query head): #{i : pos[i] <= qpos[p]},
-// counted over a (row, token slice) grid; rs.nvis holds one count per row p
-// and is zeroed by joint_prep_rows.
-constexpr int kVisSlice = 8192;
-
-__global__ __launch_bounds__(256) void joint_prep_vis(AttnGeom a, RowStats rs, const int32_t* n_cand) {
-  __shared__ int part[4];
-  if (*n_cand <= 0) return;
-  const int p = blockIdx.x;
-  const int qp = a.qpos[p];
-  const int t0 = blockIdx.y * kVisSlice, t1 = min(a.S, t0 + kVisSlice);
-  int c = 0;
-  for (int i = t0 + threadIdx.x; i < t1; i += 256) c += a.pos[i] <= qp ? 1 : 0;
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off, 64);
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = c;
+// Grid barrier: thread 0 of every block publishes the block's writes, adds
+// one arrival and waits until the arrivals reach `target`.  Returns false
+// (in every thread) if the wait timed out or another block gave up.
+__device__ bool grid_barrier(int* ctrl, int target, int* s_ok) {
   __syncthreads();
-  if (threadIdx.x == 0) atomicAdd(&rs.nvis[p], part[0] + part[1] + part[2] + part[3]);
-}
-
-hipError_t launch_joint_prepare(const AttnGeom& a, const float* o, const float* lse, RowStats rs,
-                                const JointArgs& j, hipStream_t s) {
-  hipLaunchKernelGGL(joint_prep_rows, dim3((j.total_rows + 3) / 4), dim3(256), 0, s, a, o, lse, rs, j);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(joint_prep_vis, dim3(a.W, (a.S + kVisSlice - 1) / kVisSlice), dim3(256), 0, s, a, rs, j.n_cand);
-  return hipGetLastError();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    atomicAdd(&ctrl[kBarrier], 1);
+    const long long t0 = wall_clock64();
+    int ok = 1;
+    while (__hip_atomic_load(&ctrl[kBarrier], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      if (__hip_atomic_load(&ctrl[kError], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
+          wall_clock64() - t0 > kBarrierTimeoutTicks) {
+        __hip_atomic_store(&ctrl[kError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    __threadfence();
+    *s_ok = ok;
+  }
+  __syncthreads();
+  return *s_ok != 0;
 }
 
 // One candidate x row-block test item of a round (the body of a round):
@@ -161,7 +117,9 @@ __device__ void joint_item(const JointArgs& j, const RowStats& rs, int jx, int r
     if (Ct > 0) {
       const float keep = 1.f - At;
       const float on = rs.onorm[row];
-      if (Ct >= rs.nvis[row % j.W] || !(keep > 0.f)) ratio = INFINITY;
+      int nv = 0;
+      for (int q = 0; q < j.n_vis_slices; ++q) nv += j.nvis_part[(row % j.W) * j.n_vis_slices + q];
+      if (Ct >= nv || !(keep > 0.f)) ratio = INFINITY;
       else if (on > 0.f) ratio = sqrtf(n2) / (keep * on);
       else ratio = n2 > 0.f ? INFINITY : 0.f;
     }
@@ -174,11 +132,57 @@ __device__ void joint_item(const JointArgs& j, const RowStats& rs, int jx, int r
 }
 
 __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs) {
-  namespace cg = cooperative_groups;
-  cg::grid_group grid = cg::this_grid();
   __shared__ unsigned int smax;
-  const int n_eff = min(*j.n_cand, j.max_cand);
-  if (n_eff <= 0) return;
+  __shared__ int s_ok, s_part[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t gsz = (size_t)gridDim.x * blockDim.x;
+  const int n_eff = min(min(*j.n_cand, j.max_cand), j.test_cap);
+  // phase 0: outputs, state, ||o_p|| and visible-token counts
+  for (size_t i = gid; i < (size_t)j.max_cand; i += gsz) {
+    j.accepted[i] = 0;
+    if (j.union_R) j.union_R[i] = __builtin_nanf("");
+  }
+  if (gid == 0) *j.n_accepted = 0;
+  if (n_eff <= 0) return;              // nothing to test: the same in every block
+  for (size_t i = gid; i < (size_t)j.total_rows * j.D; i += gsz) j.Dstate[i] = 0.f;
+  for (size_t i = gid; i < (size_t)j.total_rows; i += gsz) { j.Astate[i] = 0.f; j.Cstate[i] = 0; }
+  for (size_t i = gid; i < (size_t)j.window; i += gsz) j.rbuf[i] = 0u;
+  if (gid == 0) {
+    j.ctrl[kCursor] = 0;
+    j.ctrl[kPending] = -1;
+    j.ctrl[kParity] = 0;
+  }
+  for (int row = blockIdx.x * 4 + wave; row < j.total_rows; row += gridDim.x * 4) {
+    float n2 = 0.f;
+    for (int d = lane; d < j.D; d += 64) {
+      const float v = j.o[(size_t)row * j.D + d];
+      n2 += v * v;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) n2 += __shfl_xor(n2, off, 64);
+    if (lane == 0) rs.onorm[row] = sqrtf(n2);
+  }
+  // n_vis of window row p (shared by every query head): #{i : pos[i] <= qpos[p]},
+  // one partial count per (row, token slice)
+  for (int it = blockIdx.x; it < j.W * j.n_vis_slices; it += gridDim.x) {
+    const int p = it / j.n_vis_slices, sl = it % j.n_vis_slices;
+    const int qp = j.qpos[p];
+    const int t0 = sl * kVisSlice, t1 = min(j.S, t0 + kVisSlice);
+    int c = 0;
+    for (int i = t0 + (int)threadIdx.x; i < t1; i += 256) c += j.pos[i] <= qp ? 1 : 0;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off, 64);
+    if (lane == 0) s_part[wave] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) j.nvis_part[it] = s_part[0] + s_part[1] + s_part[2] + s_part[3];
+    __syncthreads();
+  }
+  int target = gridDim.x;
+  if (!grid_barrier(j.ctrl, target, &s_ok)) {
+    if (threadIdx.x == 0) *j.n_accepted = -1;
+    return;
+  }
   const int n_rb = (j.total_rows + j.rows_per_block - 1) / j.rows_per_block;
   const int items = j.window * n_rb;
   // every round decides at least one candidate: n_eff rounds suffice
@@ -189,7 +193,11 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
     if (cursor >= n_eff) break;               // the same decision in every block
     for (int it = blockIdx.x; it < items; it += gridDim.x)
       joint_item(j, rs, it / n_rb, it % n_rb, cursor, pend, par, n_eff, &smax);
-    grid.sync();
+    target += gridDim.x;
+    if (!grid_barrier(j.ctrl, target, &s_ok)) {
+      if (threadIdx.x == 0) *j.n_accepted = -1;
+      return;
+    }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
       // the first passer in order is accepted, the ones before it rejected
       int cur = cursor, acc = -1;
@@ -211,25 +219,34 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
       __hip_atomic_store(&j.ctrl[kPending], acc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&j.ctrl[kParity], par ^ 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    grid.sync();
+    target += gridDim.x;
+    if (!grid_barrier(j.ctrl, target, &s_ok)) {
+      if (threadIdx.x == 0) *j.n_accepted = -1;
+      return;
+    }
   }
 }
 
+int joint_vis_slices(int S) { return (S + kVisSlice - 1) / kVisSlice; }
+
 hipError_t launch_joint_persistent(const JointArgs& j, int max_blocks, hipStream_t s) {
-  RowStats rs{nullptr, nullptr, const_cast<float*>(j.onorm), const_cast<int*>(j.nvis)};
+  RowStats rs{nullptr, nullptr, const_cast<float*>(j.onorm), nullptr};
   const int n_rb = (j.total_rows + j.rows_per_block - 1) / j.rows_per_block;
-  int per_cu = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, joint_persistent, 256, 0);
+  // workgroups that fit on the device at once (queried once per device)
+  static int resident[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  int dev = 0, cus = 0;
-  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
-  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-  const int nb = std::max(1, std::min({j.window * n_rb, per_cu * cus, max_blocks}));
-  JointArgs ja = j;
-  void* args[] = {&ja, &rs};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(joint_persistent), dim3(nb), dim3(256), args, 0, s);
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  if (resident[dev] <= 0) {
+    int per_cu = 0, cus = 0;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, joint_persistent, 256, 0)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    resident[dev] = std::max(1, per_cu * cus);
+  }
+  const int nb = std::max(1, std::min({j.window * n_rb, resident[dev], max_blocks}));
+  hipLaunchKernelGGL(joint_persistent, dim3(nb), dim3(256), 0, s, j, rs);
+  return hipGetLastError();
 }
-
-
 
 }  // namespace ckv

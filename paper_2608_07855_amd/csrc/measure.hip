@@ -484,13 +484,21 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
 template <int D, int MODE, int NB>
 __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork pw, RowStats rs) {
   constexpr int NT = kNW * 64, KS = D / 16, DB = D / 32;
-  constexpr int NH = kRowsWG + 2;     // bound on the heads touched by one workgroup
   using St = Stager<D, NT>;
   __shared__ __align__(16) uint16_t sK[2][kTile * St::KP];
   __shared__ __align__(16) _Float16 sV[2][D * St::VP];
   __shared__ __align__(16) int sP[2][kTile];
   __shared__ int sFull[2][2];
-  __shared__ unsigned int sMax[2][2][NH];   // [buffer][page of the tile][local head]
+  // MODE 0: per (page of the block, local head) maximum ratio, flushed to
+  // global memory once after the last tile, so the tile loop issues no
+  // global atomics (a wave that waits on them stalls the whole workgroup at
+  // the tile barrier); the host bounds pages x heads by kPageRmaxCap
+  __shared__ unsigned int sRm[MODE == 0 ? kPageRmaxCap : 1];
+  // MODE 0: rows left to the fix-up kernel, published after the last tile
+  // (a row has at most one page with A > kFixA, so kRowsWG entries suffice
+  // unless the inputs hold NaN; an overflow appends to the global list)
+  __shared__ int4 sFix[MODE == 0 ? kRowsWG : 1];
+  __shared__ int sFixN, sFixBase;
   __shared__ int sMin;
   __shared__ int sItStart[kPageItemsMax], sItLen[kPageItemsMax];   // this block's pages
   __shared__ int4 sTileSeg[kPageItemsMax];    // per tile: segments (s0, n0, s1, n1)
@@ -502,6 +510,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   const int half = lane >> 5, col = lane & 31;
   int n_items = pw.n_items;
   if (MODE == 1) n_items = min(*pw.n_cand, pw.n_items);
+  if (MODE == 1 && pw.clear && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && tid < pw.n_clear)
+    pw.clear[tid] = 0;
   const int i_begin = blockIdx.x * pw.items_per_block;
   const int i_end = min(n_items, i_begin + pw.items_per_block);
   if (i_begin >= i_end) return;
@@ -537,16 +547,18 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
         for (int j = 0; j < 4; ++j) of[db][4 * i + j] = v4[j];
       }
   }
-  const float lse2 = ri.ok ? rs.lse2[ri.rg] : -INFINITY;
-  const float onorm = ri.ok ? rs.onorm[ri.rg] : 0.f;
+  const float lse2 = ri.ok ? rs.lse2[ri.rg] * pw.lse_scale : -INFINITY;   // -inf stays -inf
+  const float onorm = (MODE == 0 && ri.ok) ? rs.onorm[ri.rg] : 0.f;   // read by MODE 0 only
   const int nvis = (MODE == 0 && ri.ok) ? rs.nvis[ri.rg] : 0;   // read by MODE 0 only
   const int row0 = rblk * kRowsWG;
   const int head0 = row0 / a.W;
   const int n_heads_blk = min(a.group, (min(a.rows, row0 + kRowsWG) - 1) / a.W + 1) - head0;
   const bool wave_one_head = (a.W % 32) == 0;   // the 32 rows of a wave share one head
   const int my_hl = ri.ok ? ri.row / a.W - head0 : 0;   // this row's head inside the block
-  if (MODE == 0)
-    for (int i = tid; i < 2 * 2 * NH; i += NT) (&sMax[0][0][0])[i] = 0u;
+  if (MODE == 0) {
+    for (int i = tid; i < (i_end - i_begin) * n_heads_blk; i += NT) sRm[i] = 0u;
+    if (tid == 0) sFixN = 0;
+  }
 
   auto pstart = [&](int item) { return sItStart[item - i_begin]; };
   auto plen = [&](int item) { return sItLen[item - i_begin]; };
@@ -579,21 +591,6 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   // A row sees at least nvis tokens; a page (at most kMaxPage tokens) can
   // hold all of them only if nvis <= kMaxPage, so most waves skip the count.
   const bool need_count = MODE == 1 || __ballot(ri.ok && nvis <= kMaxPage) != 0ull;
-
-  // flush the per-head maxima of the tile in buffer bf (final after a barrier)
-  auto flush = [&](int bf, int t_it, int t_m) {
-    if (MODE == 0 && t_it >= 0 && tid < 2 * n_heads_blk) {
-      const int ps = tid / n_heads_blk, hl = tid % n_heads_blk;
-      if (ps < t_m) {
-        const float v = __uint_as_float(sMax[bf][ps][hl]);
-        const int page = t_it + ps;
-        const int h = g * a.group + head0 + hl;
-        if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], v);
-        atomic_max_nonneg(&pw.R[page], v);
-      }
-      sMax[bf][ps][hl] = 0u;
-    }
-  };
 
   // the pages of the tile in buffer b
   // page `item` of the tile in buffer b, at slot ps (a constant at each call,
@@ -695,14 +692,13 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
             ratio = INFINITY;                 // the page holds every visible token
           } else if (A > kFixA || !(keep > 0.f)) {
             if (ri.ok && half == 0) {         // ill-conditioned: recomputed by the fix-up
-              const int slot = atomicAdd(pw.fix_count, 1);
-              if (slot < pw.fix_cap) {
-                int4 ent;
-                ent.x = item;
-                ent.y = ri.rg;
-                ent.z = pstart(item);
-                ent.w = len;
-                reinterpret_cast<int4*>(pw.fix_list)[slot] = ent;
+              const int4 ent = make_int4(item, ri.rg, pstart(item), len);
+              const int ls = atomicAdd(&sFixN, 1);
+              if (ls < kRowsWG) {
+                sFix[ls] = ent;
+              } else {
+                const int slot = atomicAdd(pw.fix_count, 1);
+                if (slot < pw.fix_cap) reinterpret_cast<int4*>(pw.fix_list)[slot] = ent;
               }
             }
           } else if (onorm > 0.f) {
@@ -712,13 +708,14 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
           }
         }
         if (!ri.ok) ratio = 0.f;
+        unsigned int* rm = &sRm[(item - i_begin) * n_heads_blk + my_hl];
         if (wave_one_head) {
           float wm = ratio;
 #pragma unroll
           for (int off = 16; off >= 1; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off, 64));
-          if (lane == 0 && ri.ok) atomicMax(&sMax[b][ps][my_hl], __float_as_uint(wm));
+          if (lane == 0 && ri.ok) atomicMax(rm, __float_as_uint(wm));
         } else if (ri.ok && half == 0) {
-          atomicMax(&sMax[b][ps][my_hl], __float_as_uint(ratio));
+          atomicMax(rm, __float_as_uint(ratio));
         }
       } else if (ri.ok) {
         const size_t base_i = (size_t)item * pw.total_rows + ri.rg;
@@ -739,19 +736,40 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   issue_tile(st, 0);
   st.commit(sK[0], sV[0], sP[0], sFull[0], minq, tid);
   __syncthreads();
-  int prev_it = -1, prev_m = 0;
   for (int k = 0; k < n_tiles; ++k) {
     const int b = k & 1;
     const int t_cur = sTileIt[k], m = sTileIt[k + 1] - t_cur;
     issue_tile(st, k + 1);
-    flush(b ^ 1, prev_it, prev_m);
     process(b, t_cur, m);
-    if (k + 1 < n_tiles) st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], sFull[b ^ 1], minq, tid);
+    // unconditional: after the last tile an empty tile goes to the idle
+    // buffer, so no path leaves a load outstanding into the next iteration
+    st.commit(sK[b ^ 1], sV[b ^ 1], sP[b ^ 1], sFull[b ^ 1], minq, tid);
     __syncthreads();
-    prev_it = t_cur;
-    prev_m = m;
   }
-  flush((n_tiles - 1) & 1, prev_it, prev_m);
+  if (MODE == 0) {
+    // Eq. (7): maxima over the block's rows, per head and over heads
+    const int n_it = i_end - i_begin;
+    for (int i = tid; i < n_it; i += NT) {
+      const int page = i_begin + i;
+      unsigned int mx = 0u;
+      for (int hl = 0; hl < n_heads_blk; ++hl) {
+        const unsigned int v = sRm[i * n_heads_blk + hl];
+        mx = max(mx, v);
+        if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + g * a.group + head0 + hl],
+                                         __uint_as_float(v));
+      }
+      atomic_max_nonneg(&pw.R[page], __uint_as_float(mx));
+    }
+    const int nf = min(sFixN, kRowsWG);
+    if (nf > 0) {
+      if (tid == 0) sFixBase = atomicAdd(pw.fix_count, nf);
+      __syncthreads();
+      for (int i = tid; i < nf; i += NT) {
+        const int slot = sFixBase + i;
+        if (slot < pw.fix_cap) reinterpret_cast<int4*>(pw.fix_list)[slot] = sFix[i];
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1150,6 +1168,7 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats
 // ---------------------------------------------------------------------------
 int rows_per_block_attention() { return kRowsWG; }
 int rows_per_block_page() { return kRowsWG; }
+int page_heads_per_block(int W, int group) { return std::min(group, (kRowsWG - 1) / W + 2); }
 int token_mass_max_rows() { return kMassMaxRows; }
 
 hipError_t launch_window_attention(const AttnGeom& a, const AttnSplit& sp, hipStream_t s) {
