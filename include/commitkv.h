@@ -314,6 +314,8 @@ typedef struct ckv_accepted_pages {
  *   4. Compaction: out key/value (s, l, g, j) = in (s, l, g, I[j]) for every
  *      layer and KV head, out pos[j] = in pos[I[j]]; bytes copied verbatim.
  *      Slots j >= |I| of `out` are left untouched.
+ * Device inputs: score float32[n_seq * score_seq_stride] (whole rows may be
+ * read; entries past n_tokens[s] are ignored).
  * Host arguments: n_tokens int32[n_seq]; retired, pending ckv_page_list[n_seq];
  * pending_r_pre: host array of n_seq device pointers (NULL allowed where
  * pending[s].n_pages == 0); accepted: ckv_accepted_pages[n_seq] or NULL

@@ -822,8 +822,14 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   sa.state = token_state;
   sa.kept = kept_idx;
   sa.n_kept = n_kept;
-  CKV_LAUNCH(c, "protect", launch_protect(sa, c->stream));
-  CKV_LAUNCH(c, "select", launch_select(sa, c->stream));
+  int max_pend = 0;
+  for (int s = 0; s < ns; ++s) max_pend = std::max(max_pend, pending[s].n_pages);
+  if (select_fused_fits(max_s, max_pend)) {
+    CKV_LAUNCH(c, "select", launch_select_fused(sa, max_s, c->stream));
+  } else {
+    CKV_LAUNCH(c, "protect", launch_protect(sa, c->stream));
+    CKV_LAUNCH(c, "select", launch_select(sa, c->stream));
+  }
 
   GatherArgs ga{};
   ga.k_in = in->k;

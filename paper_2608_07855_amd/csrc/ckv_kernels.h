@@ -183,6 +183,9 @@ constexpr int kSelCtrl = 16;     // ints of per-sequence selection state
 constexpr int kSelBins = 2048;   // radix digit bins (11-bit digits)
 hipError_t launch_protect(const SelectArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+constexpr int kSelFusedMax = 32768;   // longest sequence of the one-workgroup selection
+bool select_fused_fits(int max_tokens, int max_pending);
+hipError_t launch_select_fused(const SelectArgs& a, int max_tokens, hipStream_t s);
 
 struct GatherArgs {
   const uint16_t* k_in;

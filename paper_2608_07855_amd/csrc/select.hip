@@ -17,6 +17,9 @@
 //              the lowest indices.
 //   k = min(B - #protected, #free).  The last workgroup of each histogram
 //   launch (atomic arrival counter) chooses the digit for every sequence.
+// select_fused (sequences of at most kSelFusedMax tokens and kProtLds
+//   pending pages): all of the above in one 1024-thread workgroup per
+//   sequence, keys held in registers.
 // gather_kernel: K'[s,l,g,j] = K[s,l,g,I[j]], the same for V, and
 //   pos'[s,j] = pos[s,I[j]], 16-byte vector copies of whole rows.
 #include "ckv_device.h"
@@ -428,6 +431,278 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(sel_count, grid, block, 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(sel_write, grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Fused selection for sequences of at most kSelFusedMax tokens: one
+// 1024-thread workgroup per sequence runs protection, token states, keys,
+// the threshold search and the ordered write, with the keys in registers.
+// Wave w owns tokens [w 64 KPT, (w + 1) 64 KPT); in round u lane l holds
+// token w 64 KPT + 64 u + l, so loads are coalesced and a wave's rounds
+// visit its tokens in order (ranks inside a wave come from ballots).
+// The threshold search bins the free keys of the remaining range [lo, hi]
+// into at most 2048 bins of width 2^shift (the range adapts to the keys, so
+// concentrated float scores still spread over the bins) and narrows the
+// range to the bin holding the need-th largest key until shift is 0.
+// ---------------------------------------------------------------------------
+namespace {
+constexpr int kFT = 1024;
+constexpr int kFW = kFT / 64;
+
+__device__ __forceinline__ int lanes_below(unsigned long long m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// one combining round for the most common bin of the wave, then plain atomics
+__device__ __forceinline__ void hist_add1(unsigned int* hist, uint32_t bin, bool act) {
+  const unsigned long long m = __ballot(act);
+  if (m == 0ull) return;
+  const int leader = __ffsll((long long)m) - 1;      // uniform: a scalar read of its bin
+  const uint32_t lb = (uint32_t)__builtin_amdgcn_readlane((int)bin, leader);
+  const bool same = act && bin == lb;
+  const unsigned long long sm = __ballot(same);
+  if ((int)(threadIdx.x & 63) == leader) atomicAdd(&hist[lb], (unsigned int)__popcll(sm));
+  if (act && !same) atomicAdd(&hist[bin], 1u);
+}
+}  // namespace
+
+template <int KPT>
+__global__ __launch_bounds__(kFT) void select_fused(SelectArgs a) {
+  constexpr int SPAN = KPT * kFT;
+  __shared__ uint8_t sRet[SPAN], sPro[SPAN];     // retired / protected-page marks
+  __shared__ unsigned int hist[2][kSelBins];      // double-buffered across passes
+  __shared__ float sR[kProtLds];
+  __shared__ int sLen[kProtLds], sStart[kProtLds], sOrd[kProtLds];
+  __shared__ uint8_t sProt[kProtLds];
+  __shared__ int tmp[kFW], wa[kFW], wb[kFW];
+  __shared__ uint32_t wlo[kFW], whi[kFW];
+  __shared__ uint32_t s_lo, s_hi;
+  __shared__ int s_need;
+  const int s = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the scores first: their loads overlap everything up to the keys
+  const float* sc = a.score + (size_t)s * a.score_seq_stride;
+  const int t_base = wave * 64 * KPT + lane;
+  float f[KPT];
+#pragma unroll
+  for (int u = 0; u < KPT; ++u) {
+    const int t = t_base + 64 * u;
+    f[u] = t < a.score_seq_stride ? sc[t] : 0.f;
+  }
+  const int S = a.n_tokens[s];
+  const int poff = a.pend_off[s], n = a.pend_off[s + 1] - poff;   // n <= kProtLds
+  const int roff = a.ret_off[s], nr = a.ret_off[s + 1] - roff;
+  const float* R = reinterpret_cast<const float*>(a.pend_r[s]);
+  for (int i = tid; i < SPAN / 4; i += kFT) {
+    reinterpret_cast<uint32_t*>(sRet)[i] = 0u;
+    reinterpret_cast<uint32_t*>(sPro)[i] = 0u;
+  }
+  for (int i = tid; i < kSelBins; i += kFT) hist[0][i] = 0u;
+  __syncthreads();
+  // pending pages to LDS; retired and accepted pages marked meanwhile
+  for (int i = tid; i < n; i += kFT) {
+    sR[i] = pend_key(R[i]);
+    sLen[i] = a.pend_len[poff + i];
+    sStart[i] = a.pend_start[poff + i];
+    sProt[i] = 0;
+  }
+  for (int idx = tid; idx < nr * kMaxPage; idx += kFT) {
+    const int i = idx / kMaxPage, e = idx % kMaxPage;
+    const int t = a.ret_start[roff + i] + e;
+    if (e < a.ret_len[roff + i] && t >= 0 && t < S) sRet[t] = 1;
+  }
+  if (a.acc && a.acc[s].cand) {
+    const AccPages ap = a.acc[s];
+    const int nc = min(*ap.n_cand, ap.max_cand);
+    for (int idx = tid; idx < nc * kMaxPage; idx += kFT) {
+      const int i = idx / kMaxPage, e = idx % kMaxPage;
+      if (!ap.accepted[i]) continue;
+      const int pg = ap.cand[i];
+      if (pg < 0 || pg >= ap.n_pages || e >= ap.len[pg]) continue;
+      const int t = ap.start[pg] + e;
+      if (t >= 0 && t < S) sRet[t] = 1;
+    }
+  }
+  __syncthreads();
+  // Eq. (12): pending pages ranked by (R- descending, page order), protected
+  // in that order while fewer than max_pages are taken and the tokens fit B_N
+  {
+    int G = 64;                            // lanes per page (a power of two, inside one wave)
+    while (G > 1 && G * n > kFT) G >>= 1;
+    for (int i = tid / G; i < n; i += kFT / G) {
+      const float ri = sR[i];
+      int rank = 0;
+      for (int j = tid % G; j < n; j += G) {
+        const float rj = sR[j];
+        rank += (rj > ri || (rj == ri && j < i)) ? 1 : 0;
+      }
+      for (int off = G / 2; off >= 1; off >>= 1) rank += __shfl_xor(rank, off, 64);
+      if (tid % G == 0) sOrd[rank] = i;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int taken = 0, tok = 0;
+    for (int r = 0; r < n; ++r) {
+      const int i = sOrd[r];
+      if (taken >= a.max_pages || tok + sLen[i] > a.bn) break;
+      sProt[i] = 1;
+      ++taken;
+      tok += sLen[i];
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < n * kMaxPage; idx += kFT) {
+    const int i = idx / kMaxPage, e = idx % kMaxPage;
+    const int t = sStart[i] + e;
+    if (sProt[i] && e < sLen[i] && t >= 0 && t < S) sPro[t] = 1;
+  }
+  __syncthreads();
+
+  // token states (retired wins over protected) and coded keys: 0 retired,
+  // ~0 protected, else the score's order-preserving image
+  uint32_t key[KPT];
+  int np = 0, nf = 0;
+  uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+#pragma unroll
+  for (int u = 0; u < KPT; ++u) {
+    const int t = t_base + 64 * u;
+    const bool in = t < S;
+    const uint8_t x = !in || sRet[t] ? kRet : ((sPro[t] || t >= S - a.keep_recent) ? kProt : kFree);
+    key[u] = x == kProt ? kKeyProt : (x == kRet ? kKeyRet : score_key(f[u]));
+    np += x == kProt ? 1 : 0;
+    nf += x == kFree ? 1 : 0;
+    if (x == kFree) {
+      lo = min(lo, key[u]);
+      hi = max(hi, key[u]);
+    }
+  }
+  if (a.state) {
+    uint8_t* sto = a.state + (size_t)s * a.score_seq_stride;
+    for (int t = tid; t < S; t += kFT)
+      sto[t] = sRet[t] ? kRet : ((sPro[t] || t >= S - a.keep_recent) ? kProt : kFree);
+  }
+  np = wave_sum(np);
+  nf = wave_sum(nf);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    lo = min(lo, (uint32_t)__shfl_xor((int)lo, off, 64));
+    hi = max(hi, (uint32_t)__shfl_xor((int)hi, off, 64));
+  }
+  if (lane == 0) { wa[wave] = np; wb[wave] = nf; wlo[wave] = lo; whi[wave] = hi; }
+  __syncthreads();
+  int NP = 0, NF = 0;
+#pragma unroll
+  for (int w = 0; w < kFW; ++w) {
+    NP += wa[w];
+    NF += wb[w];
+    lo = min(lo, wlo[w]);
+    hi = max(hi, whi[w]);
+  }
+  __syncthreads();
+
+  // Eq. (13): the k = min(B - #protected, #free) largest free keys
+  const int k = max(0, min(a.budget - NP, NF));
+  uint32_t T;
+  int need_eq = 0;
+  if (k == 0) {
+    T = kKeyProt - 1u;                 // no free key reaches it
+  } else if (k == NF) {
+    T = 0u;                            // every free key is above it
+  } else {
+    int need = k;
+    // at most 3 narrowings of an 11-bit bin index cover 32-bit keys
+    for (int pass = 0; pass < 3 && lo != hi; ++pass) {
+      const uint32_t range = hi - lo;
+      const int shift = max(0, 32 - __clz((int)range) - 11);
+      unsigned int* hc = hist[pass & 1];
+      // the other buffer was last read before the previous pass's final barrier
+      for (int i = tid; i < kSelBins; i += kFT) hist[(pass + 1) & 1][i] = 0u;
+#pragma unroll
+      for (int u = 0; u < KPT; ++u) {
+        const uint32_t kk = key[u];
+        const bool act = key_free(kk) && kk >= lo && kk <= hi;
+        hist_add1(hc, (kk - lo) >> shift, act);
+      }
+      __syncthreads();
+      // thread g owns bins 2(kFT-1-g) and 2(kFT-1-g)+1: an exclusive scan in
+      // thread order counts the keys in higher bins
+      const int g = kFT - 1 - tid;
+      const int h1 = (int)hc[2 * g + 1], h0 = (int)hc[2 * g];
+      int total;
+      const int above = block_scan<kFT>(h0 + h1, tmp, total);
+      int b = -1, rest = 0;
+      if (above < need && above + h1 >= need) { b = 2 * g + 1; rest = need - above; }
+      else if (above + h1 < need && above + h1 + h0 >= need) { b = 2 * g; rest = need - above - h1; }
+      if (b >= 0) {
+        const uint32_t nlo = lo + ((uint32_t)b << shift);
+        const uint32_t width = shift >= 32 ? 0xFFFFFFFFu : ((1u << shift) - 1u);
+        s_lo = nlo;
+        s_hi = min(hi, nlo + min(width, 0xFFFFFFFFu - nlo));
+        s_need = rest;
+      }
+      __syncthreads();
+      lo = s_lo;
+      hi = s_hi;
+      need = s_need;
+    }
+    T = lo;                            // lo == hi: the need-th largest key
+    need_eq = need;
+  }
+
+  // kept indices in ascending order: protected tokens, free keys above T,
+  // and the first need_eq free keys equal to T
+  int nk = 0, ne = 0;
+#pragma unroll
+  for (int u = 0; u < KPT; ++u) {
+    const uint32_t kk = key[u];
+    nk += (kk == kKeyProt || (key_free(kk) && kk > T)) ? 1 : 0;
+    ne += (key_free(kk) && kk == T) ? 1 : 0;
+  }
+  nk = wave_sum(nk);
+  ne = wave_sum(ne);
+  if (lane == 0) { wa[wave] = nk; wb[wave] = ne; }
+  __syncthreads();
+  int k_before = 0, e_before = 0;
+  for (int w = 0; w < wave; ++w) { k_before += wa[w]; e_before += wb[w]; }
+  int32_t* kept = a.kept + (size_t)s * a.budget;
+  int out = k_before + min(need_eq, e_before), eq_run = e_before;
+#pragma unroll
+  for (int u = 0; u < KPT; ++u) {
+    const int t = t_base + 64 * u;
+    const uint32_t kk = key[u];
+    const bool eq = key_free(kk) && kk == T;
+    const unsigned long long em = __ballot(eq);
+    const int eq_rank = eq_run + lanes_below(em);
+    eq_run += __popcll(em);
+    const bool keep = kk == kKeyProt || (key_free(kk) && kk > T) || (eq && eq_rank < need_eq);
+    const unsigned long long km = __ballot(keep);
+    const int pos = out + lanes_below(km);
+    out += __popcll(km);
+    if (keep && pos < a.budget) kept[pos] = t;
+  }
+  const int n_kept = min(a.budget, NP + k);
+  for (int j = n_kept + tid; j < a.budget; j += kFT) kept[j] = -1;
+  if (tid == 0) a.n_kept[s] = n_kept;
+}
+
+bool select_fused_fits(int max_tokens, int max_pending) {
+  return max_tokens <= kSelFusedMax && max_pending <= kProtLds;
+}
+
+hipError_t launch_select_fused(const SelectArgs& a, int max_tokens, hipStream_t s) {
+  const dim3 grid(a.n_seq), block(kFT);
+  // 32 keys per thread stay in registers at 1024 threads (64 would spill)
+  static_assert(kSelFusedMax == 32 * kFT, "fused selection holds 32 keys per thread");
+  if (max_tokens <= 16 * kFT) hipLaunchKernelGGL((select_fused<16>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((select_fused<32>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 

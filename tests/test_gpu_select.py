@@ -63,7 +63,7 @@ def _accepted_form(P, rng, allp, retired):
 
 
 def _run(P, ctx, n_seq, n_layers, H, d, cap, n_tokens, B, seed, keep_recent=0, eta=0.125,
-         max_pages=16, ties=False, nan=False, accepted=False):
+         max_pages=16, ties=False, nan=False, accepted=False, n_pending=40, page_div=80, maxlen=64):
     rng = np.random.default_rng(seed)
     k = torch.randint(-32768, 32767, (n_seq, n_layers, H, cap, d), dtype=torch.int16).view(torch.bfloat16).cuda()
     v = torch.randint(-32768, 32767, (n_seq, n_layers, H, cap, d), dtype=torch.int16).view(torch.bfloat16).cuda()
@@ -76,10 +76,10 @@ def _run(P, ctx, n_seq, n_layers, H, d, cap, n_tokens, B, seed, keep_recent=0, e
     retired, pending, rpre, tables = [], [], [], []
     for s in range(n_seq):
         S = n_tokens[s]
-        allp = _pages(rng, S, max(4, S // 80))
+        allp = _pages(rng, S, max(4, S // page_div), maxlen)
         rng.shuffle(allp)
         ret = sorted(allp[: len(allp) // 3])
-        pen = sorted(allp[len(allp) // 3: len(allp) // 3 + 40])
+        pen = sorted(allp[len(allp) // 3: len(allp) // 3 + n_pending])
         if s == 0 and ret and pen:
             pen = sorted(set(pen) | {ret[0]})     # a page both retired and pending
         retired.append(ret)
@@ -145,6 +145,29 @@ def test_retired_on_device(ckv):
     flags over a device candidate list (the joint test's output)."""
     P, ctx = ckv
     _run(P, ctx, 2, 2, 2, 128, 6000, [6000, 4100], 1200, seed=6, keep_recent=64, accepted=True)
+
+
+def test_one_workgroup_limit(ckv):
+    """Sequences of exactly 32768 tokens (the longest the one-workgroup
+    selection takes) and of 20001 tokens, with device-retired pages."""
+    P, ctx = ckv
+    _run(P, ctx, 2, 1, 1, 64, 32768, [32768, 20001], 8192, seed=7, keep_recent=64, accepted=True)
+
+
+def test_multi_workgroup_selection(ckv):
+    """32769 tokens: one past the one-workgroup selection, so the chunked
+    radix select runs."""
+    P, ctx = ckv
+    _run(P, ctx, 1, 1, 1, 64, 32769, [32769], 8000, seed=8, keep_recent=16, ties=True)
+
+
+def test_many_pending_pages(ckv):
+    """More than 1024 short pending pages (ranked from global memory by the
+    chunked path), most of them protected."""
+    P, ctx = ckv
+    out = _run(P, ctx, 1, 1, 1, 64, 30000, [30000], 9000, seed=9, eta=0.5, max_pages=5000,
+               n_pending=1100, page_div=10, maxlen=8)
+    assert int(out["n_kept"][0]) == 9000
 
 
 def test_long_cache_q32b_shape(ckv):
