@@ -271,8 +271,12 @@ int ckv_classify_pages(ckv_ctx* ctx, int32_t n, const float* R_pre,
  * max_cand must be >= 1.
  * Like the other calls it only enqueues work: the kernels read *n_cand on
  * the device, and the sequential greedy loop runs as speculative rounds
- * inside one cooperative launch (each round decides at least one
- * candidate, so at most min(*n_cand, max_cand) rounds run).
+ * inside one launch of at most as many workgroups as the device holds at
+ * once, separated by grid barriers (each round decides at least one
+ * candidate, so at most min(*n_cand, max_cand) rounds run).  A barrier wait
+ * is bounded (about 1.3 s): if the workgroups cannot all run at once (the
+ * device is shared with other work), every workgroup leaves and
+ * *n_accepted is set to -1 (accepted and union_R are then incomplete).
  */
 int ckv_joint_test(ckv_ctx* ctx, const ckv_kv_view* kv,
                    const ckv_window_view* win, const float* o,
