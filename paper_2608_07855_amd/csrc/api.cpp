@@ -72,7 +72,11 @@ struct ckv_ctx {
   int next_slot = 0;
   std::vector<PageEntry> pages;
   uint64_t tick = 0;
-  // small pinned buffer for device-to-host reads of counters and flags
+  // grid selection state (zero between calls), sized for sel_seq sequences
+  int32_t* sel_ctrl = nullptr;
+  uint32_t* sel_hist = nullptr;
+  int sel_seq = 0;
+  int sel_resident = -1;     // workgroups of the grid selection resident at once
   // kernel timing (events around every launch when enabled)
   bool timing = false;
   std::string timing_only;   // empty: every kernel
@@ -400,6 +404,8 @@ extern "C" int ckv_destroy(ckv_ctx* c) {
     DeviceGuard g(c->device);
     (void)hipStreamSynchronize(c->stream);
     if (c->ws) (void)hipFree(c->ws);
+    if (c->sel_ctrl) (void)hipFree(c->sel_ctrl);
+    if (c->sel_hist) (void)hipFree(c->sel_hist);
     for (auto& e : c->pages)
       if (e.dev) (void)hipFree(e.dev);
     for (auto& s : c->slots) {
@@ -838,8 +844,34 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   sa.n_kept = n_kept;
   int max_pend = 0;
   for (int s = 0; s < ns; ++s) max_pend = std::max(max_pend, pending[s].n_pages);
-  if (select_fused_fits(max_s, max_pend)) {
-    CKV_LAUNCH(c, "select", launch_select_fused(sa, max_s, c->stream));
+  if (c->sel_resident < 0) c->sel_resident = select_grid_resident();
+  if (select_grid_fits(max_s, max_pend, ns, c->sel_resident)) {
+    if (c->sel_seq < ns) {
+      // grow the persistent state; it must start zeroed (the kernel keeps it so)
+      CKV_HIP(c, hipStreamSynchronize(c->stream));
+      if (c->sel_ctrl) (void)hipFree(c->sel_ctrl);
+      if (c->sel_hist) (void)hipFree(c->sel_hist);
+      c->sel_ctrl = nullptr;
+      c->sel_hist = nullptr;
+      c->sel_seq = 0;
+      const size_t cb = (size_t)ns * ckv::kSelGridCtrl * sizeof(int32_t);
+      const size_t hb = (size_t)ns * 3 * ckv::kSelBins * sizeof(uint32_t);
+      void *pc = nullptr, *ph = nullptr;
+      if (hipMalloc(&pc, cb) != hipSuccess || hipMalloc(&ph, hb) != hipSuccess) {
+        (void)hipGetLastError();
+        if (pc) (void)hipFree(pc);
+        return fail(c, CKV_ERR_NOMEM, "selection state of %zu bytes failed", cb + hb);
+      }
+      CKV_HIP(c, hipMemset(pc, 0, cb));
+      CKV_HIP(c, hipMemset(ph, 0, hb));
+      CKV_HIP(c, hipDeviceSynchronize());
+      c->sel_ctrl = static_cast<int32_t*>(pc);
+      c->sel_hist = static_cast<uint32_t*>(ph);
+      c->sel_seq = ns;
+    }
+    sa.gctrl = c->sel_ctrl;
+    sa.ghist = c->sel_hist;
+    CKV_LAUNCH(c, "select", launch_select_grid(sa, max_s, c->stream));
   } else {
     CKV_LAUNCH(c, "protect", launch_protect(sa, c->stream));
     CKV_LAUNCH(c, "select", launch_select(sa, c->stream));

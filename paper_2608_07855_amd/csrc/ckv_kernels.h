@@ -177,15 +177,22 @@ struct SelectArgs {
   int32_t* ctrl;                 // [n_seq][kSelCtrl]
   uint32_t* hist;                // [n_seq][3][2048] digit histograms
   int32_t* wcnt;                 // [n_seq][n_chunks][2] per-chunk counts
+  // persistent state of the grid selection (zero between calls)
+  int32_t* gctrl;                // [n_seq][kSelGridCtrl]
+  uint32_t* ghist;               // [n_seq][3][kSelBins]
 };
 constexpr int kSelChunk = 2048;  // tokens per selection workgroup
 constexpr int kSelCtrl = 16;     // ints of per-sequence selection state
 constexpr int kSelBins = 2048;   // radix digit bins (11-bit digits)
 hipError_t launch_protect(const SelectArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
-constexpr int kSelFusedMax = 32768;   // longest sequence of the one-workgroup selection
-bool select_fused_fits(int max_tokens, int max_pending);
-hipError_t launch_select_fused(const SelectArgs& a, int max_tokens, hipStream_t s);
+constexpr int kSelGridChunk = 2048;       // tokens per grid-selection workgroup
+constexpr int kSelGridMaxChunks = 64;     // longest sequence: 131072 tokens
+constexpr int kSelGridPendMax = 256;      // pending pages per sequence the grid selection ranks
+constexpr int kSelGridCtrl = 8 + 2 * kSelGridMaxChunks;   // control words per sequence
+bool select_grid_fits(int max_tokens, int max_pending, int n_seq, int resident);
+int select_grid_resident();
+hipError_t launch_select_grid(const SelectArgs& a, int max_tokens, hipStream_t s);
 
 struct GatherArgs {
   const uint16_t* k_in;

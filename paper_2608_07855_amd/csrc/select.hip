@@ -17,9 +17,10 @@
 //              the lowest indices.
 //   k = min(B - #protected, #free).  The last workgroup of each histogram
 //   launch (atomic arrival counter) chooses the digit for every sequence.
-// select_fused (sequences of at most kSelFusedMax tokens and kProtLds
-//   pending pages): all of the above in one 1024-thread workgroup per
-//   sequence, keys held in registers.
+// select_grid (sequences of at most kSelGridMaxChunks chunks and
+//   kSelGridPendMax pending pages, every workgroup resident at once): all of
+//   the above in one launch of one workgroup per 2048-token chunk, phases
+//   separated by a per-sequence grid barrier.
 // gather_kernel: K'[s,l,g,j] = K[s,l,g,I[j]], the same for V, and
 //   pos'[s,j] = pos[s,I[j]], 16-byte vector copies of whole rows.
 #include "ckv_device.h"
@@ -434,22 +435,8 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// ---------------------------------------------------------------------------
-// Fused selection for sequences of at most kSelFusedMax tokens: one
-// 1024-thread workgroup per sequence runs protection, token states, keys,
-// the threshold search and the ordered write, with the keys in registers.
-// Wave w owns tokens [w 64 KPT, (w + 1) 64 KPT); in round u lane l holds
-// token w 64 KPT + 64 u + l, so loads are coalesced and a wave's rounds
-// visit its tokens in order (ranks inside a wave come from ballots).
-// The threshold search bins the free keys of the remaining range [lo, hi]
-// into at most 2048 bins of width 2^shift (the range adapts to the keys, so
-// concentrated float scores still spread over the bins) and narrows the
-// range to the bin holding the need-th largest key until shift is 0.
-// ---------------------------------------------------------------------------
+// wave-level helpers of the grid selection
 namespace {
-constexpr int kFT = 1024;
-constexpr int kFW = kFT / 64;
-
 __device__ __forceinline__ int lanes_below(unsigned long long m) {
   return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
@@ -473,70 +460,121 @@ __device__ __forceinline__ void hist_add1(unsigned int* hist, uint32_t bin, bool
 }
 }  // namespace
 
-template <int KPT>
-__global__ __launch_bounds__(kFT) void select_fused(SelectArgs a) {
-  constexpr int SPAN = KPT * kFT;
-  __shared__ uint8_t sRet[SPAN], sPro[SPAN];     // retired / protected-page marks
-  __shared__ unsigned int hist[2][kSelBins];      // double-buffered across passes
-  __shared__ float sR[kProtLds];
-  __shared__ int sLen[kProtLds], sStart[kProtLds], sOrd[kProtLds];
-  __shared__ uint8_t sProt[kProtLds];
-  __shared__ int tmp[kFW], wa[kFW], wb[kFW];
-  __shared__ uint32_t wlo[kFW], whi[kFW];
+// ---------------------------------------------------------------------------
+// Grid selection: one kQT-thread workgroup per kSelGridChunk tokens of a
+// sequence (grid: chunks x sequences), every workgroup resident at once.
+// Phases are separated by a per-sequence grid barrier with a bounded wait:
+//   0. scores, protection (every workgroup ranks the pending pages itself),
+//      token states and keys of the chunk; #protected, #free and the range
+//      of the free keys go to the sequence's control words;
+//   1. up to three narrowings of the threshold range: chunk histograms are
+//      added into a global histogram, then every workgroup makes the same
+//      choice from it;
+//   2. per-chunk counts of kept tokens and of ties at the threshold, then
+//      the ordered write at the chunk's offset.
+// The control words and histograms start at zero (allocated zeroed); the
+// last workgroup of a sequence to finish clears them again for the next
+// call, and marks a call whose barrier timed out with n_kept = -1.
+// ---------------------------------------------------------------------------
+namespace {
+constexpr int kQT = 256;
+constexpr int kQW = kQT / 64;
+constexpr int kQKPT = kSelGridChunk / kQT;   // keys per thread
+enum { qArrive = 0, qDone = 1, qNP = 2, qNF = 3, qNotLo = 4, qHi = 5, qError = 6, qCounts = 8 };
+constexpr long long kSelTimeoutTicks = 1ll << 27;   // ~1.3 s of the 100 MHz wall clock
+
+__device__ bool seq_barrier(int* ctrl, int target, int* s_ok) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    atomicAdd(&ctrl[qArrive], 1);
+    const long long t0 = wall_clock64();
+    int ok = 1;
+    while (__hip_atomic_load(&ctrl[qArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      if (__hip_atomic_load(&ctrl[qError], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
+          wall_clock64() - t0 > kSelTimeoutTicks) {
+        __hip_atomic_store(&ctrl[qError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    __threadfence();
+    *s_ok = ok;
+  }
+  __syncthreads();
+  return *s_ok != 0;
+}
+
+__device__ __forceinline__ int ld_agent(const int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+}  // namespace
+
+__global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
+  __shared__ uint8_t sRet[kSelGridChunk], sPro[kSelGridChunk];
+  __shared__ unsigned int hist[kSelBins];
+  __shared__ float sR[kSelGridPendMax];
+  __shared__ int sLen[kSelGridPendMax], sStart[kSelGridPendMax], sOrd[kSelGridPendMax];
+  __shared__ uint8_t sProt[kSelGridPendMax];
+  __shared__ int tmp[kQW], wa[kQW], wb[kQW];
+  __shared__ uint32_t wlo[kQW], whi[kQW];
   __shared__ uint32_t s_lo, s_hi;
-  __shared__ int s_need;
-  const int s = blockIdx.x;
+  __shared__ int s_need, s_ok;
+  const int s = blockIdx.y, cb = blockIdx.x, C = gridDim.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int* ctrl = a.gctrl + (size_t)s * kSelGridCtrl;
+  uint32_t* gh = a.ghist + (size_t)s * 3 * kSelBins;
+  const int c0 = cb * kSelGridChunk;
   // the scores first: their loads overlap everything up to the keys
   const float* sc = a.score + (size_t)s * a.score_seq_stride;
-  const int t_base = wave * 64 * KPT + lane;
-  float f[KPT];
+  const int t_base = c0 + wave * 64 * kQKPT + lane;
+  float f[kQKPT];
 #pragma unroll
-  for (int u = 0; u < KPT; ++u) {
+  for (int u = 0; u < kQKPT; ++u) {
     const int t = t_base + 64 * u;
     f[u] = t < a.score_seq_stride ? sc[t] : 0.f;
   }
   const int S = a.n_tokens[s];
-  const int poff = a.pend_off[s], n = a.pend_off[s + 1] - poff;   // n <= kProtLds
+  const int c1 = min(S, c0 + kSelGridChunk);          // chunk [c0, c1), empty if c0 >= S
+  const int poff = a.pend_off[s], n = a.pend_off[s + 1] - poff;   // n <= kSelGridPendMax
   const int roff = a.ret_off[s], nr = a.ret_off[s + 1] - roff;
   const float* R = reinterpret_cast<const float*>(a.pend_r[s]);
-  for (int i = tid; i < SPAN / 4; i += kFT) {
+  for (int i = tid; i < kSelGridChunk / 4; i += kQT) {
     reinterpret_cast<uint32_t*>(sRet)[i] = 0u;
     reinterpret_cast<uint32_t*>(sPro)[i] = 0u;
   }
-  for (int i = tid; i < kSelBins; i += kFT) hist[0][i] = 0u;
   __syncthreads();
-  // pending pages to LDS; retired and accepted pages marked meanwhile
-  for (int i = tid; i < n; i += kFT) {
+  // pending pages to LDS; retired and accepted pages that overlap the chunk
+  // marked meanwhile
+  for (int i = tid; i < n; i += kQT) {
     sR[i] = pend_key(R[i]);
     sLen[i] = a.pend_len[poff + i];
     sStart[i] = a.pend_start[poff + i];
     sProt[i] = 0;
   }
-  for (int idx = tid; idx < nr * kMaxPage; idx += kFT) {
-    const int i = idx / kMaxPage, e = idx % kMaxPage;
-    const int t = a.ret_start[roff + i] + e;
-    if (e < a.ret_len[roff + i] && t >= 0 && t < S) sRet[t] = 1;
+  for (int i = tid; i < nr; i += kQT) {
+    const int st = a.ret_start[roff + i], ln = a.ret_len[roff + i];
+    for (int t = max(st, c0); t < min(st + ln, c1); ++t) sRet[t - c0] = 1;
   }
   if (a.acc && a.acc[s].cand) {
     const AccPages ap = a.acc[s];
     const int nc = min(*ap.n_cand, ap.max_cand);
-    for (int idx = tid; idx < nc * kMaxPage; idx += kFT) {
-      const int i = idx / kMaxPage, e = idx % kMaxPage;
+    for (int i = tid; i < nc; i += kQT) {
       if (!ap.accepted[i]) continue;
       const int pg = ap.cand[i];
-      if (pg < 0 || pg >= ap.n_pages || e >= ap.len[pg]) continue;
-      const int t = ap.start[pg] + e;
-      if (t >= 0 && t < S) sRet[t] = 1;
+      if (pg < 0 || pg >= ap.n_pages) continue;
+      const int st = ap.start[pg], ln = ap.len[pg];
+      for (int t = max(st, c0); t < min(st + ln, c1); ++t) sRet[t - c0] = 1;
     }
   }
   __syncthreads();
   // Eq. (12): pending pages ranked by (R- descending, page order), protected
   // in that order while fewer than max_pages are taken and the tokens fit B_N
   {
-    int G = 64;                            // lanes per page (a power of two, inside one wave)
-    while (G > 1 && G * n > kFT) G >>= 1;
-    for (int i = tid / G; i < n; i += kFT / G) {
+    int G = 64;
+    while (G > 1 && G * n > kQT) G >>= 1;
+    for (int i = tid / G; i < n; i += kQT / G) {
       const float ri = sR[i];
       int rank = 0;
       for (int j = tid % G; j < n; j += G) {
@@ -559,23 +597,21 @@ __global__ __launch_bounds__(kFT) void select_fused(SelectArgs a) {
     }
   }
   __syncthreads();
-  for (int idx = tid; idx < n * kMaxPage; idx += kFT) {
-    const int i = idx / kMaxPage, e = idx % kMaxPage;
-    const int t = sStart[i] + e;
-    if (sProt[i] && e < sLen[i] && t >= 0 && t < S) sPro[t] = 1;
+  for (int i = tid; i < n; i += kQT) {
+    if (!sProt[i]) continue;
+    for (int t = max(sStart[i], c0); t < min(sStart[i] + sLen[i], c1); ++t) sPro[t - c0] = 1;
   }
   __syncthreads();
 
-  // token states (retired wins over protected) and coded keys: 0 retired,
-  // ~0 protected, else the score's order-preserving image
-  uint32_t key[KPT];
+  // token states (retired wins over protected) and coded keys
+  uint32_t key[kQKPT];
   int np = 0, nf = 0;
   uint32_t lo = 0xFFFFFFFFu, hi = 0u;
 #pragma unroll
-  for (int u = 0; u < KPT; ++u) {
-    const int t = t_base + 64 * u;
-    const bool in = t < S;
-    const uint8_t x = !in || sRet[t] ? kRet : ((sPro[t] || t >= S - a.keep_recent) ? kProt : kFree);
+  for (int u = 0; u < kQKPT; ++u) {
+    const int t = t_base + 64 * u, i = t - c0;
+    const bool in = t < c1;
+    const uint8_t x = !in || sRet[i] ? kRet : ((sPro[i] || t >= S - a.keep_recent) ? kProt : kFree);
     key[u] = x == kProt ? kKeyProt : (x == kRet ? kKeyRet : score_key(f[u]));
     np += x == kProt ? 1 : 0;
     nf += x == kFree ? 1 : 0;
@@ -586,8 +622,8 @@ __global__ __launch_bounds__(kFT) void select_fused(SelectArgs a) {
   }
   if (a.state) {
     uint8_t* sto = a.state + (size_t)s * a.score_seq_stride;
-    for (int t = tid; t < S; t += kFT)
-      sto[t] = sRet[t] ? kRet : ((sPro[t] || t >= S - a.keep_recent) ? kProt : kFree);
+    for (int t = c0 + tid; t < c1; t += kQT)
+      sto[t] = sRet[t - c0] ? kRet : ((sPro[t - c0] || t >= S - a.keep_recent) ? kProt : kFree);
   }
   np = wave_sum(np);
   nf = wave_sum(nf);
@@ -598,111 +634,163 @@ __global__ __launch_bounds__(kFT) void select_fused(SelectArgs a) {
   }
   if (lane == 0) { wa[wave] = np; wb[wave] = nf; wlo[wave] = lo; whi[wave] = hi; }
   __syncthreads();
-  int NP = 0, NF = 0;
-#pragma unroll
-  for (int w = 0; w < kFW; ++w) {
-    NP += wa[w];
-    NF += wb[w];
-    lo = min(lo, wlo[w]);
-    hi = max(hi, whi[w]);
-  }
-  __syncthreads();
-
-  // Eq. (13): the k = min(B - #protected, #free) largest free keys
-  const int k = max(0, min(a.budget - NP, NF));
-  uint32_t T;
-  int need_eq = 0;
-  if (k == 0) {
-    T = kKeyProt - 1u;                 // no free key reaches it
-  } else if (k == NF) {
-    T = 0u;                            // every free key is above it
-  } else {
-    int need = k;
-    // at most 3 narrowings of an 11-bit bin index cover 32-bit keys
-    for (int pass = 0; pass < 3 && lo != hi; ++pass) {
-      const uint32_t range = hi - lo;
-      const int shift = max(0, 32 - __clz((int)range) - 11);
-      unsigned int* hc = hist[pass & 1];
-      // the other buffer was last read before the previous pass's final barrier
-      for (int i = tid; i < kSelBins; i += kFT) hist[(pass + 1) & 1][i] = 0u;
-#pragma unroll
-      for (int u = 0; u < KPT; ++u) {
-        const uint32_t kk = key[u];
-        const bool act = key_free(kk) && kk >= lo && kk <= hi;
-        hist_add1(hc, (kk - lo) >> shift, act);
-      }
-      __syncthreads();
-      // thread g owns bins 2(kFT-1-g) and 2(kFT-1-g)+1: an exclusive scan in
-      // thread order counts the keys in higher bins
-      const int g = kFT - 1 - tid;
-      const int h1 = (int)hc[2 * g + 1], h0 = (int)hc[2 * g];
-      int total;
-      const int above = block_scan<kFT>(h0 + h1, tmp, total);
-      int b = -1, rest = 0;
-      if (above < need && above + h1 >= need) { b = 2 * g + 1; rest = need - above; }
-      else if (above + h1 < need && above + h1 + h0 >= need) { b = 2 * g; rest = need - above - h1; }
-      if (b >= 0) {
-        const uint32_t nlo = lo + ((uint32_t)b << shift);
-        const uint32_t width = shift >= 32 ? 0xFFFFFFFFu : ((1u << shift) - 1u);
-        s_lo = nlo;
-        s_hi = min(hi, nlo + min(width, 0xFFFFFFFFu - nlo));
-        s_need = rest;
-      }
-      __syncthreads();
-      lo = s_lo;
-      hi = s_hi;
-      need = s_need;
+  if (tid == 0) {
+    int NPc = 0, NFc = 0;
+    uint32_t l = 0xFFFFFFFFu, h = 0u;
+    for (int w = 0; w < kQW; ++w) { NPc += wa[w]; NFc += wb[w]; l = min(l, wlo[w]); h = max(h, whi[w]); }
+    if (NPc) atomicAdd(&ctrl[qNP], NPc);
+    if (NFc) {
+      atomicAdd(&ctrl[qNF], NFc);
+      atomicMax(reinterpret_cast<unsigned int*>(&ctrl[qNotLo]), ~l);   // the minimum, as a maximum of ~key
+      atomicMax(reinterpret_cast<unsigned int*>(&ctrl[qHi]), h);
     }
-    T = lo;                            // lo == hi: the need-th largest key
-    need_eq = need;
   }
-
-  // kept indices in ascending order: protected tokens, free keys above T,
-  // and the first need_eq free keys equal to T
-  int nk = 0, ne = 0;
-#pragma unroll
-  for (int u = 0; u < KPT; ++u) {
-    const uint32_t kk = key[u];
-    nk += (kk == kKeyProt || (key_free(kk) && kk > T)) ? 1 : 0;
-    ne += (key_free(kk) && kk == T) ? 1 : 0;
-  }
-  nk = wave_sum(nk);
-  ne = wave_sum(ne);
-  if (lane == 0) { wa[wave] = nk; wb[wave] = ne; }
-  __syncthreads();
-  int k_before = 0, e_before = 0;
-  for (int w = 0; w < wave; ++w) { k_before += wa[w]; e_before += wb[w]; }
+  int target = C;
+  bool ok = seq_barrier(ctrl, target, &s_ok);
   int32_t* kept = a.kept + (size_t)s * a.budget;
-  int out = k_before + min(need_eq, e_before), eq_run = e_before;
+  if (ok) {
+    const int NP = ld_agent(&ctrl[qNP]), NF = ld_agent(&ctrl[qNF]);
+    lo = ~(uint32_t)ld_agent(&ctrl[qNotLo]);
+    hi = (uint32_t)ld_agent(&ctrl[qHi]);
+    // Eq. (13): the k = min(B - #protected, #free) largest free keys
+    const int k = max(0, min(a.budget - NP, NF));
+    uint32_t T;
+    int need_eq = 0;
+    if (k == 0) {
+      T = kKeyProt - 1u;                 // no free key reaches it
+    } else if (k == NF) {
+      T = 0u;                            // every free key is above it
+    } else {
+      int need = k;
+      for (int pass = 0; pass < 3 && lo != hi; ++pass) {
+        const uint32_t range = hi - lo;
+        const int shift = max(0, 32 - __clz((int)range) - 11);
+        for (int i = tid; i < kSelBins; i += kQT) hist[i] = 0u;
+        __syncthreads();
 #pragma unroll
-  for (int u = 0; u < KPT; ++u) {
-    const int t = t_base + 64 * u;
-    const uint32_t kk = key[u];
-    const bool eq = key_free(kk) && kk == T;
-    const unsigned long long em = __ballot(eq);
-    const int eq_rank = eq_run + lanes_below(em);
-    eq_run += __popcll(em);
-    const bool keep = kk == kKeyProt || (key_free(kk) && kk > T) || (eq && eq_rank < need_eq);
-    const unsigned long long km = __ballot(keep);
-    const int pos = out + lanes_below(km);
-    out += __popcll(km);
-    if (keep && pos < a.budget) kept[pos] = t;
+        for (int u = 0; u < kQKPT; ++u) {
+          const uint32_t kk = key[u];
+          const bool act = key_free(kk) && kk >= lo && kk <= hi;
+          hist_add1(hist, (kk - lo) >> shift, act);
+        }
+        __syncthreads();
+        for (int i = tid; i < kSelBins; i += kQT)
+          if (hist[i]) atomicAdd(&gh[pass * kSelBins + i], hist[i]);
+        target += C;
+        if (!seq_barrier(ctrl, target, &s_ok)) { ok = false; break; }
+        // thread g owns bins 8(kQT-1-g) .. 8(kQT-1-g)+7: an exclusive scan in
+        // thread order counts the keys in higher bins
+        const int g = kQT - 1 - tid;
+        int h[8], sum = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          h[j] = (int)__hip_atomic_load(&gh[pass * kSelBins + 8 * g + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          sum += h[j];
+        }
+        int total;
+        int above = block_scan<kQT>(sum, tmp, total);
+#pragma unroll
+        for (int j = 7; j >= 0; --j) {
+          if (above < need && above + h[j] >= need) {
+            const uint32_t nlo = lo + ((uint32_t)(8 * g + j) << shift);
+            const uint32_t width = (1u << shift) - 1u;
+            s_lo = nlo;
+            s_hi = min(hi, nlo + min(width, 0xFFFFFFFFu - nlo));
+            s_need = need - above;
+          }
+          above += h[j];
+        }
+        __syncthreads();
+        lo = s_lo;
+        hi = s_hi;
+        need = s_need;
+      }
+      T = lo;                            // lo == hi: the need-th largest key
+      need_eq = need;
+    }
+    if (ok) {
+      // per-chunk counts of kept tokens and of ties at T
+      int nk = 0, ne = 0;
+#pragma unroll
+      for (int u = 0; u < kQKPT; ++u) {
+        const uint32_t kk = key[u];
+        nk += (kk == kKeyProt || (key_free(kk) && kk > T)) ? 1 : 0;
+        ne += (key_free(kk) && kk == T) ? 1 : 0;
+      }
+      nk = wave_sum(nk);
+      ne = wave_sum(ne);
+      __syncthreads();
+      if (lane == 0) { wa[wave] = nk; wb[wave] = ne; }
+      __syncthreads();
+      if (tid == 0) {
+        int tk = 0, te = 0;
+        for (int w = 0; w < kQW; ++w) { tk += wa[w]; te += wb[w]; }
+        ctrl[qCounts + 2 * cb] = tk;
+        ctrl[qCounts + 2 * cb + 1] = te;
+      }
+      target += C;
+      ok = seq_barrier(ctrl, target, &s_ok);
+    }
+    if (ok) {
+      // offsets from the chunks before this one and the waves before this one
+      int k_before = 0, e_before = 0;
+      for (int q = 0; q < cb; ++q) {
+        k_before += ld_agent(&ctrl[qCounts + 2 * q]);
+        e_before += ld_agent(&ctrl[qCounts + 2 * q + 1]);
+      }
+      for (int w = 0; w < wave; ++w) { k_before += wa[w]; e_before += wb[w]; }
+      int out = k_before + min(need_eq, e_before), eq_run = e_before;
+#pragma unroll
+      for (int u = 0; u < kQKPT; ++u) {
+        const int t = t_base + 64 * u;
+        const uint32_t kk = key[u];
+        const bool eq = key_free(kk) && kk == T;
+        const unsigned long long em = __ballot(eq);
+        const int eq_rank = eq_run + lanes_below(em);
+        eq_run += __popcll(em);
+        const bool keep = kk == kKeyProt || (key_free(kk) && kk > T) || (eq && eq_rank < need_eq);
+        const unsigned long long km = __ballot(keep);
+        const int pos = out + lanes_below(km);
+        out += __popcll(km);
+        if (keep && pos < a.budget) kept[pos] = t;
+      }
+      const int n_kept = min(a.budget, NP + k);
+      for (int j = n_kept + cb * kQT + tid; j < a.budget; j += C * kQT) kept[j] = -1;
+      if (cb == 0 && tid == 0) a.n_kept[s] = n_kept;
+    }
   }
-  const int n_kept = min(a.budget, NP + k);
-  for (int j = n_kept + tid; j < a.budget; j += kFT) kept[j] = -1;
-  if (tid == 0) a.n_kept[s] = n_kept;
+  // the last workgroup of the sequence clears the control words and the
+  // histograms for the next call (every other workgroup is done with them)
+  __syncthreads();
+  if (tid == 0) {
+    __threadfence();
+    s_ok = atomicAdd(&ctrl[qDone], 1) == C - 1;
+  }
+  __syncthreads();
+  if (s_ok) {
+    __threadfence();
+    if (tid == 0 && ld_agent(&ctrl[qError]) != 0) a.n_kept[s] = -1;
+    for (int i = tid; i < 3 * kSelBins; i += kQT) gh[i] = 0u;
+    for (int i = tid; i < kSelGridCtrl; i += kQT) ctrl[i] = 0;
+  }
 }
 
-bool select_fused_fits(int max_tokens, int max_pending) {
-  return max_tokens <= kSelFusedMax && max_pending <= kProtLds;
+bool select_grid_fits(int max_tokens, int max_pending, int n_seq, int resident) {
+  const int C = (max_tokens + kSelGridChunk - 1) / kSelGridChunk;
+  return max_pending <= kSelGridPendMax && C <= kSelGridMaxChunks && (int64_t)C * n_seq <= resident;
 }
 
-hipError_t launch_select_fused(const SelectArgs& a, int max_tokens, hipStream_t s) {
-  const dim3 grid(a.n_seq), block(kFT);
-  // 32 keys per thread stay in registers at 1024 threads (64 would spill)
-  static_assert(kSelFusedMax == 32 * kFT, "fused selection holds 32 keys per thread");
-  if (max_tokens <= 16 * kFT) hipLaunchKernelGGL((select_fused<16>), grid, block, 0, s, a);
-  else hipLaunchKernelGGL((select_fused<32>), grid, block, 0, s, a);
+int select_grid_resident() {
+  int dev = 0, per_cu = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_grid, kQT, 0) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return per_cu * cus;
+}
+
+hipError_t launch_select_grid(const SelectArgs& a, int max_tokens, hipStream_t s) {
+  const int C = (max_tokens + kSelGridChunk - 1) / kSelGridChunk;
+  hipLaunchKernelGGL(select_grid, dim3(C, a.n_seq), dim3(kQT), 0, s, a);
   return hipGetLastError();
 }
 

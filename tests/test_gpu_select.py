@@ -147,18 +147,25 @@ def test_retired_on_device(ckv):
     _run(P, ctx, 2, 2, 2, 128, 6000, [6000, 4100], 1200, seed=6, keep_recent=64, accepted=True)
 
 
-def test_one_workgroup_limit(ckv):
-    """Sequences of exactly 32768 tokens (the longest the one-workgroup
-    selection takes) and of 20001 tokens, with device-retired pages."""
+def test_unequal_sequences(ckv):
+    """32768 and 20001 tokens in one call: the shorter sequence's last
+    2048-token chunks are empty but still take part in its phases; with
+    device-retired pages."""
     P, ctx = ckv
     _run(P, ctx, 2, 1, 1, 64, 32768, [32768, 20001], 8192, seed=7, keep_recent=64, accepted=True)
 
 
-def test_multi_workgroup_selection(ckv):
-    """32769 tokens: one past the one-workgroup selection, so the chunked
-    radix select runs."""
+def test_chunk_boundary(ckv):
+    """32769 tokens: one token in the last chunk; ties in the scores."""
     P, ctx = ckv
     _run(P, ctx, 1, 1, 1, 64, 32769, [32769], 8000, seed=8, keep_recent=16, ties=True)
+
+
+def test_chunked_long_sequence(ckv):
+    """140000 tokens, past the longest sequence the one-launch selection
+    takes (64 chunks), so the chunked radix select runs."""
+    P, ctx = ckv
+    _run(P, ctx, 1, 1, 1, 64, 140000, [140000], 30000, seed=10, keep_recent=64, accepted=True)
 
 
 def test_many_pending_pages(ckv):
