@@ -529,6 +529,8 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
   int *fix_list = nullptr, *fix_count = nullptr;
   plan.add(&fix_list, 4 * (size_t)total_rows);
   plan.add(&fix_count, 1);
+  float* fpart = nullptr;
+  plan.add(&fpart, (size_t)total_rows * ckv::kFixParts * (D + 1));
   const int32_t *dstart = nullptr, *dlen = nullptr;
   if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
   if ((rc = realize(c, plan))) return rc;
@@ -554,7 +556,7 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
     pw.fix_count = fix_count;
     pw.fix_cap = total_rows;
     CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, rs, 0, max_page_len(pages), c->stream));
-    CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, sp, rs, pw, c->stream));
+    CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, sp, rs, pw, fpart, c->stream));
   }
   if (token_mass) {
     const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kTargetBlocks / a.Hkv)), 64);

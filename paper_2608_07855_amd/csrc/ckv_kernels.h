@@ -88,8 +88,10 @@ hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowSt
                               int max_len, hipStream_t s);
 hipError_t launch_token_mass(const AttnGeom& a, const RowStats& rs, float* mass, int chunk,
                              hipStream_t s);
+// fpart: workspace [fix_cap][kFixParts][D + 1] floats
+constexpr int kFixParts = 8;   // workgroups per listed (page, row) pair
 hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
-                             const PageWork& pw, hipStream_t s);
+                             const PageWork& pw, float* fpart, hipStream_t s);
 
 // classification (Eq. (8)-(10)) and candidate order
 struct ClassifyArgs {

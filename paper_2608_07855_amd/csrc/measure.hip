@@ -776,39 +776,63 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
 // B'. fix-up of ill-conditioned (page, row) pairs: o' = output without the
 // page from the other splits' partial sums plus the page's own split(s)
 // recomputed in float32 with the page excluded; ratio = ||o - o'|| / ||o||.
-// One workgroup per listed pair (grid-stride over the list).
+//
+// Each listed pair is spread over kFixParts workgroups: part j takes the
+// other splits s = j (mod kFixParts) and the j-th segment of the page's own
+// split(s), with every load of a 128-token round in flight at once, and
+// stores its partial sums (fixed order inside the part).  The final kernel
+// adds the parts in order (so the result does not depend on scheduling) and
+// takes the ratio.  Weights are taken relative to the row's log-sum-exp
+// (every weight <= 1).
 // ---------------------------------------------------------------------------
-constexpr int kFixT = 1024;       // threads of a fix-up workgroup
-constexpr int kFixGrid = 128;     // listed pairs in flight
+constexpr int kFixT = 256;        // threads of a fix-up workgroup
+constexpr int kFixGrid = 1024;    // (pair, part) items in flight
 
-// One workgroup per listed pair (grid-stride over the list), so no
-// workgroup waits for another: the other splits' partial sums as they are,
-// plus the page's own split(s) recomputed in float32 without the page.
-// Weights are taken relative to the row's log-sum-exp (every weight <= 1).
 template <int D>
-__global__ __launch_bounds__(kFixT) void page_fixup_kernel(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw) {
+__global__ __launch_bounds__(kFixT) void page_fixup_partial(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw,
+                                                            float* fpart) {
   constexpr int TPR = D / 8;                  // threads per token row (16 bytes each)
   constexpr int RPR = kFixT / TPR;            // token rows per round
-  constexpr int UNR = 4;                      // rounds whose loads are in flight together
+  constexpr int UNR = 128 / RPR;              // rounds whose loads are in flight together
   __shared__ float sacc[RPR][D + 1];
-  __shared__ float sred[2][kFixT / 64];
   const int tid = threadIdx.x, c = tid % TPR, r = tid / TPR;
   const int n = min(*pw.fix_count, pw.fix_cap);
-  for (int e = blockIdx.x; e < n; e += gridDim.x) {
+  for (int item = blockIdx.x; item < n * kFixParts; item += gridDim.x) {
+    const int e = item / kFixParts, part = item % kFixParts;
     // entry: page, global row, page start, page length
     const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
-    const int page = ent.x, rg = ent.y, st = ent.z, ln = ent.w;
+    const int rg = ent.y, st = ent.z, ln = ent.w;
     const int h = rg / a.W, p = rg % a.W, g = h / a.group, row = rg - g * a.rows;
-    const float ov = tid < D ? rs.o[(size_t)rg * D + tid] : 0.f;
     const int qp = a.qpos[p];
     const float ref = rs.lse2[rg];
     const int s0 = st / sp.chunk, s1 = (st + ln - 1) / sp.chunk;
+    // this part's segment of the page's split(s): its first round of loads
+    // is issued before the other splits' partial sums are read
+    const int t_lo = s0 * sp.chunk, t_hi = min(a.S, (s1 + 1) * sp.chunk);
+    const int seg = (((t_hi - t_lo + kFixParts - 1) / kFixParts) + RPR - 1) / RPR * RPR;
+    const int a0 = t_lo + part * seg, a1 = min(t_hi, a0 + seg);
+    const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
+    const uint16_t* vh = a.v + (int64_t)g * a.kv_head_stride;
+    const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)p * a.q_row_stride;
+    const u32x4 qc = ldg_u4(qrow + 8 * c);
+    u32x4 kc[UNR], vc[UNR];
+    int pv[UNR];
+    auto load_round = [&](int b0) {
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int t = max(a0, min(b0 + u * RPR + r, a1 - 1));
+        kc[u] = ldg_u4(kh + (int64_t)t * a.kv_tok_stride + 8 * c);
+        vc[u] = ldg_u4(vh + (int64_t)t * a.kv_tok_stride + 8 * c);
+        pv[u] = ldg_i32(a.pos + t);
+      }
+    };
+    if (a0 < a1) load_round(a0);
     float acc[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[j] = 0.f;
     float lacc = 0.f;
-    // other splits' partial sums as they are (row group r takes splits r, r+RPR, ...)
-    for (int s = r; s < sp.n_splits; s += RPR) {
+    // other splits' partial sums as they are: this part's splits, one per row group
+    for (int s = part + kFixParts * r; s < sp.n_splits; s += kFixParts * RPR) {
       if (s >= s0 && s <= s1) continue;
       const size_t idx = (size_t)(g * sp.n_splits + s) * sp.rows_pad + row;
       const float ms = sp.part_m[idx];
@@ -822,76 +846,83 @@ __global__ __launch_bounds__(kFixT) void page_fixup_kernel(AttnGeom a, AttnSplit
       }
       if (c == 0) lacc = __builtin_fmaf(w, sp.part_l[idx], lacc);
     }
-    // the page's split(s) without the page, in float32
-    float qv[8];
-    {
-      const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)p * a.q_row_stride;
-      const u32x4 qc = ldg_u4(qrow + 8 * c);
+    // the segment without the page, in float32
+    if (a0 < a1) {
+      float qv[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) qv[j] = bf16_bits_to_float(chunk_elem(qc, j));
-    }
-    const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
-    const uint16_t* vh = a.v + (int64_t)g * a.kv_head_stride;
-    const int t_lo = s0 * sp.chunk, t_hi = min(a.S, (s1 + 1) * sp.chunk);
-    for (int b0 = t_lo; b0 < t_hi; b0 += UNR * RPR) {
-      u32x4 kc[UNR], vc[UNR];
-      int pv[UNR];
+      for (int b0 = a0; b0 < a1; b0 += UNR * RPR) {
+        if (b0 != a0) load_round(b0);
 #pragma unroll
-      for (int u = 0; u < UNR; ++u) {
-        const int t = min(b0 + u * RPR + r, t_hi - 1);
-        kc[u] = ldg_u4(kh + (int64_t)t * a.kv_tok_stride + 8 * c);
-        vc[u] = ldg_u4(vh + (int64_t)t * a.kv_tok_stride + 8 * c);
-        pv[u] = ldg_i32(a.pos + t);
-      }
+        for (int u = 0; u < UNR; ++u) {
+          const int t = b0 + u * RPR + r;
+          float x = 0.f;
 #pragma unroll
-      for (int u = 0; u < UNR; ++u) {
-        const int t = b0 + u * RPR + r;
-        float x = 0.f;
+          for (int j = 0; j < 8; ++j) x = __builtin_fmaf(qv[j], bf16_bits_to_float(chunk_elem(kc[u], j)), x);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x = __builtin_fmaf(qv[j], bf16_bits_to_float(chunk_elem(kc[u], j)), x);
+          for (int off = TPR / 2; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+          const bool keep = t < a1 && pv[u] <= qp && !(t >= st && t < st + ln);
+          const float w = keep ? __builtin_amdgcn_exp2f(__builtin_fmaf(x, a.sl2, -ref)) : 0.f;
 #pragma unroll
-        for (int off = TPR / 2; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
-        const bool keep = t < t_hi && pv[u] <= qp && !(t >= st && t < st + ln);
-        const float w = keep ? __builtin_amdgcn_exp2f(__builtin_fmaf(x, a.sl2, -ref)) : 0.f;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[j] = __builtin_fmaf(w, bf16_bits_to_float(chunk_elem(vc[u], j)), acc[j]);
-        if (c == 0) lacc += w;
+          for (int j = 0; j < 8; ++j)
+            acc[j] = __builtin_fmaf(w, bf16_bits_to_float(chunk_elem(vc[u], j)), acc[j]);
+          if (c == 0) lacc += w;
+        }
       }
     }
-    __syncthreads();
 #pragma unroll
     for (int j = 0; j < 8; ++j) sacc[r][8 * c + j] = acc[j];
     if (c == 0) sacc[r][D] = lacc;
     __syncthreads();
-    // o' = sum / weight, ratio = ||o - o'|| / ||o||
-    float den = 0.f;
-    for (int i = 0; i < RPR; ++i) den += sacc[i][D];
+    // the part's sums: row groups added in order
+    float* out = fpart + ((size_t)e * kFixParts + part) * (D + 1);
+    for (int i = tid; i <= D; i += kFixT) {
+      float v = 0.f;
+      for (int k = 0; k < RPR; ++k) v += sacc[k][i];
+      out[i] = v;
+    }
+    __syncthreads();
+  }
+}
+
+// one wave per listed pair: parts added in order, ratio ||o - o'|| / ||o||
+template <int D>
+__global__ __launch_bounds__(256) void page_fixup_final(AttnGeom a, RowStats rs, PageWork pw, const float* fpart) {
+  const int lane = threadIdx.x & 63;
+  const int n = min(*pw.fix_count, pw.fix_cap);
+  for (int e = blockIdx.x * 4 + (threadIdx.x >> 6); e < n; e += gridDim.x * 4) {
+    const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
+    const int page = ent.x, rg = ent.y, h = rg / a.W;
+    const float* fp = fpart + (size_t)e * kFixParts * (D + 1);
+    float num[D / 64], den = 0.f;
+#pragma unroll
+    for (int j = 0; j < D / 64; ++j) num[j] = 0.f;
+    for (int part = 0; part < kFixParts; ++part) {
+#pragma unroll
+      for (int j = 0; j < D / 64; ++j) num[j] += fp[part * (D + 1) + lane + 64 * j];
+      den += fp[part * (D + 1) + D];
+    }
     float dd = 0.f, oo = 0.f;
-    if (tid < D) {
-      float num = 0.f;
-      for (int i = 0; i < RPR; ++i) num += sacc[i][tid];
-      const float od = den > 0.f ? num / den : 0.f;
-      dd = (ov - od) * (ov - od);
-      oo = ov * ov;
+#pragma unroll
+    for (int j = 0; j < D / 64; ++j) {
+      const float ov = rs.o[(size_t)rg * D + lane + 64 * j];
+      const float od = den > 0.f ? num[j] / den : 0.f;
+      dd += (ov - od) * (ov - od);
+      oo += ov * ov;
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
       dd += __shfl_xor(dd, off, 64);
       oo += __shfl_xor(oo, off, 64);
     }
-    if ((tid & 63) == 0 && tid < D) { sred[0][tid >> 6] = dd; sred[1][tid >> 6] = oo; }
-    __syncthreads();
-    if (tid == 0) {
-      const float D2 = sred[0][0] + (D > 64 ? sred[0][1] : 0.f);
-      const float O2 = sred[1][0] + (D > 64 ? sred[1][1] : 0.f);
+    if (lane == 0) {
       float ratio;
       if (!(den > 0.f)) ratio = INFINITY;
-      else if (O2 > 0.f) ratio = sqrtf(D2) / sqrtf(O2);
-      else ratio = D2 > 0.f ? INFINITY : 0.f;
+      else if (oo > 0.f) ratio = sqrtf(dd) / sqrtf(oo);
+      else ratio = dd > 0.f ? INFINITY : 0.f;
       if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], ratio);
       atomic_max_nonneg(&pw.R[page], ratio);
     }
-    __syncthreads();
   }
 }
 
@@ -1212,10 +1243,16 @@ hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowSt
 }
 
 hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
-                             const PageWork& pw, hipStream_t s) {
-  dim3 grid(std::min(pw.fix_cap, kFixGrid)), block(kFixT);
-  if (a.D == 128) hipLaunchKernelGGL((page_fixup_kernel<128>), grid, block, 0, s, a, sp, rs, pw);
-  else hipLaunchKernelGGL((page_fixup_kernel<64>), grid, block, 0, s, a, sp, rs, pw);
+                             const PageWork& pw, float* fpart, hipStream_t s) {
+  dim3 grid(std::min(pw.fix_cap * kFixParts, kFixGrid)), block(kFixT);
+  dim3 grid2(std::max(1, std::min((pw.fix_cap + 3) / 4, 256))), block2(256);
+  if (a.D == 128) {
+    hipLaunchKernelGGL((page_fixup_partial<128>), grid, block, 0, s, a, sp, rs, pw, fpart);
+    hipLaunchKernelGGL((page_fixup_final<128>), grid2, block2, 0, s, a, rs, pw, fpart);
+  } else {
+    hipLaunchKernelGGL((page_fixup_partial<64>), grid, block, 0, s, a, sp, rs, pw, fpart);
+    hipLaunchKernelGGL((page_fixup_final<64>), grid2, block2, 0, s, a, rs, pw, fpart);
+  }
   return hipGetLastError();
 }
 
