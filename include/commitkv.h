@@ -201,6 +201,35 @@ typedef struct ckv_cache_view {
   int32_t capacity;          /* token slots per (seq, layer, head) */
 } ckv_cache_view;
 
+/* Component switches of the method, for the ablation variants of Sec. 4.4
+ * (Table 3).  A context-wide bit set, 0 (the default) being the complete
+ * method; it applies to the calls enqueued after it is set.
+ *   CKV_POLICY_NO_PRECOMMIT   ckv_classify_pages: every page with L+ is a
+ *                             retirement candidate, whatever its pre-commit
+ *                             state (instead of H- and L+ of Eq. (10))
+ *   CKV_POLICY_NO_PERCENTILE  ckv_classify_pages: H and L of Eq. (9) from the
+ *                             absolute thresholds tau_use / tau_dead alone
+ *   CKV_POLICY_NO_JOINT       ckv_joint_test: every candidate is accepted
+ *                             (no Eq. (11) gate); union_R still reports
+ *                             R+(A u {E})
+ *   CKV_POLICY_NO_PROTECTION  ckv_select_and_compact: no pending page is
+ *                             protected (N_j empty)
+ *   CKV_POLICY_NO_LIFECYCLE   no lifecycle operation: ckv_classify_pages
+ *                             writes no candidate (n_cand = 0), and
+ *                             ckv_select_and_compact retires nothing and
+ *                             protects no pending page
+ * Returns CKV_ERR_ARG for a NULL context or an unknown bit. */
+typedef enum ckv_policy_flag {
+  CKV_POLICY_NO_PRECOMMIT = 1,
+  CKV_POLICY_NO_PERCENTILE = 2,
+  CKV_POLICY_NO_JOINT = 4,
+  CKV_POLICY_NO_PROTECTION = 8,
+  CKV_POLICY_NO_LIFECYCLE = 16
+} ckv_policy_flag;
+int ckv_set_policy(ckv_ctx* ctx, uint32_t flags);
+/* The context's current switches (0 for a NULL context). */
+uint32_t ckv_get_policy(const ckv_ctx* ctx);
+
 /* ------------------------------------------------------------- the calls */
 
 /*

@@ -17,6 +17,7 @@ float64, in the order and notation of Sec. 3:
 * Sec. 3.2, Eq. (9)-(10): high/low indicators and lifecycle states.
 * Sec. 3.3, Eq. (11) and Algorithm 1: greedy joint retirement test.
 * Sec. 3.3, Eq. (12)-(13): pending-page protection and the retained set.
+* Sec. 4.4: the ablation variants (``ABLATIONS``) switch single components off.
 
 The deletion effect is defined by brute force (``page_effects_bruteforce``):
 attention is run again with the page masked out.  ``page_effects_closed_form``
@@ -62,6 +63,14 @@ FREE, PROTECTED, RETIRED = 0, 1, 2
 # Sec. 4.1 (implementation details)
 PAPER_THRESHOLDS = dict(tau_use=0.05, tau_dead=0.01, rho_use=0.75,
                         rho_dead=0.25, tau_joint=0.01)
+
+# Sec. 4.4 ablation variants, each switching one component of the method off:
+#   no_precommit  retirement candidates from L+ alone instead of (H-, L+)
+#   no_percentile high/low from the absolute thresholds only (no rho test)
+#   no_joint      every candidate retired without the Eq. (11) gate
+#   no_protection no pending page protected (N_j empty)
+#   no_lifecycle  no lifecycle operation at all: nothing retired or protected
+ABLATIONS = ("no_precommit", "no_percentile", "no_joint", "no_protection", "no_lifecycle")
 
 
 # ----------------------------------------------------------------------------
@@ -259,39 +268,55 @@ def percentile_ranks(R):
     return less / (n - 1)
 
 
-def high_low(R, P, tau_use, tau_dead, rho_use, rho_dead):
-    """Eq. (9): H = (R >= tau_use and P >= rho_use); L = (R <= tau_dead and P <= rho_dead)."""
+def high_low(R, P, tau_use, tau_dead, rho_use, rho_dead, percentile=True):
+    """Eq. (9): H = (R >= tau_use and P >= rho_use); L = (R <= tau_dead and P <= rho_dead).
+
+    percentile=False is the Sec. 4.4 variant without percentile calibration:
+    the absolute thresholds alone decide.
+    """
     R = np.asarray(R, dtype=np.float64)
-    H = (R >= tau_use) & (P >= rho_use)
-    L = (R <= tau_dead) & (P <= rho_dead)
+    H = R >= tau_use
+    L = R <= tau_dead
+    if percentile:
+        H = H & (P >= rho_use)
+        L = L & (P <= rho_dead)
     return H, L
 
 
-def lifecycle(H_pre, L_pre, H_post, L_post):
+def lifecycle(H_pre, L_pre, H_post, L_post, precommit=True):
     """Eq. (10): candidate (H-,L+), dormant (L-,L+), newly active (L-,H+),
-    still active (H-,H+), otherwise uncertain."""
+    still active (H-,H+), otherwise uncertain.
+
+    precommit=False is the Sec. 4.4 variant without the pre-commit state:
+    every page with L+ is a candidate, whatever its pre-commit state.
+    """
     lam = np.full(len(H_pre), UNCERTAIN, dtype=np.uint8)
-    lam[H_pre & L_post] = CANDIDATE
-    lam[L_pre & L_post] = DORMANT
     lam[L_pre & H_post] = NEWLY_ACTIVE
     lam[H_pre & H_post] = STILL_ACTIVE
+    if precommit:
+        lam[H_pre & L_post] = CANDIDATE
+        lam[L_pre & L_post] = DORMANT
+    else:
+        lam[L_post] = CANDIDATE
     return lam
 
 
 def classify(R_pre, R_post, starts, tau_use=0.05, tau_dead=0.01, rho_use=0.75,
-             rho_dead=0.25, max_cand=None):
+             rho_dead=0.25, max_cand=None, ablation=()):
     """Pages of E_c -> (lambda, P_pre, P_post, ordered candidate indices).
 
     Candidate order (Sec. 3.3 and Algorithm 1): R+ ascending, then R-
-    descending, then page start ascending (reading R6).
+    descending, then page start ascending (reading R6).  ``ablation`` names
+    Sec. 4.4 variants (``ABLATIONS``); with no_lifecycle there is no candidate.
     """
     R_pre = np.asarray(R_pre, dtype=np.float64)
     R_post = np.asarray(R_post, dtype=np.float64)
+    pct = "no_percentile" not in ablation
     P_pre, P_post = percentile_ranks(R_pre), percentile_ranks(R_post)
-    H_pre, L_pre = high_low(R_pre, P_pre, tau_use, tau_dead, rho_use, rho_dead)
-    H_post, L_post = high_low(R_post, P_post, tau_use, tau_dead, rho_use, rho_dead)
-    lam = lifecycle(H_pre, L_pre, H_post, L_post)
-    idx = [j for j in range(len(lam)) if lam[j] == CANDIDATE]
+    H_pre, L_pre = high_low(R_pre, P_pre, tau_use, tau_dead, rho_use, rho_dead, pct)
+    H_post, L_post = high_low(R_post, P_post, tau_use, tau_dead, rho_use, rho_dead, pct)
+    lam = lifecycle(H_pre, L_pre, H_post, L_post, "no_precommit" not in ablation)
+    idx = [] if "no_lifecycle" in ablation else [j for j in range(len(lam)) if lam[j] == CANDIDATE]
     idx.sort(key=lambda j: (R_post[j], -R_pre[j], int(starts[j])))
     if max_cand is not None:
         idx = idx[:max_cand]
@@ -325,9 +350,11 @@ def union_effect(K, V, pos, Q, qpos, pages, members, scale=None,
 
 
 def joint_test(K, V, pos, Q, qpos, pages, cand, tau_joint=0.01, scale=None,
-               method="bruteforce"):
+               method="bruteforce", gate=True):
     """Algorithm 1: A = {}; for E in order: accept iff R+(A u {E}) <= tau_joint.
 
+    gate=False is the Sec. 4.4 variant without joint validation: every
+    candidate is accepted (union_R still reports R+(A u {E})).
     Returns (accepted bool[len(cand)], union_R float64[len(cand)]).
     """
     accepted = np.zeros(len(cand), dtype=bool)
@@ -336,7 +363,7 @@ def joint_test(K, V, pos, Q, qpos, pages, cand, tau_joint=0.01, scale=None,
     for t, j in enumerate(cand):
         r = union_effect(K, V, pos, Q, qpos, pages, A + [int(j)], scale, method)
         union_R[t] = r
-        if r <= tau_joint:
+        if r <= tau_joint or not gate:
             A.append(int(j))
             accepted[t] = True
     return accepted, union_R

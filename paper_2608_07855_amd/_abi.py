@@ -24,6 +24,15 @@ STATUS_NAMES = {0: "CKV_OK", -1: "CKV_ERR_ARG", -2: "CKV_ERR_SHAPE", -3: "CKV_ER
                 -4: "CKV_ERR_UNSUPPORTED", -5: "CKV_ERR_NOMEM", -6: "CKV_ERR_HIP",
                 -7: "CKV_ERR_NONFINITE"}
 MAX_PAGE_LEN = 64
+# ckv_policy_flag: component switches of the Sec. 4.4 ablation variants
+POLICY_NO_PRECOMMIT = 1
+POLICY_NO_PERCENTILE = 2
+POLICY_NO_JOINT = 4
+POLICY_NO_PROTECTION = 8
+POLICY_NO_LIFECYCLE = 16
+POLICY_BITS = {"no_precommit": POLICY_NO_PRECOMMIT, "no_percentile": POLICY_NO_PERCENTILE,
+               "no_joint": POLICY_NO_JOINT, "no_protection": POLICY_NO_PROTECTION,
+               "no_lifecycle": POLICY_NO_LIFECYCLE}
 
 c_i32p = ctypes.POINTER(ctypes.c_int32)
 c_f32p = ctypes.POINTER(ctypes.c_float)
@@ -85,6 +94,8 @@ SIGNATURES = {
     "ckv_version": (ctypes.c_uint32, []),
     "ckv_set_workspace_limit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t]),
     "ckv_workspace_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
+    "ckv_set_policy": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_uint32]),
+    "ckv_get_policy": (ctypes.c_uint32, [ctypes.c_void_p]),
     "ckv_set_kernel_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
     "ckv_set_kernel_timing_only": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_char_p]),
     "ckv_kernel_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32,

@@ -68,6 +68,18 @@ class Context:
     def workspace_bytes(self) -> int:
         return int(self._lib.ckv_workspace_bytes(self.handle))
 
+    def set_policy(self, *names):
+        """Switch components off for the Sec. 4.4 ablation variants: names from
+        no_precommit, no_percentile, no_joint, no_protection, no_lifecycle
+        (none: the complete method)."""
+        bits = 0
+        for n in names:
+            bits |= _abi.POLICY_BITS[n]
+        self.check(self._lib.ckv_set_policy(self.handle, bits))
+
+    def policy(self) -> int:
+        return int(self._lib.ckv_get_policy(self.handle))
+
     def set_kernel_timing(self, enable: bool):
         self.check(self._lib.ckv_set_kernel_timing(self.handle, int(bool(enable))))
 

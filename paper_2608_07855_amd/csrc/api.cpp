@@ -77,6 +77,7 @@ struct ckv_ctx {
   uint32_t* sel_hist = nullptr;
   int sel_seq = 0;
   int sel_resident = -1;     // workgroups of the grid selection resident at once
+  uint32_t policy = 0;       // CKV_POLICY_* switches (Sec. 4.4 variants)
   // kernel timing (events around every launch when enabled)
   bool timing = false;
   std::string timing_only;   // empty: every kernel
@@ -451,6 +452,17 @@ extern "C" int ckv_set_workspace_limit(ckv_ctx* c, size_t bytes) {
 
 extern "C" size_t ckv_workspace_bytes(const ckv_ctx* c) { return c ? c->ws_cap : 0; }
 
+extern "C" int ckv_set_policy(ckv_ctx* c, uint32_t flags) {
+  if (!c) return CKV_ERR_ARG;
+  constexpr uint32_t known = CKV_POLICY_NO_PRECOMMIT | CKV_POLICY_NO_PERCENTILE | CKV_POLICY_NO_JOINT |
+                             CKV_POLICY_NO_PROTECTION | CKV_POLICY_NO_LIFECYCLE;
+  if (flags & ~known) return fail(c, CKV_ERR_ARG, "unknown policy bits 0x%x", flags & ~known);
+  c->policy = flags;
+  return CKV_OK;
+}
+
+extern "C" uint32_t ckv_get_policy(const ckv_ctx* c) { return c ? c->policy : 0u; }
+
 extern "C" int ckv_set_kernel_timing_only(ckv_ctx* c, const char* name) {
   if (!c) return CKV_ERR_ARG;
   c->timing_only = name ? name : "";
@@ -593,6 +605,7 @@ extern "C" int ckv_classify_pages(ckv_ctx* c, int32_t n, const float* R_pre, con
   a.P_post = P_post;
   a.cand = cand;
   a.n_cand = n_cand;
+  a.policy = c->policy;
   Plan plan;
   plan.add(&a.is_cand, std::max(n, 1));
   if (!P_pre) plan.add(&a.P_pre, std::max(n, 1));
@@ -630,6 +643,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   j.window = kJointWindow;
   j.rows_per_block = kJointRowsPerBlock;
   j.tau = tau_joint;
+  j.accept_all = (c->policy & CKV_POLICY_NO_JOINT) != 0;
   j.accepted = accepted;
   j.union_R = union_R;
   j.n_accepted = n_accepted;
@@ -760,6 +774,15 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
       if (overlap(ins[x], inb[x], outs[y], outb[y])) return fail(c, CKV_ERR_ARG, "output cache overlaps the input");
   if (overlap(out->k, eo, out->v, eo)) return fail(c, CKV_ERR_ARG, "output K and V overlap");
   DeviceGuard g(c->device);
+
+  // Sec. 4.4 variants: without transition protection no pending page is
+  // protected; without the lifecycle mechanism nothing is retired either
+  std::vector<ckv_page_list> no_pages(ns, ckv_page_list{nullptr, nullptr, 0});
+  if (c->policy & (CKV_POLICY_NO_PROTECTION | CKV_POLICY_NO_LIFECYCLE)) pending = no_pages.data();
+  if (c->policy & CKV_POLICY_NO_LIFECYCLE) {
+    retired = no_pages.data();
+    accepted = nullptr;
+  }
 
   // accepted pages of this commit: device page tables (cached by content)
   std::vector<AccPages> acc(ns);

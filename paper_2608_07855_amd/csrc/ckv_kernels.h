@@ -107,6 +107,7 @@ struct ClassifyArgs {
   uint8_t* is_cand;       // workspace [n]
   int32_t* cand;
   int32_t* n_cand;
+  uint32_t policy;        // CKV_POLICY_* bits (Sec. 4.4 variants)
 };
 hipError_t launch_classify(const ClassifyArgs& c, hipStream_t s);
 
@@ -134,6 +135,7 @@ struct JointArgs {
   int window;             // candidates evaluated per round
   int rows_per_block;
   float tau;
+  int accept_all;         // no Eq. (11) gate: every candidate accepted
   uint8_t* accepted;
   float* union_R;
   int32_t* n_accepted;

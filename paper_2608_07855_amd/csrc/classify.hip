@@ -12,6 +12,7 @@
 // permutation without any sort.
 #include "ckv_device.h"
 #include "ckv_kernels.h"
+#include "commitkv.h"
 
 namespace ckv {
 
@@ -55,21 +56,30 @@ __global__ __launch_bounds__(kCT) void rank_kernel(ClassifyArgs c) {
   const double den = c.n > 1 ? (double)(c.n - 1) : 1.0;
   const double Pm = c.n > 1 ? less_pre / den : 0.5;
   const double Pp = c.n > 1 ? less_post / den : 0.5;
-  // Eq. (9), inclusive comparisons
-  const bool H_pre = rp >= c.tau_use && Pm >= (double)c.rho_use;
-  const bool L_pre = rp <= c.tau_dead && Pm <= (double)c.rho_dead;
-  const bool H_post = rq >= c.tau_use && Pp >= (double)c.rho_use;
-  const bool L_post = rq <= c.tau_dead && Pp <= (double)c.rho_dead;
-  // Eq. (10)
+  // Eq. (9), inclusive comparisons (absolute thresholds alone without the
+  // percentile calibration, Sec. 4.4)
+  const bool pct = !(c.policy & CKV_POLICY_NO_PERCENTILE);
+  const bool H_pre = rp >= c.tau_use && (!pct || Pm >= (double)c.rho_use);
+  const bool L_pre = rp <= c.tau_dead && (!pct || Pm <= (double)c.rho_dead);
+  const bool H_post = rq >= c.tau_use && (!pct || Pp >= (double)c.rho_use);
+  const bool L_post = rq <= c.tau_dead && (!pct || Pp <= (double)c.rho_dead);
+  // Eq. (10); without the pre-commit state (Sec. 4.4) L+ alone makes a candidate
   uint8_t lam = 0;
-  if (H_pre && L_post) lam = 1;
-  else if (L_pre && L_post) lam = 2;
-  else if (L_pre && H_post) lam = 3;
-  else if (H_pre && H_post) lam = 4;
+  if (c.policy & CKV_POLICY_NO_PRECOMMIT) {
+    if (L_post) lam = 1;
+    else if (L_pre && H_post) lam = 3;
+    else if (H_pre && H_post) lam = 4;
+  } else {
+    if (H_pre && L_post) lam = 1;
+    else if (L_pre && L_post) lam = 2;
+    else if (L_pre && H_post) lam = 3;
+    else if (H_pre && H_post) lam = 4;
+  }
   c.lambda[i] = lam;
   c.P_pre[i] = (float)Pm;
   c.P_post[i] = (float)Pp;
-  c.is_cand[i] = (lam == 1 || (c.force && c.force[i])) ? 1 : 0;
+  const bool none = (c.policy & CKV_POLICY_NO_LIFECYCLE) != 0;
+  c.is_cand[i] = (!none && (lam == 1 || (c.force && c.force[i]))) ? 1 : 0;
   c.cand[i] = -1;
 }
 

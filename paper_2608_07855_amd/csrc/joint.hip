@@ -207,7 +207,7 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
         const float r = __uint_as_float(__hip_atomic_load(&j.rbuf[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
         if (j.union_R) j.union_R[tt] = r;
         cur = tt + 1;
-        if (r <= j.tau) {
+        if (r <= j.tau || j.accept_all) {
           j.accepted[tt] = 1;
           acc = tt;
           *j.n_accepted += 1;

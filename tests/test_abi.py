@@ -66,3 +66,13 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(_abi.Thresholds) == 20
     assert ctypes.sizeof(_abi.Budget) == 16
     assert ctypes.sizeof(_abi.CacheView) == 8 * 2 + 8 * 4 + 8 + 8 + 4 * 5 + 4
+
+
+def test_policy_bits_match_header(lib):
+    text = open(os.path.join(ROOT, "include", "commitkv.h")).read()
+    hdr = {m.group(1).lower(): int(m.group(2))
+           for m in re.finditer(r"CKV_POLICY_(NO_\w+)\s*=\s*(\d+)", text)}
+    assert hdr == _abi.POLICY_BITS
+    L = _abi.load()
+    assert L.ckv_set_policy(None, 1) == _abi.CKV_ERR_ARG
+    assert L.ckv_get_policy(None) == 0

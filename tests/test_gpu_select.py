@@ -63,7 +63,8 @@ def _accepted_form(P, rng, allp, retired):
 
 
 def _run(P, ctx, n_seq, n_layers, H, d, cap, n_tokens, B, seed, keep_recent=0, eta=0.125,
-         max_pages=16, ties=False, nan=False, accepted=False, n_pending=40, page_div=80, maxlen=64):
+         max_pages=16, ties=False, nan=False, accepted=False, n_pending=40, page_div=80, maxlen=64,
+         ablation=()):
     rng = np.random.default_rng(seed)
     k = torch.randint(-32768, 32767, (n_seq, n_layers, H, cap, d), dtype=torch.int16).view(torch.bfloat16).cuda()
     v = torch.randint(-32768, 32767, (n_seq, n_layers, H, cap, d), dtype=torch.int16).view(torch.bfloat16).cuda()
@@ -94,13 +95,23 @@ def _run(P, ctx, n_seq, n_layers, H, d, cap, n_tokens, B, seed, keep_recent=0, e
         forms = [_accepted_form(P, rng, tables[s], retired[s]) for s in range(n_seq)]
         host_retired = [f[0] for f in forms]
         acc = [f[1] for f in forms]
-    out = P.ckv_select_and_compact(
-        ctx, k, v, pos, n_tokens, torch.from_numpy(score).cuda(),
-        [P.Pages([p[0] for p in r], [p[1] for p in r]) for r in host_retired],
-        [P.Pages([p[0] for p in r], [p[1] for p in r]) for r in pending],
-        [torch.from_numpy(r).cuda() if len(r) else None for r in rpre],
-        budget=B, eta=eta, max_pending_pages=max_pages, keep_recent=keep_recent, accepted=acc)
+    ctx.set_policy(*ablation)
+    try:
+        out = P.ckv_select_and_compact(
+            ctx, k, v, pos, n_tokens, torch.from_numpy(score).cuda(),
+            [P.Pages([p[0] for p in r], [p[1] for p in r]) for r in host_retired],
+            [P.Pages([p[0] for p in r], [p[1] for p in r]) for r in pending],
+            [torch.from_numpy(r).cuda() if len(r) else None for r in rpre],
+            budget=B, eta=eta, max_pending_pages=max_pages, keep_recent=keep_recent, accepted=acc)
+    finally:
+        ctx.set_policy()
     torch.cuda.synchronize()
+    # Sec. 4.4 variants on the oracle side: no protected page; no retired page
+    if "no_protection" in ablation or "no_lifecycle" in ablation:
+        pending = [[] for _ in pending]
+        rpre = [np.zeros(0, np.float32) for _ in rpre]
+    if "no_lifecycle" in ablation:
+        retired = [[] for _ in retired]
     kept = out["kept"].cpu().numpy()
     nk = out["n_kept"].cpu().numpy()
     kn, vn = k.view(torch.int16).cpu().numpy(), v.view(torch.int16).cpu().numpy()
@@ -202,3 +213,13 @@ def test_host_errors(ckv):
         P.ckv_select_and_compact(ctx, k, k.clone(), pos, [64], sc, [P.Pages([60], [8])], [E], [None],
                                  budget=16)
     assert e.value.code == -2
+
+
+@pytest.mark.parametrize("ablation", [("no_protection",), ("no_lifecycle",)])
+def test_ablation_variants(ckv, ablation):
+    """Sec. 4.4: without transition protection no pending page is protected;
+    without the lifecycle mechanism retired and accepted pages are kept
+    eligible too (only the budget and keep_recent decide)."""
+    P, ctx = ckv
+    _run(P, ctx, 2, 2, 2, 128, 6000, [6000, 4100], 1200, seed=16, keep_recent=64, accepted=True,
+         eta=0.5, ablation=ablation)

@@ -64,7 +64,7 @@ def test_percentile_non_strict_is_caught(monkeypatch):
 
 def test_lifecycle_swap_is_caught(monkeypatch):
     """Mutant: candidate defined as L- and H+ (the transition reversed)."""
-    def mutant(H_pre, L_pre, H_post, L_post):
+    def mutant(H_pre, L_pre, H_post, L_post, precommit=True):
         lam = np.full(len(H_pre), O.UNCERTAIN, np.uint8)
         lam[L_pre & H_post] = O.CANDIDATE
         lam[L_pre & L_post] = O.DORMANT

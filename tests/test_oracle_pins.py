@@ -230,6 +230,38 @@ def test_lifecycle_hand_table():
                                          O.UNCERTAIN, O.UNCERTAIN])
 
 
+def test_ablation_without_precommit_state():
+    """Sec. 4.4: candidates from L+ alone.  In the hand table above, B (H-, L+)
+    and C (L-, L+, dormant in the full method) become candidates, ordered by
+    R+ ascending: C (0.002) before B (0.01); the other states are unchanged."""
+    Rm = [0.9, 0.05, 0.001, 0.01, 0.03]
+    Rp = [0.05, 0.01, 0.002, 0.5, 0.04]
+    lam, _, _, cand = O.classify(Rm, Rp, starts=[0, 16, 32, 48, 64], ablation=("no_precommit",))
+    np.testing.assert_array_equal(lam, [O.STILL_ACTIVE, O.CANDIDATE, O.CANDIDATE,
+                                        O.NEWLY_ACTIVE, O.UNCERTAIN])
+    np.testing.assert_array_equal(cand, [2, 1])
+
+
+def test_ablation_without_percentile():
+    """Sec. 4.4: every page has R- >= tau_use and R+ <= tau_dead.  With the
+    percentile calibration only the top quartile is high before (pages 3, 4)
+    and the bottom quartile low after (pages 0, 1), so no page is a
+    candidate; with the absolute thresholds alone all five are, ordered by R+."""
+    Rm = [0.2, 0.3, 0.4, 0.5, 0.6]
+    Rp = [0.001, 0.002, 0.003, 0.004, 0.005]
+    st = [0, 16, 32, 48, 64]
+    lam, _, _, cand = O.classify(Rm, Rp, st)
+    assert cand.size == 0 and not np.any(lam == O.CANDIDATE)
+    lam2, _, _, cand2 = O.classify(Rm, Rp, st, ablation=("no_percentile",))
+    assert np.all(lam2 == O.CANDIDATE)
+    np.testing.assert_array_equal(cand2, [0, 1, 2, 3, 4])
+
+
+def test_ablation_without_lifecycle_has_no_candidate():
+    lam, _, _, cand = O.classify([0.9, 0.05], [0.001, 0.002], starts=[0, 16], ablation=("no_lifecycle",))
+    assert cand.size == 0
+
+
 def test_high_needs_both_absolute_and_percentile():
     """A page ranked first among tiny effects is not high (Sec. 3.2)."""
     H, L = O.high_low(np.array([0.02, 0.001]), np.array([1.0, 0.0]),
@@ -325,6 +357,19 @@ def test_joint_rejects_accumulated_effect():
     assert uR[1] == pytest.approx(r12, rel=1e-12)
     # page 2 carries v = (1,0) like the rest, A u {2} only renormalises
     assert uR[2] == pytest.approx(_mean_identity(V[0], m1 | O.page_mask(S, 300, 4)), rel=1e-12)
+
+
+def test_ablation_without_joint_validation_accepts_all():
+    """Sec. 4.4: without the Eq. (11) gate both small pages are retired, and
+    the union effects follow the mean identity for {0}, {0,1}, {0,1,2}."""
+    K, V, Q, pos, qpos, pages = _two_small_pages()
+    S = K.shape[1]
+    m = [O.page_mask(S, st, ln) for st, ln in pages]
+    acc, uR = O.joint_test(K, V, pos, Q, qpos, pages, [0, 1, 2], tau_joint=0.01, gate=False)
+    np.testing.assert_array_equal(acc, [True, True, True])
+    assert uR[1] == pytest.approx(_mean_identity(V[0], m[0] | m[1]), rel=1e-12)
+    assert uR[2] == pytest.approx(_mean_identity(V[0], m[0] | m[1] | m[2]), rel=1e-12)
+    assert uR[1] > 0.01
 
 
 def test_first_candidate_always_accepted():
