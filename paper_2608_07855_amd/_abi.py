@@ -1,4 +1,5 @@
-"""ctypes declarations of include/commitkv.h and the library loader.
+"""ctypes declarations of include/commitkv.h, include/commitkv_agent.h and the
+library loader.
 
 The library is the in-tree ``libcommitkv.so`` built by
 ``python -m paper_2608_07855_amd.build``.  There is no fallback: if the
@@ -84,7 +85,31 @@ class AcceptedPages(ctypes.Structure):
                 ("accepted", ctypes.c_void_p), ("max_cand", ctypes.c_int32)]
 
 
-# name -> (restype, argtypes): every entry point of include/commitkv.h
+# ckv_event_kind and the due flags of include/commitkv_agent.h
+EVENT_REASONING, EVENT_TOOL_CALL, EVENT_OBSERVATION, EVENT_PROMPT, EVENT_ANSWER = range(5)
+DUE_POST = 1
+DUE_CHECKPOINT = 2
+
+
+class AgentConfig(ctypes.Structure):
+    _fields_ = [("page_size", ctypes.c_int32), ("window", ctypes.c_int32),
+                ("n_q_heads", ctypes.c_int32), ("max_scan_pages", ctypes.c_int32),
+                ("checkpoint_every", ctypes.c_int32), ("score_layer", ctypes.c_int32),
+                ("report_detail", ctypes.c_int32), ("thresholds", Thresholds),
+                ("budget", Budget)]
+
+
+class AgentReport(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int32), ("n_pages", ctypes.c_int32),
+                ("page_start", c_i32p), ("page_len", c_i32p), ("r_pre", c_f32p),
+                ("r_post", c_f32p), ("lambda_", c_u8p), ("n_cand", ctypes.c_int32),
+                ("cand", c_i32p), ("accepted", c_u8p), ("union_r", c_f32p),
+                ("n_accepted", ctypes.c_int32), ("compacted", ctypes.c_int32),
+                ("n_before", ctypes.c_int32), ("n_kept", ctypes.c_int32),
+                ("kept", c_i32p), ("score", c_f32p)]
+
+
+# name -> (restype, argtypes): every entry point of include/*.h
 SIGNATURES = {
     "ckv_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int, ctypes.c_void_p]),
     "ckv_destroy": (ctypes.c_int, [ctypes.c_void_p]),
@@ -121,6 +146,20 @@ SIGNATURES = {
         ctypes.c_int64, ctypes.POINTER(PageList), ctypes.POINTER(PageList),
         ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(AcceptedPages), ctypes.POINTER(Budget),
         ctypes.POINTER(CacheView), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "ckv_agent_create": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(CacheView),
+                                        ctypes.POINTER(CacheView), ctypes.POINTER(AgentConfig),
+                                        ctypes.POINTER(ctypes.c_void_p)]),
+    "ckv_agent_destroy": (ctypes.c_int, [ctypes.c_void_p]),
+    "ckv_agent_append": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, ctypes.c_int32,
+                                        ctypes.c_int32, ctypes.c_int32, c_i32p]),
+    "ckv_agent_commit": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(WindowView)]),
+    "ckv_agent_post": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(WindowView)]),
+    "ckv_agent_checkpoint": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(WindowView), c_i32p]),
+    "ckv_agent_state": (ctypes.c_int, [ctypes.c_void_p, c_i32p, c_i32p,
+                                       ctypes.POINTER(ctypes.c_int64)]),
+    "ckv_agent_last_report": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(AgentReport)]),
+    "ckv_agent_pages": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, c_i32p, c_f32p,
+                                       ctypes.c_int32, c_i32p]),
 }
 
 _lib = None

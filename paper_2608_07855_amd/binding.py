@@ -307,3 +307,126 @@ def ckv_select_and_compact(ctx: Context, k_in, v_in, pos_in, n_tokens, score, re
         int(score.stride(0)), ret, pen, rptr, acc_arr, ctypes.byref(b), ctypes.byref(cout), _ptr(kept),
         _ptr(n_kept), _ptr(token_state)))
     return dict(k=k_out, v=v_out, pos=pos_out, kept=kept, n_kept=n_kept)
+
+
+# ---------------------------------------------------------------- lifecycle driver
+
+def _np(ptr, n, dtype):
+    if not ptr or n <= 0:
+        return np.zeros(0, dtype)
+    return np.ctypeslib.as_array(ptr, shape=(n,)).astype(dtype, copy=True)
+
+
+class Agent:
+    """The lifecycle driver of one agent episode (include/commitkv_agent.h,
+    Algorithm 1) over two cache buffers this object allocates:
+    k, v [1, n_layers, Hkv, capacity, d] bf16 and pos [1, capacity] int32.
+
+    ``append`` places the new tokens' keys, values and positions in the
+    current buffer (a device copy) and reports them; ``commit``, ``post`` and
+    ``checkpoint`` take the window's queries [Hq, W, d] (bf16, device) and
+    positions (int32, device) and return the call's report as NumPy arrays."""
+
+    def __init__(self, ctx: Context, n_layers: int, n_kv_heads: int, head_dim: int, capacity: int, *,
+                 page_size: int, window: int, n_q_heads: int, budget: int, eta: float = 0.125,
+                 max_pending_pages: int = 16, keep_recent: int = 0, max_scan_pages: int = 64,
+                 checkpoint_every: int = 128, score_layer: int = 0, thresholds: dict | None = None,
+                 report_detail: bool = False):
+        self.ctx = ctx
+        dev = torch.device("cuda", ctx.device)
+        shape = (1, n_layers, n_kv_heads, capacity, head_dim)
+        self.k = [torch.zeros(shape, dtype=torch.bfloat16, device=dev) for _ in range(2)]
+        self.v = [torch.zeros(shape, dtype=torch.bfloat16, device=dev) for _ in range(2)]
+        self.pos = [torch.zeros((1, capacity), dtype=torch.int32, device=dev) for _ in range(2)]
+        self._views = [cache_view(self.k[i], self.v[i], self.pos[i]) for i in range(2)]
+        th = dict(PAPER_THRESHOLDS)
+        th.update(thresholds or {})
+        cfg = _abi.AgentConfig(page_size, window, n_q_heads, max_scan_pages, checkpoint_every,
+                               score_layer, int(bool(report_detail)), Thresholds(**th),
+                               Budget(budget, eta, max_pending_pages, keep_recent))
+        h = ctypes.c_void_p()
+        ctx.check(lib().ckv_agent_create(ctx.handle, ctypes.byref(self._views[0]),
+                                         ctypes.byref(self._views[1]), ctypes.byref(cfg), ctypes.byref(h)))
+        self.handle = h
+
+    def state(self):
+        n, cur, dec = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64()
+        self.ctx.check(lib().ckv_agent_state(self.handle, ctypes.byref(n), ctypes.byref(cur), ctypes.byref(dec)))
+        return n.value, cur.value, dec.value
+
+    def cache(self):
+        """(k, v, pos, n_resident) of the buffer holding the cache."""
+        n, cur, _ = self.state()
+        return self.k[cur][0], self.v[cur][0], self.pos[cur][0], n
+
+    def append(self, kind: int, k, v, pos, decoded: bool, begins_event: bool = True) -> int:
+        """k, v: [n_layers, Hkv, n, d] bf16 (device); pos: host int array [n].
+        Returns the CKV_DUE_* flags."""
+        pos = np.ascontiguousarray(pos, dtype=np.int32)
+        n_tok = int(pos.size)
+        n, cur, _ = self.state()
+        if n + n_tok > self.k[cur].shape[3]:
+            raise CKVError(_abi.CKV_ERR_SHAPE, "cache buffer capacity exceeded")
+        if n_tok:
+            self.k[cur][0, :, :, n:n + n_tok].copy_(k)
+            self.v[cur][0, :, :, n:n + n_tok].copy_(v)
+            self.pos[cur][0, n:n + n_tok].copy_(torch.from_numpy(pos))
+        due = ctypes.c_int32()
+        self.ctx.check(lib().ckv_agent_append(self.handle, int(kind), pos.ctypes.data_as(_abi.c_i32p), n_tok,
+                                              int(bool(decoded)), int(bool(begins_event)), ctypes.byref(due)))
+        return due.value
+
+    def commit(self, q, qpos):
+        w = window_view(q, qpos)
+        self.ctx.check(lib().ckv_agent_commit(self.handle, ctypes.byref(w)))
+        return self.report()
+
+    def post(self, q, qpos):
+        w = window_view(q, qpos)
+        self.ctx.check(lib().ckv_agent_post(self.handle, ctypes.byref(w)))
+        return self.report()
+
+    def checkpoint(self, q, qpos):
+        w = window_view(q, qpos)
+        c = ctypes.c_int32()
+        self.ctx.check(lib().ckv_agent_checkpoint(self.handle, ctypes.byref(w), ctypes.byref(c)))
+        return self.report()
+
+    def report(self) -> dict:
+        r = _abi.AgentReport()
+        self.ctx.check(lib().ckv_agent_last_report(self.handle, ctypes.byref(r)))
+        n, nc = r.n_pages, r.n_cand
+        return dict(op=r.op, pages=list(zip(_np(r.page_start, n, np.int64).tolist(),
+                                            _np(r.page_len, n, np.int64).tolist())),
+                    R_pre=_np(r.r_pre, n, np.float32), R_post=_np(r.r_post, n, np.float32),
+                    lam=_np(r.lambda_, n, np.uint8), cand=_np(r.cand, nc, np.int64),
+                    accepted=_np(r.accepted, nc, np.uint8), union_R=_np(r.union_r, nc, np.float32),
+                    n_accepted=r.n_accepted, compacted=bool(r.compacted), n_before=r.n_before,
+                    kept=_np(r.kept, r.n_kept, np.int64), score=_np(r.score, r.n_before, np.float32))
+
+    def pages(self, which: str):
+        """"pending" -> [(start, len, R-)], "retired" -> [(start, len)] (absolute positions)."""
+        w = {"pending": 0, "retired": 1}[which]
+        n = ctypes.c_int32()
+        self.ctx.check(lib().ckv_agent_pages(self.handle, w, None, None, None, 0, ctypes.byref(n)))
+        m = n.value
+        st = np.zeros(max(m, 1), np.int32)
+        ln = np.zeros(max(m, 1), np.int32)
+        val = np.zeros(max(m, 1), np.float32)
+        self.ctx.check(lib().ckv_agent_pages(self.handle, w, st.ctypes.data_as(_abi.c_i32p),
+                                             ln.ctypes.data_as(_abi.c_i32p), val.ctypes.data_as(_abi.c_f32p),
+                                             m, ctypes.byref(n)))
+        if w == 0:
+            return [(int(a), int(b), float(c)) for a, b, c in zip(st[:m], ln[:m], val[:m])]
+        return [(int(a), int(b)) for a, b in zip(st[:m], ln[:m])]
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().ckv_agent_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

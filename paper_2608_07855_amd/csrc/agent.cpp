@@ -1,0 +1,544 @@
+// Multi-commit lifecycle driver of CommitKV (Algorithm 1) behind
+// include/commitkv_agent.h.  Host bookkeeping only: every measurement,
+// classification, joint test and compaction is one of the calls of
+// commitkv.h, on the context's stream.  The host keeps the resident
+// positions, so pages (identified by absolute position) are mapped to
+// resident index ranges without reading the device.
+#include "commitkv_agent.h"
+#include "ckv_host.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+using ckv::ctx_fail;
+
+namespace {
+
+struct Page {
+  int32_t start, len;          // first absolute position, token count
+  bool operator==(const Page& o) const { return start == o.start && len == o.len; }
+  bool operator<(const Page& o) const { return start < o.start || (start == o.start && len < o.len); }
+};
+
+struct Event {
+  int32_t kind, start, n;      // positions start .. start + n - 1
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct DevGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DevGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DevGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+bool pageable(int32_t kind) { return kind == CKV_EVENT_TOOL_CALL || kind == CKV_EVENT_OBSERVATION; }
+
+}  // namespace
+
+struct ckv_agent {
+  ckv_ctx* ctx = nullptr;
+  ckv_cache_view buf[2];
+  ckv_agent_config cfg;
+  int cur = 0;
+  std::vector<int32_t> res;          // resident positions, ascending
+  std::vector<Event> events;
+  int64_t decoded = 0;
+  bool pending = false;
+  size_t commit_events = 0;          // events seen when the pending commit was made
+  std::vector<Page> pend;
+  std::vector<float> pend_r;
+  std::vector<Page> retired;         // D_c, sorted by start
+
+  // device buffers (one allocation)
+  char* dev = nullptr;
+  float *d_r_pre = nullptr, *d_r_sub = nullptr, *d_r_post = nullptr, *d_union = nullptr;
+  float *d_o = nullptr, *d_lse = nullptr, *d_score = nullptr;
+  uint8_t *d_lambda = nullptr, *d_acc = nullptr;
+  int32_t *d_cand = nullptr, *d_ncand = nullptr, *d_nacc = nullptr, *d_kept = nullptr, *d_nkept = nullptr;
+  // pinned staging: uploads, then downloads
+  char* pin = nullptr;
+  float* up_r = nullptr;
+  int32_t* dn_counts = nullptr;      // n_cand, n_accepted, n_kept
+  int32_t* dn_cand = nullptr;
+  uint8_t* dn_acc = nullptr;
+  uint8_t* dn_lambda = nullptr;
+  float *dn_r = nullptr, *dn_r_post = nullptr, *dn_union = nullptr, *dn_score = nullptr;
+  int32_t* dn_kept = nullptr;
+
+  // last report
+  int32_t rep_op = 0, rep_ncand = 0, rep_nacc = 0, rep_compacted = 0, rep_before = 0, rep_nkept = 0;
+  std::vector<int32_t> rep_start, rep_len, rep_cand, rep_kept;
+  std::vector<float> rep_rpre, rep_rpost, rep_union, rep_score;
+  std::vector<uint8_t> rep_lambda, rep_acc;
+
+  int n_res() const { return (int)res.size(); }
+  int max_pages() const { return cfg.max_scan_pages; }
+
+  // resident index range of a page's positions
+  void span(const Page& p, int* i0, int* i1) const {
+    *i0 = (int)(std::lower_bound(res.begin(), res.end(), p.start) - res.begin());
+    *i1 = (int)(std::lower_bound(res.begin(), res.end(), p.start + p.len) - res.begin());
+  }
+  bool resident(const Page& p) const {
+    int a, b;
+    span(p, &a, &b);
+    return b - a == p.len;
+  }
+
+  ckv_kv_view layer_view() const {
+    const ckv_cache_view& b = buf[cur];
+    ckv_kv_view kv;
+    kv.k = b.k + (int64_t)cfg.score_layer * b.layer_stride;
+    kv.v = b.v + (int64_t)cfg.score_layer * b.layer_stride;
+    kv.head_stride = b.head_stride;
+    kv.tok_stride = b.tok_stride;
+    kv.pos = b.pos;
+    kv.n_tokens = n_res();
+    kv.n_kv_heads = b.n_kv_heads;
+    kv.head_dim = b.head_dim;
+    return kv;
+  }
+
+  // E_c: pages of tool calls and observations, fully resident, not in D_c,
+  // the max_scan_pages of largest start
+  std::vector<Page> eligible() const {
+    std::vector<Page> out;
+    for (const Event& e : events) {
+      if (!pageable(e.kind)) continue;
+      for (int off = 0; off < e.n; off += cfg.page_size) {
+        const Page p{e.start + off, std::min(cfg.page_size, e.n - off)};
+        if (std::binary_search(retired.begin(), retired.end(), p)) continue;
+        if (resident(p)) out.push_back(p);
+      }
+    }
+    std::sort(out.begin(), out.end());
+    if ((int)out.size() > max_pages()) out.erase(out.begin(), out.end() - max_pages());
+    return out;
+  }
+
+  void ranges(const std::vector<Page>& pages, std::vector<int32_t>* st, std::vector<int32_t>* ln) const {
+    st->clear();
+    ln->clear();
+    for (const Page& p : pages) {
+      int a, b;
+      span(p, &a, &b);
+      st->push_back(a);
+      ln->push_back(b - a);
+    }
+  }
+
+  int check_window(const ckv_window_view* w, const char* what) {
+    if (!w) return ctx_fail(ctx, CKV_ERR_ARG, "%s window view is NULL", what);
+    if (w->n_rows != cfg.window || w->n_q_heads != cfg.n_q_heads)
+      return ctx_fail(ctx, CKV_ERR_SHAPE, "%s window: %d rows x %d heads, agent expects %d x %d", what,
+                      w->n_rows, w->n_q_heads, cfg.window, cfg.n_q_heads);
+    return CKV_OK;
+  }
+
+  int sync() {
+    const hipError_t e = hipStreamSynchronize(ckv::ctx_stream(ctx));
+    return e == hipSuccess ? CKV_OK : ctx_fail(ctx, CKV_ERR_HIP, "stream synchronisation: %s", hipGetErrorString(e));
+  }
+
+  int copy(void* dst, const void* src, size_t bytes, hipMemcpyKind kind) {
+    if (!bytes) return CKV_OK;
+    const hipError_t e = hipMemcpyAsync(dst, src, bytes, kind, ckv::ctx_stream(ctx));
+    return e == hipSuccess ? CKV_OK : ctx_fail(ctx, CKV_ERR_HIP, "agent copy: %s", hipGetErrorString(e));
+  }
+
+  void clear_report(int op) {
+    rep_op = op;
+    rep_ncand = rep_nacc = rep_compacted = rep_before = rep_nkept = 0;
+    rep_start.clear();
+    rep_len.clear();
+    rep_cand.clear();
+    rep_kept.clear();
+    rep_rpre.clear();
+    rep_rpost.clear();
+    rep_union.clear();
+    rep_score.clear();
+    rep_lambda.clear();
+    rep_acc.clear();
+  }
+
+  void report_pages(const std::vector<Page>& pages, const std::vector<float>& r) {
+    for (const Page& p : pages) {
+      rep_start.push_back(p.start);
+      rep_len.push_back(p.len);
+    }
+    rep_rpre = r;
+  }
+};
+
+extern "C" int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* b0, const ckv_cache_view* b1,
+                                const ckv_agent_config* cfg, ckv_agent** out) {
+  if (!ctx) return CKV_ERR_ARG;
+  if (!b0 || !b1 || !cfg || !out) return ctx_fail(ctx, CKV_ERR_ARG, "agent: NULL argument");
+  *out = nullptr;
+  for (const ckv_cache_view* b : {b0, b1})
+    if (!b->k || !b->v || !b->pos) return ctx_fail(ctx, CKV_ERR_ARG, "agent: cache buffer with a NULL pointer");
+  if (b0->n_seq != 1 || b1->n_seq != 1) return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: cache buffers hold one sequence");
+  if (b0->n_layers != b1->n_layers || b0->n_kv_heads != b1->n_kv_heads || b0->head_dim != b1->head_dim ||
+      b0->capacity != b1->capacity || b0->n_layers < 1)
+    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: the two cache buffers differ in geometry");
+  const ckv_budget& bg = cfg->budget;
+  if (cfg->page_size < 1 || cfg->page_size > CKV_MAX_PAGE_LEN)
+    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: page_size %d not in [1, %d]", cfg->page_size, CKV_MAX_PAGE_LEN);
+  if (cfg->window < 1 || cfg->n_q_heads < 1 || cfg->n_q_heads % b0->n_kv_heads)
+    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: bad window rows or query heads");
+  if (cfg->max_scan_pages < 1 || cfg->max_scan_pages > 4096)
+    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: max_scan_pages %d not in [1, 4096]", cfg->max_scan_pages);
+  if (cfg->checkpoint_every < 1) return ctx_fail(ctx, CKV_ERR_ARG, "agent: checkpoint_every must be >= 1");
+  if (cfg->score_layer < 0 || cfg->score_layer >= b0->n_layers)
+    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: score_layer %d outside [0, %d)", cfg->score_layer, b0->n_layers);
+  if (bg.budget < 1 || bg.budget > b0->capacity || !(bg.eta >= 0.f && bg.eta <= 1.f) || bg.keep_recent < 0 ||
+      bg.max_pending_pages < 0)
+    return ctx_fail(ctx, CKV_ERR_ARG, "agent: bad budget (B must fit the capacity)");
+  if ((int64_t)std::floor((double)bg.eta * bg.budget) + bg.keep_recent > bg.budget)
+    return ctx_fail(ctx, CKV_ERR_BUDGET, "agent: keep_recent + B_N exceeds B");
+
+  ckv_agent* a = new (std::nothrow) ckv_agent();
+  if (!a) return ctx_fail(ctx, CKV_ERR_NOMEM, "agent: host allocation failed");
+  a->ctx = ctx;
+  a->buf[0] = *b0;
+  a->buf[1] = *b1;
+  a->cfg = *cfg;
+  const size_t M = (size_t)cfg->max_scan_pages;
+  const size_t rows = (size_t)cfg->n_q_heads * cfg->window;
+  const size_t cap = (size_t)b0->capacity, B = (size_t)bg.budget;
+  // device layout
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t o = off; off += align256(std::max<size_t>(bytes, 1)); return o; };
+  const size_t o_rpre = take(M * 4), o_rsub = take(M * 4), o_rpost = take(M * 4), o_union = take(M * 4);
+  const size_t o_o = take(rows * b0->head_dim * 4), o_lse = take(rows * 4), o_score = take(cap * 4);
+  const size_t o_lam = take(M), o_acc = take(M), o_cand = take(M * 4), o_cnt = take(16), o_kept = take(B * 4);
+  DevGuard g(ckv::ctx_device(ctx));
+  if (!g.ok) {
+    delete a;
+    return ctx_fail(ctx, CKV_ERR_HIP, "agent: cannot select the context's device");
+  }
+  if (hipMalloc((void**)&a->dev, off) != hipSuccess) {
+    delete a;
+    return ctx_fail(ctx, CKV_ERR_NOMEM, "agent: device allocation of %zu bytes failed", off);
+  }
+  char* d = a->dev;
+  a->d_r_pre = (float*)(d + o_rpre);
+  a->d_r_sub = (float*)(d + o_rsub);
+  a->d_r_post = (float*)(d + o_rpost);
+  a->d_union = (float*)(d + o_union);
+  a->d_o = (float*)(d + o_o);
+  a->d_lse = (float*)(d + o_lse);
+  a->d_score = (float*)(d + o_score);
+  a->d_lambda = (uint8_t*)(d + o_lam);
+  a->d_acc = (uint8_t*)(d + o_acc);
+  a->d_cand = (int32_t*)(d + o_cand);
+  a->d_ncand = (int32_t*)(d + o_cnt);
+  a->d_nacc = a->d_ncand + 1;
+  a->d_nkept = a->d_ncand + 2;
+  a->d_kept = (int32_t*)(d + o_kept);
+  // pinned layout
+  size_t po = 0;
+  auto ptake = [&](size_t bytes) { const size_t o = po; po += align256(std::max<size_t>(bytes, 1)); return o; };
+  const size_t p_up = ptake(M * 4), p_cnt = ptake(16), p_cand = ptake(M * 4), p_acc = ptake(M), p_lam = ptake(M);
+  const size_t p_r = ptake(M * 4), p_rpost = ptake(M * 4), p_union = ptake(M * 4), p_score = ptake(cap * 4);
+  const size_t p_kept = ptake(B * 4);
+  if (hipHostMalloc((void**)&a->pin, po, hipHostMallocDefault) != hipSuccess) {
+    (void)hipFree(a->dev);
+    delete a;
+    return ctx_fail(ctx, CKV_ERR_NOMEM, "agent: pinned allocation of %zu bytes failed", po);
+  }
+  char* p = a->pin;
+  a->up_r = (float*)(p + p_up);
+  a->dn_counts = (int32_t*)(p + p_cnt);
+  a->dn_cand = (int32_t*)(p + p_cand);
+  a->dn_acc = (uint8_t*)(p + p_acc);
+  a->dn_lambda = (uint8_t*)(p + p_lam);
+  a->dn_r = (float*)(p + p_r);
+  a->dn_r_post = (float*)(p + p_rpost);
+  a->dn_union = (float*)(p + p_union);
+  a->dn_score = (float*)(p + p_score);
+  a->dn_kept = (int32_t*)(p + p_kept);
+  *out = a;
+  return CKV_OK;
+}
+
+extern "C" int ckv_agent_destroy(ckv_agent* a) {
+  if (!a) return CKV_ERR_ARG;
+  DevGuard g(ckv::ctx_device(a->ctx));
+  (void)hipStreamSynchronize(ckv::ctx_stream(a->ctx));
+  if (a->dev) (void)hipFree(a->dev);
+  if (a->pin) (void)hipHostFree(a->pin);
+  delete a;
+  return CKV_OK;
+}
+
+extern "C" int ckv_agent_append(ckv_agent* a, int32_t kind, const int32_t* pos, int32_t n, int32_t decoded,
+                                int32_t begins_event, int32_t* due) {
+  if (!a) return CKV_ERR_ARG;
+  ckv_ctx* c = a->ctx;
+  if (kind < CKV_EVENT_REASONING || kind > CKV_EVENT_ANSWER) return ctx_fail(c, CKV_ERR_ARG, "append: unknown event kind %d", kind);
+  if (n < 0 || (n > 0 && !pos)) return ctx_fail(c, CKV_ERR_ARG, "append: bad token count or NULL positions");
+  if ((int64_t)a->n_res() + n > a->buf[0].capacity)
+    return ctx_fail(c, CKV_ERR_SHAPE, "append: %d resident + %d new tokens exceed the capacity %d", a->n_res(), n,
+                    a->buf[0].capacity);
+  const bool fresh = begins_event || a->events.empty() || a->events.back().kind != kind;
+  if (n > 0) {
+    if (!a->res.empty() && pos[0] <= a->res.back()) return ctx_fail(c, CKV_ERR_ARG, "append: positions must increase");
+    for (int i = 1; i < n; ++i)
+      if (pos[i] != pos[i - 1] + 1) return ctx_fail(c, CKV_ERR_ARG, "append: positions inside an event must be consecutive");
+    if (pos[n - 1] == INT_MAX) return ctx_fail(c, CKV_ERR_ARG, "append: position out of range");
+    if (!fresh) {
+      const Event& e = a->events.back();
+      if (pos[0] != e.start + e.n) return ctx_fail(c, CKV_ERR_ARG, "append: an event's positions must be consecutive");
+    }
+  }
+  if (n > 0 || fresh) {
+    if (fresh) a->events.push_back(Event{kind, n > 0 ? pos[0] : (a->res.empty() ? 0 : a->res.back() + 1), 0});
+    a->events.back().n += n;
+    a->res.insert(a->res.end(), pos, pos + n);
+  }
+  int flags = 0;
+  if (decoded && n > 0) {
+    const int64_t before = a->decoded;
+    a->decoded += n;
+    if (a->decoded / a->cfg.checkpoint_every > before / a->cfg.checkpoint_every) flags |= CKV_DUE_CHECKPOINT;
+  }
+  if (a->pending && a->events.size() > a->commit_events) {
+    const Event& e = a->events.back();
+    if (e.kind == CKV_EVENT_REASONING && e.n >= a->cfg.window) flags |= CKV_DUE_POST;
+  }
+  if (due) *due = flags;
+  return CKV_OK;
+}
+
+extern "C" int ckv_agent_commit(ckv_agent* a, const ckv_window_view* q_pre) {
+  if (!a) return CKV_ERR_ARG;
+  int rc;
+  if ((rc = a->check_window(q_pre, "commit"))) return rc;
+  a->clear_report(1);
+  std::vector<Page> E = a->eligible();
+  std::vector<float> r(E.size(), 0.f);
+  if (!E.empty()) {
+    std::vector<int32_t> st, ln;
+    a->ranges(E, &st, &ln);
+    const ckv_page_list pl{st.data(), ln.data(), (int32_t)E.size()};
+    const ckv_kv_view kv = a->layer_view();
+    if ((rc = ckv_measure_page_effects(a->ctx, &kv, q_pre, &pl, a->d_r_pre, nullptr, nullptr, nullptr, nullptr)))
+      return rc;
+    if ((rc = a->copy(a->dn_r, a->d_r_pre, E.size() * 4, hipMemcpyDeviceToHost)) || (rc = a->sync())) return rc;
+    std::memcpy(r.data(), a->dn_r, E.size() * 4);
+  }
+  a->pending = true;
+  a->commit_events = a->events.size();
+  a->pend = E;
+  a->pend_r = r;
+  a->report_pages(E, r);
+  return CKV_OK;
+}
+
+extern "C" int ckv_agent_post(ckv_agent* a, const ckv_window_view* q_post) {
+  if (!a) return CKV_ERR_ARG;
+  int rc;
+  if ((rc = a->check_window(q_post, "post"))) return rc;
+  a->clear_report(2);
+  if (!a->pending) return CKV_OK;
+  std::vector<Page> P;
+  std::vector<float> r;
+  for (size_t i = 0; i < a->pend.size(); ++i)
+    if (a->resident(a->pend[i])) {
+      P.push_back(a->pend[i]);
+      r.push_back(a->pend_r[i]);
+    }
+  a->report_pages(P, r);
+  const int n = (int)P.size();
+  if (n > 0) {
+    std::vector<int32_t> st, ln;
+    a->ranges(P, &st, &ln);
+    const ckv_page_list pl{st.data(), ln.data(), n};
+    const ckv_kv_view kv = a->layer_view();
+    std::memcpy(a->up_r, r.data(), (size_t)n * 4);
+    if ((rc = a->copy(a->d_r_sub, a->up_r, (size_t)n * 4, hipMemcpyHostToDevice))) return rc;
+    if ((rc = ckv_measure_page_effects(a->ctx, &kv, q_post, &pl, a->d_r_post, nullptr, a->d_o, a->d_lse, nullptr)))
+      return rc;
+    if ((rc = ckv_classify_pages(a->ctx, n, a->d_r_sub, a->d_r_post, &a->cfg.thresholds, nullptr, 0, a->d_lambda,
+                                 nullptr, nullptr, a->d_cand, a->d_ncand)))
+      return rc;
+    if ((rc = ckv_joint_test(a->ctx, &kv, q_post, a->d_o, a->d_lse, &pl, a->d_cand, a->d_ncand, n,
+                             a->cfg.thresholds.tau_joint, a->d_acc, a->d_union, a->d_nacc)))
+      return rc;
+    if ((rc = a->copy(a->dn_counts, a->d_ncand, 8, hipMemcpyDeviceToHost)) ||
+        (rc = a->copy(a->dn_cand, a->d_cand, (size_t)n * 4, hipMemcpyDeviceToHost)) ||
+        (rc = a->copy(a->dn_acc, a->d_acc, (size_t)n, hipMemcpyDeviceToHost)))
+      return rc;
+    if (a->cfg.report_detail &&
+        ((rc = a->copy(a->dn_r_post, a->d_r_post, (size_t)n * 4, hipMemcpyDeviceToHost)) ||
+         (rc = a->copy(a->dn_lambda, a->d_lambda, (size_t)n, hipMemcpyDeviceToHost)) ||
+         (rc = a->copy(a->dn_union, a->d_union, (size_t)n * 4, hipMemcpyDeviceToHost))))
+      return rc;
+    if ((rc = a->sync())) return rc;
+    const int nc = a->dn_counts[0], na = a->dn_counts[1];
+    if (na < 0)
+      return ctx_fail(a->ctx, CKV_ERR_UNSUPPORTED,
+                      "post: the joint test could not hold its workgroups resident at once (device busy)");
+    if (nc < 0 || nc > n) return ctx_fail(a->ctx, CKV_ERR_HIP, "post: candidate count %d out of range", nc);
+    a->rep_ncand = nc;
+    a->rep_nacc = na;
+    a->rep_cand.assign(a->dn_cand, a->dn_cand + nc);
+    a->rep_acc.assign(a->dn_acc, a->dn_acc + nc);
+    if (a->cfg.report_detail) {
+      a->rep_rpost.assign(a->dn_r_post, a->dn_r_post + n);
+      a->rep_lambda.assign(a->dn_lambda, a->dn_lambda + n);
+      a->rep_union.assign(a->dn_union, a->dn_union + nc);
+    }
+    for (int i = 0; i < nc; ++i) {
+      const int j = a->rep_cand[i];
+      if (j < 0 || j >= n) return ctx_fail(a->ctx, CKV_ERR_HIP, "post: candidate index %d out of range", j);
+      if (a->rep_acc[i] && !std::binary_search(a->retired.begin(), a->retired.end(), P[j]))
+        a->retired.insert(std::upper_bound(a->retired.begin(), a->retired.end(), P[j]), P[j]);
+    }
+  }
+  a->pending = false;
+  a->pend.clear();
+  a->pend_r.clear();
+  return CKV_OK;
+}
+
+extern "C" int ckv_agent_checkpoint(ckv_agent* a, const ckv_window_view* q_score, int32_t* compacted) {
+  if (!a) return CKV_ERR_ARG;
+  int rc;
+  if ((rc = a->check_window(q_score, "checkpoint"))) return rc;
+  a->clear_report(3);
+  if (compacted) *compacted = 0;
+  const int S = a->n_res();
+  a->rep_before = S;
+  const uint32_t policy = ckv_get_policy(a->ctx);
+  // resident parts of the retired pages (sorted, disjoint)
+  std::vector<int32_t> rs, rl;
+  for (const Page& p : a->retired) {
+    int i0, i1;
+    a->span(p, &i0, &i1);
+    if (i1 > i0) {
+      rs.push_back(i0);
+      rl.push_back(i1 - i0);
+    }
+  }
+  const bool ret_active = !rs.empty() && !(policy & CKV_POLICY_NO_LIFECYCLE);
+  if (S <= a->cfg.budget.budget && !ret_active) return CKV_OK;
+  // protectable pending pages
+  std::vector<Page> P;
+  std::vector<float> r;
+  if (a->pending)
+    for (size_t i = 0; i < a->pend.size(); ++i)
+      if (a->resident(a->pend[i])) {
+        P.push_back(a->pend[i]);
+        r.push_back(a->pend_r[i]);
+      }
+  std::vector<int32_t> ps, pl;
+  a->ranges(P, &ps, &pl);
+  if (!P.empty()) {
+    std::memcpy(a->up_r, r.data(), r.size() * 4);
+    if ((rc = a->copy(a->d_r_sub, a->up_r, r.size() * 4, hipMemcpyHostToDevice))) return rc;
+  }
+  const ckv_kv_view kv = a->layer_view();
+  const ckv_page_list none{nullptr, nullptr, 0};
+  if ((rc = ckv_measure_page_effects(a->ctx, &kv, q_score, &none, nullptr, nullptr, nullptr, nullptr, a->d_score)))
+    return rc;
+  const ckv_page_list ret_list{rs.data(), rl.data(), (int32_t)rs.size()};
+  const ckv_page_list pend_list{ps.data(), pl.data(), (int32_t)ps.size()};
+  const float* rptr = P.empty() ? nullptr : a->d_r_sub;
+  const int32_t n_tok = S;
+  if ((rc = ckv_select_and_compact(a->ctx, &a->buf[a->cur], &n_tok, a->d_score, a->buf[0].capacity, &ret_list,
+                                   &pend_list, &rptr, nullptr, &a->cfg.budget, &a->buf[1 - a->cur], a->d_kept,
+                                   a->d_nkept, nullptr)))
+    return rc;
+  const int B = a->cfg.budget.budget;
+  if ((rc = a->copy(a->dn_counts + 2, a->d_nkept, 4, hipMemcpyDeviceToHost)) ||
+      (rc = a->copy(a->dn_kept, a->d_kept, (size_t)B * 4, hipMemcpyDeviceToHost)))
+    return rc;
+  if (a->cfg.report_detail && (rc = a->copy(a->dn_score, a->d_score, (size_t)S * 4, hipMemcpyDeviceToHost)))
+    return rc;
+  if ((rc = a->sync())) return rc;
+  const int nk = a->dn_counts[2];
+  if (nk < 0) return ctx_fail(a->ctx, CKV_ERR_UNSUPPORTED, "checkpoint: the selection could not hold its workgroups resident at once");
+  if (nk > B || nk > S) return ctx_fail(a->ctx, CKV_ERR_HIP, "checkpoint: kept count %d out of range", nk);
+  std::vector<int32_t> kept(a->dn_kept, a->dn_kept + nk);
+  std::vector<int32_t> npos(nk);
+  for (int j = 0; j < nk; ++j) {
+    if (kept[j] < 0 || kept[j] >= S || (j && kept[j] <= kept[j - 1]))
+      return ctx_fail(a->ctx, CKV_ERR_HIP, "checkpoint: kept index list is not ascending inside the cache");
+    npos[j] = a->res[kept[j]];
+  }
+  a->res.swap(npos);
+  a->cur = 1 - a->cur;
+  std::vector<Page> keep_ret;
+  for (const Page& p : a->retired) {
+    int i0, i1;
+    a->span(p, &i0, &i1);
+    if (i1 > i0) keep_ret.push_back(p);
+  }
+  a->retired.swap(keep_ret);
+  a->rep_compacted = 1;
+  a->rep_nkept = nk;
+  a->rep_kept.swap(kept);
+  if (a->cfg.report_detail) a->rep_score.assign(a->dn_score, a->dn_score + S);
+  if (compacted) *compacted = 1;
+  return CKV_OK;
+}
+
+extern "C" int ckv_agent_state(const ckv_agent* a, int32_t* n_resident, int32_t* current, int64_t* decoded) {
+  if (!a) return CKV_ERR_ARG;
+  if (n_resident) *n_resident = a->n_res();
+  if (current) *current = a->cur;
+  if (decoded) *decoded = a->decoded;
+  return CKV_OK;
+}
+
+extern "C" int ckv_agent_last_report(const ckv_agent* a, ckv_agent_report* o) {
+  if (!a || !o) return CKV_ERR_ARG;
+  std::memset(o, 0, sizeof *o);
+  o->op = a->rep_op;
+  o->n_pages = (int32_t)a->rep_start.size();
+  o->page_start = a->rep_start.data();
+  o->page_len = a->rep_len.data();
+  o->r_pre = a->rep_rpre.data();
+  o->r_post = a->rep_rpost.empty() ? nullptr : a->rep_rpost.data();
+  o->lambda = a->rep_lambda.empty() ? nullptr : a->rep_lambda.data();
+  o->n_cand = a->rep_ncand;
+  o->cand = a->rep_cand.data();
+  o->accepted = a->rep_acc.data();
+  o->union_r = a->rep_union.empty() ? nullptr : a->rep_union.data();
+  o->n_accepted = a->rep_nacc;
+  o->compacted = a->rep_compacted;
+  o->n_before = a->rep_before;
+  o->n_kept = a->rep_nkept;
+  o->kept = a->rep_kept.data();
+  o->score = a->rep_score.empty() ? nullptr : a->rep_score.data();
+  return CKV_OK;
+}
+
+extern "C" int ckv_agent_pages(const ckv_agent* a, int32_t which, int32_t* start, int32_t* len, float* value,
+                               int32_t cap, int32_t* n) {
+  if (!a || (which != 0 && which != 1) || cap < 0 || (cap > 0 && (!start || !len))) return CKV_ERR_ARG;
+  const std::vector<Page>& L = which == 0 ? a->pend : a->retired;
+  const int m = std::min<int>(cap, (int)L.size());
+  for (int i = 0; i < m; ++i) {
+    start[i] = L[i].start;
+    len[i] = L[i].len;
+    if (value) value[i] = which == 0 ? a->pend_r[i] : 0.f;
+  }
+  if (n) *n = (int32_t)L.size();
+  return CKV_OK;
+}

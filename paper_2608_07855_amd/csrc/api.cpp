@@ -4,6 +4,7 @@
 // anything is enqueued, so no kernel ever sees an out-of-range page or a
 // misaligned row.
 #include "commitkv.h"
+#include "ckv_host.h"
 #include "ckv_kernels.h"
 
 #include <hip/hip_runtime.h>
@@ -15,7 +16,6 @@
 #include <cstdio>
 #include <cstring>
 #include <new>
-#include <string>
 #include <string>
 #include <vector>
 
@@ -122,6 +122,24 @@ struct DeviceGuard {
     if (prev >= 0) (void)hipSetDevice(prev);
   }
 };
+
+}  // namespace
+
+namespace ckv {
+int ctx_fail(ckv_ctx* c, int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c) c->err = buf;
+  return code;
+}
+hipStream_t ctx_stream(const ckv_ctx* c) { return c->stream; }
+int ctx_device(const ckv_ctx* c) { return c->device; }
+}  // namespace ckv
+
+namespace {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 

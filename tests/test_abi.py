@@ -4,6 +4,7 @@ import ctypes
 import glob
 import os
 import re
+import subprocess
 
 import pytest
 
@@ -76,3 +77,40 @@ def test_policy_bits_match_header(lib):
     L = _abi.load()
     assert L.ckv_set_policy(None, 1) == _abi.CKV_ERR_ARG
     assert L.ckv_get_policy(None) == 0
+
+
+def test_agent_null_handling(lib):
+    L = _abi.load()
+    assert L.ckv_agent_destroy(None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_append(None, 0, None, 0, 0, 0, None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_commit(None, None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_post(None, None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_checkpoint(None, None, None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_state(None, None, None, None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_last_report(None, None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_pages(None, 0, None, None, None, 0, None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_create(None, None, None, None, None) == _abi.CKV_ERR_ARG
+
+
+def _c_layout(tmp_path, struct, fields, header="commitkv_agent.h"):
+    """sizeof and field offsets of a header struct, as gcc lays it out."""
+    src = tmp_path / "layout.c"
+    body = "".join(f'  printf("%zu\\n", offsetof({struct}, {f}));\n' for f in fields)
+    src.write_text(f'#include <stdio.h>\n#include <stddef.h>\n#include "{header}"\n'
+                   f'int main(void) {{\n  printf("%zu\\n", sizeof({struct}));\n{body}  return 0;\n}}\n')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()
+    return int(out[0]), [int(x) for x in out[1:]]
+
+
+@pytest.mark.parametrize("struct,cls", [("ckv_agent_config", "AgentConfig"), ("ckv_agent_report", "AgentReport"),
+                                        ("ckv_cache_view", "CacheView"), ("ckv_kv_view", "KVView"),
+                                        ("ckv_window_view", "WindowView"), ("ckv_budget", "Budget")])
+def test_struct_layouts_match_gcc(tmp_path, struct, cls):
+    C = getattr(_abi, cls)
+    names = [f[0] for f in C._fields_]
+    cnames = ["lambda" if n == "lambda_" else n for n in names]
+    size, offs = _c_layout(tmp_path, struct, cnames)
+    assert ctypes.sizeof(C) == size
+    assert [getattr(C, n).offset for n in names] == offs
