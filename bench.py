@@ -23,7 +23,9 @@ Prints one JSON line.  ``value`` = cached tokens scored per second per layer,
 the compaction bandwidth and per-kernel times (HIP events recorded by the
 library on its stream).  ``roofline`` is for the kernel with the largest
 total time; ``cpu_baseline`` times the fp64 oracle on a bounded sample on the
-host cores.
+host cores.  ``agent`` runs whole synthetic agent episodes of a 36-layer stack
+through the lifecycle driver (Algorithm 1) and reports the driver's time per
+commit, post-commit step and checkpoint.
 """
 from __future__ import annotations
 
@@ -58,6 +60,9 @@ def parse():
     ap.add_argument("--copies", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-agent", action="store_true",
+                    help="skip the lifecycle-driver leg (whole agent episodes, Algorithm 1)")
+    ap.add_argument("--agent-seqs", type=int, default=4)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (5 launches), the known-size "
                          "reference that scales the FETCH_SIZE / WRITE_SIZE counters")
@@ -154,6 +159,68 @@ class Setup:
             accepted=[(self.pages, cl["cand"], cl["n_cand"], jt["accepted"], self.max_cand)],
             kept=self.kept, n_kept=self.n_kept)
         self.last = dict(cl=cl, jt=jt, sel=out)
+
+
+def agent_leg(n_seq):
+    """Whole agent episodes through the lifecycle driver (ckv_agent_*): the
+    Qwen3-8B-shaped stack (36 layers, 32 query / 8 KV heads, d 128), budget
+    16384, 64-row windows, 32-token pages, a checkpoint every 128 decoded
+    tokens, one driver per episode.  The engine's part (writing each new
+    token's keys and values, drawing window queries) is synthetic torch work
+    outside the timed calls; every commit, post and checkpoint is timed on
+    the host around the call (each returns after the context's stream has
+    finished it)."""
+    import torch
+
+    import paper_2608_07855_amd as P
+    from synth.trajectory import TRAJECTORIES, make_trajectory, schedule
+
+    cfg = TRAJECTORIES["q8b_agent"]
+    ctx = P.Context(0)
+    L, Hkv, d, Hq, W = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads, cfg.window
+    t = dict(commit=0.0, post=0.0, checkpoint=0.0)
+    n = dict(commit=0, post=0, checkpoint=0, compacted=0)
+    moved, turns, tokens = 0, [], 0
+    for s in range(n_seq):
+        traj = make_trajectory(cfg, seed=0, seq=s)
+        turns.append(sum(1 for e in traj.events if e[0] == 0))
+        tokens += traj.n_tokens
+        ag = P.Agent(ctx, L, Hkv, d, cfg.capacity, page_size=cfg.page_size, window=W, n_q_heads=Hq,
+                     budget=cfg.budget, eta=cfg.eta, max_pending_pages=cfg.max_pending_pages,
+                     keep_recent=cfg.keep_recent, max_scan_pages=cfg.max_scan_pages,
+                     checkpoint_every=cfg.checkpoint_every, score_layer=cfg.score_layer)
+        g = torch.Generator(device="cuda")
+        g.manual_seed(1000 + s)
+        for act in schedule(traj):
+            if act[0] == "append":
+                _, kind, p0, p1, dec, first = act
+                k = torch.randn((L, Hkv, p1 - p0, d), generator=g, device="cuda").to(torch.bfloat16)
+                v = torch.randn((L, Hkv, p1 - p0, d), generator=g, device="cuda").to(torch.bfloat16)
+                ag.append(kind, k, v, np.arange(p0, p1), dec, first)
+                continue
+            q = torch.randn((Hq, W, d), generator=g, device="cuda").to(torch.bfloat16)
+            qp = torch.arange(act[1], act[1] + W, dtype=torch.int32, device="cuda")
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            r = getattr(ag, act[0])(q, qp)
+            t[act[0]] += time.perf_counter() - t0
+            n[act[0]] += 1
+            if act[0] == "checkpoint" and r["compacted"]:
+                n["compacted"] += 1
+                moved += len(r["kept"]) * (L * Hkv * d * 2 * 2 * 2 + 4 * 2)
+        ag.close()
+    ctx.close()
+    total = sum(t.values())
+    log(f"[bench] agent leg: {n_seq} episodes, {tokens} tokens, driver time {total:.3f}s")
+    return dict(
+        workload=f"qwen3-8b-shaped stack, {L} layers (Hq {Hq}, Hkv {Hkv}, d {d}), {n_seq} agent episodes "
+                 f"of {cfg.turns_lo}-{cfg.turns_hi} turns, budget {cfg.budget}, {W}-row windows, "
+                 f"{cfg.page_size}-token pages, a checkpoint every {cfg.checkpoint_every} decoded tokens",
+        turns=turns, tokens=tokens, driver_seconds=total, tokens_per_s=tokens / total if total else None,
+        commits=n["commit"], posts=n["post"], checkpoints=n["checkpoint"], compactions=n["compacted"],
+        ms_per_commit=1e3 * t["commit"] / max(n["commit"], 1), ms_per_post=1e3 * t["post"] / max(n["post"], 1),
+        ms_per_checkpoint=1e3 * t["checkpoint"] / max(n["checkpoint"], 1),
+        compaction_GBps=moved / t["checkpoint"] / 1e9 if t["checkpoint"] > 0 else None)
 
 
 def kernel_work(w, L, name, launches_per_step):
@@ -306,6 +373,7 @@ def main():
         roof["algorithmic_bytes_per_launch"] = byt
         roof["algorithmic_flop_per_launch"] = flop
         roof["avg_launch_us"] = avg_s * 1e6
+    agent = None if args.no_agent else agent_leg(args.agent_seqs)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, L, args.cpu_seconds)
@@ -327,6 +395,7 @@ def main():
         n_kept=n_kept,
         roofline=roof,
         cpu_baseline=cpu,
+        agent=agent,
     )
     print(json.dumps(res), flush=True)
 
