@@ -7,6 +7,8 @@
  *
  *   ckv_measure_page_effects  Sec. 3.2, Eq. (5)-(8): window deletion effect
  *                             R(E;Q) of every event page, for one window.
+ *   ckv_measure_recorded      the same from the window outputs the engine
+ *                             recorded (per-page pass only).
  *   ckv_classify_pages        Sec. 3.2, Eq. (8)-(10): percentile ranks, high/low
  *                             indicators, lifecycle states; Sec. 3.3: ordered
  *                             completion candidates.
@@ -263,6 +265,27 @@ int ckv_measure_page_effects(ckv_ctx* ctx, const ckv_kv_view* kv,
                              const ckv_page_list* pages, float* R,
                              float* R_head, float* o, float* lse,
                              float* token_mass);
+
+/*
+ * Recorded-output variant of ckv_measure_page_effects (Sec. 3.2: the engine
+ * records the window's attention outputs during its forward pass).  o
+ * [n_q_heads * n_rows * head_dim] (16-byte aligned) and lse [n_q_heads *
+ * n_rows] (natural log; -inf for a row that sees no token) are INPUTS: the
+ * outputs and log-sum-exp of the window rows over this cache, as
+ * ckv_measure_page_effects would return them.  Only the per-page pass (and
+ * the token mass) runs; R, R_head and token_mass are as there.
+ * Pages carrying between 0.5 and 0.99 of a row's mass are evaluated from
+ * their own tokens in float32, with 1 - A taken against the recorded
+ * log-sum-exp, so the rounding of lse and of the page's logits bounds their
+ * relative error by a few ulp(lse)/(1 - A); above 0.99 the row's output
+ * without the page is recomputed from all of its other tokens (for up to
+ * 1024 such (page, row) pairs per call).
+ */
+int ckv_measure_recorded(ckv_ctx* ctx, const ckv_kv_view* kv,
+                         const ckv_window_view* win,
+                         const ckv_page_list* pages, const float* o,
+                         const float* lse, float* R, float* R_head,
+                         float* token_mass);
 
 /*
  * Lifecycle classification of the n pages of E_c (Sec. 3.2, Eq. (8)-(10)).

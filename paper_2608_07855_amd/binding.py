@@ -232,6 +232,27 @@ def ckv_measure_page_effects(ctx: Context, kv: KVView, win: WindowView, pages: P
                 lse=None if lse is None else lse.view(Hq, W), token_mass=token_mass)
 
 
+def ckv_measure_recorded(ctx: Context, kv: KVView, win: WindowView, pages: Pages, o, lse, *,
+                         R=None, R_head=None, token_mass=None, want=("R",)):
+    """Deletion effect of every page from recorded window outputs o [Hq, W, d]
+    and log-sum-exp lse [Hq, W] (float32, device)."""
+    dev = torch.device("cuda", ctx.device)
+    Hq = win.n_q_heads
+    if o.dtype != torch.float32 or lse.dtype != torch.float32 or not o.is_contiguous() or not lse.is_contiguous():
+        raise ValueError("o and lse must be contiguous float32 tensors")
+    if R is None:
+        R = _f32(max(pages.n, 1), dev)
+    if R_head is None and "R_head" in want:
+        R_head = _f32(max(pages.n * Hq, 1), dev)
+    if token_mass is None and "token_mass" in want:
+        token_mass = _f32(kv.n_tokens, dev)
+    pl = pages.view()
+    ctx.check(lib().ckv_measure_recorded(ctx.handle, ctypes.byref(kv), ctypes.byref(win), ctypes.byref(pl),
+                                         _ptr(o), _ptr(lse), _ptr(R), _ptr(R_head), _ptr(token_mass)))
+    return dict(R=R[:pages.n], R_head=None if R_head is None else R_head[:pages.n * Hq].view(pages.n, Hq),
+                token_mass=token_mass)
+
+
 def ckv_classify_pages(ctx: Context, R_pre, R_post, thresholds: dict | None = None, *,
                        force=None, max_cand: int = 0):
     n = int(R_pre.numel())

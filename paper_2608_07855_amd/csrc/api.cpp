@@ -585,8 +585,88 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
     pw.fix_list = fix_list;
     pw.fix_count = fix_count;
     pw.fix_cap = total_rows;
+    pw.fix_a = ckv::kFixA;
     CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, rs, 0, max_page_len(pages), c->stream));
-    CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, sp, rs, pw, fpart, c->stream));
+    CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, sp, rs, pw, fpart, ckv::kFixParts, c->stream));
+  }
+  if (token_mass) {
+    const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kTargetBlocks / a.Hkv)), 64);
+    CKV_LAUNCH(c, "token_mass", launch_token_mass(a, rs, token_mass, mchunk, c->stream));
+  }
+  return CKV_OK;
+}
+
+extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win,
+                                    const ckv_page_list* pages, const float* o, const float* lse, float* R,
+                                    float* R_head, float* token_mass) {
+  if (!c) return CKV_ERR_ARG;
+  c->err.clear();
+  int rc;
+  if ((rc = check_kv(c, kv)) || (rc = check_win(c, win, kv)) || (rc = check_pages(c, pages, kv->n_tokens, "measured")))
+    return rc;
+  if (!o || !lse) return fail(c, CKV_ERR_ARG, "recorded o or lse is NULL");
+  if (!aligned16(o)) return fail(c, CKV_ERR_ARG, "recorded o must be 16-byte aligned");
+  if (pages->n_pages > 0 && !R) return fail(c, CKV_ERR_ARG, "R is NULL");
+  if (token_mass && (win->n_q_heads / kv->n_kv_heads) * win->n_rows > token_mass_max_rows())
+    return fail(c, CKV_ERR_UNSUPPORTED, "token_mass supports at most %d window rows per KV head",
+                token_mass_max_rows());
+  DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
+
+  const AttnGeom a = make_geom(kv, win);
+  const int n = pages->n_pages, total_rows = a.Hq * a.W;
+  RowStats rs{const_cast<float*>(o), nullptr, nullptr, nullptr};
+  Plan plan;
+  plan.add(&rs.lse2, total_rows);
+  plan.add(&rs.onorm, total_rows);
+  plan.add(&rs.nvis, total_rows);
+  int* nvis_part = nullptr;
+  plan.add(&nvis_part, (size_t)a.W * recorded_slices(a.S));
+  int *fix_list = nullptr, *fix_count = nullptr;
+  plan.add(&fix_list, 4 * (size_t)total_rows);
+  plan.add(&fix_count, 1);
+  // pairs whose output without the page comes from the complement pass
+  const int cap2 = std::min(total_rows, ckv::kFixComplementCap);
+  int *list2 = nullptr, *count2 = nullptr;
+  plan.add(&list2, 4 * (size_t)cap2);
+  plan.add(&count2, 1);
+  float* fpart = nullptr;
+  plan.add(&fpart, (size_t)cap2 * ckv::kFixPartsRow * (a.D + 1));
+  const int32_t *dstart = nullptr, *dlen = nullptr;
+  if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
+  if ((rc = realize(c, plan))) return rc;
+
+  ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
+              token_mass ? (size_t)a.S : 0, fix_count, count2, 1};
+  CKV_LAUNCH(c, "recorded_rows", launch_recorded_rows(a, o, lse, rs, nvis_part, zl, c->stream));
+  if (n > 0) {
+    PageWork pw{};
+    pw.start = dstart;
+    pw.len = dlen;
+    pw.n_items = n;
+    pw.n_pages = n;
+    pw.items_per_block = std::min(items_per_block(n, a.Hkv * ceil_div(a.rows, rows_per_block_page())),
+                                  ckv::kPageRmaxCap / page_heads_per_block(a.W, a.group));
+    pw.R = R;
+    pw.R_head = R_head;
+    pw.lse_scale = 1.f;
+    pw.Hq = a.Hq;
+    pw.total_rows = total_rows;
+    pw.fix_list = fix_list;
+    pw.fix_count = fix_count;
+    pw.fix_cap = total_rows;
+    pw.fix_a = ckv::kFixARecorded;
+    CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, rs, 0, max_page_len(pages), c->stream));
+    CKV_LAUNCH(c, "page_fixup_recorded", launch_page_fixup_recorded(a, rs, pw, list2, count2, cap2,
+                                                                    ckv::kFixAComplement, c->stream));
+    // the complement pass: one split covering the whole row, so the fix-up
+    // recomputes every token of the row except the page's
+    PageWork pw2 = pw;
+    pw2.fix_list = list2;
+    pw2.fix_count = count2;
+    pw2.fix_cap = cap2;
+    AttnSplit whole{(int)round_up(a.S, 64), 1, 0, nullptr, nullptr, nullptr, nullptr};
+    CKV_LAUNCH(c, "page_fixup_complement", launch_page_fixup(a, whole, rs, pw2, fpart, ckv::kFixPartsRow, c->stream));
   }
   if (token_mass) {
     const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kTargetBlocks / a.Hkv)), 64);

@@ -66,7 +66,11 @@ struct PageWork {
                           // when rs.lse2 holds natural-log values)
   int* clear;             // MODE 1: words set to zero by workgroup (0, 0, 0) (or null)
   int n_clear;
+  float fix_a;            // MODE 0: pairs with A > fix_a (>= 0.5) go to the fix-up list
 };
+
+constexpr float kFixA = 0.9f;           // fix-up threshold after this library's window pass
+constexpr float kFixARecorded = 0.5f;   // ... with recorded window outputs
 
 struct ZeroList {
   float* p0; size_t n0;
@@ -88,10 +92,24 @@ hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowSt
                               int max_len, hipStream_t s);
 hipError_t launch_token_mass(const AttnGeom& a, const RowStats& rs, float* mass, int chunk,
                              hipStream_t s);
-// fpart: workspace [fix_cap][kFixParts][D + 1] floats
-constexpr int kFixParts = 8;   // workgroups per listed (page, row) pair
+// fpart: workspace [fix_cap][parts][D + 1] floats; each listed pair is spread
+// over `parts` workgroups
+constexpr int kFixParts = 8;        // after the window pass: the page's own split(s)
+constexpr int kFixPartsRow = 32;    // recorded outputs: every other token of the row
 hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
-                             const PageWork& pw, float* fpart, hipStream_t s);
+                             const PageWork& pw, float* fpart, int parts, hipStream_t s);
+
+// recorded window outputs: row statistics from the caller's o and natural-log
+// lse (nvis_part: workspace [W][recorded_slices(S)] ints), and the fix-up of
+// the listed pairs from the page's own tokens
+int recorded_slices(int S);
+hipError_t launch_recorded_rows(const AttnGeom& a, const float* o, const float* lse, const RowStats& rs,
+                                int* nvis_part, const ZeroList& zl, hipStream_t s);
+// pairs with A > a_hi go to list2 (int4 entries, count2 zeroed before, at most cap2)
+hipError_t launch_page_fixup_recorded(const AttnGeom& a, const RowStats& rs, const PageWork& pw, int* list2,
+                                      int* count2, int cap2, float a_hi, hipStream_t s);
+constexpr float kFixAComplement = 0.99f;   // recorded outputs: above this, the complement pass
+constexpr int kFixComplementCap = 1024;    // pairs the complement pass takes per call
 
 // classification (Eq. (8)-(10)) and candidate order
 struct ClassifyArgs {
