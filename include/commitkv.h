@@ -337,6 +337,25 @@ int ckv_joint_test(ckv_ctx* ctx, const ckv_kv_view* kv,
                    int32_t max_cand, float tau_joint, uint8_t* accepted,
                    float* union_R, int32_t* n_accepted);
 
+/*
+ * Pooled base score, the SnapKV-style variant of the score that fills the
+ * budget (the window mass smoothed over neighbouring tokens, so the tokens
+ * around a heavily attended one are kept with it).  For sequence s and token
+ * t < n_tokens[s]: out[s*seq_stride + t] = the max (CKV_POOL_MAX; NaN
+ * entries are ignored, NaN only if the whole window is) or the mean
+ * (CKV_POOL_MEAN, float32 sum in index order divided by the count) of
+ * score[s*seq_stride + j] over the tokens j in [t - kernel/2, t + kernel/2]
+ * inside [0, n_tokens[s]).
+ * score, out: device float32[n_seq * seq_stride], not overlapping; n_tokens:
+ * HOST int32[n_seq], each <= seq_stride; kernel odd in [1, 255].
+ * Entries past n_tokens[s] are not written.
+ */
+#define CKV_POOL_MAX 0
+#define CKV_POOL_MEAN 1
+int ckv_pool_scores(ckv_ctx* ctx, const float* score, float* out, int32_t n_seq,
+                    int64_t seq_stride, const int32_t* n_tokens, int32_t kernel,
+                    int32_t mode);
+
 /* Pages retired by the joint test of the current commit, resolved on the
  * device so that the checkpoint needs no host round trip (Algorithm 1: the
  * accepted set joins the retired set before the budget is applied).  Page

@@ -30,7 +30,8 @@
  *     resident; percentiles rank among them; their R^- is the stored value.
  *     Accepted candidates join D_c (Algorithm 1).
  *   - A checkpoint scores tokens with the token mass of its window on the
- *     scoring layer (one index set for every layer, Eq. (4)), protects the
+ *     scoring layer (pooled when pool_kernel > 1; one index set for every
+ *     layer, Eq. (4)), protects the
  *     fully resident pending pages (Eq. (12)), excludes every resident token
  *     of D_c, and keeps at most B tokens (Eq. (13)).  With at most B resident
  *     tokens and no resident retired token it changes nothing.  A page of D_c
@@ -78,6 +79,10 @@ typedef struct ckv_agent_config {
                                 to the host report as well */
   ckv_thresholds thresholds; /* Eq. (9), (11) */
   ckv_budget budget;         /* Eq. (12)-(13) */
+  int32_t pool_kernel;       /* 0 or 1: the token mass is the base score; odd
+                                k > 1: the token mass pooled over k tokens
+                                (ckv_pool_scores) */
+  int32_t pool_mode;         /* CKV_POOL_MAX or CKV_POOL_MEAN */
 } ckv_agent_config;
 
 /* Create an agent over two cache buffers of one sequence (n_seq == 1, the

@@ -48,6 +48,10 @@ Readings taken where the paper is silent:
 * R10 the base score used to fill the budget is the SnapKV-style window mass
       max_h sum_{p in Q+} a_{h,p,i} (``token_mass``); the selection accepts
       any float32 score.
+* R12 the pooled variant of the base score (``pool_scores``) smooths the
+      aggregated score over the odd window [t - k//2, t + k//2] clipped to
+      the cache: max pooling ignores NaN entries (NaN only if all are), mean
+      pooling divides the window's sum by the number of tokens in it.
 """
 from __future__ import annotations
 
@@ -439,6 +443,20 @@ def select_tokens(score, state, B):
     ranked = sorted(free.tolist(), key=lambda i: (-score[i], i))
     keep = np.array(sorted(prot.tolist() + ranked[:k]), dtype=np.int64)
     return keep
+
+
+def pool_scores(score, kernel, mode="max"):
+    """Reading R12: pooled base score, one output per token."""
+    x = np.asarray(score, dtype=np.float64)
+    n, h = x.size, kernel // 2
+    out = np.empty(n)
+    for t in range(n):
+        win = x[max(0, t - h):min(n, t + h + 1)]
+        if mode == "max":
+            out[t] = np.nan if np.all(np.isnan(win)) else np.nanmax(win)
+        else:
+            out[t] = win.sum() / win.size
+    return out
 
 
 def compact(K, V, pos, keep):

@@ -33,7 +33,8 @@ takes the same ones):
       post-commit effect can no longer be measured).
 * L5  a checkpoint follows every C decoded tokens (Sec. 4.1: 128).  Its base
       score is the token mass of the last W resident tokens as the window,
-      on one designated scoring layer; one index set serves every layer
+      on one designated scoring layer, pooled over pool_kernel tokens when
+      that is above 1 (reading R12); one index set serves every layer
       (Eq. (4)).  With at most B resident tokens and no resident retired
       token a checkpoint changes nothing.
 * L6  accepted pages join D_c (Algorithm 1) and stay resident until the next
@@ -52,7 +53,7 @@ TOOL_CALL, OBSERVATION = 1, 2      # event kinds that are cut into pages (Sec. 3
 class Agent:
     def __init__(self, n_layers, n_kv_heads, head_dim, page_size, budget, eta=0.125,
                  max_pending_pages=16, max_scan_pages=64, keep_recent=0, score_layer=0,
-                 thresholds=None, ablation=(), method="closed"):
+                 thresholds=None, ablation=(), method="closed", pool_kernel=0, pool_mode="max"):
         self.G = page_size
         self.B = budget
         self.eta = eta
@@ -63,6 +64,7 @@ class Agent:
         self.th = dict(O.PAPER_THRESHOLDS if thresholds is None else thresholds)
         self.ablation = tuple(ablation)
         self.method = method
+        self.pool = (pool_kernel, pool_mode)
         self.K = [np.zeros((n_kv_heads, 0, head_dim), np.uint16) for _ in range(n_layers)]
         self.V = [np.zeros((n_kv_heads, 0, head_dim), np.uint16) for _ in range(n_layers)]
         self.pos = np.zeros(0, np.int64)
@@ -179,8 +181,12 @@ class Agent:
         return m
 
     def base_score(self, Q, qpos):
+        """L5: token mass of the window, pooled (reading R12) when pool_kernel > 1."""
         K, V, pos = self._layer()
-        return O.token_mass(K, V, pos, Q, qpos)
+        m = O.token_mass(K, V, pos, Q, qpos)
+        if self.pool[0] > 1:
+            m = O.pool_scores(m, *self.pool)
+        return m
 
     def checkpoint_lists(self):
         """L4, L6: (protectable pending pages with their R^-, retired pages

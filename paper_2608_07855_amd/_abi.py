@@ -85,6 +85,8 @@ class AcceptedPages(ctypes.Structure):
                 ("accepted", ctypes.c_void_p), ("max_cand", ctypes.c_int32)]
 
 
+POOL_MAX, POOL_MEAN = 0, 1
+
 # ckv_event_kind and the due flags of include/commitkv_agent.h
 EVENT_REASONING, EVENT_TOOL_CALL, EVENT_OBSERVATION, EVENT_PROMPT, EVENT_ANSWER = range(5)
 DUE_POST = 1
@@ -96,7 +98,7 @@ class AgentConfig(ctypes.Structure):
                 ("n_q_heads", ctypes.c_int32), ("max_scan_pages", ctypes.c_int32),
                 ("checkpoint_every", ctypes.c_int32), ("score_layer", ctypes.c_int32),
                 ("report_detail", ctypes.c_int32), ("thresholds", Thresholds),
-                ("budget", Budget)]
+                ("budget", Budget), ("pool_kernel", ctypes.c_int32), ("pool_mode", ctypes.c_int32)]
 
 
 class AgentReport(ctypes.Structure):
@@ -145,6 +147,8 @@ SIGNATURES = {
         ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(PageList), ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p]),
+    "ckv_pool_scores": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                       ctypes.c_int64, c_i32p, ctypes.c_int32, ctypes.c_int32]),
     "ckv_select_and_compact": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.POINTER(CacheView), c_i32p, ctypes.c_void_p,
         ctypes.c_int64, ctypes.POINTER(PageList), ctypes.POINTER(PageList),

@@ -253,6 +253,19 @@ def ckv_measure_recorded(ctx: Context, kv: KVView, win: WindowView, pages: Pages
                 token_mass=token_mass)
 
 
+def ckv_pool_scores(ctx: Context, score, n_tokens, kernel: int = 7, mode: str = "max", out=None):
+    """score: float32 [n_seq, stride] (device); n_tokens: ints per sequence."""
+    if score.dtype != torch.float32 or score.dim() != 2 or score.stride(1) != 1:
+        raise ValueError("score must be float32 [n_seq, stride] with a contiguous last axis")
+    if out is None:
+        out = torch.zeros_like(score)
+    nt = np.ascontiguousarray(n_tokens, dtype=np.int32)
+    ctx.check(lib().ckv_pool_scores(ctx.handle, _ptr(score), _ptr(out), score.shape[0], score.stride(0),
+                                    nt.ctypes.data_as(_abi.c_i32p), int(kernel),
+                                    {"max": _abi.POOL_MAX, "mean": _abi.POOL_MEAN}[mode]))
+    return out
+
+
 def ckv_classify_pages(ctx: Context, R_pre, R_post, thresholds: dict | None = None, *,
                        force=None, max_cand: int = 0):
     n = int(R_pre.numel())
@@ -352,7 +365,7 @@ class Agent:
                  page_size: int, window: int, n_q_heads: int, budget: int, eta: float = 0.125,
                  max_pending_pages: int = 16, keep_recent: int = 0, max_scan_pages: int = 64,
                  checkpoint_every: int = 128, score_layer: int = 0, thresholds: dict | None = None,
-                 report_detail: bool = False):
+                 report_detail: bool = False, pool_kernel: int = 0, pool_mode: str = "max"):
         self.ctx = ctx
         dev = torch.device("cuda", ctx.device)
         shape = (1, n_layers, n_kv_heads, capacity, head_dim)
@@ -364,7 +377,8 @@ class Agent:
         th.update(thresholds or {})
         cfg = _abi.AgentConfig(page_size, window, n_q_heads, max_scan_pages, checkpoint_every,
                                score_layer, int(bool(report_detail)), Thresholds(**th),
-                               Budget(budget, eta, max_pending_pages, keep_recent))
+                               Budget(budget, eta, max_pending_pages, keep_recent), int(pool_kernel),
+                               {"max": _abi.POOL_MAX, "mean": _abi.POOL_MEAN}[pool_mode])
         h = ctypes.c_void_p()
         ctx.check(lib().ckv_agent_create(ctx.handle, ctypes.byref(self._views[0]),
                                          ctypes.byref(self._views[1]), ctypes.byref(cfg), ctypes.byref(h)))

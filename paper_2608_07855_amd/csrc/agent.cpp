@@ -65,7 +65,7 @@ struct ckv_agent {
   // device buffers (one allocation)
   char* dev = nullptr;
   float *d_r_pre = nullptr, *d_r_sub = nullptr, *d_r_post = nullptr, *d_union = nullptr;
-  float *d_o = nullptr, *d_lse = nullptr, *d_score = nullptr;
+  float *d_o = nullptr, *d_lse = nullptr, *d_score = nullptr, *d_pooled = nullptr;
   uint8_t *d_lambda = nullptr, *d_acc = nullptr;
   int32_t *d_cand = nullptr, *d_ncand = nullptr, *d_nacc = nullptr, *d_kept = nullptr, *d_nkept = nullptr;
   // pinned staging: uploads, then downloads
@@ -204,6 +204,9 @@ extern "C" int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* b0, const ck
   if (cfg->checkpoint_every < 1) return ctx_fail(ctx, CKV_ERR_ARG, "agent: checkpoint_every must be >= 1");
   if (cfg->score_layer < 0 || cfg->score_layer >= b0->n_layers)
     return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: score_layer %d outside [0, %d)", cfg->score_layer, b0->n_layers);
+  if (cfg->pool_kernel < 0 || cfg->pool_kernel > 255 || (cfg->pool_kernel > 1 && cfg->pool_kernel % 2 == 0) ||
+      (cfg->pool_mode != CKV_POOL_MAX && cfg->pool_mode != CKV_POOL_MEAN))
+    return ctx_fail(ctx, CKV_ERR_ARG, "agent: pool_kernel must be 0 or odd <= 255, pool_mode max or mean");
   if (bg.budget < 1 || bg.budget > b0->capacity || !(bg.eta >= 0.f && bg.eta <= 1.f) || bg.keep_recent < 0 ||
       bg.max_pending_pages < 0)
     return ctx_fail(ctx, CKV_ERR_ARG, "agent: bad budget (B must fit the capacity)");
@@ -224,6 +227,7 @@ extern "C" int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* b0, const ck
   auto take = [&](size_t bytes) { const size_t o = off; off += align256(std::max<size_t>(bytes, 1)); return o; };
   const size_t o_rpre = take(M * 4), o_rsub = take(M * 4), o_rpost = take(M * 4), o_union = take(M * 4);
   const size_t o_o = take(rows * b0->head_dim * 4), o_lse = take(rows * 4), o_score = take(cap * 4);
+  const size_t o_pooled = take(cap * 4);
   const size_t o_lam = take(M), o_acc = take(M), o_cand = take(M * 4), o_cnt = take(16), o_kept = take(B * 4);
   DevGuard g(ckv::ctx_device(ctx));
   if (!g.ok) {
@@ -242,6 +246,7 @@ extern "C" int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* b0, const ck
   a->d_o = (float*)(d + o_o);
   a->d_lse = (float*)(d + o_lse);
   a->d_score = (float*)(d + o_score);
+  a->d_pooled = (float*)(d + o_pooled);
   a->d_lambda = (uint8_t*)(d + o_lam);
   a->d_acc = (uint8_t*)(d + o_acc);
   a->d_cand = (int32_t*)(d + o_cand);
@@ -456,11 +461,19 @@ extern "C" int ckv_agent_checkpoint(ckv_agent* a, const ckv_window_view* q_score
   const ckv_page_list none{nullptr, nullptr, 0};
   if ((rc = ckv_measure_page_effects(a->ctx, &kv, q_score, &none, nullptr, nullptr, nullptr, nullptr, a->d_score)))
     return rc;
+  const float* score = a->d_score;
+  if (a->cfg.pool_kernel > 1) {
+    const int32_t nt = S;
+    if ((rc = ckv_pool_scores(a->ctx, a->d_score, a->d_pooled, 1, a->buf[0].capacity, &nt, a->cfg.pool_kernel,
+                              a->cfg.pool_mode)))
+      return rc;
+    score = a->d_pooled;
+  }
   const ckv_page_list ret_list{rs.data(), rl.data(), (int32_t)rs.size()};
   const ckv_page_list pend_list{ps.data(), pl.data(), (int32_t)ps.size()};
   const float* rptr = P.empty() ? nullptr : a->d_r_sub;
   const int32_t n_tok = S;
-  if ((rc = ckv_select_and_compact(a->ctx, &a->buf[a->cur], &n_tok, a->d_score, a->buf[0].capacity, &ret_list,
+  if ((rc = ckv_select_and_compact(a->ctx, &a->buf[a->cur], &n_tok, score, a->buf[0].capacity, &ret_list,
                                    &pend_list, &rptr, nullptr, &a->cfg.budget, &a->buf[1 - a->cur], a->d_kept,
                                    a->d_nkept, nullptr)))
     return rc;
@@ -468,7 +481,7 @@ extern "C" int ckv_agent_checkpoint(ckv_agent* a, const ckv_window_view* q_score
   if ((rc = a->copy(a->dn_counts + 2, a->d_nkept, 4, hipMemcpyDeviceToHost)) ||
       (rc = a->copy(a->dn_kept, a->d_kept, (size_t)B * 4, hipMemcpyDeviceToHost)))
     return rc;
-  if (a->cfg.report_detail && (rc = a->copy(a->dn_score, a->d_score, (size_t)S * 4, hipMemcpyDeviceToHost)))
+  if (a->cfg.report_detail && (rc = a->copy(a->dn_score, score, (size_t)S * 4, hipMemcpyDeviceToHost)))
     return rc;
   if ((rc = a->sync())) return rc;
   const int nk = a->dn_counts[2];

@@ -802,6 +802,34 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   return CKV_OK;
 }
 
+extern "C" int ckv_pool_scores(ckv_ctx* c, const float* score, float* out, int32_t n_seq, int64_t seq_stride,
+                               const int32_t* n_tokens, int32_t kernel, int32_t mode) {
+  if (!c) return CKV_ERR_ARG;
+  c->err.clear();
+  if (n_seq < 0 || (n_seq > 0 && (!score || !out || !n_tokens)))
+    return fail(c, CKV_ERR_ARG, "pool: NULL pointer or negative n_seq");
+  if (kernel < 1 || kernel > 255 || kernel % 2 == 0) return fail(c, CKV_ERR_ARG, "pool: kernel must be odd, 1..255");
+  if (mode != CKV_POOL_MAX && mode != CKV_POOL_MEAN) return fail(c, CKV_ERR_ARG, "pool: unknown mode %d", mode);
+  int max_tokens = 0;
+  for (int s = 0; s < n_seq; ++s) {
+    if (n_tokens[s] < 0 || n_tokens[s] > seq_stride)
+      return fail(c, CKV_ERR_SHAPE, "pool: n_tokens[%d] = %d outside [0, %lld]", s, n_tokens[s], (long long)seq_stride);
+    max_tokens = std::max(max_tokens, (int)n_tokens[s]);
+  }
+  if (n_seq == 0 || max_tokens == 0) return CKV_OK;
+  // the output may not overlap the input (each thread reads its neighbours)
+  const char *a0 = reinterpret_cast<const char*>(score), *b0 = reinterpret_cast<const char*>(out);
+  const int64_t bytes = ((int64_t)(n_seq - 1) * seq_stride + max_tokens) * 4;
+  if (a0 < b0 + bytes && b0 < a0 + bytes) return fail(c, CKV_ERR_ARG, "pool: out overlaps score");
+  DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
+  const int32_t* dn = nullptr;
+  int rc = cached_copy(c, std::vector<int32_t>(n_tokens, n_tokens + n_seq), &dn);
+  if (rc) return rc;
+  CKV_LAUNCH(c, "pool", launch_pool(score, out, seq_stride, dn, n_seq, max_tokens, kernel, mode, c->stream));
+  return CKV_OK;
+}
+
 extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, const int32_t* n_tokens,
                                       const float* score, int64_t score_seq_stride,
                                       const ckv_page_list* retired, const ckv_page_list* pending,

@@ -234,4 +234,8 @@ struct GatherArgs {
 };
 hipError_t launch_gather(const GatherArgs& g, hipStream_t s);
 
+// pooled base score: n_tokens device int32[n_seq]; windows of `kernel` (odd) tokens
+hipError_t launch_pool(const float* score, float* out, int64_t stride, const int32_t* n_tokens, int n_seq,
+                       int max_tokens, int kernel, int mode, hipStream_t s);
+
 }  // namespace ckv

@@ -842,4 +842,38 @@ hipError_t launch_gather(const GatherArgs& g, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Pooled base score (the SnapKV-style variant of the score that fills the
+// budget): out[t] = max (mode 0) or mean (mode 1) of score[j] over the tokens
+// j in [t - h, t + h] that lie inside [0, n_tokens), h = kernel / 2.  The max
+// ignores NaN entries (NaN only if the whole window is); the mean adds the
+// window in index order in float32.  One thread per token;
+// grid: (token blocks, sequences).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void pool_kernel(const float* score, float* out, int64_t stride,
+                                                   const int32_t* n_tokens, int half, int mode) {
+  const int s = blockIdx.y;
+  const int n = n_tokens[s];
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= n) return;
+  const float* x = score + (int64_t)s * stride;
+  const int j0 = max(0, t - half), j1 = min(n - 1, t + half);
+  float acc = mode == 0 ? -INFINITY : 0.f;
+  bool any = false;   // max: a window of NaN only gives NaN
+  for (int j = j0; j <= j1; ++j) {
+    const float v = x[j];
+    any = any || v == v;
+    acc = mode == 0 ? fmaxf(acc, v) : acc + v;
+  }
+  out[(int64_t)s * stride + t] = mode == 0 ? (any ? acc : NAN) : acc / (float)(j1 - j0 + 1);
+}
+
+hipError_t launch_pool(const float* score, float* out, int64_t stride, const int32_t* n_tokens, int n_seq,
+                       int max_tokens, int kernel, int mode, hipStream_t s) {
+  if (max_tokens <= 0 || n_seq <= 0) return hipSuccess;
+  dim3 grid((max_tokens + 255) / 256, n_seq), block(256);
+  hipLaunchKernelGGL(pool_kernel, grid, block, 0, s, score, out, stride, n_tokens, kernel / 2, mode);
+  return hipGetLastError();
+}
+
 }  // namespace ckv

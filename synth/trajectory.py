@@ -83,6 +83,8 @@ class TrajectoryConfig:
     forced_frac: float = 0.0     # fraction of pages forced to a high-to-low transition
     forced_pre: float = 20.0     # attention-mass factor of tool-call queries on forced pages
     forced_post: float = 0.02    # ... of reasoning queries
+    pool_kernel: int = 0         # base score pooled over this many tokens (0: not pooled)
+    pool_mode: str = "max"
 
     @property
     def capacity(self) -> int:

@@ -10,7 +10,8 @@ def oracle_agent(cfg, **over):
     kw = dict(n_layers=cfg.n_layers, n_kv_heads=cfg.n_kv_heads, head_dim=cfg.head_dim,
               page_size=cfg.page_size, budget=cfg.budget, eta=cfg.eta,
               max_pending_pages=cfg.max_pending_pages, max_scan_pages=cfg.max_scan_pages,
-              keep_recent=cfg.keep_recent, score_layer=cfg.score_layer)
+              keep_recent=cfg.keep_recent, score_layer=cfg.score_layer, pool_kernel=cfg.pool_kernel,
+              pool_mode=cfg.pool_mode)
     kw.update(over)
     return OracleAgent(**kw)
 

@@ -49,7 +49,7 @@ def _gpu_agent(P, ctx, cfg):
                    budget=cfg.budget, eta=cfg.eta, max_pending_pages=cfg.max_pending_pages,
                    keep_recent=cfg.keep_recent, max_scan_pages=cfg.max_scan_pages,
                    checkpoint_every=cfg.checkpoint_every, score_layer=cfg.score_layer,
-                   report_detail=True)
+                   report_detail=True, pool_kernel=cfg.pool_kernel, pool_mode=cfg.pool_mode)
 
 
 def _expected_due(acts, i):
@@ -186,6 +186,15 @@ def test_paper_operating_point_episode(ckv):
                             forced_post=0.005, heavy_frac=0.003)
     s = run_lockstep(P, ctx, make_trajectory(cfg, seed=0, n_turns=6))
     assert s["compacted"] >= 1 and s["commit"] >= 5
+
+
+@pytest.mark.parametrize("mode", ["max", "mean"])
+def test_pooled_score_episode(ckv, mode):
+    """The SnapKV-style pooled base score (7 tokens) at every checkpoint."""
+    P, ctx = ckv
+    cfg = scaled_trajectory("tiny_agent", pool_kernel=7, pool_mode=mode)
+    s = run_lockstep(P, ctx, make_trajectory(cfg, seed=5, n_turns=6))
+    assert s["compacted"] >= 2
 
 
 @pytest.mark.parametrize("ablation", [("no_protection",), ("no_joint",), ("no_precommit",)])

@@ -223,3 +223,29 @@ def test_ablation_variants(ckv, ablation):
     P, ctx = ckv
     _run(P, ctx, 2, 2, 2, 128, 6000, [6000, 4100], 1200, seed=16, keep_recent=64, accepted=True,
          eta=0.5, ablation=ablation)
+
+
+@pytest.mark.parametrize("mode", ["max", "mean"])
+def test_pool_scores(ckv, mode):
+    """The pooled base score (reading R12): max pooling bit-exact, mean
+    pooling to float32 rounding; ragged sequences, ties, NaN, kernel 1."""
+    P, ctx = ckv
+    rng = np.random.default_rng(9)
+    n_seq, stride = 3, 5000
+    sc = rng.standard_normal((n_seq, stride)).astype(np.float32)
+    sc[0, 100:110] = np.nan
+    sc[1, ::50] = 7.0
+    nt = [5000, 4321, 1]
+    for k in (1, 7, 63):
+        out = P.ckv_pool_scores(ctx, torch.from_numpy(sc).cuda(), nt, k, mode)
+        torch.cuda.synchronize()
+        out = out.cpu().numpy()
+        for s in range(n_seq):
+            want = O.pool_scores(sc[s, :nt[s]], k, mode)
+            if mode == "max":
+                np.testing.assert_array_equal(out[s, :nt[s]], want.astype(np.float32))
+            else:
+                np.testing.assert_allclose(out[s, :nt[s]], want, rtol=1e-5, atol=1e-5)
+            assert np.all(out[s, nt[s]:] == 0)
+    with pytest.raises(P.CKVError):
+        P.ckv_pool_scores(ctx, torch.from_numpy(sc).cuda(), nt, 4, mode)     # even kernel

@@ -471,3 +471,23 @@ def test_compaction_is_one_index_set():
         assert np.array_equal(Kc[:, :, j], K[:, :, i])
         assert np.array_equal(Vc[:, :, j], V[:, :, i])
         assert pc[j] == pos[i]
+
+
+# ---------------------------------------------------------------- pooled base score (R12)
+def test_pool_max_equals_library_filter():
+    from scipy.ndimage import maximum_filter1d
+    x = np.random.default_rng(5).standard_normal(300)
+    for k in (1, 3, 7, 31):
+        np.testing.assert_array_equal(O.pool_scores(x, k, "max"), maximum_filter1d(x, k, mode="nearest"))
+
+
+def test_pool_mean_hand_example():
+    np.testing.assert_allclose(O.pool_scores([1, 2, 3, 4, 5], 3, "mean"), [1.5, 2, 3, 4, 4.5])
+    np.testing.assert_allclose(O.pool_scores([1, 2, 3, 4, 5], 5, "mean"), [2, 2.5, 3, 3.5, 4])
+
+
+def test_pool_identity_and_nan():
+    x = np.array([0.3, -1.0, 2.0, np.nan, 0.5])
+    np.testing.assert_array_equal(O.pool_scores(x[:3], 1, "max"), x[:3])
+    np.testing.assert_array_equal(O.pool_scores(x, 3, "max"), [0.3, 2.0, 2.0, 2.0, 0.5])
+    assert np.isnan(O.pool_scores(x, 3, "mean")[2]) and O.pool_scores(x, 3, "mean")[0] == (0.3 - 1.0) / 2
