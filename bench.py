@@ -26,7 +26,8 @@ total time; ``cpu_baseline`` times the fp64 oracle on a bounded sample on the
 host cores.  ``recorded`` times the per-page pass alone from recorded window
 outputs (ckv_measure_recorded).  ``agent`` runs whole synthetic agent episodes of a 36-layer stack
 through the lifecycle driver (Algorithm 1) and reports the driver's time per
-commit, post-commit step and checkpoint.
+commit, post-commit step and checkpoint; ``agent_paper_point`` does the same
+at the paper's operating point (W 8, G 16, budget 4096, 40 layers).
 """
 from __future__ import annotations
 
@@ -198,11 +199,13 @@ def recorded_leg(st, steps):
                      "(ckv_measure_recorded); no window-attention pass")
 
 
-def agent_leg(n_seq):
-    """Whole agent episodes through the lifecycle driver (ckv_agent_*): the
-    Qwen3-8B-shaped stack (36 layers, 32 query / 8 KV heads, d 128), budget
-    16384, 64-row windows, 32-token pages, a checkpoint every 128 decoded
-    tokens, one driver per episode.  The engine's part (writing each new
+def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped"):
+    """Whole agent episodes through the lifecycle driver (ckv_agent_*), one
+    driver per episode: by default the Qwen3-8B-shaped stack (36 layers, 32
+    query / 8 KV heads, d 128), budget 16384, 64-row windows, 32-token pages;
+    ``paper_agent`` is the paper's operating point on a Qwen3-14B-shaped
+    stack (40 layers, 40 / 8 heads, W 8, G 16, budget 4096); a checkpoint
+    every 128 decoded tokens in both.  The engine's part (writing each new
     token's keys and values, drawing window queries) is synthetic torch work
     outside the timed calls; every commit, post and checkpoint is timed on
     the host around the call (each returns after the context's stream has
@@ -212,7 +215,7 @@ def agent_leg(n_seq):
     import paper_2608_07855_amd as P
     from synth.trajectory import TRAJECTORIES, make_trajectory, schedule
 
-    cfg = TRAJECTORIES["q8b_agent"]
+    cfg = TRAJECTORIES[traj]
     ctx = P.Context(0)
     L, Hkv, d, Hq, W = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads, cfg.window
     t = dict(commit=0.0, post=0.0, checkpoint=0.0)
@@ -252,7 +255,7 @@ def agent_leg(n_seq):
     total = sum(t.values())
     log(f"[bench] agent leg: {n_seq} episodes, {tokens} tokens, driver time {total:.3f}s")
     return dict(
-        workload=f"qwen3-8b-shaped stack, {L} layers (Hq {Hq}, Hkv {Hkv}, d {d}), {n_seq} agent episodes "
+        workload=f"{shape} stack, {L} layers (Hq {Hq}, Hkv {Hkv}, d {d}), {n_seq} agent episodes "
                  f"of {cfg.turns_lo}-{cfg.turns_hi} turns, budget {cfg.budget}, {W}-row windows, "
                  f"{cfg.page_size}-token pages, a checkpoint every {cfg.checkpoint_every} decoded tokens",
         turns=turns, tokens=tokens, driver_seconds=total, tokens_per_s=tokens / total if total else None,
@@ -419,6 +422,7 @@ def main():
         roof["avg_launch_us"] = avg_s * 1e6
     recorded = recorded_leg(st, args.steps)
     agent = None if args.no_agent else agent_leg(args.agent_seqs)
+    agent_paper = None if args.no_agent else agent_leg(2, "paper_agent", "qwen3-14b-shaped, paper operating point")
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, L, args.cpu_seconds)
@@ -442,6 +446,7 @@ def main():
         cpu_baseline=cpu,
         recorded=recorded,
         agent=agent,
+        agent_paper_point=agent_paper,
     )
     print(json.dumps(res), flush=True)
 
