@@ -66,6 +66,8 @@ def parse():
     ap.add_argument("--no-agent", action="store_true",
                     help="skip the lifecycle-driver leg (whole agent episodes, Algorithm 1)")
     ap.add_argument("--agent-seqs", type=int, default=4)
+    ap.add_argument("--no-recorded", action="store_true",
+                    help="skip the recorded-output leg (ckv_measure_recorded)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (5 launches), the known-size "
                          "reference that scales the FETCH_SIZE / WRITE_SIZE counters")
@@ -420,7 +422,7 @@ def main():
         roof["algorithmic_bytes_per_launch"] = byt
         roof["algorithmic_flop_per_launch"] = flop
         roof["avg_launch_us"] = avg_s * 1e6
-    recorded = recorded_leg(st, args.steps)
+    recorded = None if args.no_recorded else recorded_leg(st, args.steps)
     agent = None if args.no_agent else agent_leg(args.agent_seqs)
     agent_paper = None if args.no_agent else agent_leg(2, "paper_agent", "qwen3-14b-shaped, paper operating point")
     cpu = None
