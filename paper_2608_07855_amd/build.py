@@ -20,7 +20,7 @@ OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libcommitkv.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["api.cpp", "agent.cpp", "measure.hip", "classify.hip", "joint.hip", "select.hip"]
+SOURCES = ["api.cpp", "agent.cpp", "measure.hip", "recorded.hip", "classify.hip", "joint.hip", "select.hip"]
 
 COMMON = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -929,149 +929,6 @@ __global__ __launch_bounds__(256) void page_fixup_final(AttnGeom a, RowStats rs,
 }
 
 // ---------------------------------------------------------------------------
-// Recorded window outputs.  The engine records o_p and the log-sum-exp of
-// every window row during its forward pass; given those, only the per-page
-// pass (and the token mass) has to run.  Two small kernels supply what the
-// page kernel reads per row (log-sum-exp in log2 units, ||o_p||, visible
-// token count), and the fix-up recomputes the ill-conditioned pairs from the
-// page's own tokens.
-// ---------------------------------------------------------------------------
-constexpr int kVisSlices = 64;        // cache slices counted per window row
-
-// block (window row p, slice): tokens of the slice visible to row p
-__global__ __launch_bounds__(256) void recorded_count_kernel(AttnGeom a, int* nvis_part, int n_slices) {
-  __shared__ int red[4];
-  const int p = blockIdx.x / n_slices, slice = blockIdx.x % n_slices;
-  const int per = (a.S + n_slices - 1) / n_slices;
-  const int t0 = slice * per, t1 = min(a.S, t0 + per);
-  const int qp = a.qpos[p];
-  int c = 0;
-  for (int t = t0 + (int)threadIdx.x; t < t1; t += 256) c += a.pos[t] <= qp ? 1 : 0;
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off, 64);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = c;
-  __syncthreads();
-  if (threadIdx.x == 0) nvis_part[p * n_slices + slice] = red[0] + red[1] + red[2] + red[3];
-}
-
-// one wave per window row: lse2 = lse log2(e), ||o_p||, n_vis; also zeroes
-// the outputs later kernels reduce into (as the combine kernel does)
-template <int D>
-__global__ __launch_bounds__(256) void recorded_rows_kernel(AttnGeom a, const float* o, const float* lse,
-                                                            RowStats rs, const int* nvis_part, int n_slices,
-                                                            ZeroList zl) {
-  const int lane = threadIdx.x & 63;
-  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t gsz = (size_t)gridDim.x * blockDim.x;
-  for (size_t i = gid; i < zl.n0; i += gsz) zl.p0[i] = 0.f;
-  for (size_t i = gid; i < zl.n1; i += gsz) zl.p1[i] = 0.f;
-  for (size_t i = gid; i < zl.n2; i += gsz) zl.p2[i] = 0.f;
-  if (zl.i0 && gid == 0) *zl.i0 = 0;
-  for (size_t i = gid; i < zl.n1i; i += gsz) zl.i1[i] = 0;
-  const int rg = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (rg >= a.Hq * a.W) return;
-  const int p = rg % a.W;
-  float n2 = 0.f;
-#pragma unroll
-  for (int j = 0; j < D / 64; ++j) {
-    const float ov = o[(size_t)rg * D + lane + 64 * j];
-    n2 += ov * ov;
-  }
-  int nv = lane < n_slices ? nvis_part[p * n_slices + lane] : 0;
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    n2 += __shfl_xor(n2, off, 64);
-    nv += __shfl_xor(nv, off, 64);
-  }
-  if (lane == 0) {
-    const float l = lse[rg];
-    rs.lse2[rg] = l == -INFINITY ? -INFINITY : l * kLog2e;
-    rs.onorm[rg] = sqrtf(n2);
-    rs.nvis[rg] = nv;
-  }
-}
-
-// one wave per listed pair (page E, window row): with weights relative to
-// the recorded log-sum-exp, A = sum_{i in E} w_i and u = sum_{i in E} w_i v_i
-// in float32 from the page's tokens, and Eq. (6):
-// ratio = ||u - A o|| / ((1 - A) ||o||); +inf when E holds every visible token.
-// 1 - A is then known to a few ulp of the log-sum-exp only, so a pair with
-// A > a_hi is appended to list2 instead (while it has room): the
-// complement pass computes its output without the page from every other
-// token of the row.
-template <int D>
-__global__ __launch_bounds__(256) void page_fixup_recorded(AttnGeom a, RowStats rs, PageWork pw, int4* list2,
-                                                           int* count2, int cap2, float a_hi) {
-  constexpr int J = D / 64;
-  const int lane = threadIdx.x & 63;
-  const int n = min(*pw.fix_count, pw.fix_cap);
-  for (int e = blockIdx.x * 4 + (threadIdx.x >> 6); e < n; e += gridDim.x * 4) {
-    const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
-    const int page = ent.x, rg = ent.y, st = ent.z, ln = ent.w;
-    const int h = rg / a.W, p = rg % a.W, g = h / a.group;
-    const int qp = a.qpos[p];
-    const float ref = rs.lse2[rg];
-    const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
-    const uint16_t* vh = a.v + (int64_t)g * a.kv_head_stride;
-    const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)p * a.q_row_stride;
-    float qv[J], ov[J], u[J];
-    float A = 0.f;
-    int cnt = 0;
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-      qv[j] = bf16_bits_to_float(qrow[lane + 64 * j]);
-      ov[j] = rs.o[(size_t)rg * D + lane + 64 * j];
-      u[j] = 0.f;
-    }
-    for (int t = st; t < st + ln; ++t) {
-      if (a.pos[t] > qp) continue;              // the same token for every lane
-      float x = 0.f;
-#pragma unroll
-      for (int j = 0; j < J; ++j)
-        x = __builtin_fmaf(qv[j], bf16_bits_to_float(kh[(int64_t)t * a.kv_tok_stride + lane + 64 * j]), x);
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
-      const float w = __builtin_amdgcn_exp2f(__builtin_fmaf(x, a.sl2, -ref));
-      A += w;
-      ++cnt;
-#pragma unroll
-      for (int j = 0; j < J; ++j)
-        u[j] = __builtin_fmaf(w, bf16_bits_to_float(vh[(int64_t)t * a.kv_tok_stride + lane + 64 * j]), u[j]);
-    }
-    float rr = 0.f, oo = 0.f;
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-      const float r = __builtin_fmaf(-A, ov[j], u[j]);
-      rr += r * r;
-      oo += ov[j] * ov[j];
-    }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      rr += __shfl_xor(rr, off, 64);
-      oo += __shfl_xor(oo, off, 64);
-    }
-    if (cnt > 0 && cnt < rs.nvis[rg] && A > a_hi) {
-      int slot = 0;
-      if (lane == 0) slot = atomicAdd(count2, 1);
-      slot = __shfl(slot, 0, 64);
-      if (slot < cap2) {
-        if (lane == 0) list2[slot] = ent;
-        continue;
-      }
-    }
-    if (lane == 0 && cnt > 0) {
-      const float den = 1.f - A;
-      float ratio;
-      if (cnt >= rs.nvis[rg] || !(den > 0.f)) ratio = INFINITY;
-      else if (oo > 0.f) ratio = sqrtf(rr) / (den * sqrtf(oo));
-      else ratio = rr > 0.f ? INFINITY : 0.f;
-      if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], ratio);
-      atomic_max_nonneg(&pw.R[page], ratio);
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
 // C. window-attention mass of every token: max_h sum_p a_hpi
 //
 // Workgroup (token chunk, KV head g).  A (query head, 32-row block) pair is
@@ -1398,33 +1255,6 @@ hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowSt
     hipLaunchKernelGGL((page_fixup_partial<64>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
     hipLaunchKernelGGL((page_fixup_final<64>), grid2, block2, 0, s, a, rs, pw, fpart, parts);
   }
-  return hipGetLastError();
-}
-
-int recorded_slices(int S) { return std::max(1, std::min(kVisSlices, (S + 1023) / 1024)); }
-
-hipError_t launch_recorded_rows(const AttnGeom& a, const float* o, const float* lse, const RowStats& rs,
-                                int* nvis_part, const ZeroList& zl, hipStream_t s) {
-  const int ns = recorded_slices(a.S);
-  hipLaunchKernelGGL(recorded_count_kernel, dim3(a.W * ns), dim3(256), 0, s, a, nvis_part, ns);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  dim3 grid((a.Hq * a.W + 3) / 4), block(256);
-  if (a.D == 128)
-    hipLaunchKernelGGL((recorded_rows_kernel<128>), grid, block, 0, s, a, o, lse, rs, nvis_part, ns, zl);
-  else
-    hipLaunchKernelGGL((recorded_rows_kernel<64>), grid, block, 0, s, a, o, lse, rs, nvis_part, ns, zl);
-  return hipGetLastError();
-}
-
-hipError_t launch_page_fixup_recorded(const AttnGeom& a, const RowStats& rs, const PageWork& pw, int* list2,
-                                      int* count2, int cap2, float a_hi, hipStream_t s) {
-  dim3 grid(std::max(1, std::min((pw.fix_cap + 3) / 4, 256))), block(256);
-  int4* l2 = reinterpret_cast<int4*>(list2);
-  if (a.D == 128)
-    hipLaunchKernelGGL((page_fixup_recorded<128>), grid, block, 0, s, a, rs, pw, l2, count2, cap2, a_hi);
-  else
-    hipLaunchKernelGGL((page_fixup_recorded<64>), grid, block, 0, s, a, rs, pw, l2, count2, cap2, a_hi);
   return hipGetLastError();
 }
 
