@@ -30,6 +30,9 @@ constexpr float kLog2eHost = 1.4426950408889634f;   // log2(e): natural-log LSE 
 constexpr int kJointWindow = 32;       // candidates tested per joint round
 constexpr int kJointRowsPerBlock = 64;
 constexpr int kTargetBlocks = 256;     // one 8-wave workgroup per compute unit
+// the token-mass kernel (64 VGPRs, 40 KB of LDS) keeps two workgroups per
+// compute unit busy: 512 token chunks measured 31.7 us against 35.3 us with 256
+constexpr int kMassBlocks = 512;
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
@@ -590,7 +593,7 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
     CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, sp, rs, pw, fpart, ckv::kFixParts, c->stream));
   }
   if (token_mass) {
-    const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kTargetBlocks / a.Hkv)), 64);
+    const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kMassBlocks / a.Hkv)), 64);
     CKV_LAUNCH(c, "token_mass", launch_token_mass(a, rs, token_mass, mchunk, c->stream));
   }
   return CKV_OK;
@@ -669,7 +672,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
     CKV_LAUNCH(c, "page_fixup_complement", launch_page_fixup(a, whole, rs, pw2, fpart, ckv::kFixPartsRow, c->stream));
   }
   if (token_mass) {
-    const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kTargetBlocks / a.Hkv)), 64);
+    const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kMassBlocks / a.Hkv)), 64);
     CKV_LAUNCH(c, "token_mass", launch_token_mass(a, rs, token_mass, mchunk, c->stream));
   }
   return CKV_OK;
