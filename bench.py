@@ -24,7 +24,7 @@ the compaction bandwidth and per-kernel times (HIP events recorded by the
 library on its stream).  ``roofline`` is for the kernel with the largest
 total time; ``cpu_baseline`` times the fp64 oracle on a bounded sample on the
 host cores.  ``recorded`` times the per-page pass alone from recorded window
-outputs (ckv_measure_recorded).  ``agent`` runs whole synthetic agent episodes of a 36-layer stack
+outputs (ckv_measure_recorded); ``paged`` the measurement over a paged pool.  ``agent`` runs whole synthetic agent episodes of a 36-layer stack
 through the lifecycle driver (Algorithm 1) and reports the driver's time per
 commit, post-commit step and checkpoint; ``agent_paper_point`` does the same
 at the paper's operating point (W 8, G 16, budget 4096, 40 layers).
@@ -199,6 +199,46 @@ def recorded_leg(st, steps):
     return dict(ms_per_step=ms, tokens_per_s=toks / (ms / 1e3),
                 note="pre + post page effects and token mass from recorded window outputs "
                      "(ckv_measure_recorded); no window-attention pass")
+
+
+def paged_leg(st, steps):
+    """The measurement passes (pre and post, with token mass) over a paged
+    pool: the layer's tokens scattered over 1.5 S rows of each head's
+    storage, addressed through a slot table (ckv_kv_view.slot)."""
+    import torch
+    P, L, w = st.P, st.L, st.w
+    S = w.n_tokens
+    rows = S + S // 2
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+    slot = torch.randperm(rows, generator=g, device="cuda")[:S].to(torch.int32)
+    kp = torch.zeros((w.n_kv_heads, rows, w.head_dim), dtype=torch.bfloat16, device="cuda")
+    vp = torch.zeros_like(kp)
+    kp[:, slot.long()] = st.k[0]
+    vp[:, slot.long()] = st.v[0]
+    kv_pre = P.kv_view(kp, vp, st.pos, n_tokens=L.layout.s_pre, slot=slot[:L.layout.s_pre].contiguous())
+    kv_post = P.kv_view(kp, vp, st.pos, slot=slot)
+
+    def step():
+        P.ckv_measure_page_effects(st.ctx, kv_pre, st.win_pre, st.pages, R=st.R_pre)
+        P.ckv_measure_page_effects(st.ctx, kv_post, st.win_post, st.pages, R=st.R_post, o=st.o, lse=st.lse,
+                                   token_mass=st.mass)
+
+    for _ in range(3):
+        step()
+    gc.collect()
+    gc.disable()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    gc.enable()
+    toks = L.layout.s_pre + S
+    return dict(ms_per_step=ms, tokens_per_s=toks / (ms / 1e3),
+                note="pre + post measurement with token mass over a paged pool of 1.5 S rows "
+                     "(slot table); one pool, so the key/value rows may be reused from the Infinity Cache")
 
 
 def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped"):
@@ -423,6 +463,7 @@ def main():
         roof["algorithmic_flop_per_launch"] = flop
         roof["avg_launch_us"] = avg_s * 1e6
     recorded = None if args.no_recorded else recorded_leg(st, args.steps)
+    paged = None if args.no_recorded else paged_leg(st, args.steps)
     agent = None if args.no_agent else agent_leg(args.agent_seqs)
     agent_paper = None if args.no_agent else agent_leg(2, "paper_agent", "qwen3-14b-shaped, paper operating point")
     cpu = None
@@ -447,6 +488,7 @@ def main():
         roofline=roof,
         cpu_baseline=cpu,
         recorded=recorded,
+        paged=paged,
         agent=agent,
         agent_paper_point=agent_paper,
     )

@@ -136,9 +136,14 @@ int ckv_reset_kernel_stats(ckv_ctx* ctx);
 /* ------------------------------------------------------------------ views */
 
 /* Resident KV cache of ONE layer of ONE sequence (Sec. 3.1, Eq. (3)):
- * key (g, t, e) is k[g*head_stride + t*tok_stride + e] for KV head g < n_kv_heads,
- * token t < n_tokens, width e < head_dim; same for v.  pos[t] is the token's
- * absolute position p_t (Sec. 3.1), used for causal visibility p_t <= p. */
+ * key (g, t, e) is k[g*head_stride + row(t)*tok_stride + e] for KV head
+ * g < n_kv_heads, token t < n_tokens, width e < head_dim; same for v.
+ * row(t) = t for a contiguous cache.  For a paged pool (a block table with
+ * one token per entry, as serving engines keep it) slot is a device
+ * int32[n_tokens] and row(t) = slot[t], a row of the pool's pool_rows rows
+ * (values outside [0, pool_rows) are clamped to the last row: wrong but in
+ * bounds).  pos[t] is the token's absolute position p_t (Sec. 3.1), used for
+ * causal visibility p_t <= p; it is indexed by token, not by row. */
 typedef struct ckv_kv_view {
   const uint16_t* k;
   const uint16_t* v;
@@ -148,6 +153,8 @@ typedef struct ckv_kv_view {
   int32_t n_tokens;      /* S >= 1 */
   int32_t n_kv_heads;    /* H_kv >= 1 */
   int32_t head_dim;      /* d: 64 or 128 */
+  const int32_t* slot;   /* device int32[n_tokens], or NULL: contiguous */
+  int32_t pool_rows;     /* rows of the pool when slot is given */
 } ckv_kv_view;
 
 /* Query window Q (Sec. 3.1, Eq. (5)): post-RoPE queries of the W window
@@ -397,6 +404,10 @@ typedef struct ckv_accepted_pages {
  * (an entry with cand == NULL adds nothing).  Device outputs: kept_idx int32[n_seq * B]
  * (row s holds I, entries past n_kept[s] are -1), n_kept int32[n_seq],
  * token_state uint8[n_seq * score_seq_stride] (optional).
+ * `out` may be NULL: then only steps 1-3 run (kept_idx, n_kept, token_state)
+ * and no byte is copied; only in->n_seq and in->capacity are read.  A
+ * caller whose cache is a paged pool (ckv_kv_view.slot) applies I to its
+ * block table instead, which moves no key or value.
  * Errors: CKV_ERR_BUDGET if keep_recent + B_N > B; CKV_ERR_ARG if `out`
  * overlaps `in`; CKV_ERR_SHAPE if out->capacity < B or shapes differ.
  */

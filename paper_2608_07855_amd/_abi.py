@@ -45,7 +45,8 @@ class KVView(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
                 ("head_stride", ctypes.c_int64), ("tok_stride", ctypes.c_int64),
                 ("pos", ctypes.c_void_p), ("n_tokens", ctypes.c_int32),
-                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32)]
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("slot", ctypes.c_void_p), ("pool_rows", ctypes.c_int32)]
 
 
 class WindowView(ctypes.Structure):

@@ -133,20 +133,30 @@ def _check_bf16(t, name, ndim):
         raise ValueError(f"{name}: expected a cuda bfloat16 tensor of {ndim} dims with a contiguous last axis")
 
 
-def kv_view(k, v, pos, n_tokens: int | None = None) -> KVView:
-    """k, v: [Hkv, S_cap, d] bf16 (same strides); pos: int32 [>= n_tokens]."""
+def kv_view(k, v, pos, n_tokens: int | None = None, slot=None) -> KVView:
+    """k, v: [Hkv, S_cap, d] bf16 (same strides); pos: int32 [>= n_tokens].
+    With ``slot`` (int32 [n_tokens], device), k and v are a paged pool of
+    S_cap rows and token t lives in row slot[t]."""
     _check_bf16(k, "k", 3)
     _check_bf16(v, "v", 3)
     if k.shape != v.shape or k.stride() != v.stride():
         raise ValueError("k and v must have the same shape and strides")
     if pos.dtype != torch.int32 or not pos.is_cuda:
         raise ValueError("pos must be a cuda int32 tensor")
-    S = k.shape[1] if n_tokens is None else int(n_tokens)
-    if not 1 <= S <= k.shape[1] or pos.numel() < S:
-        raise ValueError("n_tokens out of range")
+    if slot is not None:
+        if slot.dtype != torch.int32 or not slot.is_cuda or not slot.is_contiguous():
+            raise ValueError("slot must be a contiguous cuda int32 tensor")
+        S = slot.numel() if n_tokens is None else int(n_tokens)
+        if not 1 <= S <= slot.numel() or pos.numel() < S:
+            raise ValueError("n_tokens out of range")
+    else:
+        S = k.shape[1] if n_tokens is None else int(n_tokens)
+        if not 1 <= S <= k.shape[1] or pos.numel() < S:
+            raise ValueError("n_tokens out of range")
     view = KVView(k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1), pos.data_ptr(), S,
-                  k.shape[0], k.shape[2])
-    view._keep = (k, v, pos)      # the struct holds raw pointers: keep the tensors alive
+                  k.shape[0], k.shape[2], slot.data_ptr() if slot is not None else None,
+                  k.shape[1] if slot is not None else 0)
+    view._keep = (k, v, pos, slot)   # the struct holds raw pointers: keep the tensors alive
     return view
 
 
@@ -302,24 +312,29 @@ def ckv_select_and_compact(ctx: Context, k_in, v_in, pos_in, n_tokens, score, re
                            pending_r_pre, *, budget: int, eta: float = 0.125,
                            max_pending_pages: int = 16, keep_recent: int = 0,
                            k_out=None, v_out=None, pos_out=None, token_state=None,
-                           accepted=None, kept=None, n_kept=None):
+                           accepted=None, kept=None, n_kept=None, compact: bool = True):
     """k_in, v_in: [n_seq, n_layers, Hkv, capacity, d] bf16; pos_in: [n_seq, capacity] int32;
     n_tokens: host ints [n_seq]; score: [n_seq, stride] fp32; retired, pending: lists of
     Pages (one per sequence); pending_r_pre: list of fp32 device tensors (or None).
     accepted: optional list (one per sequence) of None or (Pages, cand, n_cand,
-    accepted flags, max_cand) -- pages retired on the device by the joint test."""
+    accepted flags, max_cand) -- pages retired on the device by the joint test.
+    compact=False runs the selection only (no output cache; k_in, v_in only
+    give the shape)."""
     ns, L, H, cap, d = k_in.shape
     dev = k_in.device
-    if k_out is None:
+    if not compact:
+        k_out = v_out = pos_out = None
+    elif k_out is None:
         k_out = torch.empty((ns, L, H, budget, d), dtype=torch.bfloat16, device=dev)
         v_out = torch.empty_like(k_out)
-    if pos_out is None:
+    if pos_out is None and compact:
         pos_out = torch.empty((ns, budget), dtype=torch.int32, device=dev)
     if kept is None:
         kept = torch.empty((ns, budget), dtype=torch.int32, device=dev)
     if n_kept is None:
         n_kept = torch.empty(ns, dtype=torch.int32, device=dev)   # written by the call
-    cin, cout = cache_view(k_in, v_in, pos_in), cache_view(k_out, v_out, pos_out)
+    cin = cache_view(k_in, v_in, pos_in)
+    cout = cache_view(k_out, v_out, pos_out) if compact else None
     acc_arr, keep = None, []
     if accepted is not None:
         acc_arr = (AcceptedPages * ns)()
@@ -338,7 +353,8 @@ def ckv_select_and_compact(ctx: Context, k_in, v_in, pos_in, n_tokens, score, re
     b = Budget(int(budget), float(eta), int(max_pending_pages), int(keep_recent))
     ctx.check(lib().ckv_select_and_compact(
         ctx.handle, ctypes.byref(cin), nt.ctypes.data_as(_abi.c_i32p), _ptr(score),
-        int(score.stride(0)), ret, pen, rptr, acc_arr, ctypes.byref(b), ctypes.byref(cout), _ptr(kept),
+        int(score.stride(0)), ret, pen, rptr, acc_arr, ctypes.byref(b),
+        ctypes.byref(cout) if cout is not None else None, _ptr(kept),
         _ptr(n_kept), _ptr(token_state)))
     return dict(k=k_out, v=v_out, pos=pos_out, kept=kept, n_kept=n_kept)
 

@@ -109,6 +109,8 @@ struct ckv_agent {
     kv.n_tokens = n_res();
     kv.n_kv_heads = b.n_kv_heads;
     kv.head_dim = b.head_dim;
+    kv.slot = nullptr;
+    kv.pool_rows = 0;
     return kv;
   }
 

@@ -330,10 +330,13 @@ int check_kv(ckv_ctx* c, const ckv_kv_view* kv) {
     return fail(c, CKV_ERR_ARG, "K/V rows must be 16-byte aligned (strides multiples of 8)");
   if (kv->tok_stride < kv->head_dim || kv->head_stride < 0)
     return fail(c, CKV_ERR_SHAPE, "K/V strides too small");
+  if (kv->slot && (kv->pool_rows < 1 || (reinterpret_cast<uintptr_t>(kv->slot) & 3u)))
+    return fail(c, CKV_ERR_ARG, "paged view: pool_rows must be >= 1 and slot 4-byte aligned");
   // the kernels address a token of one head with a 32-bit element offset
-  // (24-bit multiply of token index and stride)
-  if (kv->tok_stride >= (1 << 24) || (int64_t)kv->n_tokens * kv->tok_stride >= ((int64_t)1 << 31))
-    return fail(c, CKV_ERR_UNSUPPORTED, "n_tokens * tok_stride must stay below 2^31 elements");
+  // (24-bit multiply of row index and stride)
+  const int64_t rows = kv->slot ? kv->pool_rows : kv->n_tokens;
+  if (kv->tok_stride >= (1 << 24) || rows >= (1 << 24) || rows * kv->tok_stride >= ((int64_t)1 << 31))
+    return fail(c, CKV_ERR_UNSUPPORTED, "rows * tok_stride must stay below 2^31 elements");
   return CKV_OK;
 }
 
@@ -386,6 +389,8 @@ AttnGeom make_geom(const ckv_kv_view* kv, const ckv_window_view* w) {
   a.rows = a.group * a.W;
   const float scale = w->scale > 0.f ? w->scale : 1.0f / std::sqrt((float)kv->head_dim);
   a.sl2 = scale * 1.4426950408889634f;
+  a.slot = kv->slot;
+  a.pool_last = kv->slot ? (uint32_t)(kv->pool_rows - 1) : 0u;
   return a;
 }
 
@@ -842,20 +847,25 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
                                       uint8_t* token_state) {
   if (!c) return CKV_ERR_ARG;
   c->err.clear();
-  if (!in || !out || !n_tokens || !score || !retired || !pending || !budget || !kept_idx || !n_kept)
+  if (!in || !n_tokens || !score || !retired || !pending || !budget || !kept_idx || !n_kept)
     return fail(c, CKV_ERR_ARG, "NULL argument");
-  if (!in->k || !in->v || !in->pos || !out->k || !out->v || !out->pos) return fail(c, CKV_ERR_ARG, "NULL cache pointer");
-  if (in->n_seq < 1 || in->n_layers < 1 || in->n_kv_heads < 1) return fail(c, CKV_ERR_SHAPE, "empty cache shape");
-  if (in->head_dim != 64 && in->head_dim != 128) return fail(c, CKV_ERR_SHAPE, "head_dim %d unsupported", in->head_dim);
-  if (out->n_seq != in->n_seq || out->n_layers != in->n_layers || out->n_kv_heads != in->n_kv_heads ||
-      out->head_dim != in->head_dim)
-    return fail(c, CKV_ERR_SHAPE, "input and output caches differ in shape");
-  const ckv_cache_view* vv[2] = {in, out};
-  for (const ckv_cache_view* v : vv) {
-    if (!aligned16(v->k) || !aligned16(v->v) || v->tok_stride % 8 || v->head_stride % 8 || v->layer_stride % 8 ||
-        v->seq_stride % 8)
-      return fail(c, CKV_ERR_ARG, "cache rows must be 16-byte aligned (strides multiples of 8)");
-    if (v->tok_stride < v->head_dim || v->capacity < 1) return fail(c, CKV_ERR_SHAPE, "cache strides or capacity");
+  if (in->n_seq < 1 || in->capacity < 1) return fail(c, CKV_ERR_SHAPE, "empty cache shape");
+  if (out) {
+    if (!in->k || !in->v || !in->pos || !out->k || !out->v || !out->pos)
+      return fail(c, CKV_ERR_ARG, "NULL cache pointer");
+    if (in->n_layers < 1 || in->n_kv_heads < 1) return fail(c, CKV_ERR_SHAPE, "empty cache shape");
+    if (in->head_dim != 64 && in->head_dim != 128)
+      return fail(c, CKV_ERR_SHAPE, "head_dim %d unsupported", in->head_dim);
+    if (out->n_seq != in->n_seq || out->n_layers != in->n_layers || out->n_kv_heads != in->n_kv_heads ||
+        out->head_dim != in->head_dim)
+      return fail(c, CKV_ERR_SHAPE, "input and output caches differ in shape");
+    const ckv_cache_view* vv[2] = {in, out};
+    for (const ckv_cache_view* v : vv) {
+      if (!aligned16(v->k) || !aligned16(v->v) || v->tok_stride % 8 || v->head_stride % 8 || v->layer_stride % 8 ||
+          v->seq_stride % 8)
+        return fail(c, CKV_ERR_ARG, "cache rows must be 16-byte aligned (strides multiples of 8)");
+      if (v->tok_stride < v->head_dim || v->capacity < 1) return fail(c, CKV_ERR_SHAPE, "cache strides or capacity");
+    }
   }
   const int B = budget->budget;
   if (B < 1 || !(budget->eta >= 0.f && budget->eta <= 1.f) || budget->max_pending_pages < 0 || budget->keep_recent < 0)
@@ -863,7 +873,7 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   const int bn = (int)std::floor((double)budget->eta * (double)B);
   if ((int64_t)budget->keep_recent + bn > B)
     return fail(c, CKV_ERR_BUDGET, "keep_recent (%d) + B_N (%d) exceeds the budget %d", budget->keep_recent, bn, B);
-  if (out->capacity < B) return fail(c, CKV_ERR_SHAPE, "output capacity %d < budget %d", out->capacity, B);
+  if (out && out->capacity < B) return fail(c, CKV_ERR_SHAPE, "output capacity %d < budget %d", out->capacity, B);
   const int ns = in->n_seq;
   for (int s = 0; s < ns; ++s) {
     if (n_tokens[s] < 1 || n_tokens[s] > in->capacity || n_tokens[s] > score_seq_stride)
@@ -881,6 +891,7 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
     }
   }
   // the output must not overlap the input (bytes of K, V and positions)
+  if (out) {
   auto extent = [](const ckv_cache_view* v) {
     return ((int64_t)(v->n_seq - 1) * v->seq_stride + (int64_t)(v->n_layers - 1) * v->layer_stride +
             (int64_t)(v->n_kv_heads - 1) * v->head_stride + (int64_t)(v->capacity - 1) * v->tok_stride +
@@ -902,6 +913,7 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
     for (int y = 0; y < 3; ++y)
       if (overlap(ins[x], inb[x], outs[y], outb[y])) return fail(c, CKV_ERR_ARG, "output cache overlaps the input");
   if (overlap(out->k, eo, out->v, eo)) return fail(c, CKV_ERR_ARG, "output K and V overlap");
+  }
   DeviceGuard g(c->device);
 
   // Sec. 4.4 variants: without transition protection no pending page is
@@ -1031,6 +1043,7 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
     CKV_LAUNCH(c, "select", launch_select(sa, c->stream));
   }
 
+  if (!out) return CKV_OK;   // selection only: the caller applies I (e.g. to a paged block table)
   GatherArgs ga{};
   ga.k_in = in->k;
   ga.v_in = in->v;

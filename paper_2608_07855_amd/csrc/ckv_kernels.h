@@ -21,6 +21,9 @@ struct AttnGeom {
   int Hq, W, group;                        // group = Hq / Hkv
   int rows;                                // window rows per KV head = group * W
   float sl2;                               // softmax scale * log2(e)
+  const int32_t* slot;                     // paged pool: token t is row slot[t] of each head
+                                           // (clamped to pool_last), or null: row t
+  uint32_t pool_last;                      // last row of the pool
 };
 
 // split-sequence partials of pass A

@@ -59,7 +59,10 @@ constexpr int kRowsWG = 32 * kNW;    // window rows per workgroup
 // [width][slot] fp16 (slot = vt_slot(offset)), positions as int32 (INT_MAX
 // for offsets past a segment's length, whose K and V rows are zero).
 // ---------------------------------------------------------------------------
-template <int D, int NT>
+// PG: the cache is a paged pool, token t's key and value rows are row
+// slot[t] (clamped to the pool) of each head's storage; positions stay by
+// token.
+template <int D, int NT, bool PG = false>
 struct Stager {
   static constexpr int KP = D + 8;              // K tile row stride (elements)
   static constexpr int VP = kTile + 8;          // V^T tile row stride (halves)
@@ -78,11 +81,15 @@ struct Stager {
   // segments read token 0.  r depends only on the thread, so the slot test
   // is a per-thread constant.
   __device__ __forceinline__ static uint32_t row_off(int r, int s0, int n0, int s1, int n1, uint32_t ts,
-                                                     bool& ok) {
+                                                     const int32_t* slot, uint32_t last, bool& ok) {
     const bool hi = r >= 32;
     const int o = r & 31;
     ok = o < (hi ? n1 : n0);
-    return ok ? __umul24((uint32_t)((hi ? s1 : s0) + o), ts) : 0u;
+    if constexpr (PG) {
+      return __umul24(min((uint32_t)slot[ok ? (hi ? s1 : s0) + o : 0], last), ts);
+    } else {
+      return ok ? __umul24((uint32_t)((hi ? s1 : s0) + o), ts) : 0u;
+    }
   }
 
   // Loads are unconditional: a token outside the segments reads token 0,
@@ -90,13 +97,13 @@ struct Stager {
   // the offset's position is INT_MAX, so every row masks its score to -inf
   // and its weight is exactly 0 (values are finite).
   __device__ __forceinline__ void issue(const uint16_t* kh, const uint16_t* vh, uint32_t ts,
-                                        const int32_t* pos, int s0, int n0, int s1, int n1,
-                                        int tid) {
+                                        const int32_t* slot, uint32_t last, const int32_t* pos, int s0,
+                                        int n0, int s1, int n1, int tid) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * NT;
       bool ok;
-      const uint32_t e = row_off((c / CPR) & (kTile - 1), s0, n0, s1, n1, ts, ok);
+      const uint32_t e = row_off((c / CPR) & (kTile - 1), s0, n0, s1, n1, ts, slot, last, ok);
       kr[i] = ldg_u4(kh + ((c < KCH ? e : 0u) + (c % CPR) * 8));
     }
 #pragma unroll
@@ -106,15 +113,13 @@ struct Stager {
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         bool ok;
-        const uint32_t e = row_off(2 * tp + j, s0, n0, s1, n1, ts, ok);
+        const uint32_t e = row_off(2 * tp + j, s0, n0, s1, n1, ts, slot, last, ok);
         vr[i][j] = ldg_u4(vh + ((u < VU ? e : 0u) + cg * 8));
       }
     }
-    bool ok;
     const int r = tid & 63;
     const int t = (r >= 32 ? s1 : s0) + (r & 31);
-    row_off(r, s0, n0, s1, n1, ts, ok);
-    ok = ok && tid < kTile;
+    const bool ok = (r & 31) < (r >= 32 ? n1 : n0) && tid < kTile;
     pr = ldg_i32(pos + (ok ? t : 0));
     pok = ok;
   }
@@ -270,10 +275,10 @@ __device__ __forceinline__ void pv_half(const _Float16* sV, int tb, int col, int
 // ---------------------------------------------------------------------------
 // A. split window attention
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, bool PG>
 __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom a, AttnSplit sp) {
   constexpr int NT = kNW * 64, KS = D / 16, DB = D / 32;
-  using St = Stager<D, NT>;
+  using St = Stager<D, NT, PG>;
   __shared__ __align__(16) uint16_t sK[2][kTile * St::KP];
   __shared__ __align__(16) _Float16 sV[2][D * St::VP];
   __shared__ __align__(16) int sP[2][kTile];
@@ -306,7 +311,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
   auto issue = [&](St& st, int it) {
     const int t0 = t_begin + it * kTile;
     const int n = it < n_tiles ? min(kTile, t_end - t0) : 0;
-    st.issue(kh, vh, (uint32_t)a.kv_tok_stride, a.pos, t0, min(32, n), t0 + 32, max(0, n - 32), tid);
+    st.issue(kh, vh, (uint32_t)a.kv_tok_stride, a.slot, a.pool_last, a.pos, t0, min(32, n), t0 + 32,
+             max(0, n - 32), tid);
   };
   auto compute = [&](int b) {
     if (wave_on) {
@@ -482,10 +488,10 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
 // derives the same tile sequence from the page lengths.
 // ---------------------------------------------------------------------------
 // NB: 32-token slots a page may span (1 when every page has <= 32 tokens).
-template <int D, int MODE, int NB>
+template <int D, int MODE, int NB, bool PG>
 __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork pw, RowStats rs) {
   constexpr int NT = kNW * 64, KS = D / 16, DB = D / 32;
-  using St = Stager<D, NT>;
+  using St = Stager<D, NT, PG>;
   __shared__ __align__(16) uint16_t sK[2][kTile * St::KP];
   __shared__ __align__(16) _Float16 sV[2][D * St::VP];
   __shared__ __align__(16) int sP[2][kTile];
@@ -587,7 +593,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   // index past the end is an empty segment (its loads read token 0).
   auto issue_tile = [&](St& st, int k) {
     const int4 sg = k < n_tiles ? sTileSeg[k] : make_int4(0, 0, 0, 0);
-    st.issue(kh, vh, (uint32_t)a.kv_tok_stride, a.pos, sg.x, sg.y, sg.z, sg.w, tid);
+    st.issue(kh, vh, (uint32_t)a.kv_tok_stride, a.slot, a.pool_last, a.pos, sg.x, sg.y, sg.z, sg.w, tid);
   };
   // A row sees at least nvis tokens; a page (at most kMaxPage tokens) can
   // hold all of them only if nvis <= kMaxPage, so most waves skip the count.
@@ -789,7 +795,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
 constexpr int kFixT = 256;        // threads of a fix-up workgroup
 constexpr int kFixGrid = 1024;    // (pair, part) items in flight
 
-template <int D>
+template <int D, bool PG>
 __global__ __launch_bounds__(kFixT) void page_fixup_partial(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw,
                                                             float* fpart, int parts) {
   constexpr int TPR = D / 8;                  // threads per token row (16 bytes each)
@@ -822,8 +828,9 @@ __global__ __launch_bounds__(kFixT) void page_fixup_partial(AttnGeom a, AttnSpli
 #pragma unroll
       for (int u = 0; u < UNR; ++u) {
         const int t = max(a0, min(b0 + u * RPR + r, a1 - 1));
-        kc[u] = ldg_u4(kh + (int64_t)t * a.kv_tok_stride + 8 * c);
-        vc[u] = ldg_u4(vh + (int64_t)t * a.kv_tok_stride + 8 * c);
+        const int64_t row = PG ? (int64_t)min((uint32_t)a.slot[t], a.pool_last) : t;
+        kc[u] = ldg_u4(kh + row * a.kv_tok_stride + 8 * c);
+        vc[u] = ldg_u4(vh + row * a.kv_tok_stride + 8 * c);
         pv[u] = ldg_i32(a.pos + t);
       }
     };
@@ -940,7 +947,7 @@ __global__ __launch_bounds__(256) void page_fixup_final(AttnGeom a, RowStats rs,
 constexpr int kMassMaxRows = 2048;   // window rows per KV head the mass kernel supports
 constexpr int kMassMaxPairs = kMassMaxRows / 32;
 
-template <int D>
+template <int D, bool PG>
 __global__ __launch_bounds__(kNW * 64) void token_mass_kernel(AttnGeom a, RowStats rs, float* mass,
                                                               int chunk) {
   constexpr int NT = kNW * 64, KS = D / 16;
@@ -972,7 +979,9 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_kernel(AttnGeom a, RowSta
       const int c = tid + i * NT;
       const int tr = (c / CPR) & (kTile - 1);
       const bool ok = c < KCH && tr < nv;
-      const u32x4 v = ldg_u4(kh + (int64_t)(ok ? t0 + tr : 0) * a.kv_tok_stride + (c % CPR) * 8);
+      const int tk = ok ? t0 + tr : 0;
+      const int64_t row = PG ? (int64_t)min((uint32_t)a.slot[tk], a.pool_last) : tk;
+      const u32x4 v = ldg_u4(kh + row * a.kv_tok_stride + (c % CPR) * 8);
       kr[i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
     }
     const bool okp = tid < nv;
@@ -1047,7 +1056,7 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_kernel(AttnGeom a, RowSta
 // window position skips the visibility test.  Workgroup z takes pairs
 // [8 PPW z, 8 PPW (z+1)), whole heads only (8 PPW is a multiple of the row
 // blocks per head); heads of other z-slices meet in the atomic max.
-template <int D, int PPW>
+template <int D, int PPW, bool PG>
 __global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats rs, float* mass, int chunk) {
   constexpr int NT = kNW * 64, KS = D / 16;
   constexpr int KP = D + 8, CPR = D / 8, KCH = kTile * CPR, KPT = (KCH + NT - 1) / NT;
@@ -1118,7 +1127,9 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats
       const int c = tid + i * NT;
       const int tr = (c / CPR) & (kTile - 1);
       const bool ok = c < KCH && tr < nv;
-      st.kr[i] = ldg_u4(kh + (int64_t)(ok ? t0 + tr : 0) * a.kv_tok_stride + (c % CPR) * 8);
+      const int tk = ok ? t0 + tr : 0;
+      const int64_t row = PG ? (int64_t)min((uint32_t)a.slot[tk], a.pool_last) : tk;
+      st.kr[i] = ldg_u4(kh + row * a.kv_tok_stride + (c % CPR) * 8);
     }
     st.pok = tid < nv;
     st.pr = ldg_i32(a.pos + (st.pok ? t0 + tid : 0));
@@ -1207,8 +1218,14 @@ int token_mass_max_rows() { return kMassMaxRows; }
 hipError_t launch_window_attention(const AttnGeom& a, const AttnSplit& sp, hipStream_t s) {
   const int nrb = (a.rows + kRowsWG - 1) / kRowsWG;
   dim3 grid(sp.n_splits, nrb, a.Hkv), block(kNW * 64);
-  if (a.D == 128) hipLaunchKernelGGL((window_attention_kernel<128>), grid, block, 0, s, a, sp);
-  else hipLaunchKernelGGL((window_attention_kernel<64>), grid, block, 0, s, a, sp);
+  const bool pg = a.slot != nullptr;
+  if (a.D == 128) {
+    if (pg) hipLaunchKernelGGL((window_attention_kernel<128, true>), grid, block, 0, s, a, sp);
+    else hipLaunchKernelGGL((window_attention_kernel<128, false>), grid, block, 0, s, a, sp);
+  } else {
+    if (pg) hipLaunchKernelGGL((window_attention_kernel<64, true>), grid, block, 0, s, a, sp);
+    else hipLaunchKernelGGL((window_attention_kernel<64, false>), grid, block, 0, s, a, sp);
+  }
   return hipGetLastError();
 }
 
@@ -1227,11 +1244,16 @@ hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowSt
   const int nblk = (pw.n_items + pw.items_per_block - 1) / pw.items_per_block;
   if (nblk == 0) return hipSuccess;
   dim3 grid(nblk, nrb, a.Hkv), block(kNW * 64);
-  const bool two = max_len > 32;
-#define CKV_PAGE_LAUNCH(DD, MM)                                                                  \
-  do {                                                                                           \
-    if (two) hipLaunchKernelGGL((page_kernel<DD, MM, 2>), grid, block, 0, s, a, pw, rs);         \
-    else hipLaunchKernelGGL((page_kernel<DD, MM, 1>), grid, block, 0, s, a, pw, rs);             \
+  const bool two = max_len > 32, pg = a.slot != nullptr;
+#define CKV_PAGE_LAUNCH(DD, MM)                                                                   \
+  do {                                                                                            \
+    if (pg) {                                                                                     \
+      if (two) hipLaunchKernelGGL((page_kernel<DD, MM, 2, true>), grid, block, 0, s, a, pw, rs);  \
+      else hipLaunchKernelGGL((page_kernel<DD, MM, 1, true>), grid, block, 0, s, a, pw, rs);      \
+    } else {                                                                                      \
+      if (two) hipLaunchKernelGGL((page_kernel<DD, MM, 2, false>), grid, block, 0, s, a, pw, rs); \
+      else hipLaunchKernelGGL((page_kernel<DD, MM, 1, false>), grid, block, 0, s, a, pw, rs);     \
+    }                                                                                             \
   } while (0)
   if (a.D == 128) {
     if (mode == 0) CKV_PAGE_LAUNCH(128, 0);
@@ -1248,11 +1270,14 @@ hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowSt
                              const PageWork& pw, float* fpart, int parts, hipStream_t s) {
   dim3 grid(std::max(1, std::min(pw.fix_cap * parts, kFixGrid))), block(kFixT);
   dim3 grid2(std::max(1, std::min((pw.fix_cap + 3) / 4, 256))), block2(256);
+  const bool pg = a.slot != nullptr;
   if (a.D == 128) {
-    hipLaunchKernelGGL((page_fixup_partial<128>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
+    if (pg) hipLaunchKernelGGL((page_fixup_partial<128, true>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
+    else hipLaunchKernelGGL((page_fixup_partial<128, false>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
     hipLaunchKernelGGL((page_fixup_final<128>), grid2, block2, 0, s, a, rs, pw, fpart, parts);
   } else {
-    hipLaunchKernelGGL((page_fixup_partial<64>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
+    if (pg) hipLaunchKernelGGL((page_fixup_partial<64, true>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
+    else hipLaunchKernelGGL((page_fixup_partial<64, false>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
     hipLaunchKernelGGL((page_fixup_final<64>), grid2, block2, 0, s, a, rs, pw, fpart, parts);
   }
   return hipGetLastError();
@@ -1262,21 +1287,33 @@ hipError_t launch_token_mass(const AttnGeom& a, const RowStats& rs, float* mass,
                              hipStream_t s) {
   const int nrb = (a.W + 31) / 32, n_pairs = a.group * nrb;
   const int ppw = n_pairs <= kNW ? 1 : 2;
+  const bool pg = a.slot != nullptr;
   if ((kNW * ppw) % nrb == 0) {
     const int nz = (n_pairs + kNW * ppw - 1) / (kNW * ppw);
     dim3 grid((a.S + chunk - 1) / chunk, a.Hkv, nz), block(kNW * 64);
+#define CKV_MASS_LAUNCH(DD, PP)                                                                       \
+  do {                                                                                                \
+    if (pg) hipLaunchKernelGGL((token_mass_fast<DD, PP, true>), grid, block, 0, s, a, rs, mass, chunk); \
+    else hipLaunchKernelGGL((token_mass_fast<DD, PP, false>), grid, block, 0, s, a, rs, mass, chunk);   \
+  } while (0)
     if (a.D == 128) {
-      if (ppw == 1) hipLaunchKernelGGL((token_mass_fast<128, 1>), grid, block, 0, s, a, rs, mass, chunk);
-      else hipLaunchKernelGGL((token_mass_fast<128, 2>), grid, block, 0, s, a, rs, mass, chunk);
+      if (ppw == 1) CKV_MASS_LAUNCH(128, 1);
+      else CKV_MASS_LAUNCH(128, 2);
     } else {
-      if (ppw == 1) hipLaunchKernelGGL((token_mass_fast<64, 1>), grid, block, 0, s, a, rs, mass, chunk);
-      else hipLaunchKernelGGL((token_mass_fast<64, 2>), grid, block, 0, s, a, rs, mass, chunk);
+      if (ppw == 1) CKV_MASS_LAUNCH(64, 1);
+      else CKV_MASS_LAUNCH(64, 2);
     }
+#undef CKV_MASS_LAUNCH
     return hipGetLastError();
   }
   dim3 grid((a.S + chunk - 1) / chunk, a.Hkv), block(kNW * 64);
-  if (a.D == 128) hipLaunchKernelGGL((token_mass_kernel<128>), grid, block, 0, s, a, rs, mass, chunk);
-  else hipLaunchKernelGGL((token_mass_kernel<64>), grid, block, 0, s, a, rs, mass, chunk);
+  if (a.D == 128) {
+    if (pg) hipLaunchKernelGGL((token_mass_kernel<128, true>), grid, block, 0, s, a, rs, mass, chunk);
+    else hipLaunchKernelGGL((token_mass_kernel<128, false>), grid, block, 0, s, a, rs, mass, chunk);
+  } else {
+    if (pg) hipLaunchKernelGGL((token_mass_kernel<64, true>), grid, block, 0, s, a, rs, mass, chunk);
+    else hipLaunchKernelGGL((token_mass_kernel<64, false>), grid, block, 0, s, a, rs, mass, chunk);
+  }
   return hipGetLastError();
 }
 

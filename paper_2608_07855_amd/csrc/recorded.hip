@@ -83,7 +83,7 @@ __global__ __launch_bounds__(256) void recorded_rows_kernel(AttnGeom a, const fl
 // Scores: four lanes per token (a quarter of the width each), 16 tokens per
 // pass; every key, position and query load of the pair is issued before the
 // first product, and the values of a pass's 16 tokens are loaded together.
-template <int D>
+template <int D, bool PG>
 __global__ __launch_bounds__(256) void page_fixup_recorded(AttnGeom a, RowStats rs, PageWork pw, int4* list2,
                                                            int* count2, int cap2, float a_hi) {
   constexpr int J = D / 64;            // widths lane + 64 j of u
@@ -108,8 +108,9 @@ __global__ __launch_bounds__(256) void page_fixup_recorded(AttnGeom a, RowStats 
     for (int ps = 0; ps < NP; ++ps) {
       const int i = ps * 16 + tk;
       const int t = st + min(i, ln - 1);           // in-range address for every lane
+      const int64_t row = PG ? (int64_t)min((uint32_t)a.slot[t], a.pool_last) : t;
 #pragma unroll
-      for (int c = 0; c < QC; ++c) kc[ps][c] = ldg_u4(kh + (int64_t)t * a.kv_tok_stride + 8 * (sub * QC + c));
+      for (int c = 0; c < QC; ++c) kc[ps][c] = ldg_u4(kh + row * a.kv_tok_stride + 8 * (sub * QC + c));
       pv[ps] = i < ln ? ldg_i32(a.pos + t) : INT_MAX;
     }
     float ov[J];
@@ -153,8 +154,9 @@ __global__ __launch_bounds__(256) void page_fixup_recorded(AttnGeom a, RowStats 
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int t = st + min(ps * 16 + i, ln - 1);
+        const int64_t row = PG ? (int64_t)min((uint32_t)a.slot[t], a.pool_last) : t;
 #pragma unroll
-        for (int j = 0; j < J; ++j) vv[i][j] = bf16_bits_to_float(vh[(int64_t)t * a.kv_tok_stride + lane + 64 * j]);
+        for (int j = 0; j < J; ++j) vv[i][j] = bf16_bits_to_float(vh[row * a.kv_tok_stride + lane + 64 * j]);
       }
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
@@ -216,10 +218,14 @@ hipError_t launch_page_fixup_recorded(const AttnGeom& a, const RowStats& rs, con
                                       int* count2, int cap2, float a_hi, hipStream_t s) {
   dim3 grid(std::max(1, std::min((pw.fix_cap + 3) / 4, 256))), block(256);
   int4* l2 = reinterpret_cast<int4*>(list2);
-  if (a.D == 128)
-    hipLaunchKernelGGL((page_fixup_recorded<128>), grid, block, 0, s, a, rs, pw, l2, count2, cap2, a_hi);
-  else
-    hipLaunchKernelGGL((page_fixup_recorded<64>), grid, block, 0, s, a, rs, pw, l2, count2, cap2, a_hi);
+  const bool pg = a.slot != nullptr;
+  if (a.D == 128) {
+    if (pg) hipLaunchKernelGGL((page_fixup_recorded<128, true>), grid, block, 0, s, a, rs, pw, l2, count2, cap2, a_hi);
+    else hipLaunchKernelGGL((page_fixup_recorded<128, false>), grid, block, 0, s, a, rs, pw, l2, count2, cap2, a_hi);
+  } else {
+    if (pg) hipLaunchKernelGGL((page_fixup_recorded<64, true>), grid, block, 0, s, a, rs, pw, l2, count2, cap2, a_hi);
+    else hipLaunchKernelGGL((page_fixup_recorded<64, false>), grid, block, 0, s, a, rs, pw, l2, count2, cap2, a_hi);
+  }
   return hipGetLastError();
 }
 

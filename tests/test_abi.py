@@ -61,7 +61,7 @@ def test_version_and_null_handling(lib):
 
 def test_struct_layouts_match_header():
     # field order and sizes of the views as the header declares them
-    assert ctypes.sizeof(_abi.KVView) == 8 + 8 + 8 + 8 + 8 + 4 * 3 + 4
+    assert ctypes.sizeof(_abi.KVView) == 8 + 8 + 8 + 8 + 8 + 4 * 3 + 4 + 8 + 4 + 4
     assert ctypes.sizeof(_abi.WindowView) == 8 + 8 + 8 + 8 + 4 * 3 + 4
     assert ctypes.sizeof(_abi.PageList) == 8 + 8 + 4 + 4
     assert ctypes.sizeof(_abi.Thresholds) == 20
