@@ -24,7 +24,9 @@ the compaction bandwidth and per-kernel times (HIP events recorded by the
 library on its stream).  ``roofline`` is for the kernel with the largest
 total time; ``cpu_baseline`` times the fp64 oracle on a bounded sample on the
 host cores.  ``recorded`` times the per-page pass alone from recorded window
-outputs (ckv_measure_recorded); ``paged`` the measurement over a paged pool.  ``agent`` runs whole synthetic agent episodes of a 36-layer stack
+outputs (ckv_measure_recorded); ``paged`` the measurement over a paged pool;
+``stack`` the per-layer measurement of 36 layers x 4 sequences at 65536
+tokens through the batched call.  ``agent`` runs whole synthetic agent episodes of a 36-layer stack
 through the lifecycle driver (Algorithm 1) and reports the driver's time per
 commit, post-commit step and checkpoint; ``agent_paper_point`` does the same
 at the paper's operating point (W 8, G 16, budget 4096, 40 layers).
@@ -66,6 +68,8 @@ def parse():
     ap.add_argument("--no-agent", action="store_true",
                     help="skip the lifecycle-driver leg (whole agent episodes, Algorithm 1)")
     ap.add_argument("--agent-seqs", type=int, default=4)
+    ap.add_argument("--no-stack", action="store_true",
+                    help="skip the 144-problem stack leg (36 layers x 4 sequences at 65536 tokens)")
     ap.add_argument("--no-recorded", action="store_true",
                     help="skip the recorded-output leg (ckv_measure_recorded)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -239,6 +243,71 @@ def paged_leg(st, steps):
     return dict(ms_per_step=ms, tokens_per_s=toks / (ms / 1e3),
                 note="pre + post measurement with token mass over a paged pool of 1.5 S rows "
                      "(slot table); one pool, so the key/value rows may be reused from the Infinity Cache")
+
+
+def stack_leg(steps):
+    """Per-layer scoring of the full Qwen3-8B-shaped stack: 36 layers x 4
+    sequences at 65536 cached tokens (144 problems, 38.6 GB of keys and
+    values), each step running the pre- and the post-commit measurement of
+    every problem through the batched call (ckv_measure_page_effects_batch).
+    Event layouts and page tables come from the seeded generator; keys,
+    values and queries are drawn by torch on the device (timing only)."""
+    import torch
+
+    import paper_2608_07855_amd as P
+    from synth import WORKLOADS, make_layout
+    from synth.workloads import rng_for
+
+    w = WORKLOADS["q8b_stack"]
+    S, Hkv, Hq, d, W = w.n_tokens, w.n_kv_heads, w.n_q_heads, w.head_dim, w.window
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+
+    def bf16(shape):
+        return torch.randn(shape, generator=g, device="cuda").to(torch.bfloat16)
+
+    ctx = P.Context(0)
+    kv_pre, kv_post, w_pre, w_post, pages, keep = [], [], [], [], [], []
+    tokens = 0
+    for sq in range(w.n_seq):
+        lay = make_layout(w, rng_for(w, 0, sq, 0, 0))
+        pos = torch.arange(S, dtype=torch.int32, device="cuda")
+        qp_pre = torch.from_numpy(lay.qrows_pre.astype(np.int32)).cuda()
+        qp_post = torch.from_numpy(lay.qrows_post.astype(np.int32)).cuda()
+        pg = P.Pages(lay.page_start, lay.page_len)
+        for _ in range(w.n_layers):
+            k, v = bf16((Hkv, S, d)), bf16((Hkv, S, d))
+            q1, q2 = bf16((Hq, W, d)), bf16((Hq, W, d))
+            keep += [k, v, q1, q2, pos, qp_pre, qp_post]
+            kv_pre.append(P.kv_view(k, v, pos, n_tokens=lay.s_pre))
+            kv_post.append(P.kv_view(k, v, pos))
+            w_pre.append(P.window_view(q1, qp_pre))
+            w_post.append(P.window_view(q2, qp_post))
+            pages.append(pg)
+            tokens += lay.s_pre + S
+    n = len(kv_pre)
+    R = [torch.empty(max(p.n, 1), dtype=torch.float32, device="cuda") for p in pages]
+
+    def step():
+        P.ckv_measure_page_effects_batch(ctx, kv_pre, w_pre, pages, R=R)
+        P.ckv_measure_page_effects_batch(ctx, kv_post, w_post, pages, R=R)
+
+    step()
+    gc.collect()
+    gc.disable()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    gc.enable()
+    ctx.close()
+    del keep
+    torch.cuda.empty_cache()
+    return dict(workload=f"qwen3-8b-shaped stack: {w.n_layers} layers x {w.n_seq} sequences at {S} cached tokens "
+                         f"({n} problems), pre + post measurement per layer", problems=n,
+                ms_per_step=ms, tokens_per_s=tokens / (ms / 1e3), tokens_per_step=tokens)
 
 
 def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped"):
@@ -464,6 +533,7 @@ def main():
         roof["avg_launch_us"] = avg_s * 1e6
     recorded = None if args.no_recorded else recorded_leg(st, args.steps)
     paged = None if args.no_recorded else paged_leg(st, args.steps)
+    stack = None if args.no_stack else stack_leg(3)
     agent = None if args.no_agent else agent_leg(args.agent_seqs)
     agent_paper = None if args.no_agent else agent_leg(2, "paper_agent", "qwen3-14b-shaped, paper operating point")
     cpu = None
@@ -489,6 +559,7 @@ def main():
         cpu_baseline=cpu,
         recorded=recorded,
         paged=paged,
+        stack=stack,
         agent=agent,
         agent_paper_point=agent_paper,
     )

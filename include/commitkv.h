@@ -274,6 +274,24 @@ int ckv_measure_page_effects(ckv_ctx* ctx, const ckv_kv_view* kv,
                              float* token_mass);
 
 /*
+ * Batched form of ckv_measure_page_effects for many (layer, sequence)
+ * problems, such as every layer of every sequence in a batch: problem i
+ * reads kv[i], win[i], pages[i] (arrays of n views) and writes R[i],
+ * R_head[i], o[i], lse[i], token_mass[i] (host arrays of n device pointers;
+ * an optional array may be NULL as a whole or hold NULL entries).  Every
+ * problem is validated before anything is enqueued; the problems then run
+ * in order on the context's stream, reusing one workspace.  A workspace or
+ * HIP failure part-way returns the error with the earlier problems enqueued.
+ */
+int ckv_measure_page_effects_batch(ckv_ctx* ctx, int32_t n,
+                                   const ckv_kv_view* kv,
+                                   const ckv_window_view* win,
+                                   const ckv_page_list* pages,
+                                   float* const* R, float* const* R_head,
+                                   float* const* o, float* const* lse,
+                                   float* const* token_mass);
+
+/*
  * Recorded-output variant of ckv_measure_page_effects (Sec. 3.2: the engine
  * records the window's attention outputs during its forward pass).  o
  * [n_q_heads * n_rows * head_dim] (16-byte aligned) and lse [n_q_heads *

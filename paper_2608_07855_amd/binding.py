@@ -242,6 +242,43 @@ def ckv_measure_page_effects(ctx: Context, kv: KVView, win: WindowView, pages: P
                 lse=None if lse is None else lse.view(Hq, W), token_mass=token_mass)
 
 
+def ckv_measure_page_effects_batch(ctx: Context, kvs, wins, pages, *, R=None, want=("R",)):
+    """Problem i: kvs[i], wins[i], pages[i] (Pages).  Returns one dict per
+    problem, as ckv_measure_page_effects does."""
+    n = len(kvs)
+    dev = torch.device("cuda", ctx.device)
+    outs = []
+    for i in range(n):
+        Hq, W, d = wins[i].n_q_heads, wins[i].n_rows, kvs[i].head_dim
+        np_ = pages[i].n
+        outs.append(dict(
+            R=R[i] if R is not None else _f32(max(np_, 1), dev),
+            R_head=_f32(max(np_ * Hq, 1), dev) if "R_head" in want else None,
+            o=_f32(Hq * W * d, dev) if "o" in want else None,
+            lse=_f32(Hq * W, dev) if "lse" in want else None,
+            token_mass=_f32(kvs[i].n_tokens, dev) if "token_mass" in want else None))
+    kv_arr = (KVView * n)(*kvs)
+    win_arr = (WindowView * n)(*wins)
+    views = [p.view() for p in pages]
+    pg_arr = (PageList * n)(*views)
+
+    def ptrs(key):
+        if all(o[key] is None for o in outs):
+            return None
+        return (ctypes.c_void_p * n)(*[(o[key].data_ptr() if o[key] is not None else 0) for o in outs])
+    arrs = [ptrs(k) for k in ("R", "R_head", "o", "lse", "token_mass")]
+    ctx.check(lib().ckv_measure_page_effects_batch(ctx.handle, n, kv_arr, win_arr, pg_arr, *arrs))
+    res = []
+    for i, o in enumerate(outs):
+        np_, Hq, W, d = pages[i].n, wins[i].n_q_heads, wins[i].n_rows, kvs[i].head_dim
+        res.append(dict(R=o["R"][:np_],
+                        R_head=None if o["R_head"] is None else o["R_head"][:np_ * Hq].view(np_, Hq),
+                        o=None if o["o"] is None else o["o"].view(Hq, W, d),
+                        lse=None if o["lse"] is None else o["lse"].view(Hq, W),
+                        token_mass=o["token_mass"]))
+    return res
+
+
 def ckv_measure_recorded(ctx: Context, kv: KVView, win: WindowView, pages: Pages, o, lse, *,
                          R=None, R_head=None, token_mass=None, want=("R",)):
     """Deletion effect of every page from recorded window outputs o [Hq, W, d]

@@ -604,6 +604,37 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
   return CKV_OK;
 }
 
+extern "C" int ckv_measure_page_effects_batch(ckv_ctx* c, int32_t n, const ckv_kv_view* kv,
+                                              const ckv_window_view* win, const ckv_page_list* pages,
+                                              float* const* R, float* const* R_head, float* const* o,
+                                              float* const* lse, float* const* token_mass) {
+  if (!c) return CKV_ERR_ARG;
+  c->err.clear();
+  if (n < 0 || (n > 0 && (!kv || !win || !pages || !R))) return fail(c, CKV_ERR_ARG, "batch: NULL arrays or n < 0");
+  for (int i = 0; i < n; ++i) {
+    int rc;
+    if ((rc = check_kv(c, &kv[i])) || (rc = check_win(c, &win[i], &kv[i])) ||
+        (rc = check_pages(c, &pages[i], kv[i].n_tokens, "measured"))) {
+      const std::string m = c->err;
+      return fail(c, rc, "batch problem %d: %s", i, m.c_str());
+    }
+    if (pages[i].n_pages > 0 && !R[i]) return fail(c, CKV_ERR_ARG, "batch problem %d: R is NULL", i);
+    if (token_mass && token_mass[i] &&
+        (win[i].n_q_heads / kv[i].n_kv_heads) * win[i].n_rows > token_mass_max_rows())
+      return fail(c, CKV_ERR_UNSUPPORTED, "batch problem %d: too many window rows for token_mass", i);
+  }
+  for (int i = 0; i < n; ++i) {
+    const int rc = ckv_measure_page_effects(c, &kv[i], &win[i], &pages[i], R[i], R_head ? R_head[i] : nullptr,
+                                            o ? o[i] : nullptr, lse ? lse[i] : nullptr,
+                                            token_mass ? token_mass[i] : nullptr);
+    if (rc) {
+      const std::string m = c->err;
+      return fail(c, rc, "batch problem %d: %s", i, m.c_str());
+    }
+  }
+  return CKV_OK;
+}
+
 extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win,
                                     const ckv_page_list* pages, const float* o, const float* lse, float* R,
                                     float* R_head, float* token_mass) {

@@ -114,3 +114,9 @@ def test_struct_layouts_match_gcc(tmp_path, struct, cls):
     size, offs = _c_layout(tmp_path, struct, cnames)
     assert ctypes.sizeof(C) == size
     assert [getattr(C, n).offset for n in names] == offs
+
+
+def test_batch_null_handling(lib):
+    L = _abi.load()
+    assert L.ckv_measure_page_effects_batch(None, 0, None, None, None, None, None, None, None, None) \
+        == _abi.CKV_ERR_ARG

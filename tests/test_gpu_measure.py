@@ -170,3 +170,35 @@ def test_dominant_page(ckv, which):
     assert A.max() > 0.999
     assert_scores_close(got["R"], R, "R")
     assert_scores_close(got["R_head"], Rh, "R_head")
+
+
+def test_batch_matches_single_calls(ckv):
+    """ckv_measure_page_effects_batch over problems of different shapes (head
+    width, grouping, window, prefix) gives, problem by problem, exactly what
+    the single call gives."""
+    P, ctx = ckv
+    probs = []
+    for case, which in (("tiny", "pre"), ("tiny", "post"), ("d128_ragged", "post"), ("w8_mha", "pre")):
+        L = make_layer(CASES[case], seed=21)
+        dl = LayerOnDevice(L)
+        if which == "pre":
+            kv = P.kv_view(dl.k, dl.v, dl.pos, n_tokens=L.layout.s_pre)
+            win = P.window_view(dl.q_pre, dl.qpos_pre)
+        else:
+            kv = P.kv_view(dl.k, dl.v, dl.pos)
+            win = P.window_view(dl.q_post, dl.qpos_post)
+        probs.append((kv, win, P.Pages(L.layout.page_start, L.layout.page_len), dl))
+    want = ("R", "R_head", "o", "lse", "token_mass")
+    batch = P.ckv_measure_page_effects_batch(ctx, [p[0] for p in probs], [p[1] for p in probs],
+                                             [p[2] for p in probs], want=want)
+    single = [P.ckv_measure_page_effects(ctx, kv, win, pg, want=want) for kv, win, pg, _ in probs]
+    torch.cuda.synchronize()
+    for b, s in zip(batch, single):
+        for k in want:
+            assert np.array_equal(b[k].cpu().numpy().view(np.uint32), s[k].cpu().numpy().view(np.uint32)), k
+    # a bad problem is reported before anything runs
+    bad = P.Pages([0], [65])
+    with pytest.raises(P.CKVError) as e:
+        P.ckv_measure_page_effects_batch(ctx, [probs[0][0], probs[1][0]], [probs[0][1], probs[1][1]],
+                                         [probs[0][2], bad])
+    assert e.value.code == -2 and "problem 1" in str(e.value)
