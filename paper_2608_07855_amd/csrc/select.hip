@@ -480,7 +480,11 @@ namespace {
 constexpr int kQT = 256;
 constexpr int kQW = kQT / 64;
 constexpr int kQKPT = kSelGridChunk / kQT;   // keys per thread
-enum { qArrive = 0, qDone = 1, qNP = 2, qNF = 3, qNotLo = 4, qHi = 5, qError = 6, qCounts = 8 };
+enum { qArrive = 0, qDone = 1, qNP = 2, qNF = 3, qNotLo = 4, qHi = 5, qError = 6, qCand = 7, qCounts = 8 };
+// when the threshold bin of the first pass holds at most this many free
+// keys, they are listed (in the histogram rows of the later passes) and every
+// workgroup finishes the selection on the list in LDS: no further grid pass
+constexpr int kCandMax = kSelBins;
 constexpr long long kSelTimeoutTicks = 1ll << 27;   // ~1.3 s of the 100 MHz wall clock
 
 __device__ bool seq_barrier(int* ctrl, int target, int* s_ok) {
@@ -520,7 +524,9 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
   __shared__ int tmp[kQW], wa[kQW], wb[kQW];
   __shared__ uint32_t wlo[kQW], whi[kQW];
   __shared__ uint32_t s_lo, s_hi;
-  __shared__ int s_need, s_ok;
+  __shared__ int s_need, s_ok, s_m, s_cnt[3];
+  __shared__ uint32_t sCk[kCandMax];
+  __shared__ int sCi[kCandMax];
   const int s = blockIdx.y, cb = blockIdx.x, C = gridDim.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int* ctrl = a.gctrl + (size_t)s * kSelGridCtrl;
@@ -656,6 +662,8 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
     const int k = max(0, min(a.budget - NP, NF));
     uint32_t T;
     int need_eq = 0;
+    bool listed = false;                 // threshold decided from the candidate list
+    int k_before = 0, e_before = 0;      // kept tokens and ties at T in the chunks before this one
     if (k == 0) {
       T = kKeyProt - 1u;                 // no free key reaches it
     } else if (k == NF) {
@@ -697,6 +705,7 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
             s_lo = nlo;
             s_hi = min(hi, nlo + min(width, 0xFFFFFFFFu - nlo));
             s_need = need - above;
+            s_m = h[j];
           }
           above += h[j];
         }
@@ -704,12 +713,107 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
         lo = s_lo;
         hi = s_hi;
         need = s_need;
+        // few keys left in the bin: list them instead of narrowing further
+        if (pass == 0 && lo != hi && s_m <= kCandMax) {
+          listed = true;
+          break;
+        }
       }
-      T = lo;                            // lo == hi: the need-th largest key
-      need_eq = need;
+      if (ok && listed) {
+        // every free key in [lo, hi] goes to the sequence's candidate list
+        // (the histogram rows of the later passes, unused on this path);
+        // the chunk publishes how many of its tokens are kept outright
+        uint32_t* gc = gh + kSelBins;
+        int nk = 0;
+#pragma unroll
+        for (int u = 0; u < kQKPT; ++u) {
+          const uint32_t kk = key[u];
+          nk += (kk == kKeyProt || (key_free(kk) && kk > hi)) ? 1 : 0;
+          const bool inb = key_free(kk) && kk >= lo && kk <= hi;
+          const unsigned long long m = __ballot(inb);
+          int base = 0;
+          if (m && lane == 0) base = atomicAdd(&ctrl[qCand], __popcll(m));
+          base = __shfl(base, 0, 64);
+          const int slot = base + lanes_below(m);
+          if (inb && slot < kCandMax) {
+            gc[2 * slot] = kk;
+            gc[2 * slot + 1] = (uint32_t)(t_base + 64 * u);
+          }
+        }
+        nk = wave_sum(nk);
+        __syncthreads();
+        if (lane == 0) wa[wave] = nk;
+        __syncthreads();
+        if (tid == 0) {
+          int tk = 0;
+          for (int w = 0; w < kQW; ++w) tk += wa[w];
+          ctrl[qCounts + 2 * cb] = tk;
+        }
+        target += C;
+        ok = seq_barrier(ctrl, target, &s_ok);
+        if (ok) {
+          const int M = min(ld_agent(&ctrl[qCand]), kCandMax);
+          for (int i = tid; i < M; i += kQT) {
+            sCk[i] = __hip_atomic_load(&gc[2 * i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            sCi[i] = (int)__hip_atomic_load(&gc[2 * i + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+          if (tid < 3) s_cnt[tid] = 0;
+          // the same narrowing as the grid passes, on the list in LDS
+          while (lo != hi) {
+            const uint32_t range = hi - lo;
+            const int shift = max(0, 32 - __clz((int)range) - 11);
+            for (int i = tid; i < kSelBins; i += kQT) hist[i] = 0u;
+            __syncthreads();
+            for (int i = tid; i < M; i += kQT) {
+              const uint32_t kk = sCk[i];
+              if (kk >= lo && kk <= hi) atomicAdd(&hist[(kk - lo) >> shift], 1u);
+            }
+            __syncthreads();
+            const int g = kQT - 1 - tid;
+            int h[8], sum = 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              h[j] = (int)hist[8 * g + j];
+              sum += h[j];
+            }
+            int total;
+            int above = block_scan<kQT>(sum, tmp, total);
+#pragma unroll
+            for (int j = 7; j >= 0; --j) {
+              if (above < need && above + h[j] >= need) {
+                const uint32_t nlo = lo + ((uint32_t)(8 * g + j) << shift);
+                const uint32_t width = (1u << shift) - 1u;
+                s_lo = nlo;
+                s_hi = min(hi, nlo + min(width, 0xFFFFFFFFu - nlo));
+                s_need = need - above;
+              }
+              above += h[j];
+            }
+            __syncthreads();
+            lo = s_lo;
+            hi = s_hi;
+            need = s_need;
+          }
+          T = lo;                        // the need-th largest key; need ties at T are kept
+          need_eq = need;
+          // what the chunks before this one hold of the listed keys
+          for (int i = tid; i < M; i += kQT) {
+            if (sCi[i] >= c0) continue;
+            if (sCk[i] > T) atomicAdd(&s_cnt[1], 1);
+            else if (sCk[i] == T) atomicAdd(&s_cnt[2], 1);
+          }
+          __syncthreads();
+          k_before = s_cnt[1];
+          e_before = s_cnt[2];
+          for (int q = 0; q < cb; ++q) k_before += ld_agent(&ctrl[qCounts + 2 * q]);
+        }
+      } else {
+        T = lo;                          // lo == hi: the need-th largest key
+        need_eq = need;
+      }
     }
     if (ok) {
-      // per-chunk counts of kept tokens and of ties at T
+      // per-wave counts of kept tokens and of ties at T
       int nk = 0, ne = 0;
 #pragma unroll
       for (int u = 0; u < kQKPT; ++u) {
@@ -722,22 +826,25 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
       __syncthreads();
       if (lane == 0) { wa[wave] = nk; wb[wave] = ne; }
       __syncthreads();
-      if (tid == 0) {
-        int tk = 0, te = 0;
-        for (int w = 0; w < kQW; ++w) { tk += wa[w]; te += wb[w]; }
-        ctrl[qCounts + 2 * cb] = tk;
-        ctrl[qCounts + 2 * cb + 1] = te;
+      if (!listed) {
+        // the chunks' totals, exchanged through the control words
+        if (tid == 0) {
+          int tk = 0, te = 0;
+          for (int w = 0; w < kQW; ++w) { tk += wa[w]; te += wb[w]; }
+          ctrl[qCounts + 2 * cb] = tk;
+          ctrl[qCounts + 2 * cb + 1] = te;
+        }
+        target += C;
+        ok = seq_barrier(ctrl, target, &s_ok);
+        if (ok)
+          for (int q = 0; q < cb; ++q) {
+            k_before += ld_agent(&ctrl[qCounts + 2 * q]);
+            e_before += ld_agent(&ctrl[qCounts + 2 * q + 1]);
+          }
       }
-      target += C;
-      ok = seq_barrier(ctrl, target, &s_ok);
     }
     if (ok) {
       // offsets from the chunks before this one and the waves before this one
-      int k_before = 0, e_before = 0;
-      for (int q = 0; q < cb; ++q) {
-        k_before += ld_agent(&ctrl[qCounts + 2 * q]);
-        e_before += ld_agent(&ctrl[qCounts + 2 * q + 1]);
-      }
       for (int w = 0; w < wave; ++w) { k_before += wa[w]; e_before += wb[w]; }
       int out = k_before + min(need_eq, e_before), eq_run = e_before;
 #pragma unroll
