@@ -428,7 +428,7 @@ extern "C" int ckv_create(ckv_ctx** out, int device, void* hip_stream) {
 extern "C" int ckv_destroy(ckv_ctx* c) {
   if (!c) return CKV_ERR_ARG;
   {
-    DeviceGuard g(c->device);
+    DeviceGuard g(c->device);   // best effort: the context is freed whatever happens
     (void)hipStreamSynchronize(c->stream);
     if (c->ws) (void)hipFree(c->ws);
     if (c->sel_ctrl) (void)hipFree(c->sel_ctrl);
@@ -452,6 +452,7 @@ extern "C" int ckv_destroy(ckv_ctx* c) {
 extern "C" int ckv_set_stream(ckv_ctx* c, void* hip_stream) {
   if (!c) return CKV_ERR_ARG;
   DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
   CKV_HIP(c, hipStreamSynchronize(c->stream));
   c->stream = static_cast<hipStream_t>(hip_stream);
   return CKV_OK;
@@ -460,6 +461,7 @@ extern "C" int ckv_set_stream(ckv_ctx* c, void* hip_stream) {
 extern "C" int ckv_sync(ckv_ctx* c) {
   if (!c) return CKV_ERR_ARG;
   DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
   CKV_HIP(c, hipStreamSynchronize(c->stream));
   return CKV_OK;
 }
@@ -498,6 +500,7 @@ extern "C" int ckv_set_kernel_timing_only(ckv_ctx* c, const char* name) {
 extern "C" int ckv_set_kernel_timing(ckv_ctx* c, int enable) {
   if (!c) return CKV_ERR_ARG;
   DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
   int rc = resolve_timings(c);
   if (rc) return rc;
   c->timing = enable != 0;
@@ -508,6 +511,7 @@ extern "C" int ckv_kernel_stats(ckv_ctx* c, int32_t idx, const char** name, doub
                                 int64_t* launches) {
   if (!c) return CKV_ERR_ARG;
   DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
   int rc = resolve_timings(c);
   if (rc) return rc;
   if (idx < 0 || idx >= (int32_t)c->knames.size()) return CKV_ERR_ARG;
@@ -520,6 +524,7 @@ extern "C" int ckv_kernel_stats(ckv_ctx* c, int32_t idx, const char** name, doub
 extern "C" int ckv_reset_kernel_stats(ckv_ctx* c) {
   if (!c) return CKV_ERR_ARG;
   DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
   int rc = resolve_timings(c);
   if (rc) return rc;
   std::fill(c->ktotal.begin(), c->ktotal.end(), 0.0);
@@ -727,6 +732,7 @@ extern "C" int ckv_classify_pages(ckv_ctx* c, int32_t n, const float* R_pre, con
   if (!(t.tau_dead <= t.tau_use) || !(t.rho_dead <= t.rho_use))
     return fail(c, CKV_ERR_ARG, "thresholds must satisfy tau_dead <= tau_use and rho_dead <= rho_use");
   DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
   ClassifyArgs a{};
   a.n = n;
   a.R_pre = R_pre;
@@ -767,6 +773,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   if (max_cand < 1) return fail(c, CKV_ERR_SHAPE, "max_cand must be >= 1");
   if (!std::isfinite(tau_joint)) return fail(c, CKV_ERR_ARG, "tau_joint must be finite");
   DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
   const AttnGeom a = make_geom(kv, win);
   const int total_rows = a.Hq * a.W, D = a.D;
   // the residual pass reads the caller's o and natural-log lse directly
@@ -946,6 +953,7 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   if (overlap(out->k, eo, out->v, eo)) return fail(c, CKV_ERR_ARG, "output K and V overlap");
   }
   DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
 
   // Sec. 4.4 variants: without transition protection no pending page is
   // protected; without the lifecycle mechanism nothing is retired either
