@@ -101,3 +101,60 @@ def test_protect_skip_instead_of_stop_is_caught(monkeypatch):
     monkeypatch.setattr(OM, "protect_pending", mutant)
     got = OM.protect_pending([0, 4, 8, 10, 14], [4, 4, 2, 4, 1], [0.5, 0.9, 0.7, 0.7, 0.1], 64)
     assert not np.array_equal(got, [1, 2])
+
+
+# ---------------------------------------------------------------- lifecycle driver (Algorithm 1)
+def test_driver_scan_cap_oldest_is_caught(monkeypatch):
+    """Mutant: the scan cap keeps the oldest pages instead of the newest."""
+    import oracle.lifecycle as OL
+    from tests.test_oracle_lifecycle import CALL, OBS, _push
+    real = OL.Agent.eligible
+
+    def mutant(self):
+        cap, self.max_scan = self.max_scan, 0
+        pages = real(self)
+        self.max_scan = cap
+        return pages[:cap]
+    monkeypatch.setattr(OL.Agent, "eligible", mutant)
+    a = OL.Agent(1, 1, 2, page_size=4, budget=1000, max_scan_pages=2)
+    p = _push(a, CALL, 0, [[0, 0]] * 12, [[1, 0]] * 12)
+    _push(a, OBS, p, [[0, 0]] * 6, [[1, 0]] * 6)
+    assert a.eligible() != [(12, 4), (16, 2)]
+
+
+def test_driver_checkpoint_keeping_retired_is_caught(monkeypatch):
+    """Mutant: a checkpoint under the budget skips compaction even though a
+    retired page is resident (the hand-built page then stays)."""
+    import math
+    import oracle.lifecycle as OL
+    from tests.test_oracle_lifecycle import _hand_episode
+    real = OL.Agent.checkpoint
+
+    def mutant(self, Q, qpos, score=None):
+        if self.pos.size <= self.B:
+            return dict(compacted=False)
+        return real(self, Q, qpos, score)
+    monkeypatch.setattr(OL.Agent, "checkpoint", mutant)
+    a, _ = _hand_episode()
+    q_post = np.array([[[-2000 * math.sqrt(2.0)] * 2] * 2])
+    a.post(q_post, np.array([48, 49]))
+    a.checkpoint(q_post, np.array([48, 49]))
+    assert np.isin(np.arange(16, 20), a.pos).any()      # the pin's expectation fails
+
+
+def test_driver_protecting_partial_pages_is_caught(monkeypatch):
+    """Mutant: pending pages that lost tokens are still offered for protection."""
+    import oracle.lifecycle as OL
+    from tests.test_oracle_lifecycle import _hand_episode
+
+    def mutant(self):
+        pend, r = list(self.pending[0]), np.asarray(self.pending[1], np.float64)
+        return pend, r, []
+    monkeypatch.setattr(OL.Agent, "checkpoint_lists", mutant)
+    a, rep = _hand_episode()
+    a.B = 32
+    score = np.zeros(a.pos.size, np.float32)
+    score[:32] = 1.0
+    a.checkpoint(None, None, score=score)
+    lost = [p for p in rep["pages"] if not a.fully_resident(p)]
+    assert any(p in a.checkpoint_lists()[0] for p in lost)
