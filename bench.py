@@ -29,7 +29,10 @@ outputs (ckv_measure_recorded); ``paged`` the measurement over a paged pool;
 tokens through the batched call.  ``agent`` runs whole synthetic agent episodes of a 36-layer stack
 through the lifecycle driver (Algorithm 1) and reports the driver's time per
 commit, post-commit step and checkpoint; ``agent_paper_point`` does the same
-at the paper's operating point (W 8, G 16, budget 4096, 40 layers).
+at the paper's operating point (W 8, G 16, budget 4096, 40 layers), and
+``agent_paged`` runs the first workload's episodes with a paged agent (pool
+rows in scattered order; a checkpoint re-indexes the slot table instead of
+moving keys and values).
 """
 from __future__ import annotations
 
@@ -310,7 +313,7 @@ def stack_leg(steps):
                 ms_per_step=ms, tokens_per_s=tokens / (ms / 1e3), tokens_per_step=tokens)
 
 
-def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped"):
+def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped", paged=False):
     """Whole agent episodes through the lifecycle driver (ckv_agent_*), one
     driver per episode: by default the Qwen3-8B-shaped stack (36 layers, 32
     query / 8 KV heads, d 128), budget 16384, 64-row windows, 32-token pages;
@@ -320,7 +323,9 @@ def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped"):
     token's keys and values, drawing window queries) is synthetic torch work
     outside the timed calls; every commit, post and checkpoint is timed on
     the host around the call (each returns after the context's stream has
-    finished it)."""
+    finished it).  ``paged``: the agent scores one layer's pool through its
+    slot table, and a checkpoint selects and re-indexes the table (the
+    engine's per-layer pools stay where they are)."""
     import torch
 
     import paper_2608_07855_amd as P
@@ -332,21 +337,26 @@ def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped"):
     t = dict(commit=0.0, post=0.0, checkpoint=0.0)
     n = dict(commit=0, post=0, checkpoint=0, compacted=0)
     moved, turns, tokens = 0, [], 0
+    # a paged agent holds only the scoring layer's pool: the other layers'
+    # pools are the engine's and the driver never touches them
+    L_alloc = 1 if paged else L
     for s in range(n_seq):
         traj = make_trajectory(cfg, seed=0, seq=s)
         turns.append(sum(1 for e in traj.events if e[0] == 0))
         tokens += traj.n_tokens
-        ag = P.Agent(ctx, L, Hkv, d, cfg.capacity, page_size=cfg.page_size, window=W, n_q_heads=Hq,
+        extra = dict(paged=True, pool_rows=cfg.capacity + 4096, row_seed=s) if paged else {}
+        ag = P.Agent(ctx, L_alloc, Hkv, d, cfg.capacity, page_size=cfg.page_size, window=W, n_q_heads=Hq,
                      budget=cfg.budget, eta=cfg.eta, max_pending_pages=cfg.max_pending_pages,
                      keep_recent=cfg.keep_recent, max_scan_pages=cfg.max_scan_pages,
-                     checkpoint_every=cfg.checkpoint_every, score_layer=cfg.score_layer)
+                     checkpoint_every=cfg.checkpoint_every, score_layer=0 if paged else cfg.score_layer,
+                     **extra)
         g = torch.Generator(device="cuda")
         g.manual_seed(1000 + s)
         for act in schedule(traj):
             if act[0] == "append":
                 _, kind, p0, p1, dec, first = act
-                k = torch.randn((L, Hkv, p1 - p0, d), generator=g, device="cuda").to(torch.bfloat16)
-                v = torch.randn((L, Hkv, p1 - p0, d), generator=g, device="cuda").to(torch.bfloat16)
+                k = torch.randn((L_alloc, Hkv, p1 - p0, d), generator=g, device="cuda").to(torch.bfloat16)
+                v = torch.randn((L_alloc, Hkv, p1 - p0, d), generator=g, device="cuda").to(torch.bfloat16)
                 ag.append(kind, k, v, np.arange(p0, p1), dec, first)
                 continue
             q = torch.randn((Hq, W, d), generator=g, device="cuda").to(torch.bfloat16)
@@ -360,7 +370,8 @@ def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped"):
             n[act[0]] += 1
             if act[0] == "checkpoint" and r["compacted"]:
                 n["compacted"] += 1
-                moved += len(r["kept"]) * (L * Hkv * d * 2 * 2 * 2 + 4 * 2)
+                if not paged:
+                    moved += len(r["kept"]) * (L * Hkv * d * 2 * 2 * 2 + 4 * 2)
         ag.close()
     ctx.close()
     total = sum(t.values())
@@ -368,12 +379,13 @@ def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped"):
     return dict(
         workload=f"{shape} stack, {L} layers (Hq {Hq}, Hkv {Hkv}, d {d}), {n_seq} agent episodes "
                  f"of {cfg.turns_lo}-{cfg.turns_hi} turns, budget {cfg.budget}, {W}-row windows, "
-                 f"{cfg.page_size}-token pages, a checkpoint every {cfg.checkpoint_every} decoded tokens",
+                 f"{cfg.page_size}-token pages, a checkpoint every {cfg.checkpoint_every} decoded tokens"
+                 + (", paged agent (pool rows in scattered order)" if paged else ""),
         turns=turns, tokens=tokens, driver_seconds=total, tokens_per_s=tokens / total if total else None,
         commits=n["commit"], posts=n["post"], checkpoints=n["checkpoint"], compactions=n["compacted"],
         ms_per_commit=1e3 * t["commit"] / max(n["commit"], 1), ms_per_post=1e3 * t["post"] / max(n["post"], 1),
         ms_per_checkpoint=1e3 * t["checkpoint"] / max(n["checkpoint"], 1),
-        compaction_GBps=moved / t["checkpoint"] / 1e9 if t["checkpoint"] > 0 else None)
+        compaction_GBps=moved / t["checkpoint"] / 1e9 if t["checkpoint"] > 0 and not paged else None)
 
 
 def kernel_work(w, L, name, launches_per_step):
@@ -536,6 +548,7 @@ def main():
     stack = None if args.no_stack else stack_leg(3)
     agent = None if args.no_agent else agent_leg(args.agent_seqs)
     agent_paper = None if args.no_agent else agent_leg(2, "paper_agent", "qwen3-14b-shaped, paper operating point")
+    agent_paged = None if args.no_agent else agent_leg(args.agent_seqs, paged=True)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, L, args.cpu_seconds)
@@ -562,6 +575,7 @@ def main():
         stack=stack,
         agent=agent,
         agent_paper_point=agent_paper,
+        agent_paged=agent_paged,
     )
     print(json.dumps(res), flush=True)
 

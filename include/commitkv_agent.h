@@ -93,6 +93,22 @@ typedef struct ckv_agent_config {
 int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* buf0, const ckv_cache_view* buf1,
                      const ckv_agent_config* cfg, ckv_agent** out);
 
+/* Create an agent over a paged cache (vLLM-style block pool; CommitKV's
+ * Eq. (4) index set then moves no key or value).  pool: the scoring layer's
+ * pool, with k, v, n_kv_heads, head_dim, head_stride, tok_stride and
+ * pool_rows set (pos, n_tokens and slot are ignored); the caller owns the
+ * pool of every layer and writes each token's keys and values into the row
+ * it reports with ckv_agent_append_rows.  capacity: the most tokens the
+ * sequence holds at once (budget <= capacity <= pool_rows).  The agent keeps
+ * the slot table (pool row of every resident token, in position order) and
+ * the positions on the device, double-buffered; a checkpoint selects I_j
+ * (Eq. (12)-(13)) and gathers both tables through I_j, and the rows of the
+ * tokens it drops are returned by ckv_agent_rows(which = 1).  cfg's
+ * score_layer is not used (the pool is the scoring layer's; it must be
+ * >= 0).  Errors as ckv_agent_create. */
+int ckv_agent_create_paged(ckv_ctx* ctx, const ckv_kv_view* pool, int32_t capacity,
+                           const ckv_agent_config* cfg, ckv_agent** out);
+
 /* Free the agent's buffers (after waiting for the context's stream). */
 int ckv_agent_destroy(ckv_agent* agent);
 
@@ -111,6 +127,15 @@ int ckv_agent_destroy(ckv_agent* agent);
  * CKV_ERR_ARG for bad positions or kind. */
 int ckv_agent_append(ckv_agent* agent, int32_t kind, const int32_t* pos, int32_t n,
                      int32_t decoded, int32_t begins_event, int32_t* due);
+
+/* The paged form of ckv_agent_append: rows: HOST int32[n], the pool rows
+ * holding the n tokens (in [0, pool_rows); the caller allocates them and
+ * must not reuse a row before a checkpoint frees it).  The slot table and
+ * positions are copied to the device on the context's stream.  Errors as
+ * ckv_agent_append, and CKV_ERR_ARG for a row outside the pool or an agent
+ * created with ckv_agent_create. */
+int ckv_agent_append_rows(ckv_agent* agent, int32_t kind, const int32_t* pos, const int32_t* rows,
+                          int32_t n, int32_t decoded, int32_t begins_event, int32_t* due);
 
 /* Commit at the end of a tool call (Algorithm 1): E_c is formed and R^- is
  * measured over the window q_pre (Eq. (5)-(8)); the pages become pending. */
@@ -160,6 +185,14 @@ int ckv_agent_last_report(const ckv_agent* agent, ckv_agent_report* out);
  * At most cap entries are written; *n receives the list's length. */
 int ckv_agent_pages(const ckv_agent* agent, int32_t which, int32_t* start, int32_t* len,
                     float* value, int32_t cap, int32_t* n);
+
+/* Host copies of per-token lists: which = 0, the pool rows of the resident
+ * tokens in position order, and which = 1, the rows the last checkpoint
+ * released (empty if it compacted nothing), both for paged agents only
+ * (CKV_ERR_ARG otherwise); which = 2, the positions of the resident tokens
+ * (any agent).  At most cap entries are written; *n receives the list's
+ * length. */
+int ckv_agent_rows(const ckv_agent* agent, int32_t which, int32_t* rows, int32_t cap, int32_t* n);
 
 #ifdef __cplusplus
 }

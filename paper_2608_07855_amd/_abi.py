@@ -173,6 +173,11 @@ SIGNATURES = {
     "ckv_agent_last_report": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(AgentReport)]),
     "ckv_agent_pages": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, c_i32p, c_f32p,
                                        ctypes.c_int32, c_i32p]),
+    "ckv_agent_create_paged": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(KVView), ctypes.c_int32,
+                                              ctypes.POINTER(AgentConfig), ctypes.POINTER(ctypes.c_void_p)]),
+    "ckv_agent_append_rows": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, c_i32p, ctypes.c_int32,
+                                             ctypes.c_int32, ctypes.c_int32, c_i32p]),
+    "ckv_agent_rows": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, c_i32p, ctypes.c_int32, c_i32p]),
 }
 
 _lib = None

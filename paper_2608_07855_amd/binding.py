@@ -406,26 +406,33 @@ def _np(ptr, n, dtype):
 
 class Agent:
     """The lifecycle driver of one agent episode (include/commitkv_agent.h,
-    Algorithm 1) over two cache buffers this object allocates:
-    k, v [1, n_layers, Hkv, capacity, d] bf16 and pos [1, capacity] int32.
+    Algorithm 1).
 
-    ``append`` places the new tokens' keys, values and positions in the
-    current buffer (a device copy) and reports them; ``commit``, ``post`` and
-    ``checkpoint`` take the window's queries [Hq, W, d] (bf16, device) and
-    positions (int32, device) and return the call's report as NumPy arrays."""
+    Contiguous (default): two cache buffers this object allocates,
+    k, v [1, n_layers, Hkv, capacity, d] bf16 and pos [1, capacity] int32; a
+    checkpoint compacts the cache into the other buffer.
+    Paged (``paged=True``): one pool per layer, kp, vp [n_layers, Hkv,
+    pool_rows, d] bf16 (``pool_rows`` defaults to the capacity), and a free
+    list of rows standing in for a serving engine's block allocator; a
+    checkpoint only re-indexes the agent's slot table and returns the rows of
+    the dropped tokens to the free list.  ``row_seed`` shuffles the free list
+    so that consecutive tokens land in scattered rows.
+
+    ``append`` places the new tokens' keys, values and positions (a device
+    copy) and reports them; ``commit``, ``post`` and ``checkpoint`` take the
+    window's queries [Hq, W, d] (bf16, device) and positions (int32, device)
+    and return the call's report as NumPy arrays."""
 
     def __init__(self, ctx: Context, n_layers: int, n_kv_heads: int, head_dim: int, capacity: int, *,
                  page_size: int, window: int, n_q_heads: int, budget: int, eta: float = 0.125,
                  max_pending_pages: int = 16, keep_recent: int = 0, max_scan_pages: int = 64,
                  checkpoint_every: int = 128, score_layer: int = 0, thresholds: dict | None = None,
-                 report_detail: bool = False, pool_kernel: int = 0, pool_mode: str = "max"):
+                 report_detail: bool = False, pool_kernel: int = 0, pool_mode: str = "max",
+                 paged: bool = False, pool_rows: int | None = None, row_seed: int | None = None):
         self.ctx = ctx
+        self.paged = bool(paged)
+        self.handle = None
         dev = torch.device("cuda", ctx.device)
-        shape = (1, n_layers, n_kv_heads, capacity, head_dim)
-        self.k = [torch.zeros(shape, dtype=torch.bfloat16, device=dev) for _ in range(2)]
-        self.v = [torch.zeros(shape, dtype=torch.bfloat16, device=dev) for _ in range(2)]
-        self.pos = [torch.zeros((1, capacity), dtype=torch.int32, device=dev) for _ in range(2)]
-        self._views = [cache_view(self.k[i], self.v[i], self.pos[i]) for i in range(2)]
         th = dict(PAPER_THRESHOLDS)
         th.update(thresholds or {})
         cfg = _abi.AgentConfig(page_size, window, n_q_heads, max_scan_pages, checkpoint_every,
@@ -433,8 +440,28 @@ class Agent:
                                Budget(budget, eta, max_pending_pages, keep_recent), int(pool_kernel),
                                {"max": _abi.POOL_MAX, "mean": _abi.POOL_MEAN}[pool_mode])
         h = ctypes.c_void_p()
-        ctx.check(lib().ckv_agent_create(ctx.handle, ctypes.byref(self._views[0]),
-                                         ctypes.byref(self._views[1]), ctypes.byref(cfg), ctypes.byref(h)))
+        if self.paged:
+            rows = capacity if pool_rows is None else int(pool_rows)
+            shape = (n_layers, n_kv_heads, rows, head_dim)
+            self.kp = torch.zeros(shape, dtype=torch.bfloat16, device=dev)
+            self.vp = torch.zeros(shape, dtype=torch.bfloat16, device=dev)
+            order = np.arange(rows)
+            if row_seed is not None:
+                order = np.random.default_rng(row_seed).permutation(rows)
+            self.free = [int(r) for r in order[::-1]]      # pop() takes the next row
+            kl, vl = self.kp[score_layer], self.vp[score_layer]
+            self._pool = _abi.KVView(kl.data_ptr(), vl.data_ptr(), kl.stride(0), kl.stride(1), None, 0,
+                                     n_kv_heads, head_dim, None, rows)
+            ctx.check(lib().ckv_agent_create_paged(ctx.handle, ctypes.byref(self._pool), int(capacity),
+                                                   ctypes.byref(cfg), ctypes.byref(h)))
+        else:
+            shape = (1, n_layers, n_kv_heads, capacity, head_dim)
+            self.k = [torch.zeros(shape, dtype=torch.bfloat16, device=dev) for _ in range(2)]
+            self.v = [torch.zeros(shape, dtype=torch.bfloat16, device=dev) for _ in range(2)]
+            self.pos = [torch.zeros((1, capacity), dtype=torch.int32, device=dev) for _ in range(2)]
+            self._views = [cache_view(self.k[i], self.v[i], self.pos[i]) for i in range(2)]
+            ctx.check(lib().ckv_agent_create(ctx.handle, ctypes.byref(self._views[0]),
+                                             ctypes.byref(self._views[1]), ctypes.byref(cfg), ctypes.byref(h)))
         self.handle = h
 
     def state(self):
@@ -442,9 +469,25 @@ class Agent:
         self.ctx.check(lib().ckv_agent_state(self.handle, ctypes.byref(n), ctypes.byref(cur), ctypes.byref(dec)))
         return n.value, cur.value, dec.value
 
+    def rows(self, which: str = "resident") -> np.ndarray:
+        """"resident": pool rows of the resident tokens (paged); "freed": rows
+        the last checkpoint released (paged); "pos": resident positions."""
+        w = {"resident": 0, "freed": 1, "pos": 2}[which]
+        n = ctypes.c_int32()
+        self.ctx.check(lib().ckv_agent_rows(self.handle, w, None, 0, ctypes.byref(n)))
+        out = np.zeros(max(n.value, 1), np.int32)
+        self.ctx.check(lib().ckv_agent_rows(self.handle, w, out.ctypes.data_as(_abi.c_i32p), n.value,
+                                            ctypes.byref(n)))
+        return out[:n.value]
+
     def cache(self):
-        """(k, v, pos, n_resident) of the buffer holding the cache."""
+        """(k, v, pos, n_resident): k, v [n_layers, Hkv, >= n, d]; for a paged
+        agent a gathered copy of the resident rows."""
         n, cur, _ = self.state()
+        if self.paged:
+            idx = torch.from_numpy(self.rows("resident").astype(np.int64)).to(self.kp.device)
+            pos = torch.from_numpy(self.rows("pos")).to(self.kp.device)
+            return self.kp[:, :, idx], self.vp[:, :, idx], pos, n
         return self.k[cur][0], self.v[cur][0], self.pos[cur][0], n
 
     def append(self, kind: int, k, v, pos, decoded: bool, begins_event: bool = True) -> int:
@@ -453,13 +496,29 @@ class Agent:
         pos = np.ascontiguousarray(pos, dtype=np.int32)
         n_tok = int(pos.size)
         n, cur, _ = self.state()
+        due = ctypes.c_int32()
+        if self.paged:
+            if n_tok > len(self.free):
+                raise CKVError(_abi.CKV_ERR_SHAPE, "pool has no free rows left")
+            rows = np.array([self.free.pop() for _ in range(n_tok)], np.int32)
+            if n_tok:
+                idx = torch.from_numpy(rows.astype(np.int64)).to(self.kp.device)
+                self.kp.index_copy_(2, idx, k)
+                self.vp.index_copy_(2, idx, v)
+            try:
+                self.ctx.check(lib().ckv_agent_append_rows(
+                    self.handle, int(kind), pos.ctypes.data_as(_abi.c_i32p), rows.ctypes.data_as(_abi.c_i32p),
+                    n_tok, int(bool(decoded)), int(bool(begins_event)), ctypes.byref(due)))
+            except CKVError:
+                self.free.extend(rows[::-1].tolist())
+                raise
+            return due.value
         if n + n_tok > self.k[cur].shape[3]:
             raise CKVError(_abi.CKV_ERR_SHAPE, "cache buffer capacity exceeded")
         if n_tok:
             self.k[cur][0, :, :, n:n + n_tok].copy_(k)
             self.v[cur][0, :, :, n:n + n_tok].copy_(v)
             self.pos[cur][0, n:n + n_tok].copy_(torch.from_numpy(pos))
-        due = ctypes.c_int32()
         self.ctx.check(lib().ckv_agent_append(self.handle, int(kind), pos.ctypes.data_as(_abi.c_i32p), n_tok,
                                               int(bool(decoded)), int(bool(begins_event)), ctypes.byref(due)))
         return due.value
@@ -478,6 +537,8 @@ class Agent:
         w = window_view(q, qpos)
         c = ctypes.c_int32()
         self.ctx.check(lib().ckv_agent_checkpoint(self.handle, ctypes.byref(w), ctypes.byref(c)))
+        if self.paged and c.value:
+            self.free.extend(self.rows("freed").tolist())
         return self.report()
 
     def report(self) -> dict:

@@ -48,11 +48,30 @@ bool pageable(int32_t kind) { return kind == CKV_EVENT_TOOL_CALL || kind == CKV_
 
 }  // namespace
 
+// paged agents: the slot table and the positions follow a checkpoint's
+// index set, rows[j] = rows_in[I[j]], pos[j] = pos_in[I[j]]
+__global__ void gather_rows_kernel(const int32_t* rows_in, const int32_t* pos_in, const int32_t* kept, int n,
+                                   int32_t* rows_out, int32_t* pos_out) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j < n) {
+    const int i = kept[j];
+    rows_out[j] = rows_in[i];
+    pos_out[j] = pos_in[i];
+  }
+}
+
 struct ckv_agent {
   ckv_ctx* ctx = nullptr;
   ckv_cache_view buf[2];
   ckv_agent_config cfg;
   int cur = 0;
+  int capacity = 0;                  // token slots
+  bool paged = false;
+  ckv_kv_view pool{};                // paged: the scoring layer's pool
+  int32_t *d_rows[2] = {nullptr, nullptr}, *d_pos[2] = {nullptr, nullptr};   // paged, by resident index
+  int32_t *up_pos = nullptr, *up_rows = nullptr;   // paged: pinned staging, by resident index
+  std::vector<int32_t> rows;         // paged: pool row of each resident token
+  std::vector<int32_t> freed;        // paged: rows released by the last checkpoint
   std::vector<int32_t> res;          // resident positions, ascending
   std::vector<Event> events;
   int64_t decoded = 0;
@@ -99,6 +118,13 @@ struct ckv_agent {
   }
 
   ckv_kv_view layer_view() const {
+    if (paged) {
+      ckv_kv_view kv = pool;
+      kv.pos = d_pos[cur];
+      kv.n_tokens = n_res();
+      kv.slot = d_rows[cur];
+      return kv;
+    }
     const ckv_cache_view& b = buf[cur];
     ckv_kv_view kv;
     kv.k = b.k + (int64_t)cfg.score_layer * b.layer_stride;
@@ -185,59 +211,52 @@ struct ckv_agent {
   }
 };
 
-extern "C" int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* b0, const ckv_cache_view* b1,
-                                const ckv_agent_config* cfg, ckv_agent** out) {
-  if (!ctx) return CKV_ERR_ARG;
-  if (!b0 || !b1 || !cfg || !out) return ctx_fail(ctx, CKV_ERR_ARG, "agent: NULL argument");
-  *out = nullptr;
-  for (const ckv_cache_view* b : {b0, b1})
-    if (!b->k || !b->v || !b->pos) return ctx_fail(ctx, CKV_ERR_ARG, "agent: cache buffer with a NULL pointer");
-  if (b0->n_seq != 1 || b1->n_seq != 1) return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: cache buffers hold one sequence");
-  if (b0->n_layers != b1->n_layers || b0->n_kv_heads != b1->n_kv_heads || b0->head_dim != b1->head_dim ||
-      b0->capacity != b1->capacity || b0->n_layers < 1)
-    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: the two cache buffers differ in geometry");
+namespace {
+
+// configuration checks shared by both forms of the agent
+int check_config(ckv_ctx* ctx, const ckv_agent_config* cfg, int n_kv_heads, int n_layers, int capacity) {
   const ckv_budget& bg = cfg->budget;
   if (cfg->page_size < 1 || cfg->page_size > CKV_MAX_PAGE_LEN)
     return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: page_size %d not in [1, %d]", cfg->page_size, CKV_MAX_PAGE_LEN);
-  if (cfg->window < 1 || cfg->n_q_heads < 1 || cfg->n_q_heads % b0->n_kv_heads)
+  if (cfg->window < 1 || cfg->n_q_heads < 1 || cfg->n_q_heads % n_kv_heads)
     return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: bad window rows or query heads");
   if (cfg->max_scan_pages < 1 || cfg->max_scan_pages > 4096)
     return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: max_scan_pages %d not in [1, 4096]", cfg->max_scan_pages);
   if (cfg->checkpoint_every < 1) return ctx_fail(ctx, CKV_ERR_ARG, "agent: checkpoint_every must be >= 1");
-  if (cfg->score_layer < 0 || cfg->score_layer >= b0->n_layers)
-    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: score_layer %d outside [0, %d)", cfg->score_layer, b0->n_layers);
+  if (cfg->score_layer < 0 || cfg->score_layer >= n_layers)
+    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: score_layer %d outside [0, %d)", cfg->score_layer, n_layers);
   if (cfg->pool_kernel < 0 || cfg->pool_kernel > 255 || (cfg->pool_kernel > 1 && cfg->pool_kernel % 2 == 0) ||
       (cfg->pool_mode != CKV_POOL_MAX && cfg->pool_mode != CKV_POOL_MEAN))
     return ctx_fail(ctx, CKV_ERR_ARG, "agent: pool_kernel must be 0 or odd <= 255, pool_mode max or mean");
-  if (bg.budget < 1 || bg.budget > b0->capacity || !(bg.eta >= 0.f && bg.eta <= 1.f) || bg.keep_recent < 0 ||
+  if (bg.budget < 1 || bg.budget > capacity || !(bg.eta >= 0.f && bg.eta <= 1.f) || bg.keep_recent < 0 ||
       bg.max_pending_pages < 0)
     return ctx_fail(ctx, CKV_ERR_ARG, "agent: bad budget (B must fit the capacity)");
   if ((int64_t)std::floor((double)bg.eta * bg.budget) + bg.keep_recent > bg.budget)
     return ctx_fail(ctx, CKV_ERR_BUDGET, "agent: keep_recent + B_N exceeds B");
+  return CKV_OK;
+}
 
-  ckv_agent* a = new (std::nothrow) ckv_agent();
-  if (!a) return ctx_fail(ctx, CKV_ERR_NOMEM, "agent: host allocation failed");
-  a->ctx = ctx;
-  a->buf[0] = *b0;
-  a->buf[1] = *b1;
-  a->cfg = *cfg;
+// device buffers and pinned staging (one allocation each)
+int alloc_agent(ckv_agent* a, int head_dim) {
+  ckv_ctx* ctx = a->ctx;
+  const ckv_agent_config* cfg = &a->cfg;
   const size_t M = (size_t)cfg->max_scan_pages;
   const size_t rows = (size_t)cfg->n_q_heads * cfg->window;
-  const size_t cap = (size_t)b0->capacity, B = (size_t)bg.budget;
-  // device layout
+  const size_t cap = (size_t)a->capacity, B = (size_t)cfg->budget.budget;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off += align256(std::max<size_t>(bytes, 1)); return o; };
   const size_t o_rpre = take(M * 4), o_rsub = take(M * 4), o_rpost = take(M * 4), o_union = take(M * 4);
-  const size_t o_o = take(rows * b0->head_dim * 4), o_lse = take(rows * 4), o_score = take(cap * 4);
+  const size_t o_o = take(rows * head_dim * 4), o_lse = take(rows * 4), o_score = take(cap * 4);
   const size_t o_pooled = take(cap * 4);
   const size_t o_lam = take(M), o_acc = take(M), o_cand = take(M * 4), o_cnt = take(16), o_kept = take(B * 4);
+  size_t o_tab[4] = {0, 0, 0, 0};
+  if (a->paged)
+    for (int i = 0; i < 4; ++i) o_tab[i] = take(cap * 4);
   DevGuard g(ckv::ctx_device(ctx));
-  if (!g.ok) {
-    delete a;
-    return ctx_fail(ctx, CKV_ERR_HIP, "agent: cannot select the context's device");
-  }
+  if (!g.ok) return ctx_fail(ctx, CKV_ERR_HIP, "agent: cannot select the context's device");
   if (hipMalloc((void**)&a->dev, off) != hipSuccess) {
-    delete a;
+    (void)hipGetLastError();
+    a->dev = nullptr;
     return ctx_fail(ctx, CKV_ERR_NOMEM, "agent: device allocation of %zu bytes failed", off);
   }
   char* d = a->dev;
@@ -256,15 +275,25 @@ extern "C" int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* b0, const ck
   a->d_nacc = a->d_ncand + 1;
   a->d_nkept = a->d_ncand + 2;
   a->d_kept = (int32_t*)(d + o_kept);
-  // pinned layout
+  if (a->paged) {
+    a->d_rows[0] = (int32_t*)(d + o_tab[0]);
+    a->d_rows[1] = (int32_t*)(d + o_tab[1]);
+    a->d_pos[0] = (int32_t*)(d + o_tab[2]);
+    a->d_pos[1] = (int32_t*)(d + o_tab[3]);
+  }
   size_t po = 0;
   auto ptake = [&](size_t bytes) { const size_t o = po; po += align256(std::max<size_t>(bytes, 1)); return o; };
   const size_t p_up = ptake(M * 4), p_cnt = ptake(16), p_cand = ptake(M * 4), p_acc = ptake(M), p_lam = ptake(M);
   const size_t p_r = ptake(M * 4), p_rpost = ptake(M * 4), p_union = ptake(M * 4), p_score = ptake(cap * 4);
   const size_t p_kept = ptake(B * 4);
+  size_t p_tab[2] = {0, 0};
+  if (a->paged) {
+    p_tab[0] = ptake(cap * 4);
+    p_tab[1] = ptake(cap * 4);
+  }
   if (hipHostMalloc((void**)&a->pin, po, hipHostMallocDefault) != hipSuccess) {
-    (void)hipFree(a->dev);
-    delete a;
+    (void)hipGetLastError();
+    a->pin = nullptr;
     return ctx_fail(ctx, CKV_ERR_NOMEM, "agent: pinned allocation of %zu bytes failed", po);
   }
   char* p = a->pin;
@@ -278,29 +307,103 @@ extern "C" int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* b0, const ck
   a->dn_union = (float*)(p + p_union);
   a->dn_score = (float*)(p + p_score);
   a->dn_kept = (int32_t*)(p + p_kept);
+  if (a->paged) {
+    a->up_pos = (int32_t*)(p + p_tab[0]);
+    a->up_rows = (int32_t*)(p + p_tab[1]);
+  }
+  return CKV_OK;
+}
+
+void free_agent(ckv_agent* a) {
+  DevGuard g(ckv::ctx_device(a->ctx));
+  (void)hipStreamSynchronize(ckv::ctx_stream(a->ctx));
+  if (a->dev) (void)hipFree(a->dev);
+  if (a->pin) (void)hipHostFree(a->pin);
+  delete a;
+}
+
+}  // namespace
+
+extern "C" int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* b0, const ckv_cache_view* b1,
+                                const ckv_agent_config* cfg, ckv_agent** out) {
+  if (!ctx) return CKV_ERR_ARG;
+  if (!b0 || !b1 || !cfg || !out) return ctx_fail(ctx, CKV_ERR_ARG, "agent: NULL argument");
+  *out = nullptr;
+  for (const ckv_cache_view* b : {b0, b1})
+    if (!b->k || !b->v || !b->pos) return ctx_fail(ctx, CKV_ERR_ARG, "agent: cache buffer with a NULL pointer");
+  if (b0->n_seq != 1 || b1->n_seq != 1) return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: cache buffers hold one sequence");
+  if (b0->n_layers != b1->n_layers || b0->n_kv_heads != b1->n_kv_heads || b0->head_dim != b1->head_dim ||
+      b0->capacity != b1->capacity || b0->n_layers < 1)
+    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: the two cache buffers differ in geometry");
+  int rc;
+  if ((rc = check_config(ctx, cfg, b0->n_kv_heads, b0->n_layers, b0->capacity))) return rc;
+  ckv_agent* a = new (std::nothrow) ckv_agent();
+  if (!a) return ctx_fail(ctx, CKV_ERR_NOMEM, "agent: host allocation failed");
+  a->ctx = ctx;
+  a->buf[0] = *b0;
+  a->buf[1] = *b1;
+  a->cfg = *cfg;
+  a->capacity = b0->capacity;
+  if ((rc = alloc_agent(a, b0->head_dim))) {
+    free_agent(a);
+    return rc;
+  }
+  *out = a;
+  return CKV_OK;
+}
+
+extern "C" int ckv_agent_create_paged(ckv_ctx* ctx, const ckv_kv_view* pool, int32_t capacity,
+                                      const ckv_agent_config* cfg, ckv_agent** out) {
+  if (!ctx) return CKV_ERR_ARG;
+  if (!pool || !cfg || !out) return ctx_fail(ctx, CKV_ERR_ARG, "agent: NULL argument");
+  *out = nullptr;
+  if (!pool->k || !pool->v) return ctx_fail(ctx, CKV_ERR_ARG, "agent: pool with a NULL pointer");
+  if (pool->head_dim != 64 && pool->head_dim != 128)
+    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: head_dim %d unsupported", pool->head_dim);
+  if (pool->n_kv_heads < 1 || pool->pool_rows < 1 || pool->tok_stride < pool->head_dim || pool->head_stride < 0)
+    return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: bad pool geometry");
+  if ((reinterpret_cast<uintptr_t>(pool->k) & 15u) || (reinterpret_cast<uintptr_t>(pool->v) & 15u) ||
+      pool->tok_stride % 8 || pool->head_stride % 8)
+    return ctx_fail(ctx, CKV_ERR_ARG, "agent: pool rows must be 16-byte aligned");
+  if (capacity < 1 || capacity > pool->pool_rows) return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: capacity outside [1, pool_rows]");
+  int rc;
+  if ((rc = check_config(ctx, cfg, pool->n_kv_heads, cfg->score_layer + 1, capacity))) return rc;
+  ckv_agent* a = new (std::nothrow) ckv_agent();
+  if (!a) return ctx_fail(ctx, CKV_ERR_NOMEM, "agent: host allocation failed");
+  a->ctx = ctx;
+  a->cfg = *cfg;
+  a->capacity = capacity;
+  a->paged = true;
+  a->pool = *pool;
+  a->pool.pos = nullptr;
+  a->pool.slot = nullptr;
+  a->pool.n_tokens = 0;
+  if ((rc = alloc_agent(a, pool->head_dim))) {
+    free_agent(a);
+    return rc;
+  }
   *out = a;
   return CKV_OK;
 }
 
 extern "C" int ckv_agent_destroy(ckv_agent* a) {
   if (!a) return CKV_ERR_ARG;
-  DevGuard g(ckv::ctx_device(a->ctx));
-  (void)hipStreamSynchronize(ckv::ctx_stream(a->ctx));
-  if (a->dev) (void)hipFree(a->dev);
-  if (a->pin) (void)hipHostFree(a->pin);
-  delete a;
+  free_agent(a);
   return CKV_OK;
 }
 
-extern "C" int ckv_agent_append(ckv_agent* a, int32_t kind, const int32_t* pos, int32_t n, int32_t decoded,
-                                int32_t begins_event, int32_t* due) {
-  if (!a) return CKV_ERR_ARG;
+namespace {
+
+// positions checks and event bookkeeping shared by both appends; rows (paged
+// agents) are staged for the device before the host state changes
+int record_tokens(ckv_agent* a, int32_t kind, const int32_t* pos, const int32_t* rows, int32_t n, int32_t decoded,
+                  int32_t begins_event, int32_t* due) {
   ckv_ctx* c = a->ctx;
   if (kind < CKV_EVENT_REASONING || kind > CKV_EVENT_ANSWER) return ctx_fail(c, CKV_ERR_ARG, "append: unknown event kind %d", kind);
   if (n < 0 || (n > 0 && !pos)) return ctx_fail(c, CKV_ERR_ARG, "append: bad token count or NULL positions");
-  if ((int64_t)a->n_res() + n > a->buf[0].capacity)
+  if ((int64_t)a->n_res() + n > a->capacity)
     return ctx_fail(c, CKV_ERR_SHAPE, "append: %d resident + %d new tokens exceed the capacity %d", a->n_res(), n,
-                    a->buf[0].capacity);
+                    a->capacity);
   const bool fresh = begins_event || a->events.empty() || a->events.back().kind != kind;
   if (n > 0) {
     if (!a->res.empty() && pos[0] <= a->res.back()) return ctx_fail(c, CKV_ERR_ARG, "append: positions must increase");
@@ -311,6 +414,22 @@ extern "C" int ckv_agent_append(ckv_agent* a, int32_t kind, const int32_t* pos, 
       const Event& e = a->events.back();
       if (pos[0] != e.start + e.n) return ctx_fail(c, CKV_ERR_ARG, "append: an event's positions must be consecutive");
     }
+  }
+  if (a->paged && n > 0) {
+    if (!rows) return ctx_fail(c, CKV_ERR_ARG, "append: NULL rows");
+    for (int i = 0; i < n; ++i)
+      if (rows[i] < 0 || rows[i] >= a->pool.pool_rows)
+        return ctx_fail(c, CKV_ERR_ARG, "append: row %d outside the pool", rows[i]);
+    // staging slots [n_res, n_res + n) are not reused before the next
+    // checkpoint, which waits for the stream
+    const int r0 = a->n_res();
+    std::memcpy(a->up_pos + r0, pos, (size_t)n * 4);
+    std::memcpy(a->up_rows + r0, rows, (size_t)n * 4);
+    int rc;
+    if ((rc = a->copy(a->d_pos[a->cur] + r0, a->up_pos + r0, (size_t)n * 4, hipMemcpyHostToDevice)) ||
+        (rc = a->copy(a->d_rows[a->cur] + r0, a->up_rows + r0, (size_t)n * 4, hipMemcpyHostToDevice)))
+      return rc;
+    a->rows.insert(a->rows.end(), rows, rows + n);
   }
   if (n > 0 || fresh) {
     if (fresh) a->events.push_back(Event{kind, n > 0 ? pos[0] : (a->res.empty() ? 0 : a->res.back() + 1), 0});
@@ -329,6 +448,22 @@ extern "C" int ckv_agent_append(ckv_agent* a, int32_t kind, const int32_t* pos, 
   }
   if (due) *due = flags;
   return CKV_OK;
+}
+
+}  // namespace
+
+extern "C" int ckv_agent_append(ckv_agent* a, int32_t kind, const int32_t* pos, int32_t n, int32_t decoded,
+                                int32_t begins_event, int32_t* due) {
+  if (!a) return CKV_ERR_ARG;
+  if (a->paged) return ctx_fail(a->ctx, CKV_ERR_ARG, "append: a paged agent takes ckv_agent_append_rows");
+  return record_tokens(a, kind, pos, nullptr, n, decoded, begins_event, due);
+}
+
+extern "C" int ckv_agent_append_rows(ckv_agent* a, int32_t kind, const int32_t* pos, const int32_t* rows, int32_t n,
+                                     int32_t decoded, int32_t begins_event, int32_t* due) {
+  if (!a) return CKV_ERR_ARG;
+  if (!a->paged) return ctx_fail(a->ctx, CKV_ERR_ARG, "append_rows: the agent owns cache buffers (ckv_agent_append)");
+  return record_tokens(a, kind, pos, rows, n, decoded, begins_event, due);
 }
 
 extern "C" int ckv_agent_commit(ckv_agent* a, const ckv_window_view* q_pre) {
@@ -429,6 +564,7 @@ extern "C" int ckv_agent_checkpoint(ckv_agent* a, const ckv_window_view* q_score
   if ((rc = a->check_window(q_score, "checkpoint"))) return rc;
   a->clear_report(3);
   if (compacted) *compacted = 0;
+  a->freed.clear();
   const int S = a->n_res();
   a->rep_before = S;
   const uint32_t policy = ckv_get_policy(a->ctx);
@@ -466,7 +602,7 @@ extern "C" int ckv_agent_checkpoint(ckv_agent* a, const ckv_window_view* q_score
   const float* score = a->d_score;
   if (a->cfg.pool_kernel > 1) {
     const int32_t nt = S;
-    if ((rc = ckv_pool_scores(a->ctx, a->d_score, a->d_pooled, 1, a->buf[0].capacity, &nt, a->cfg.pool_kernel,
+    if ((rc = ckv_pool_scores(a->ctx, a->d_score, a->d_pooled, 1, a->capacity, &nt, a->cfg.pool_kernel,
                               a->cfg.pool_mode)))
       return rc;
     score = a->d_pooled;
@@ -475,9 +611,13 @@ extern "C" int ckv_agent_checkpoint(ckv_agent* a, const ckv_window_view* q_score
   const ckv_page_list pend_list{ps.data(), pl.data(), (int32_t)ps.size()};
   const float* rptr = P.empty() ? nullptr : a->d_r_sub;
   const int32_t n_tok = S;
-  if ((rc = ckv_select_and_compact(a->ctx, &a->buf[a->cur], &n_tok, score, a->buf[0].capacity, &ret_list,
-                                   &pend_list, &rptr, nullptr, &a->cfg.budget, &a->buf[1 - a->cur], a->d_kept,
-                                   a->d_nkept, nullptr)))
+  ckv_cache_view index_only{};        // paged: selection only, the slot table follows below
+  index_only.n_seq = 1;
+  index_only.capacity = a->capacity;
+  const ckv_cache_view* in = a->paged ? &index_only : &a->buf[a->cur];
+  const ckv_cache_view* out = a->paged ? nullptr : &a->buf[1 - a->cur];
+  if ((rc = ckv_select_and_compact(a->ctx, in, &n_tok, score, a->capacity, &ret_list, &pend_list, &rptr, nullptr,
+                                   &a->cfg.budget, out, a->d_kept, a->d_nkept, nullptr)))
     return rc;
   const int B = a->cfg.budget.budget;
   if ((rc = a->copy(a->dn_counts + 2, a->d_nkept, 4, hipMemcpyDeviceToHost)) ||
@@ -495,6 +635,25 @@ extern "C" int ckv_agent_checkpoint(ckv_agent* a, const ckv_window_view* q_score
     if (kept[j] < 0 || kept[j] >= S || (j && kept[j] <= kept[j - 1]))
       return ctx_fail(a->ctx, CKV_ERR_HIP, "checkpoint: kept index list is not ascending inside the cache");
     npos[j] = a->res[kept[j]];
+  }
+  if (a->paged) {
+    // the slot table and positions follow I; rows of the other tokens are free
+    if (nk > 0) {
+      hipLaunchKernelGGL(gather_rows_kernel, dim3((nk + 255) / 256), dim3(256), 0, ckv::ctx_stream(a->ctx),
+                         a->d_rows[a->cur], a->d_pos[a->cur], a->d_kept, nk, a->d_rows[1 - a->cur],
+                         a->d_pos[1 - a->cur]);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return ctx_fail(a->ctx, CKV_ERR_HIP, "checkpoint: row gather: %s", hipGetErrorString(e));
+    }
+    std::vector<uint8_t> keep(S, 0);
+    for (int j = 0; j < nk; ++j) keep[kept[j]] = 1;
+    std::vector<int32_t> nrows(nk);
+    a->freed.clear();
+    for (int i = 0, j = 0; i < S; ++i) {
+      if (keep[i]) nrows[j++] = a->rows[i];
+      else a->freed.push_back(a->rows[i]);
+    }
+    a->rows.swap(nrows);
   }
   a->res.swap(npos);
   a->cur = 1 - a->cur;
@@ -554,6 +713,15 @@ extern "C" int ckv_agent_pages(const ckv_agent* a, int32_t which, int32_t* start
     len[i] = L[i].len;
     if (value) value[i] = which == 0 ? a->pend_r[i] : 0.f;
   }
+  if (n) *n = (int32_t)L.size();
+  return CKV_OK;
+}
+
+extern "C" int ckv_agent_rows(const ckv_agent* a, int32_t which, int32_t* rows, int32_t cap, int32_t* n) {
+  if (!a || which < 0 || which > 2 || (which < 2 && !a->paged) || cap < 0 || (cap > 0 && !rows)) return CKV_ERR_ARG;
+  const std::vector<int32_t>& L = which == 0 ? a->rows : which == 1 ? a->freed : a->res;
+  const int m = std::min<int>(cap, (int)L.size());
+  if (m > 0) std::memcpy(rows, L.data(), (size_t)m * 4);
   if (n) *n = (int32_t)L.size();
   return CKV_OK;
 }

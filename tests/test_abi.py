@@ -90,6 +90,9 @@ def test_agent_null_handling(lib):
     assert L.ckv_agent_last_report(None, None) == _abi.CKV_ERR_ARG
     assert L.ckv_agent_pages(None, 0, None, None, None, 0, None) == _abi.CKV_ERR_ARG
     assert L.ckv_agent_create(None, None, None, None, None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_create_paged(None, None, 0, None, None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_append_rows(None, 0, None, None, 0, 0, 0, None) == _abi.CKV_ERR_ARG
+    assert L.ckv_agent_rows(None, 0, None, 0, None) == _abi.CKV_ERR_ARG
 
 
 def _c_layout(tmp_path, struct, fields, header="commitkv_agent.h"):

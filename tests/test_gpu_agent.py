@@ -43,13 +43,16 @@ def ckv():
     ctx.close()
 
 
-def _gpu_agent(P, ctx, cfg):
+def _gpu_agent(P, ctx, cfg, paged=None):
+    """paged: None for the two-buffer agent, else the row seed of a paged
+    agent whose pool has a few more rows than the capacity."""
+    extra = {} if paged is None else dict(paged=True, pool_rows=cfg.capacity + 37, row_seed=paged)
     return P.Agent(ctx, cfg.n_layers, cfg.n_kv_heads, cfg.head_dim, cfg.capacity,
                    page_size=cfg.page_size, window=cfg.window, n_q_heads=cfg.n_q_heads,
                    budget=cfg.budget, eta=cfg.eta, max_pending_pages=cfg.max_pending_pages,
                    keep_recent=cfg.keep_recent, max_scan_pages=cfg.max_scan_pages,
                    checkpoint_every=cfg.checkpoint_every, score_layer=cfg.score_layer,
-                   report_detail=True, pool_kernel=cfg.pool_kernel, pool_mode=cfg.pool_mode)
+                   report_detail=True, pool_kernel=cfg.pool_kernel, pool_mode=cfg.pool_mode, **extra)
 
 
 def _expected_due(acts, i):
@@ -65,6 +68,10 @@ def _expected_due(acts, i):
 def _check_cache(ga, oa, cfg):
     k, v, pos, n = ga.cache()
     assert n == oa.pos.size
+    if ga.paged:
+        rows = ga.rows("resident")
+        assert rows.size == n and np.unique(rows).size == n
+        assert sorted(ga.free + rows.tolist()) == list(range(ga.kp.shape[2]))
     np.testing.assert_array_equal(pos[:n].cpu().numpy(), oa.pos)
     kb = k[:, :, :n].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     vb = v[:, :, :n].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
@@ -73,9 +80,9 @@ def _check_cache(ga, oa, cfg):
         np.testing.assert_array_equal(vb[l], oa.V[l])
 
 
-def run_lockstep(P, ctx, traj, ablation=()):
+def run_lockstep(P, ctx, traj, ablation=(), paged=None):
     cfg = traj.cfg
-    ga = _gpu_agent(P, ctx, cfg)
+    ga = _gpu_agent(P, ctx, cfg, paged)
     oa = oracle_agent(cfg, ablation=ablation)
     acts = schedule(traj)
     stats = dict(commit=0, post=0, cand=0, accepted=0, compacted=0, excused=0)
@@ -197,6 +204,24 @@ def test_pooled_score_episode(ckv, mode):
     assert s["compacted"] >= 2
 
 
+@pytest.mark.parametrize("seed", [0, 3])
+def test_paged_episode(ckv, seed):
+    """A paged agent (slot table over scattered pool rows, checkpoints that
+    move no key or value) in lock step with the oracle: the same bars as the
+    two-buffer agent; the resident rows, gathered, must equal the oracle's
+    cache bit for bit, and every pool row is either resident or free."""
+    P, ctx = ckv
+    s = run_lockstep(P, ctx, make_trajectory(TRAJECTORIES["tiny_agent"], seed=seed, n_turns=8), paged=seed + 11)
+    assert s["compacted"] >= 2 and s["post"] >= 5
+
+
+def test_paged_pooled_episode(ckv):
+    P, ctx = ckv
+    cfg = scaled_trajectory("tiny_agent", pool_kernel=7, pool_mode="max")
+    s = run_lockstep(P, ctx, make_trajectory(cfg, seed=5, n_turns=6), paged=2)
+    assert s["compacted"] >= 2
+
+
 @pytest.mark.parametrize("ablation", [("no_protection",), ("no_joint",), ("no_precommit",)])
 def test_ablation_episode(ckv, ablation):
     P, ctx = ckv
@@ -231,3 +256,32 @@ def test_host_errors(ckv):
     with pytest.raises(P.CKVError) as e:
         P.Agent(ctx, 2, 1, 64, 256, page_size=16, window=16, n_q_heads=4, budget=512)   # B > capacity
     assert e.value.code == -1
+
+
+def test_paged_host_errors(ckv):
+    import ctypes
+    from paper_2608_07855_amd import _abi
+    P, ctx = ckv
+    cfg = TRAJECTORIES["tiny_agent"]
+    ga = _gpu_agent(P, ctx, cfg, paged=0)
+    gb = _gpu_agent(P, ctx, cfg)
+    L = P.lib()
+    try:
+        pos = np.arange(4, dtype=np.int32)
+        bad = np.array([0, 1, ga.kp.shape[2], 3], np.int32)          # a row outside the pool
+        i32 = lambda a: a.ctypes.data_as(_abi.c_i32p)
+        assert L.ckv_agent_append_rows(ga.handle, 3, i32(pos), i32(bad), 4, 0, 1, None) == _abi.CKV_ERR_ARG
+        assert L.ckv_agent_append(ga.handle, 3, i32(pos), 4, 0, 1, None) == _abi.CKV_ERR_ARG
+        assert L.ckv_agent_append_rows(gb.handle, 3, i32(pos), i32(pos), 4, 0, 1, None) == _abi.CKV_ERR_ARG
+        n = ctypes.c_int32()
+        assert L.ckv_agent_rows(gb.handle, 0, None, 0, ctypes.byref(n)) == _abi.CKV_ERR_ARG
+        assert ga.state()[0] == 0 and ga.rows("resident").size == 0
+        k = torch.zeros((cfg.n_layers, cfg.n_kv_heads, 4, cfg.head_dim), dtype=torch.bfloat16, device="cuda")
+        ga.append(3, k, k, pos, False)
+        assert ga.rows("pos").tolist() == pos.tolist() and ga.rows("resident").size == 4
+    finally:
+        ga.close()
+        gb.close()
+    with pytest.raises(P.CKVError) as e:                           # capacity above the pool's rows
+        P.Agent(ctx, 2, 1, 64, 512, page_size=16, window=16, n_q_heads=4, budget=256, paged=True, pool_rows=300)
+    assert e.value.code == -2
