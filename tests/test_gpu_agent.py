@@ -43,10 +43,10 @@ def ckv():
     ctx.close()
 
 
-def _gpu_agent(P, ctx, cfg, paged=None):
+def _gpu_agent(P, ctx, cfg, paged=None, spare_rows=37):
     """paged: None for the two-buffer agent, else the row seed of a paged
-    agent whose pool has a few more rows than the capacity."""
-    extra = {} if paged is None else dict(paged=True, pool_rows=cfg.capacity + 37, row_seed=paged)
+    agent whose pool has spare_rows more rows than the capacity."""
+    extra = {} if paged is None else dict(paged=True, pool_rows=cfg.capacity + spare_rows, row_seed=paged)
     return P.Agent(ctx, cfg.n_layers, cfg.n_kv_heads, cfg.head_dim, cfg.capacity,
                    page_size=cfg.page_size, window=cfg.window, n_q_heads=cfg.n_q_heads,
                    budget=cfg.budget, eta=cfg.eta, max_pending_pages=cfg.max_pending_pages,
@@ -80,9 +80,9 @@ def _check_cache(ga, oa, cfg):
         np.testing.assert_array_equal(vb[l], oa.V[l])
 
 
-def run_lockstep(P, ctx, traj, ablation=(), paged=None):
+def run_lockstep(P, ctx, traj, ablation=(), paged=None, spare_rows=37):
     cfg = traj.cfg
-    ga = _gpu_agent(P, ctx, cfg, paged)
+    ga = _gpu_agent(P, ctx, cfg, paged, spare_rows)
     oa = oracle_agent(cfg, ablation=ablation)
     acts = schedule(traj)
     stats = dict(commit=0, post=0, cand=0, accepted=0, compacted=0, excused=0)
@@ -213,6 +213,36 @@ def test_paged_episode(ckv, seed):
     P, ctx = ckv
     s = run_lockstep(P, ctx, make_trajectory(TRAJECTORIES["tiny_agent"], seed=seed, n_turns=8), paged=seed + 11)
     assert s["compacted"] >= 2 and s["post"] >= 5
+
+
+def test_paged_tight_pool_episode(ckv):
+    """A pool of exactly the capacity: after the first checkpoints every
+    append reuses rows that a checkpoint freed, in scattered order."""
+    P, ctx = ckv
+    s = run_lockstep(P, ctx, make_trajectory(TRAJECTORIES["tiny_agent"], seed=4, n_turns=8), paged=9,
+                     spare_rows=0)
+    assert s["compacted"] >= 2
+
+
+def test_paged_paper_operating_point_episode(ckv):
+    """The paper's operating point (W 8, G 16, a Qwen3-14B-shaped layer)
+    through a paged agent."""
+    P, ctx = ckv
+    cfg = scaled_trajectory("paper_agent", n_layers=2, score_layer=1, budget=2048, obs_hi=768,
+                            reason_hi=384, prompt_hi=512, forced_frac=0.1, forced_pre=100.0,
+                            forced_post=0.005, heavy_frac=0.003)
+    s = run_lockstep(P, ctx, make_trajectory(cfg, seed=1, n_turns=6), paged=5)
+    assert s["compacted"] >= 1 and s["commit"] >= 5
+
+
+def test_paged_ablation_episode(ckv):
+    P, ctx = ckv
+    ctx.set_policy("no_protection")
+    try:
+        run_lockstep(P, ctx, make_trajectory(TRAJECTORIES["tiny_agent"], seed=2, n_turns=6), ("no_protection",),
+                     paged=3)
+    finally:
+        ctx.set_policy()
 
 
 def test_paged_pooled_episode(ckv):
