@@ -32,7 +32,10 @@ commit, post-commit step and checkpoint; ``agent_paper_point`` does the same
 at the paper's operating point (W 8, G 16, budget 4096, 40 layers), and
 ``agent_paged`` runs the first workload's episodes with a paged agent (pool
 rows in scattered order; a checkpoint re-indexes the slot table instead of
-moving keys and values).
+moving keys and values).  ``step_ms_events`` gives the median and 10th / 90th
+percentiles of single steps timed with events; ``configs`` the pre + post
+measurement alone on every synthetic workload (2K to 128K cached tokens, the
+forced-page stress case included) with its roofline fraction.
 """
 from __future__ import annotations
 
@@ -73,6 +76,8 @@ def parse():
     ap.add_argument("--agent-seqs", type=int, default=4)
     ap.add_argument("--no-stack", action="store_true",
                     help="skip the 144-problem stack leg (36 layers x 4 sequences at 65536 tokens)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload pre + post measurement leg")
     ap.add_argument("--no-recorded", action="store_true",
                     help="skip the recorded-output leg (ckv_measure_recorded)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -388,6 +393,72 @@ def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped", paged=False):
         compaction_GBps=moved / t["checkpoint"] / 1e9 if t["checkpoint"] > 0 and not paged else None)
 
 
+def pct(ms):
+    """median and 10th / 90th percentiles of a list of times"""
+    a = np.asarray(ms, dtype=np.float64)
+    return dict(median=float(np.median(a)), p10=float(np.percentile(a, 10)), p90=float(np.percentile(a, 90)))
+
+
+def event_times(fn, reps):
+    """fn(i) for i < reps, each bracketed by events on the current stream
+    (the library's stream); per-call milliseconds"""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    gc.collect()
+    gc.disable()
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(ev):
+        a.record()
+        fn(i)
+        b.record()
+    torch.cuda.synchronize()
+    gc.enable()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
+def configs_leg(names=("tiny", "q8b", "q32b", "stress"), reps=30):
+    """Cached tokens scored per second per layer on each synthetic workload:
+    the pre and post measurement calls (R written; no token mass,
+    classification or selection), each repetition bracketed by events, with
+    the K/V copies rotated so that no call finds its cache in the 256 MB
+    Infinity Cache.  ``roof_frac`` = t_roof / t_median with t_roof =
+    max(bytes / 8 TB/s, FLOPs / 2.5 PFLOP/s) for one read of the resident
+    keys, values and positions of both passes and the two products
+    (Q K^T, P V) over them."""
+    import torch
+    from synth import WORKLOADS
+
+    out = {}
+    for name in names:
+        w = WORKLOADS[name]
+        st = Setup(w, 2 if w.n_tokens > 65536 else 4)
+        P, n = st.P, len(st.k)
+
+        def run(i):
+            P.ckv_measure_page_effects(st.ctx, st.kv_pre[(2 * i) % n], st.win_pre, st.pages, R=st.R_pre)
+            P.ckv_measure_page_effects(st.ctx, st.kv_post[(2 * i + 1) % n], st.win_post, st.pages, R=st.R_post)
+
+        for i in range(5):
+            run(i)
+        ms = event_times(run, reps)
+        toks = int(st.L.layout.s_pre) + w.n_tokens
+        byt = toks * (w.n_kv_heads * w.head_dim * 2 * 2 + 4)
+        flop = 4.0 * w.n_q_heads * w.window * toks * w.head_dim
+        t_roof = max(byt / 8.0e12, flop / 2.5e15) * 1e3
+        q = pct(ms)
+        out[name] = dict(n_tokens=w.n_tokens, s_pre=int(st.L.layout.s_pre), pages=st.n_pages,
+                         shape=f"Hq {w.n_q_heads} Hkv {w.n_kv_heads} d {w.head_dim} W {w.window} "
+                               f"G {w.page_size}",
+                         ms=q, tokens_per_s=toks / (q["median"] / 1e3), roof_ms=t_roof,
+                         roof_frac=t_roof / q["median"])
+        log(f"[bench] config {name}: median {q['median']:.3f} ms for pre + post")
+        st.ctx.close()
+        del st, run
+        gc.collect()
+        torch.cuda.empty_cache()
+    return out
+
+
 def kernel_work(w, L, name, launches_per_step):
     """Algorithmic bytes and FLOPs per launch of a library kernel."""
     Hq, Hkv, W, d, S, Sp = w.n_q_heads, w.n_kv_heads, w.window, w.head_dim, w.n_tokens, L.layout.s_pre
@@ -519,8 +590,10 @@ def main():
     tokens = L.layout.s_pre + w.n_tokens
     value = tokens / (ms / 1e3)
     log(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step")
+    # distribution of single steps (events around each), after the timed run
+    step_dist = pct(event_times(lambda i: st.step(10_000 + i), max(args.steps, 30)))
     meas = sum(per_kernel.get(k, {}).get("ms_per_step", 0.0)
-               for k in ("window_attention", "combine", "page_effect", "token_mass"))
+               for k in ("window_attention", "combine", "page_effect", "page_fixup", "token_mass"))
     sel_ms = sum(per_kernel.get(k, {}).get("ms_per_step", 0.0) for k in ("protect", "select", "gather"))
     g_ms = per_kernel.get("gather", {}).get("ms_per_step", 0.0)
     n_kept = int(st.last["sel"]["n_kept"][0].item())
@@ -549,12 +622,14 @@ def main():
     agent = None if args.no_agent else agent_leg(args.agent_seqs)
     agent_paper = None if args.no_agent else agent_leg(2, "paper_agent", "qwen3-14b-shaped, paper operating point")
     agent_paged = None if args.no_agent else agent_leg(args.agent_seqs, paged=True)
+    configs = None if args.no_configs else configs_leg()
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, L, args.cpu_seconds)
     res = dict(
         metric=METRIC, value=value, unit="tokens/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
-        ms_per_step=ms, higher_is_better=True, scaling="weak", vs_baseline=None, dtype="bf16",
+        ms_per_step=ms, step_ms_events=step_dist, higher_is_better=True, scaling="weak", vs_baseline=None,
+        dtype="bf16",
         data="synthetic",
         config=dict(workload="qwen3-8b-shaped layer, 32768 cached tokens (Hq 32, Hkv 8, d 128, "
                              "32-token pages, 64-row windows, budget 8192)" if w.name == "q8b" else w.name,
@@ -576,6 +651,7 @@ def main():
         agent=agent,
         agent_paper_point=agent_paper,
         agent_paged=agent_paged,
+        configs=configs,
     )
     print(json.dumps(res), flush=True)
 
