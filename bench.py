@@ -531,7 +531,13 @@ def cpu_baseline(w, L, budget_s):
     per_step = spent * Hq / len(heads)
     log(f"[bench] cpu oracle: {len(heads)} of {Hq} query heads in {spent:.1f}s "
         f"(wall {time.time() - t_all:.1f}s) -> {per_step:.1f}s per full pre+post pass")
-    return dict(value=(Sp + S) / per_step, unit="tokens/s", cores=cores, kind="oracle",
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:
+        pass
+    return dict(value=(Sp + S) / per_step, unit="tokens/s", cores=cores, kind="oracle", cpu_model=model,
                 sample=f"closed-form fp64 oracle, pre+post deletion effects of all {len(L.pages)} pages "
                        f"for query heads 0..{len(heads) - 1} of {Hq}, time scaled by {Hq}/{len(heads)}")
 
