@@ -105,7 +105,9 @@ int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* buf0, const ckv_cache_v
  * (Eq. (12)-(13)) and gathers both tables through I_j, and the rows of the
  * tokens it drops are returned by ckv_agent_rows(which = 1).  cfg's
  * score_layer is not used (the pool is the scoring layer's; it must be
- * >= 0).  Errors as ckv_agent_create. */
+ * >= 0).  Errors as ckv_agent_create, and CKV_ERR_UNSUPPORTED for a pool
+ * whose pool_rows * tok_stride reaches 2^31 elements (the limit of
+ * ckv_kv_view). */
 int ckv_agent_create_paged(ckv_ctx* ctx, const ckv_kv_view* pool, int32_t capacity,
                            const ckv_agent_config* cfg, ckv_agent** out);
 

@@ -366,6 +366,10 @@ extern "C" int ckv_agent_create_paged(ckv_ctx* ctx, const ckv_kv_view* pool, int
       pool->tok_stride % 8 || pool->head_stride % 8)
     return ctx_fail(ctx, CKV_ERR_ARG, "agent: pool rows must be 16-byte aligned");
   if (capacity < 1 || capacity > pool->pool_rows) return ctx_fail(ctx, CKV_ERR_SHAPE, "agent: capacity outside [1, pool_rows]");
+  // the measurement kernels form row offsets with a 24-bit multiply
+  if (pool->tok_stride >= (1 << 24) || pool->pool_rows >= (1 << 24) ||
+      (int64_t)pool->pool_rows * pool->tok_stride >= ((int64_t)1 << 31))
+    return ctx_fail(ctx, CKV_ERR_UNSUPPORTED, "agent: pool_rows * tok_stride must stay below 2^31 elements");
   int rc;
   if ((rc = check_config(ctx, cfg, pool->n_kv_heads, cfg->score_layer + 1, capacity))) return rc;
   ckv_agent* a = new (std::nothrow) ckv_agent();
