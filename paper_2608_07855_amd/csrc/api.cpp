@@ -30,6 +30,9 @@ constexpr float kLog2eHost = 1.4426950408889634f;   // log2(e): natural-log LSE 
 constexpr int kJointWindow = 32;       // candidates tested per joint round
 constexpr int kJointRowsPerBlock = 64;
 constexpr int kTargetBlocks = 256;     // one 8-wave workgroup per compute unit
+// the fix-up recomputes a dominant page's whole split for one row, so long
+// splits make it expensive: splits hold at most this many tokens
+constexpr int kMaxSplitTokens = 8192;
 // the token-mass kernel (64 VGPRs, 40 KB of LDS) keeps two workgroups per
 // compute unit busy: 512 token chunks measured 31.7 us against 35.3 us with 256
 constexpr int kMassBlocks = 512;
@@ -553,7 +556,8 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
   const int D = a.D, n = pages->n_pages, total_rows = a.Hq * a.W;
   const int rpb = rows_per_block_attention();
   const int nrb = ceil_div(a.rows, rpb);
-  int n_splits = std::max(1, std::min(ceil_div(a.S, 64), ceil_div(kTargetBlocks, a.Hkv * nrb)));
+  int n_splits = std::max(1, std::min(ceil_div(a.S, 64),
+                                      std::max(ceil_div(kTargetBlocks, a.Hkv * nrb), ceil_div(a.S, kMaxSplitTokens))));
   const int chunk = (int)round_up(ceil_div(a.S, n_splits), 64);
   n_splits = ceil_div(a.S, chunk);
 
