@@ -556,6 +556,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   }
   const float lse2 = ri.ok ? rs.lse2[ri.rg] * pw.lse_scale : -INFINITY;   // -inf stays -inf
   const float onorm = (MODE == 0 && ri.ok) ? rs.onorm[ri.rg] : 0.f;   // read by MODE 0 only
+  const float inv_onorm = onorm > 0.f ? 1.f / onorm : 0.f;
   const int nvis = (MODE == 0 && ri.ok) ? rs.nvis[ri.rg] : 0;   // read by MODE 0 only
   const int row0 = rblk * kRowsWG;
   const int head0 = row0 / a.W;
@@ -709,7 +710,10 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
               }
             }
           } else if (onorm > 0.f) {
-            ratio = f * sqrtf(n2) / (keep * onorm);
+            // hardware square root and reciprocal (about 1 ulp each): the
+            // ratio's tolerance is four orders of magnitude looser, and the
+            // IEEE sequences cost some 35 instructions per page
+            ratio = f * __builtin_amdgcn_sqrtf(n2) * inv_onorm * __builtin_amdgcn_rcpf(keep);
           } else {
             ratio = n2 > 0.f ? INFINITY : 0.f;
           }
