@@ -29,7 +29,8 @@ outputs (ckv_measure_recorded); ``paged`` the measurement over a paged pool;
 tokens through the batched call.  ``agent`` runs whole synthetic agent episodes of a 36-layer stack
 through the lifecycle driver (Algorithm 1) and reports the driver's time per
 commit, post-commit step and checkpoint; ``agent_paper_point`` does the same
-at the paper's operating point (W 8, G 16, budget 4096, 40 layers), and
+at the paper's operating point (W 8, G 16, budget 4096, 40 layers;
+``agent_paper_budgets`` repeats it at budgets 2048 and 8192), and
 ``agent_paged`` runs the first workload's episodes with a paged agent (pool
 rows in scattered order; a checkpoint re-indexes the slot table instead of
 moving keys and values).  ``step_ms_events`` gives the median and 10th / 90th
@@ -318,7 +319,7 @@ def stack_leg(steps):
                 ms_per_step=ms, tokens_per_s=tokens / (ms / 1e3), tokens_per_step=tokens)
 
 
-def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped", paged=False):
+def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped", paged=False, budget=None):
     """Whole agent episodes through the lifecycle driver (ckv_agent_*), one
     driver per episode: by default the Qwen3-8B-shaped stack (36 layers, 32
     query / 8 KV heads, d 128), budget 16384, 64-row windows, 32-token pages;
@@ -334,9 +335,9 @@ def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped", paged=False):
     import torch
 
     import paper_2608_07855_amd as P
-    from synth.trajectory import TRAJECTORIES, make_trajectory, schedule
+    from synth.trajectory import TRAJECTORIES, make_trajectory, scaled_trajectory, schedule
 
-    cfg = TRAJECTORIES[traj]
+    cfg = TRAJECTORIES[traj] if budget is None else scaled_trajectory(traj, budget=budget)
     ctx = P.Context(0)
     L, Hkv, d, Hq, W = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads, cfg.window
     t = dict(commit=0.0, post=0.0, checkpoint=0.0)
@@ -627,6 +628,10 @@ def main():
     stack = None if args.no_stack else stack_leg(3)
     agent = None if args.no_agent else agent_leg(args.agent_seqs)
     agent_paper = None if args.no_agent else agent_leg(2, "paper_agent", "qwen3-14b-shaped, paper operating point")
+    # the paper's other budgets (Sec. 4.1: B in {2048, 4096, 8192})
+    agent_paper_budgets = None if args.no_agent else {
+        str(b): agent_leg(2, "paper_agent", "qwen3-14b-shaped, paper operating point", budget=b)
+        for b in (2048, 8192)}
     agent_paged = None if args.no_agent else agent_leg(args.agent_seqs, paged=True)
     configs = None if args.no_configs else configs_leg()
     cpu = None
@@ -656,6 +661,7 @@ def main():
         stack=stack,
         agent=agent,
         agent_paper_point=agent_paper,
+        agent_paper_budgets=agent_paper_budgets,
         agent_paged=agent_paged,
         configs=configs,
     )
