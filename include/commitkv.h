@@ -303,8 +303,8 @@ int ckv_measure_page_effects_batch(ckv_ctx* ctx, int32_t n,
  * their own tokens in float32, with 1 - A taken against the recorded
  * log-sum-exp, so the rounding of lse and of the page's logits bounds their
  * relative error by a few ulp(lse)/(1 - A); above 0.99 the row's output
- * without the page is recomputed from all of its other tokens (for up to
- * 1024 such (page, row) pairs per call).
+ * without the page is recomputed from all of its other tokens (every such
+ * (page, row) pair, however many rows have one).
  */
 int ckv_measure_recorded(ckv_ctx* ctx, const ckv_kv_view* kv,
                          const ckv_window_view* win,

@@ -78,6 +78,7 @@ struct ckv_ctx {
   int next_slot = 0;
   std::vector<PageEntry> pages;
   uint64_t tick = 0;
+  uint64_t call_tick = 0;   // first tick of the current call: entries used since are not evicted
   // grid selection state (zero between calls), sized for sel_seq sequences
   int32_t* sel_ctrl = nullptr;
   uint32_t* sel_hist = nullptr;
@@ -148,6 +149,12 @@ int ctx_device(const ckv_ctx* c) { return c->device; }
 namespace {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// start of an API call: clears the message and opens a new cache scope
+void begin_call(ckv_ctx* c) {
+  c->err.clear();
+  c->call_tick = c->tick + 1;
+}
 
 int ensure_ws(ckv_ctx* c, size_t need) {
   if (need <= c->ws_cap) return CKV_OK;
@@ -264,6 +271,12 @@ int upload(ckv_ctx* c, const void* src, size_t bytes, void* dst) {
 // device copy of an int32 array, cached by content: an unchanged array is
 // not copied again (the entries have their own allocations, so later calls'
 // workspace never overwrites them)
+//
+// A call may take several copies (one per sequence, then the argument blob
+// that points at them): an entry used since the call began (used >=
+// call_tick) is never evicted, so the cache grows past kPageCacheEntries for
+// such a call instead of overwriting or freeing a table the call's kernels
+// are about to read.
 int cached_copy(ckv_ctx* c, std::vector<int32_t>&& key, const int32_t** dev) {
   ++c->tick;
   for (auto& e : c->pages) {
@@ -278,8 +291,12 @@ int cached_copy(ckv_ctx* c, std::vector<int32_t>&& key, const int32_t** dev) {
     c->pages.emplace_back();
     e = &c->pages.back();
   } else {
-    e = &*std::min_element(c->pages.begin(), c->pages.end(),
-                           [](const PageEntry& a, const PageEntry& b) { return a.used < b.used; });
+    for (auto& x : c->pages)
+      if (x.used < c->call_tick && (!e || x.used < e->used)) e = &x;
+    if (!e) {
+      c->pages.emplace_back();
+      e = &c->pages.back();
+    }
   }
   const size_t bytes = key.size() * sizeof(int32_t);
   if (e->cap < bytes) {
@@ -537,11 +554,49 @@ extern "C" int ckv_reset_kernel_stats(ckv_ctx* c) {
 
 // ------------------------------------------------------------- the calls
 
-extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win,
-                                        const ckv_page_list* pages, float* R, float* R_head, float* o,
-                                        float* lse, float* token_mass) {
-  if (!c) return CKV_ERR_ARG;
-  c->err.clear();
+namespace {
+
+// Workspace of one measurement call for a given number of token splits.
+struct MeasureBufs {
+  AttnSplit sp{};
+  RowStats rs{};
+  int* fix_list = nullptr;
+  int* fix_count = nullptr;
+  float* fpart = nullptr;
+};
+
+void plan_measure(const AttnGeom& a, int n_splits, float* o, Plan& plan, MeasureBufs& b) {
+  const int D = a.D, total_rows = a.Hq * a.W;
+  const int rpb = rows_per_block_attention();
+  const int nrb = ceil_div(a.rows, rpb);
+  const int chunk = (int)round_up(ceil_div(a.S, n_splits), 64);
+  n_splits = ceil_div(a.S, chunk);
+  b.sp = AttnSplit{chunk, n_splits, nrb * rpb, nullptr, nullptr, nullptr, nullptr};
+  b.rs = RowStats{o, nullptr, nullptr, nullptr};
+  const size_t nsr = (size_t)a.Hkv * n_splits * b.sp.rows_pad;
+  plan.add(&b.sp.part_o, nsr * D);
+  plan.add(&b.sp.part_m, nsr);
+  plan.add(&b.sp.part_l, nsr);
+  plan.add(&b.sp.part_c, nsr);
+  if (!o) plan.add(&b.rs.o, (size_t)total_rows * D);
+  plan.add(&b.rs.lse2, total_rows);
+  plan.add(&b.rs.onorm, total_rows);
+  plan.add(&b.rs.nvis, total_rows);
+  plan.add(&b.fix_list, 4 * (size_t)total_rows);
+  plan.add(&b.fix_count, 1);
+  plan.add(&b.fpart, (size_t)total_rows * ckv::kFixParts * (D + 1));
+}
+
+// splits of the window pass: about one workgroup per compute unit, and at
+// most kMaxSplitTokens tokens per split
+int default_splits(const AttnGeom& a) {
+  const int nrb = ceil_div(a.rows, rows_per_block_attention());
+  return std::max(1, std::min(ceil_div(a.S, 64),
+                              std::max(ceil_div(kTargetBlocks, a.Hkv * nrb), ceil_div(a.S, kMaxSplitTokens))));
+}
+
+int check_measure(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win, const ckv_page_list* pages,
+                  const float* R, const float* token_mass) {
   int rc;
   if ((rc = check_kv(c, kv)) || (rc = check_win(c, win, kv)) || (rc = check_pages(c, pages, kv->n_tokens, "measured")))
     return rc;
@@ -549,43 +604,18 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
   if (token_mass && (win->n_q_heads / kv->n_kv_heads) * win->n_rows > token_mass_max_rows())
     return fail(c, CKV_ERR_UNSUPPORTED, "token_mass supports at most %d window rows per KV head",
                 token_mass_max_rows());
-  DeviceGuard g(c->device);
-  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
+  return CKV_OK;
+}
 
-  const AttnGeom a = make_geom(kv, win);
-  const int D = a.D, n = pages->n_pages, total_rows = a.Hq * a.W;
-  const int rpb = rows_per_block_attention();
-  const int nrb = ceil_div(a.rows, rpb);
-  int n_splits = std::max(1, std::min(ceil_div(a.S, 64),
-                                      std::max(ceil_div(kTargetBlocks, a.Hkv * nrb), ceil_div(a.S, kMaxSplitTokens))));
-  const int chunk = (int)round_up(ceil_div(a.S, n_splits), 64);
-  n_splits = ceil_div(a.S, chunk);
-
-  AttnSplit sp{chunk, n_splits, nrb * rpb, nullptr, nullptr, nullptr, nullptr};
-  RowStats rs{o, nullptr, nullptr, nullptr};
-  Plan plan;
-  const size_t nsr = (size_t)a.Hkv * n_splits * sp.rows_pad;
-  plan.add(&sp.part_o, nsr * D);
-  plan.add(&sp.part_m, nsr);
-  plan.add(&sp.part_l, nsr);
-  plan.add(&sp.part_c, nsr);
-  if (!o) plan.add(&rs.o, (size_t)total_rows * D);
-  plan.add(&rs.lse2, total_rows);
-  plan.add(&rs.onorm, total_rows);
-  plan.add(&rs.nvis, total_rows);
-  int *fix_list = nullptr, *fix_count = nullptr;
-  plan.add(&fix_list, 4 * (size_t)total_rows);
-  plan.add(&fix_count, 1);
-  float* fpart = nullptr;
-  plan.add(&fpart, (size_t)total_rows * ckv::kFixParts * (D + 1));
-  const int32_t *dstart = nullptr, *dlen = nullptr;
-  if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
-  if ((rc = realize(c, plan))) return rc;
-
-  CKV_LAUNCH(c, "window_attention", launch_window_attention(a, sp, c->stream));
+// the kernels of one measurement call, enqueued on the context's stream
+int enqueue_measure(ckv_ctx* c, const AttnGeom& a, const MeasureBufs& b, const int32_t* dstart,
+                    const int32_t* dlen, const ckv_page_list* pages, float* R, float* R_head, float* lse,
+                    float* token_mass) {
+  const int n = pages->n_pages, total_rows = a.Hq * a.W;
+  CKV_LAUNCH(c, "window_attention", launch_window_attention(a, b.sp, c->stream));
   ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
-              token_mass ? (size_t)a.S : 0, fix_count, nullptr, 0};
-  CKV_LAUNCH(c, "combine", launch_combine(a, sp, rs, lse, zl, c->stream));
+              token_mass ? (size_t)a.S : 0, b.fix_count, nullptr, 0};
+  CKV_LAUNCH(c, "combine", launch_combine(a, b.sp, b.rs, lse, zl, c->stream));
   if (n > 0) {
     PageWork pw{};
     pw.start = dstart;
@@ -599,18 +629,40 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
     pw.lse_scale = 1.f;
     pw.Hq = a.Hq;
     pw.total_rows = total_rows;
-    pw.fix_list = fix_list;
-    pw.fix_count = fix_count;
+    pw.fix_list = b.fix_list;
+    pw.fix_count = b.fix_count;
     pw.fix_cap = total_rows;
     pw.fix_a = ckv::kFixA;
-    CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, rs, 0, max_page_len(pages), c->stream));
-    CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, sp, rs, pw, fpart, ckv::kFixParts, c->stream));
+    CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, b.rs, 0, max_page_len(pages), c->stream));
+    CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, b.sp, b.rs, pw, b.fpart, ckv::kFixParts, 0, c->stream));
   }
   if (token_mass) {
     const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kMassBlocks / a.Hkv)), 64);
-    CKV_LAUNCH(c, "token_mass", launch_token_mass(a, rs, token_mass, mchunk, c->stream));
+    CKV_LAUNCH(c, "token_mass", launch_token_mass(a, b.rs, token_mass, mchunk, c->stream));
   }
   return CKV_OK;
+}
+
+}  // namespace
+
+extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win,
+                                        const ckv_page_list* pages, float* R, float* R_head, float* o,
+                                        float* lse, float* token_mass) {
+  if (!c) return CKV_ERR_ARG;
+  begin_call(c);
+  int rc;
+  if ((rc = check_measure(c, kv, win, pages, R, token_mass))) return rc;
+  DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
+
+  const AttnGeom a = make_geom(kv, win);
+  Plan plan;
+  MeasureBufs b;
+  plan_measure(a, default_splits(a), o, plan, b);
+  const int32_t *dstart = nullptr, *dlen = nullptr;
+  if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
+  if ((rc = realize(c, plan))) return rc;
+  return enqueue_measure(c, a, b, dstart, dlen, pages, R, R_head, lse, token_mass);
 }
 
 extern "C" int ckv_measure_page_effects_batch(ckv_ctx* c, int32_t n, const ckv_kv_view* kv,
@@ -618,7 +670,7 @@ extern "C" int ckv_measure_page_effects_batch(ckv_ctx* c, int32_t n, const ckv_k
                                               float* const* R, float* const* R_head, float* const* o,
                                               float* const* lse, float* const* token_mass) {
   if (!c) return CKV_ERR_ARG;
-  c->err.clear();
+  begin_call(c);
   if (n < 0 || (n > 0 && (!kv || !win || !pages || !R))) return fail(c, CKV_ERR_ARG, "batch: NULL arrays or n < 0");
   for (int i = 0; i < n; ++i) {
     int rc;
@@ -648,7 +700,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
                                     const ckv_page_list* pages, const float* o, const float* lse, float* R,
                                     float* R_head, float* token_mass) {
   if (!c) return CKV_ERR_ARG;
-  c->err.clear();
+  begin_call(c);
   int rc;
   if ((rc = check_kv(c, kv)) || (rc = check_win(c, win, kv)) || (rc = check_pages(c, pages, kv->n_tokens, "measured")))
     return rc;
@@ -673,13 +725,16 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
   int *fix_list = nullptr, *fix_count = nullptr;
   plan.add(&fix_list, 4 * (size_t)total_rows);
   plan.add(&fix_count, 1);
-  // pairs whose output without the page comes from the complement pass
-  const int cap2 = std::min(total_rows, ckv::kFixComplementCap);
+  // pairs whose output without the page comes from the complement pass: a
+  // row has at most one page with A > 0.5, so the list holds every row; the
+  // pass spreads its pairs over a fixed number of (pair, part) items
+  const int cap2 = total_rows;
+  const int items2 = std::max(ckv::kFixComplementItems, total_rows);
   int *list2 = nullptr, *count2 = nullptr;
   plan.add(&list2, 4 * (size_t)cap2);
   plan.add(&count2, 1);
   float* fpart = nullptr;
-  plan.add(&fpart, (size_t)cap2 * ckv::kFixPartsRow * (a.D + 1));
+  plan.add(&fpart, (size_t)items2 * (a.D + 1));
   const int32_t *dstart = nullptr, *dlen = nullptr;
   if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
   if ((rc = realize(c, plan))) return rc;
@@ -714,7 +769,8 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
     pw2.fix_count = count2;
     pw2.fix_cap = cap2;
     AttnSplit whole{(int)round_up(a.S, 64), 1, 0, nullptr, nullptr, nullptr, nullptr};
-    CKV_LAUNCH(c, "page_fixup_complement", launch_page_fixup(a, whole, rs, pw2, fpart, ckv::kFixPartsRow, c->stream));
+    CKV_LAUNCH(c, "page_fixup_complement",
+               launch_page_fixup(a, whole, rs, pw2, fpart, ckv::kFixPartsRow, items2, c->stream));
   }
   if (token_mass) {
     const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kMassBlocks / a.Hkv)), 64);
@@ -728,7 +784,7 @@ extern "C" int ckv_classify_pages(ckv_ctx* c, int32_t n, const float* R_pre, con
                                   uint8_t* lambda, float* P_pre, float* P_post, int32_t* cand,
                                   int32_t* n_cand) {
   if (!c) return CKV_ERR_ARG;
-  c->err.clear();
+  begin_call(c);
   if (n < 0) return fail(c, CKV_ERR_SHAPE, "n < 0");
   if (!n_cand) return fail(c, CKV_ERR_ARG, "n_cand is NULL");
   if (n > 0 && (!R_pre || !R_post || !lambda || !cand)) return fail(c, CKV_ERR_ARG, "NULL input or output array");
@@ -768,7 +824,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
                               const int32_t* n_cand, int32_t max_cand, float tau_joint, uint8_t* accepted,
                               float* union_R, int32_t* n_accepted) {
   if (!c) return CKV_ERR_ARG;
-  c->err.clear();
+  begin_call(c);
   int rc;
   if ((rc = check_kv(c, kv)) || (rc = check_win(c, win, kv)) || (rc = check_pages(c, pages, kv->n_tokens, "joint")))
     return rc;
@@ -801,6 +857,10 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   j.S = a.S;
   j.n_vis_slices = joint_vis_slices(a.S);
   j.test_cap = pages->n_pages > 0 ? max_cand : 0;
+  j.geo = a;
+  j.lse = lse;
+  j.n_pages = pages->n_pages;
+  j.cand = cand;
   float *resid, *resA, *Dst, *Ast;
   int *resC, *Cst;
   Plan plan;
@@ -814,9 +874,14 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   plan.add(&Cst, 2 * (size_t)total_rows);
   plan.add(&j.ctrl, 8);
   plan.add(&j.rbuf, kJointWindow);
+  plan.add(&j.in_acc, std::max(pages->n_pages, 1));
+  plan.add(&j.fix_list, 2 * (size_t)kJointWindow * total_rows);
+  plan.add(&j.fpart, (size_t)ckv::kJointFixItems * (D + 1));
   const int32_t *dstart = nullptr, *dlen = nullptr;
   if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
   if ((rc = realize(c, plan))) return rc;
+  j.pstart = dstart;
+  j.plen = dlen;
   j.resid = resid;
   j.resA = resA;
   j.resC = resC;
@@ -855,7 +920,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
 extern "C" int ckv_pool_scores(ckv_ctx* c, const float* score, float* out, int32_t n_seq, int64_t seq_stride,
                                const int32_t* n_tokens, int32_t kernel, int32_t mode) {
   if (!c) return CKV_ERR_ARG;
-  c->err.clear();
+  begin_call(c);
   if (n_seq < 0 || (n_seq > 0 && (!score || !out || !n_tokens)))
     return fail(c, CKV_ERR_ARG, "pool: NULL pointer or negative n_seq");
   if (kernel < 1 || kernel > 255 || kernel % 2 == 0) return fail(c, CKV_ERR_ARG, "pool: kernel must be odd, 1..255");
@@ -888,7 +953,7 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
                                       const ckv_cache_view* out, int32_t* kept_idx, int32_t* n_kept,
                                       uint8_t* token_state) {
   if (!c) return CKV_ERR_ARG;
-  c->err.clear();
+  begin_call(c);
   if (!in || !n_tokens || !score || !retired || !pending || !budget || !kept_idx || !n_kept)
     return fail(c, CKV_ERR_ARG, "NULL argument");
   if (in->n_seq < 1 || in->capacity < 1) return fail(c, CKV_ERR_SHAPE, "empty cache shape");

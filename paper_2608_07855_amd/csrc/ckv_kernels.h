@@ -95,12 +95,15 @@ hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowSt
                               int max_len, hipStream_t s);
 hipError_t launch_token_mass(const AttnGeom& a, const RowStats& rs, float* mass, int chunk,
                              hipStream_t s);
-// fpart: workspace [fix_cap][parts][D + 1] floats; each listed pair is spread
-// over `parts` workgroups
+// fpart: workspace of [fix_cap][parts][D + 1] floats, or of [item_budget][D + 1]
+// when item_budget > 0; each listed pair is spread over `parts` workgroups,
+// or, with an item budget, over min(parts, item_budget / pairs) of them (at
+// least 1, read from the device count), so every listed pair fits however
+// many there are (item_budget >= fix_cap)
 constexpr int kFixParts = 8;        // after the window pass: the page's own split(s)
 constexpr int kFixPartsRow = 32;    // recorded outputs: every other token of the row
 hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
-                             const PageWork& pw, float* fpart, int parts, hipStream_t s);
+                             const PageWork& pw, float* fpart, int parts, int item_budget, hipStream_t s);
 
 // recorded window outputs: row statistics from the caller's o and natural-log
 // lse (nvis_part: workspace [W][recorded_slices(S)] ints), and the fix-up of
@@ -112,7 +115,8 @@ hipError_t launch_recorded_rows(const AttnGeom& a, const float* o, const float* 
 hipError_t launch_page_fixup_recorded(const AttnGeom& a, const RowStats& rs, const PageWork& pw, int* list2,
                                       int* count2, int cap2, float a_hi, hipStream_t s);
 constexpr float kFixAComplement = 0.99f;   // recorded outputs: above this, the complement pass
-constexpr int kFixComplementCap = 1024;    // pairs the complement pass takes per call
+constexpr int kFixComplementItems = 32768; // (pair, part) items of the complement pass's workspace
+                                           // (at least one per window row)
 
 // classification (Eq. (8)-(10)) and candidate order
 struct ClassifyArgs {
@@ -160,7 +164,21 @@ struct JointArgs {
   uint8_t* accepted;
   float* union_R;
   int32_t* n_accepted;
+  // recomputation by definition of (candidate, row) pairs whose union mass
+  // exceeds kJointFixA (Eq. (6) is ill-conditioned there)
+  AttnGeom geo;           // the post-commit cache and window
+  const float* lse;       // [rows] natural-log log-sum-exp of each window row
+  const int32_t* pstart;  // [n_pages] page table (sorted, disjoint)
+  const int32_t* plen;
+  int n_pages;
+  const int32_t* cand;    // [max_cand] page of each candidate
+  uint8_t* in_acc;        // [n_pages] accepted so far (phase 0 clears it)
+  int* fix_list;          // [window * rows] (slot, row) pairs flagged in a round
+  float* fpart;           // [kJointFixItems][D + 1] partial sums of the fix-up
 };
+constexpr float kJointFixA = 0.9f;      // union mass above which a pair is recomputed
+constexpr int kJointFixItems = 32768;   // (pair, part) items of the fix-up workspace
+constexpr int kJointFixParts = 16;      // parts a pair's row is split into at most
 int joint_vis_slices(int S);
 hipError_t launch_joint_persistent(const JointArgs& j, int max_blocks, hipStream_t s);
 

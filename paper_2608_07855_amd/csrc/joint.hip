@@ -24,6 +24,15 @@
 // decides at least one candidate, so the loop ends within max_cand rounds.
 // A barrier wait is bounded: if the workgroups cannot all run at once (a
 // device shared with other work), every block leaves and *n_accepted = -1.
+//
+// A union that holds nearly all of a row's attention mass makes Eq. (6)
+// ill-conditioned: o - o^{\X} = D / (1 - A_X) divides float32 cancellation
+// by a small 1 - A_X.  A (candidate, row) pair whose union mass exceeds
+// kJointFixA is therefore left out of the closed form and listed; after the
+// round's tests every workgroup recomputes the listed pairs by definition --
+// the row's output over the tokens outside the union, o', in float32 from
+// the keys and values -- and the ratio ||o - o'|| / ||o|| joins the
+// candidate's maximum before the decision.
 #include "ckv_device.h"
 #include "ckv_kernels.h"
 
@@ -33,7 +42,7 @@
 namespace ckv {
 
 // control words (cleared by the residual pass before this kernel starts)
-enum { kCursor = 0, kPending = 1, kBarrier = 2, kError = 3, kParity = 4 };
+enum { kCursor = 0, kPending = 1, kBarrier = 2, kError = 3, kParity = 4, kFixN = 5 };
 constexpr long long kBarrierTimeoutTicks = 1ll << 27;   // ~1.3 s of the 100 MHz wall clock
 constexpr int kVisSlice = 8192;                         // tokens per visible-count item
 
@@ -119,9 +128,19 @@ __device__ void joint_item(const JointArgs& j, const RowStats& rs, int jx, int r
       const float on = rs.onorm[row];
       int nv = 0;
       for (int q = 0; q < j.n_vis_slices; ++q) nv += j.nvis_part[(row % j.W) * j.n_vis_slices + q];
-      if (Ct >= nv || !(keep > 0.f)) ratio = INFINITY;
-      else if (on > 0.f) ratio = sqrtf(n2) / (keep * on);
-      else ratio = n2 > 0.f ? INFINITY : 0.f;
+      if (Ct >= nv) {
+        ratio = INFINITY;
+      } else if (At > kJointFixA) {
+        // recomputed by definition after the round's tests
+        if (lane == 0) {
+          const int slot = atomicAdd(&j.ctrl[kFixN], 1);
+          if (slot < j.window * j.total_rows) reinterpret_cast<int2*>(j.fix_list)[slot] = make_int2(jx, row);
+        }
+      } else if (on > 0.f) {
+        ratio = sqrtf(n2) / (keep * on);
+      } else {
+        ratio = n2 > 0.f ? INFINITY : 0.f;
+      }
     }
     wmax = fmaxf(wmax, ratio);
   }
@@ -131,9 +150,127 @@ __device__ void joint_item(const JointArgs& j, const RowStats& rs, int jx, int r
   __syncthreads();
 }
 
+// Fix-up of listed pairs e0 .. e0 + np - 1, `parts` items per pair: item
+// (e, part) sums w_i and w_i v_i over its slice of the row's tokens that are
+// visible and outside the union (accepted pages and the candidate's page),
+// with w_i = 2^(x_i - lse) <= 1, and writes the (D + 1) sums to fpart.
+// Thread layout: D / 8 threads per token (16 bytes of its key and value
+// each), 256 / (D / 8) tokens per round.
+template <int D, bool PG>
+__device__ void joint_fix_partial(const JointArgs& j, int cursor, int e0, int np, int parts, float* sacc) {
+  constexpr int TPR = D / 8, RPR = 256 / TPR;
+  const AttnGeom& a = j.geo;
+  const int tid = threadIdx.x, c = tid % TPR, r = tid / TPR;
+  for (int item = blockIdx.x; item < np * parts; item += gridDim.x) {
+    const int e = e0 + item / parts, part = item % parts;
+    const int2 ent = reinterpret_cast<const int2*>(j.fix_list)[e];
+    const int rg = ent.y;
+    const int cp = j.cand[cursor + ent.x];   // the candidate's page
+    const int h = rg / a.W, p = rg % a.W, g = h / a.group;
+    const int qp = a.qpos[p];
+    const float ref = j.lse[rg] * kLog2e;
+    const int seg = ((a.S + parts - 1) / parts + RPR - 1) / RPR * RPR;
+    const int a0 = part * seg, a1 = min(a.S, a0 + seg);
+    const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
+    const uint16_t* vh = a.v + (int64_t)g * a.kv_head_stride;
+    const u32x4 qc = ldg_u4(a.q + (int64_t)h * a.q_head_stride + (int64_t)p * a.q_row_stride + 8 * c);
+    float qv[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) qv[m] = bf16_bits_to_float(chunk_elem(qc, m));
+    float acc[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) acc[m] = 0.f;
+    float lacc = 0.f;
+    // first page whose end lies past this thread's first token
+    int pp = 0;
+    {
+      int lo = 0, hi = j.n_pages;
+      const int t0 = a0 + r;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (j.pstart[mid] + j.plen[mid] <= t0) lo = mid + 1;
+        else hi = mid;
+      }
+      pp = lo;
+    }
+    for (int b0 = a0; b0 < a1; b0 += RPR) {
+      const int t = b0 + r;
+      const int tt = min(t, a1 - 1);
+      const int64_t row = PG ? (int64_t)min((uint32_t)a.slot[tt], a.pool_last) : tt;
+      const u32x4 kc = ldg_u4(kh + row * a.kv_tok_stride + 8 * c);
+      const u32x4 vc = ldg_u4(vh + row * a.kv_tok_stride + 8 * c);
+      float x = 0.f;
+#pragma unroll
+      for (int m = 0; m < 8; ++m) x = __builtin_fmaf(qv[m], bf16_bits_to_float(chunk_elem(kc, m)), x);
+#pragma unroll
+      for (int off = TPR / 2; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+      while (pp < j.n_pages && j.pstart[pp] + j.plen[pp] <= tt) ++pp;
+      const bool in_union = pp < j.n_pages && j.pstart[pp] <= tt && (pp == cp || j.in_acc[pp] != 0);
+      const bool keep = t < a1 && ldg_i32(a.pos + tt) <= qp && !in_union;
+      const float w = keep ? __builtin_amdgcn_exp2f(__builtin_fmaf(x, a.sl2, -ref)) : 0.f;
+#pragma unroll
+      for (int m = 0; m < 8; ++m) acc[m] = __builtin_fmaf(w, bf16_bits_to_float(chunk_elem(vc, m)), acc[m]);
+      if (c == 0) lacc += w;
+    }
+#pragma unroll
+    for (int m = 0; m < 8; ++m) sacc[r * (D + 1) + 8 * c + m] = acc[m];
+    if (c == 0) sacc[r * (D + 1) + D] = lacc;
+    __syncthreads();
+    // the item's sums: token rows added in order
+    float* out = j.fpart + ((size_t)(e - e0) * parts + part) * (D + 1);
+    for (int i = tid; i <= D; i += 256) {
+      float v = 0.f;
+      for (int k = 0; k < RPR; ++k) v += sacc[k * (D + 1) + i];
+      out[i] = v;
+    }
+    __syncthreads();
+  }
+}
+
+// One wave per listed pair: parts added in order, o' = sum w v / sum w and
+// ||o - o'|| / ||o|| raised into the candidate's round maximum.
+template <int D>
+__device__ void joint_fix_final(const JointArgs& j, int e0, int np, int parts) {
+  const int lane = threadIdx.x & 63;
+  for (int e = e0 + blockIdx.x * 4 + (threadIdx.x >> 6); e < e0 + np; e += gridDim.x * 4) {
+    const int2 ent = reinterpret_cast<const int2*>(j.fix_list)[e];
+    const int rg = ent.y;
+    const float* fp = j.fpart + (size_t)(e - e0) * parts * (D + 1);
+    float num[D / 64], den = 0.f;
+#pragma unroll
+    for (int m = 0; m < D / 64; ++m) num[m] = 0.f;
+    for (int part = 0; part < parts; ++part) {
+#pragma unroll
+      for (int m = 0; m < D / 64; ++m) num[m] += fp[part * (D + 1) + lane + 64 * m];
+      den += fp[part * (D + 1) + D];
+    }
+    float dd = 0.f, oo = 0.f;
+#pragma unroll
+    for (int m = 0; m < D / 64; ++m) {
+      const float ov = j.o[(size_t)rg * D + lane + 64 * m];
+      const float od = den > 0.f ? num[m] / den : 0.f;
+      dd += (ov - od) * (ov - od);
+      oo += ov * ov;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      dd += __shfl_xor(dd, off, 64);
+      oo += __shfl_xor(oo, off, 64);
+    }
+    if (lane == 0) {
+      float ratio;
+      if (!(den > 0.f)) ratio = INFINITY;
+      else if (oo > 0.f) ratio = sqrtf(dd) / sqrtf(oo);
+      else ratio = dd > 0.f ? INFINITY : 0.f;
+      atomicMax(&j.rbuf[ent.x], __float_as_uint(ratio));
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs) {
   __shared__ unsigned int smax;
   __shared__ int s_ok, s_part[4];
+  __shared__ float sacc[32 * 65];    // fix-up: RPR token rows x (D + 1) sums (16 x 129 for D = 128)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const size_t gsz = (size_t)gridDim.x * blockDim.x;
@@ -148,6 +285,7 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
   for (size_t i = gid; i < (size_t)j.total_rows * j.D; i += gsz) j.Dstate[i] = 0.f;
   for (size_t i = gid; i < (size_t)j.total_rows; i += gsz) { j.Astate[i] = 0.f; j.Cstate[i] = 0; }
   for (size_t i = gid; i < (size_t)j.window; i += gsz) j.rbuf[i] = 0u;
+  for (size_t i = gid; i < (size_t)j.n_pages; i += gsz) j.in_acc[i] = 0;
   if (gid == 0) {
     j.ctrl[kCursor] = 0;
     j.ctrl[kPending] = -1;
@@ -198,6 +336,34 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
       if (threadIdx.x == 0) *j.n_accepted = -1;
       return;
     }
+    // listed pairs, recomputed by definition in chunks that fit the
+    // workspace (the same count and chunks in every block)
+    const int nfix = min(__hip_atomic_load(&j.ctrl[kFixN], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+                         j.window * j.total_rows);
+    for (int e0 = 0; e0 < nfix; e0 += kJointFixItems) {
+      const int np = min(nfix - e0, kJointFixItems);
+      const int parts = max(1, min(kJointFixParts, kJointFixItems / np));
+      const bool pg = j.geo.slot != nullptr;
+      if (j.D == 128) {
+        if (pg) joint_fix_partial<128, true>(j, cursor, e0, np, parts, sacc);
+        else joint_fix_partial<128, false>(j, cursor, e0, np, parts, sacc);
+      } else {
+        if (pg) joint_fix_partial<64, true>(j, cursor, e0, np, parts, sacc);
+        else joint_fix_partial<64, false>(j, cursor, e0, np, parts, sacc);
+      }
+      target += gridDim.x;
+      if (!grid_barrier(j.ctrl, target, &s_ok)) {
+        if (threadIdx.x == 0) *j.n_accepted = -1;
+        return;
+      }
+      if (j.D == 128) joint_fix_final<128>(j, e0, np, parts);
+      else joint_fix_final<64>(j, e0, np, parts);
+      target += gridDim.x;
+      if (!grid_barrier(j.ctrl, target, &s_ok)) {
+        if (threadIdx.x == 0) *j.n_accepted = -1;
+        return;
+      }
+    }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
       // the first passer in order is accepted, the ones before it rejected
       int cur = cursor, acc = -1;
@@ -211,10 +377,13 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
           j.accepted[tt] = 1;
           acc = tt;
           *j.n_accepted += 1;
+          const int ap = j.cand[tt];
+          if (ap >= 0 && ap < j.n_pages) j.in_acc[ap] = 1;
           break;
         }
       }
       for (int k = 0; k < j.window; ++k) __hip_atomic_store(&j.rbuf[k], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&j.ctrl[kFixN], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&j.ctrl[kCursor], cur, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&j.ctrl[kPending], acc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&j.ctrl[kParity], par ^ 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -799,15 +799,21 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
 constexpr int kFixT = 256;        // threads of a fix-up workgroup
 constexpr int kFixGrid = 1024;    // (pair, part) items in flight
 
+// parts per listed pair: fixed, or within an item budget for n pairs
+__device__ __forceinline__ int fix_parts(int parts, int item_budget, int n) {
+  return item_budget > 0 ? max(1, min(parts, item_budget / max(n, 1))) : parts;
+}
+
 template <int D, bool PG>
 __global__ __launch_bounds__(kFixT) void page_fixup_partial(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw,
-                                                            float* fpart, int parts) {
+                                                            float* fpart, int parts, int item_budget) {
   constexpr int TPR = D / 8;                  // threads per token row (16 bytes each)
   constexpr int RPR = kFixT / TPR;            // token rows per round
   constexpr int UNR = 128 / RPR;              // rounds whose loads are in flight together
   __shared__ float sacc[RPR][D + 1];
   const int tid = threadIdx.x, c = tid % TPR, r = tid / TPR;
   const int n = min(*pw.fix_count, pw.fix_cap);
+  parts = fix_parts(parts, item_budget, n);
   for (int item = blockIdx.x; item < n * parts; item += gridDim.x) {
     const int e = item / parts, part = item % parts;
     // entry: page, global row, page start, page length
@@ -900,9 +906,10 @@ __global__ __launch_bounds__(kFixT) void page_fixup_partial(AttnGeom a, AttnSpli
 // one wave per listed pair: parts added in order, ratio ||o - o'|| / ||o||
 template <int D>
 __global__ __launch_bounds__(256) void page_fixup_final(AttnGeom a, RowStats rs, PageWork pw, const float* fpart,
-                                                        int parts) {
+                                                        int parts, int item_budget) {
   const int lane = threadIdx.x & 63;
   const int n = min(*pw.fix_count, pw.fix_cap);
+  parts = fix_parts(parts, item_budget, n);
   for (int e = blockIdx.x * 4 + (threadIdx.x >> 6); e < n; e += gridDim.x * 4) {
     const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
     const int page = ent.x, rg = ent.y, h = rg / a.W;
@@ -1271,18 +1278,19 @@ hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowSt
 }
 
 hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
-                             const PageWork& pw, float* fpart, int parts, hipStream_t s) {
+                             const PageWork& pw, float* fpart, int parts, int item_budget, hipStream_t s) {
   dim3 grid(std::max(1, std::min(pw.fix_cap * parts, kFixGrid))), block(kFixT);
   dim3 grid2(std::max(1, std::min((pw.fix_cap + 3) / 4, 256))), block2(256);
   const bool pg = a.slot != nullptr;
+  const int ib = item_budget;
   if (a.D == 128) {
-    if (pg) hipLaunchKernelGGL((page_fixup_partial<128, true>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
-    else hipLaunchKernelGGL((page_fixup_partial<128, false>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
-    hipLaunchKernelGGL((page_fixup_final<128>), grid2, block2, 0, s, a, rs, pw, fpart, parts);
+    if (pg) hipLaunchKernelGGL((page_fixup_partial<128, true>), grid, block, 0, s, a, sp, rs, pw, fpart, parts, ib);
+    else hipLaunchKernelGGL((page_fixup_partial<128, false>), grid, block, 0, s, a, sp, rs, pw, fpart, parts, ib);
+    hipLaunchKernelGGL((page_fixup_final<128>), grid2, block2, 0, s, a, rs, pw, fpart, parts, ib);
   } else {
-    if (pg) hipLaunchKernelGGL((page_fixup_partial<64, true>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
-    else hipLaunchKernelGGL((page_fixup_partial<64, false>), grid, block, 0, s, a, sp, rs, pw, fpart, parts);
-    hipLaunchKernelGGL((page_fixup_final<64>), grid2, block2, 0, s, a, rs, pw, fpart, parts);
+    if (pg) hipLaunchKernelGGL((page_fixup_partial<64, true>), grid, block, 0, s, a, sp, rs, pw, fpart, parts, ib);
+    else hipLaunchKernelGGL((page_fixup_partial<64, false>), grid, block, 0, s, a, sp, rs, pw, fpart, parts, ib);
+    hipLaunchKernelGGL((page_fixup_final<64>), grid2, block2, 0, s, a, rs, pw, fpart, parts, ib);
   }
   return hipGetLastError();
 }

@@ -142,3 +142,66 @@ def test_stress_forced_pages_small(ckv):
     uR = out["union_R"].cpu().numpy()[:nc]
     print(f"[joint] stress: {acc.sum()} of {nc} accepted")
     _check_replay(L, cand, acc, uR, 0.01, method="closed")
+
+
+def _dominant_union_layer(seed=31):
+    """One KV head shared by 4 query heads (d 128, 1536 tokens, 8 window rows,
+    32 pages of 32 tokens).  Page 3's keys follow query row (head 0, row 0),
+    so that page alone carries > 0.99 of the row's mass; pages 10 and 11
+    follow row (head 1, row 2) so that each carries just under half of it and
+    their union > 0.9 (Eq. (6) is ill-conditioned there)."""
+    rng = np.random.default_rng(seed)
+    S, d, Hq, W = 1536, 128, 4, 8
+    q = bf16_bits(rng.standard_normal((Hq, W, d)).astype(np.float32))
+    qf = O.as_f64(q)
+    k = rng.standard_normal((1, S, d))
+    k[0, 352:384] = qf[0, 0] + 0.05 * rng.standard_normal((32, d))
+    k[0, 576:640] = 0.57 * qf[1, 2] + 0.05 * rng.standard_normal((64, d))
+    v = rng.standard_normal((1, S, d))
+    kb, vb = bf16_bits(k.astype(np.float32)), bf16_bits(v.astype(np.float32))
+    pos = np.arange(S, dtype=np.int32)
+    qpos = np.arange(S, S + W, dtype=np.int32)
+    pages = [(256 + 32 * i, 32) for i in range(32)]
+    return kb, vb, q, pos, qpos, pages
+
+
+def _union_mass(kb, vb, q, pos, qpos, pages, members, h, p):
+    K, V, Q = O.as_f64(kb), O.as_f64(vb), O.as_f64(q)
+    s = O.head_logits(Q[h], K[0], 1 / np.sqrt(K.shape[2]))
+    a, _ = O.attend(s, O.visibility(pos, qpos), V[0])
+    return float(sum(a[p, st:st + ln].sum() for st, ln in (pages[j] for j in members)))
+
+
+@pytest.mark.parametrize("order,tau", [([10, 3, 11, 0, 1, 5], 1e30), ([0, 3, 1, 10, 11, 2, 4], 0.5),
+                                       ([3, 10, 11, 6], 1e30)])
+def test_joint_dominant_union(ckv, order, tau):
+    """Unions whose mass in some row exceeds 0.9 (a dominant candidate with
+    A > 0.99, and two pages of about 0.47 each) are recomputed by definition
+    (Eq. (6) through the output without the union); every union effect is
+    replayed by brute force at 2e-3 and every decision checked."""
+    P, ctx = ckv
+    kb, vb, q, pos, qpos, pages = _dominant_union_layer()
+    # the construction does what it says (oracle, fp64)
+    assert _union_mass(kb, vb, q, pos, qpos, pages, [3], 0, 0) > 0.99
+    a10 = _union_mass(kb, vb, q, pos, qpos, pages, [10], 1, 2)
+    a_pair = _union_mass(kb, vb, q, pos, qpos, pages, [10, 11], 1, 2)
+    assert a10 < 0.9 < a_pair, (a10, a_pair)
+    print(f"[joint] dominant union: order={order} tau={tau} A(10)={a10:.4f} A(10,11)={a_pair:.4f}", flush=True)
+    kv = P.kv_view(dev_bf16(kb), dev_bf16(vb), dev_i32(pos))
+    win = P.window_view(dev_bf16(q), dev_i32(qpos))
+    pl = P.Pages([p[0] for p in pages], [p[1] for p in pages])
+    m = P.ckv_measure_page_effects(ctx, kv, win, pl, want=("R", "o", "lse"))
+    cand = torch.tensor(order, dtype=torch.int32, device="cuda")
+    ncand = torch.tensor([len(order)], dtype=torch.int32, device="cuda")
+    out = P.ckv_joint_test(ctx, kv, win, m["o"], m["lse"], pl, cand, ncand, len(order), tau)
+    torch.cuda.synchronize()
+    acc = out["accepted"].cpu().numpy()
+    uR = out["union_R"].cpu().numpy()
+    assert int(out["n_accepted"].item()) == int(acc.sum())
+    print(f"[joint] accepted {acc.astype(int).tolist()} union_R {np.round(uR, 4).tolist()}", flush=True)
+    ref = O.joint_replay(kb, vb, pos, q, qpos, pages, order, acc, method="bruteforce")
+    assert_scores_close(uR, ref, "union_R (dominant unions)")
+    for t, (a, r) in enumerate(zip(acc, ref)):
+        if abs(r - tau) <= REL_TOL * tau:
+            continue
+        assert bool(a) == (r <= tau), f"step {t}: gpu {'accept' if a else 'reject'} but R_ref={r} tau={tau}"

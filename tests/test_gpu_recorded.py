@@ -223,3 +223,48 @@ def test_recorded_argument_errors(ckv):
     with pytest.raises(P.CKVError) as e:          # misaligned recorded outputs
         P.ckv_measure_recorded(ctx, kv, win, pages, o[1:], lse)
     assert e.value.code == -1
+
+
+def test_recorded_many_dominant_pairs(ckv):
+    """1280 window rows (32 query heads x 40 rows over 4 KV heads), each with
+    a page that carries > 0.99 of its mass: every (page, row) pair goes
+    through the complement pass (more pairs than the pass's 1024-pair
+    chunk), and R, R_head match the fp64 oracle at 2e-3."""
+    P, ctx = ckv
+    rng = np.random.default_rng(44)
+    S, d, Hq, Hkv, W = 2048, 128, 32, 4, 40
+    u = rng.standard_normal(d)
+    q = bf16_bits((u + 0.3 * rng.standard_normal((Hq, W, d))).astype(np.float32))
+    k = rng.standard_normal((Hkv, S, d))
+    pages = [(512 + 32 * i, 32) for i in range(32)]
+    dom = [3 + 5 * g for g in range(Hkv)]
+    for g, j in enumerate(dom):
+        st = pages[j][0]
+        k[g, st:st + 32] = u + 0.05 * rng.standard_normal((32, d))
+    v = rng.standard_normal((Hkv, S, d))
+    kb, vb = bf16_bits(k.astype(np.float32)), bf16_bits(v.astype(np.float32))
+    pos = np.arange(S, dtype=np.int32)
+    qpos = np.arange(S, S + W, dtype=np.int32)
+    o, lse, _ = O.window_outputs(kb, vb, pos, q, qpos)
+    # every row's dominant page holds > 0.99 of the mass (oracle, fp64)
+    K, V, Q = O.as_f64(kb), O.as_f64(vb), O.as_f64(q)
+    vis = O.visibility(pos, qpos)
+    amin = 1.0
+    for h in range(Hq):
+        g = h // (Hq // Hkv)
+        a, _ = O.attend(O.head_logits(Q[h], K[g], 1 / np.sqrt(d)), vis, V[g])
+        st = pages[dom[g]][0]
+        amin = min(amin, float(a[:, st:st + 32].sum(1).min()))
+    print(f"[recorded] many dominant pairs: {Hq * W} rows, smallest dominant mass {amin:.5f}", flush=True)
+    assert amin > 0.99
+    from tests.gpu_util import dev_bf16, dev_i32, assert_scores_close
+    kv = P.kv_view(dev_bf16(kb), dev_bf16(vb), dev_i32(pos))
+    win = P.window_view(dev_bf16(q), dev_i32(qpos))
+    pl = P.Pages([p[0] for p in pages], [p[1] for p in pages])
+    out = P.ckv_measure_recorded(ctx, kv, win, pl, torch.from_numpy(np.ascontiguousarray(o, np.float32)).cuda(),
+                                 torch.from_numpy(np.ascontiguousarray(lse, np.float32)).cuda(),
+                                 want=("R", "R_head"))
+    torch.cuda.synchronize()
+    R, Rh = O.page_effects(kb, vb, pos, q, qpos, pages, method="closed")
+    assert_scores_close(out["R"].cpu().numpy(), R, "R (many dominant pairs)")
+    assert_scores_close(out["R_head"].cpu().numpy().reshape(Rh.shape), Rh, "R_head (many dominant pairs)")
