@@ -274,6 +274,32 @@ int ckv_measure_page_effects(ckv_ctx* ctx, const ckv_kv_view* kv,
                              float* token_mass);
 
 /*
+ * ckv_measure_page_effects for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same arguments, outputs and errors, but the call allocates
+ * nothing -- no hipMalloc/hipFree, no pinned upload buffers, no events.  Its
+ * working memory (split partial sums, row statistics, fix-up lists and the
+ * page table, copied from the host arrays with hipMemcpyAsync) lives in one
+ * static device array of 64 MiB that the library holds on every GPU it runs
+ * on until the process ends.  When the split partials of the regular call
+ * would not fit, the window pass uses fewer, longer token splits (results
+ * then differ from the regular call's only by float32 summation order); a
+ * shape whose working memory exceeds 64 MiB even with one split fails with
+ * CKV_ERR_UNSUPPORTED before anything is enqueued.  Kernel timing is not
+ * recorded for this call.
+ *
+ * Every call on one GPU shares that GPU's array, and the array keeps the
+ * last call's contents (each call clears what it needs zeroed): two such
+ * calls whose work overlaps on one GPU (two contexts on two streams without
+ * ordering between them) race and give undefined results.
+ */
+int ckv_measure_page_effects_noalloc(ckv_ctx* ctx, const ckv_kv_view* kv,
+                                     const ckv_window_view* win,
+                                     const ckv_page_list* pages, float* R,
+                                     float* R_head, float* o, float* lse,
+                                     float* token_mass);
+
+/*
  * Batched form of ckv_measure_page_effects for many (layer, sequence)
  * problems, such as every layer of every sequence in a batch: problem i
  * reads kv[i], win[i], pages[i] (arrays of n views) and writes R[i],

@@ -135,6 +135,10 @@ SIGNATURES = {
         ctypes.c_void_p, ctypes.POINTER(KVView), ctypes.POINTER(WindowView),
         ctypes.POINTER(PageList), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p]),
+    "ckv_measure_page_effects_noalloc": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.POINTER(KVView), ctypes.POINTER(WindowView),
+        ctypes.POINTER(PageList), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p]),
     "ckv_measure_page_effects_batch": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(KVView), ctypes.POINTER(WindowView),
         ctypes.POINTER(PageList), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,

@@ -218,9 +218,11 @@ def _f32(n, device, fill=None):
 
 def ckv_measure_page_effects(ctx: Context, kv: KVView, win: WindowView, pages: Pages, *,
                              R=None, R_head=None, o=None, lse=None, token_mass=None,
-                             want=("R",)):
+                             want=("R",), noalloc=False):
     """Window deletion effect of every page.  ``want`` names the optional
-    outputs to allocate when not given: "R_head", "o", "lse", "token_mass"."""
+    outputs to allocate when not given: "R_head", "o", "lse", "token_mass".
+    ``noalloc`` calls ckv_measure_page_effects_noalloc (the library allocates
+    nothing; outputs are still allocated here unless given)."""
     dev = torch.device("cuda", ctx.device)
     Hq, W, d = win.n_q_heads, win.n_rows, kv.head_dim
     if R is None:
@@ -234,9 +236,9 @@ def ckv_measure_page_effects(ctx: Context, kv: KVView, win: WindowView, pages: P
     if token_mass is None and "token_mass" in want:
         token_mass = _f32(kv.n_tokens, dev)
     pl = pages.view()
-    ctx.check(lib().ckv_measure_page_effects(
-        ctx.handle, ctypes.byref(kv), ctypes.byref(win), ctypes.byref(pl), _ptr(R),
-        _ptr(R_head), _ptr(o), _ptr(lse), _ptr(token_mass)))
+    fn = lib().ckv_measure_page_effects_noalloc if noalloc else lib().ckv_measure_page_effects
+    ctx.check(fn(ctx.handle, ctypes.byref(kv), ctypes.byref(win), ctypes.byref(pl), _ptr(R),
+                 _ptr(R_head), _ptr(o), _ptr(lse), _ptr(token_mass)))
     return dict(R=R[:pages.n], R_head=None if R_head is None else R_head[:pages.n * Hq].view(pages.n, Hq),
                 o=None if o is None else o.view(Hq, W, d),
                 lse=None if lse is None else lse.view(Hq, W), token_mass=token_mass)

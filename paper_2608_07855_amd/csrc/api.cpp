@@ -15,6 +15,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -24,6 +25,7 @@ using namespace ckv;
 namespace {
 
 constexpr size_t kAlign = 256;
+constexpr int kMaxDevices = 64;
 constexpr int kPinnedSlots = 4;
 constexpr int kPageCacheEntries = 16;
 constexpr float kLog2eHost = 1.4426950408889634f;   // log2(e): natural-log LSE to log2 units
@@ -67,6 +69,14 @@ struct Plan {
 
 }  // namespace
 
+// Static device scratch of the allocation-free measurement call: every GPU
+// the library runs on holds one copy for the life of the process.  In host
+// code `scratch` names a host-side stand-in, not device memory: its device
+// address (per device) comes from hipGetSymbolAddress at context creation,
+// and only that address is ever handed to kernels or copies.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 struct ckv_ctx {
   int device = 0;
   hipStream_t stream = nullptr;
@@ -85,6 +95,8 @@ struct ckv_ctx {
   int sel_seq = 0;
   int sel_resident = -1;     // workgroups of the grid selection resident at once
   uint32_t policy = 0;       // CKV_POLICY_* switches (Sec. 4.4 variants)
+  void* scratch = nullptr;   // device address of the static scratch on this device
+  std::string scratch_err;
   // kernel timing (events around every launch when enabled)
   bool timing = false;
   std::string timing_only;   // empty: every kernel
@@ -441,6 +453,29 @@ extern "C" int ckv_create(ckv_ctx** out, int device, void* hip_stream) {
   if (!c) return CKV_ERR_NOMEM;
   c->device = device;
   c->stream = static_cast<hipStream_t>(hip_stream);
+  {
+    // the static scratch's address on this device, looked up once per device
+    // with the device current
+    static std::mutex mu;
+    static void* addr[kMaxDevices];
+    static hipError_t err[kMaxDevices];
+    static bool done[kMaxDevices];
+    std::lock_guard<std::mutex> lock(mu);
+    if (device < kMaxDevices) {
+      if (!done[device]) {
+        DeviceGuard g(device);
+        void* p = nullptr;
+        err[device] = g.ok ? hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) : hipErrorInvalidDevice;
+        if (err[device] != hipSuccess) (void)hipGetLastError();
+        addr[device] = err[device] == hipSuccess ? p : nullptr;
+        done[device] = true;
+      }
+      c->scratch = addr[device];
+      if (!c->scratch) c->scratch_err = hipGetErrorString(err[device]);
+    } else {
+      c->scratch_err = "device index beyond the scratch table";
+    }
+  }
   *out = c;
   return CKV_OK;
 }
@@ -663,6 +698,54 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
   if ((rc = page_table(c, pages, &dstart, &dlen))) return rc;
   if ((rc = realize(c, plan))) return rc;
   return enqueue_measure(c, a, b, dstart, dlen, pages, R, R_head, lse, token_mass);
+}
+
+extern "C" int ckv_measure_page_effects_noalloc(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win,
+                                                const ckv_page_list* pages, float* R, float* R_head, float* o,
+                                                float* lse, float* token_mass) {
+  if (!c) return CKV_ERR_ARG;
+  begin_call(c);
+  int rc;
+  if ((rc = check_measure(c, kv, win, pages, R, token_mass))) return rc;
+  DeviceGuard g(c->device);
+  if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
+  if (!c->scratch) return fail(c, CKV_ERR_HIP, "the device's static scratch is unavailable: %s", c->scratch_err.c_str());
+
+  const AttnGeom a = make_geom(kv, win);
+  const int n = pages->n_pages;
+  const size_t table = round_up(std::max<size_t>(2 * (size_t)n * sizeof(int32_t), 1), kAlign);
+  // as many splits as the regular call uses, fewer if the split partials
+  // would not fit the static scratch
+  int splits = default_splits(a);
+  Plan plan;
+  MeasureBufs b;
+  for (;; --splits) {
+    plan = Plan();
+    plan_measure(a, splits, o, plan, b);
+    if (table + plan.total <= kScratchBytes || splits == 1) break;
+  }
+  if (table + plan.total > kScratchBytes)
+    return fail(c, CKV_ERR_UNSUPPORTED,
+                "the allocation-free call needs %zu bytes of scratch for this shape; it holds %zu",
+                table + plan.total, (size_t)kScratchBytes);
+  char* base = static_cast<char*>(c->scratch);
+  int32_t* dtab = reinterpret_cast<int32_t*>(base);
+  size_t off = table;
+  for (auto& it : plan.items) {
+    *it.dst = base + off;
+    off += round_up(std::max<size_t>(it.bytes, 1), kAlign);
+  }
+  if (n > 0) {
+    CKV_HIP(c, hipMemcpyAsync(dtab, pages->start, n * sizeof(int32_t), hipMemcpyHostToDevice, c->stream));
+    CKV_HIP(c, hipMemcpyAsync(dtab + n, pages->len, n * sizeof(int32_t), hipMemcpyHostToDevice, c->stream));
+  }
+  // no kernel timing here: its events are created on demand
+  const bool timing = c->timing;
+  c->timing = false;
+  rc = enqueue_measure(c, a, b, n > 0 ? dtab : nullptr, n > 0 ? dtab + n : nullptr, pages, R, R_head, lse,
+                       token_mass);
+  c->timing = timing;
+  return rc;
 }
 
 extern "C" int ckv_measure_page_effects_batch(ckv_ctx* c, int32_t n, const ckv_kv_view* kv,
