@@ -158,6 +158,16 @@ def test_retired_on_device(ckv):
     _run(P, ctx, 2, 2, 2, 128, 6000, [6000, 4100], 1200, seed=6, keep_recent=64, accepted=True)
 
 
+def test_many_sequences_with_accepted_pages(ckv):
+    """20 sequences, each with its own device page table of accepted
+    candidates: the call takes 20 page-table copies plus the argument blob
+    that points at them, more than the copy cache's 16 entries, and none of
+    the copies this call uses may be evicted before its kernels run."""
+    P, ctx = ckv
+    lens = [2500 + 37 * s for s in range(20)]
+    _run(P, ctx, 20, 1, 1, 64, 3300, lens, 900, seed=11, keep_recent=16, accepted=True)
+
+
 def test_unequal_sequences(ckv):
     """32768 and 20001 tokens in one call: the shorter sequence's last
     2048-token chunks are empty but still take part in its phases; with
