@@ -34,6 +34,13 @@
  *    the call's work (ckv_sync, or stream/event synchronisation).
  *  - Counts produced on the device (n_cand, n_accepted, n_kept) stay on the
  *    device so that calls can be chained without host round trips.
+ *  - Errors found on the device: a NaN or infinite value that reaches a
+ *    window row's output or log-sum-exp (non-finite keys, values or queries,
+ *    or non-finite recorded outputs) latches a flag the context keeps in
+ *    pinned host memory.  ckv_sync returns CKV_ERR_NONFINITE after the wait,
+ *    and so does the first call that starts after the detecting kernel has
+ *    finished (that call then enqueues nothing); either clears the flag.
+ *    The outputs of the call whose inputs were non-finite are not valid.
  *  - Return value: CKV_OK (0) or a negative ckv_status.  No C++ exception
  *    crosses the ABI.  ckv_last_error() gives a message for the last failure
  *    on the context.
@@ -65,7 +72,7 @@ typedef enum ckv_status {
   CKV_ERR_UNSUPPORTED = -4, /* valid request outside what this build handles */
   CKV_ERR_NOMEM = -5,       /* workspace allocation failed or exceeds the limit */
   CKV_ERR_HIP = -6,         /* a HIP runtime call failed */
-  CKV_ERR_NONFINITE = -7    /* reserved: non-finite input detected on device */
+  CKV_ERR_NONFINITE = -7    /* non-finite input detected on the device (latched) */
 } ckv_status;
 
 /* Lifecycle states, Sec. 3.2 Eq. (10). */
@@ -238,6 +245,22 @@ typedef enum ckv_policy_flag {
 int ckv_set_policy(ckv_ctx* ctx, uint32_t flags);
 /* The context's current switches (0 for a NULL context). */
 uint32_t ckv_get_policy(const ckv_ctx* ctx);
+
+/*
+ * Bound of one grid-wide wait (microseconds of the device wall clock) in the
+ * one-launch kernels of ckv_joint_test (Algorithm 1's sequential rounds) and
+ * of the grid selection in ckv_select_and_compact.  Their workgroups
+ * synchronise through counters in device memory, which needs every
+ * workgroup resident at once; on a device shared with other work that may
+ * not hold, and a wait that passes the bound makes every workgroup of the
+ * call leave, with *n_accepted = -1 or n_kept[s] = -1 as the result (the
+ * outputs are then not valid; the lifecycle driver turns it into
+ * CKV_ERR_UNSUPPORTED).  Default 1342177 us (about 1.3 s).  0 makes a wait
+ * give up at once unless every workgroup has already arrived, which forces
+ * the failure path (for tests of the caller's handling).  Returns
+ * CKV_ERR_ARG for a negative or absurd value.
+ */
+int ckv_set_barrier_timeout_us(ckv_ctx* ctx, int64_t us);
 
 /* ------------------------------------------------------------- the calls */
 

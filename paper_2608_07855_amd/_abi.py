@@ -124,6 +124,7 @@ SIGNATURES = {
     "ckv_workspace_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
     "ckv_set_policy": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_uint32]),
     "ckv_get_policy": (ctypes.c_uint32, [ctypes.c_void_p]),
+    "ckv_set_barrier_timeout_us": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64]),
     "ckv_set_kernel_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
     "ckv_set_kernel_timing_only": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_char_p]),
     "ckv_kernel_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32,

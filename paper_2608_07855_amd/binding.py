@@ -77,6 +77,11 @@ class Context:
             bits |= _abi.POLICY_BITS[n]
         self.check(self._lib.ckv_set_policy(self.handle, bits))
 
+    def set_barrier_timeout_us(self, us: int):
+        """Bound of a grid-wide wait in the joint test and the grid
+        selection (0: give up unless every workgroup has arrived)."""
+        self.check(self._lib.ckv_set_barrier_timeout_us(self.handle, int(us)))
+
     def policy(self) -> int:
         return int(self._lib.ckv_get_policy(self.handle))
 

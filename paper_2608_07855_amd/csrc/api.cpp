@@ -95,6 +95,11 @@ struct ckv_ctx {
   int sel_seq = 0;
   int sel_resident = -1;     // workgroups of the grid selection resident at once
   uint32_t policy = 0;       // CKV_POLICY_* switches (Sec. 4.4 variants)
+  long long barrier_ticks = ckv::kBarrierTicksDefault;   // grid-barrier wait bound
+  // latched non-finite flag: a pinned, device-mapped host word the kernels
+  // set; reported (and cleared) by the next call or by ckv_sync
+  volatile uint32_t* nf_host = nullptr;
+  uint32_t* nf_dev = nullptr;
   void* scratch = nullptr;   // device address of the static scratch on this device
   std::string scratch_err;
   // kernel timing (events around every launch when enabled)
@@ -166,6 +171,16 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 void begin_call(ckv_ctx* c) {
   c->err.clear();
   c->call_tick = c->tick + 1;
+}
+
+// A non-finite value latched by an earlier call's kernels (visible once
+// those kernels have finished) is reported once, then cleared.
+int latched_nonfinite(ckv_ctx* c) {
+  if (!c->nf_host || *c->nf_host == 0u) return CKV_OK;
+  *c->nf_host = 0u;
+  return fail(c, CKV_ERR_NONFINITE,
+              "a NaN or infinite value reached the window outputs or log-sum-exp of an earlier call "
+              "on this context (non-finite keys, values or queries, or recorded outputs)");
 }
 
 int ensure_ws(ckv_ctx* c, size_t need) {
@@ -454,6 +469,21 @@ extern "C" int ckv_create(ckv_ctx** out, int device, void* hip_stream) {
   c->device = device;
   c->stream = static_cast<hipStream_t>(hip_stream);
   {
+    DeviceGuard g(device);
+    void* h = nullptr;
+    void* d = nullptr;
+    if (!g.ok || hipHostMalloc(&h, 256, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess ||
+        hipHostGetDevicePointer(&d, h, 0) != hipSuccess) {
+      (void)hipGetLastError();
+      if (h) (void)hipHostFree(h);
+      delete c;
+      return CKV_ERR_HIP;
+    }
+    std::memset(h, 0, 256);
+    c->nf_host = static_cast<volatile uint32_t*>(h);
+    c->nf_dev = static_cast<uint32_t*>(d);
+  }
+  {
     // the static scratch's address on this device, looked up once per device
     // with the device current
     static std::mutex mu;
@@ -494,6 +524,7 @@ extern "C" int ckv_destroy(ckv_ctx* c) {
       if (s.ev) (void)hipEventDestroy(s.ev);
       if (s.host) (void)hipHostFree(s.host);
     }
+    if (c->nf_host) (void)hipHostFree(const_cast<uint32_t*>(c->nf_host));
     for (auto& t : c->timed) {
       (void)hipEventDestroy(t.a);
       (void)hipEventDestroy(t.b);
@@ -518,7 +549,7 @@ extern "C" int ckv_sync(ckv_ctx* c) {
   DeviceGuard g(c->device);
   if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
   CKV_HIP(c, hipStreamSynchronize(c->stream));
-  return CKV_OK;
+  return latched_nonfinite(c);
 }
 
 extern "C" const char* ckv_last_error(const ckv_ctx* c) { return c ? c->err.c_str() : "NULL context"; }
@@ -545,6 +576,13 @@ extern "C" int ckv_set_policy(ckv_ctx* c, uint32_t flags) {
 }
 
 extern "C" uint32_t ckv_get_policy(const ckv_ctx* c) { return c ? c->policy : 0u; }
+
+extern "C" int ckv_set_barrier_timeout_us(ckv_ctx* c, int64_t us) {
+  if (!c) return CKV_ERR_ARG;
+  if (us < 0 || us > (int64_t)1 << 40) return fail(c, CKV_ERR_ARG, "barrier timeout %lld us out of range", (long long)us);
+  c->barrier_ticks = us * 100;   // the device wall clock runs at 100 MHz
+  return CKV_OK;
+}
 
 extern "C" int ckv_set_kernel_timing_only(ckv_ctx* c, const char* name) {
   if (!c) return CKV_ERR_ARG;
@@ -649,7 +687,7 @@ int enqueue_measure(ckv_ctx* c, const AttnGeom& a, const MeasureBufs& b, const i
   const int n = pages->n_pages, total_rows = a.Hq * a.W;
   CKV_LAUNCH(c, "window_attention", launch_window_attention(a, b.sp, c->stream));
   ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
-              token_mass ? (size_t)a.S : 0, b.fix_count, nullptr, 0};
+              token_mass ? (size_t)a.S : 0, b.fix_count, nullptr, 0, c->nf_dev};
   CKV_LAUNCH(c, "combine", launch_combine(a, b.sp, b.rs, lse, zl, c->stream));
   if (n > 0) {
     PageWork pw{};
@@ -685,6 +723,7 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
                                         float* lse, float* token_mass) {
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
+  if (int rc0 = latched_nonfinite(c)) return rc0;
   int rc;
   if ((rc = check_measure(c, kv, win, pages, R, token_mass))) return rc;
   DeviceGuard g(c->device);
@@ -705,6 +744,7 @@ extern "C" int ckv_measure_page_effects_noalloc(ckv_ctx* c, const ckv_kv_view* k
                                                 float* lse, float* token_mass) {
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
+  if (int rc0 = latched_nonfinite(c)) return rc0;
   int rc;
   if ((rc = check_measure(c, kv, win, pages, R, token_mass))) return rc;
   DeviceGuard g(c->device);
@@ -754,6 +794,7 @@ extern "C" int ckv_measure_page_effects_batch(ckv_ctx* c, int32_t n, const ckv_k
                                               float* const* lse, float* const* token_mass) {
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
+  if (int rc0 = latched_nonfinite(c)) return rc0;
   if (n < 0 || (n > 0 && (!kv || !win || !pages || !R))) return fail(c, CKV_ERR_ARG, "batch: NULL arrays or n < 0");
   for (int i = 0; i < n; ++i) {
     int rc;
@@ -784,6 +825,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
                                     float* R_head, float* token_mass) {
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
+  if (int rc0 = latched_nonfinite(c)) return rc0;
   int rc;
   if ((rc = check_kv(c, kv)) || (rc = check_win(c, win, kv)) || (rc = check_pages(c, pages, kv->n_tokens, "measured")))
     return rc;
@@ -823,7 +865,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
   if ((rc = realize(c, plan))) return rc;
 
   ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
-              token_mass ? (size_t)a.S : 0, fix_count, count2, 1};
+              token_mass ? (size_t)a.S : 0, fix_count, count2, 1, c->nf_dev};
   CKV_LAUNCH(c, "recorded_rows", launch_recorded_rows(a, o, lse, rs, nvis_part, zl, c->stream));
   if (n > 0) {
     PageWork pw{};
@@ -868,6 +910,7 @@ extern "C" int ckv_classify_pages(ckv_ctx* c, int32_t n, const float* R_pre, con
                                   int32_t* n_cand) {
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
+  if (int rc0 = latched_nonfinite(c)) return rc0;
   if (n < 0) return fail(c, CKV_ERR_SHAPE, "n < 0");
   if (!n_cand) return fail(c, CKV_ERR_ARG, "n_cand is NULL");
   if (n > 0 && (!R_pre || !R_post || !lambda || !cand)) return fail(c, CKV_ERR_ARG, "NULL input or output array");
@@ -908,6 +951,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
                               float* union_R, int32_t* n_accepted) {
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
+  if (int rc0 = latched_nonfinite(c)) return rc0;
   int rc;
   if ((rc = check_kv(c, kv)) || (rc = check_win(c, win, kv)) || (rc = check_pages(c, pages, kv->n_tokens, "joint")))
     return rc;
@@ -930,6 +974,8 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   j.window = kJointWindow;
   j.rows_per_block = kJointRowsPerBlock;
   j.tau = tau_joint;
+  j.nonfinite = c->nf_dev;
+  j.barrier_ticks = c->barrier_ticks;
   j.accept_all = (c->policy & CKV_POLICY_NO_JOINT) != 0;
   j.accepted = accepted;
   j.union_R = union_R;
@@ -1004,6 +1050,7 @@ extern "C" int ckv_pool_scores(ckv_ctx* c, const float* score, float* out, int32
                                const int32_t* n_tokens, int32_t kernel, int32_t mode) {
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
+  if (int rc0 = latched_nonfinite(c)) return rc0;
   if (n_seq < 0 || (n_seq > 0 && (!score || !out || !n_tokens)))
     return fail(c, CKV_ERR_ARG, "pool: NULL pointer or negative n_seq");
   if (kernel < 1 || kernel > 255 || kernel % 2 == 0) return fail(c, CKV_ERR_ARG, "pool: kernel must be odd, 1..255");
@@ -1037,6 +1084,7 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
                                       uint8_t* token_state) {
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
+  if (int rc0 = latched_nonfinite(c)) return rc0;
   if (!in || !n_tokens || !score || !retired || !pending || !budget || !kept_idx || !n_kept)
     return fail(c, CKV_ERR_ARG, "NULL argument");
   if (in->n_seq < 1 || in->capacity < 1) return fail(c, CKV_ERR_SHAPE, "empty cache shape");
@@ -1199,6 +1247,7 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   sa.state = token_state;
   sa.kept = kept_idx;
   sa.n_kept = n_kept;
+  sa.barrier_ticks = c->barrier_ticks;
   int max_pend = 0;
   for (int s = 0; s < ns; ++s) max_pend = std::max(max_pend, pending[s].n_pages);
   if (c->sel_resident < 0) c->sel_resident = select_grid_resident();

@@ -81,7 +81,15 @@ struct ZeroList {
   float* p2; size_t n2;
   int* i0;               // one int set to zero (or null)
   int* i1; size_t n1i;   // ints set to zero
+  uint32_t* nonfinite;   // latched flag (host memory), set when a window row's
+                         // output or log-sum-exp is NaN or infinite (or null)
 };
+
+// Latch the non-finite flag: a plain system-scope store to the context's
+// pinned host word (idempotent, so concurrent setters need no atomics).
+__device__ __forceinline__ void latch_nonfinite(uint32_t* flag) {
+  if (flag) __hip_atomic_store(flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
 
 int rows_per_block_attention();
 int rows_per_block_page();
@@ -160,6 +168,8 @@ struct JointArgs {
   int window;             // candidates evaluated per round
   int rows_per_block;
   float tau;
+  long long barrier_ticks; // bound of a grid-barrier wait (100 MHz wall clock ticks)
+  uint32_t* nonfinite;    // latched when an o or lse row is NaN or infinite (or null)
   int accept_all;         // no Eq. (11) gate: every candidate accepted
   uint8_t* accepted;
   float* union_R;
@@ -223,7 +233,9 @@ struct SelectArgs {
   // persistent state of the grid selection (zero between calls)
   int32_t* gctrl;                // [n_seq][kSelGridCtrl]
   uint32_t* ghist;               // [n_seq][3][kSelBins]
+  long long barrier_ticks;       // bound of a per-sequence barrier wait (100 MHz ticks)
 };
+constexpr long long kBarrierTicksDefault = 1ll << 27;   // ~1.34 s of the 100 MHz wall clock
 constexpr int kSelChunk = 2048;  // tokens per selection workgroup
 constexpr int kSelCtrl = 16;     // ints of per-sequence selection state
 constexpr int kSelBins = 2048;   // radix digit bins (11-bit digits)

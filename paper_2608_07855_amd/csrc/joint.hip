@@ -43,13 +43,12 @@ namespace ckv {
 
 // control words (cleared by the residual pass before this kernel starts)
 enum { kCursor = 0, kPending = 1, kBarrier = 2, kError = 3, kParity = 4, kFixN = 5 };
-constexpr long long kBarrierTimeoutTicks = 1ll << 27;   // ~1.3 s of the 100 MHz wall clock
 constexpr int kVisSlice = 8192;                         // tokens per visible-count item
 
 // Grid barrier: thread 0 of every block publishes the block's writes, adds
 // one arrival and waits until the arrivals reach `target`.  Returns false
 // (in every thread) if the wait timed out or another block gave up.
-__device__ bool grid_barrier(int* ctrl, int target, int* s_ok) {
+__device__ bool grid_barrier(int* ctrl, int target, long long timeout, int* s_ok) {
   __syncthreads();
   if (threadIdx.x == 0) {
     __threadfence();
@@ -58,7 +57,7 @@ __device__ bool grid_barrier(int* ctrl, int target, int* s_ok) {
     int ok = 1;
     while (__hip_atomic_load(&ctrl[kBarrier], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
       if (__hip_atomic_load(&ctrl[kError], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
-          wall_clock64() - t0 > kBarrierTimeoutTicks) {
+          wall_clock64() - t0 >= timeout) {
         __hip_atomic_store(&ctrl[kError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         ok = 0;
         break;
@@ -299,7 +298,10 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) n2 += __shfl_xor(n2, off, 64);
-    if (lane == 0) rs.onorm[row] = sqrtf(n2);
+    if (lane == 0) {
+      rs.onorm[row] = sqrtf(n2);
+      if (!(n2 <= 3.4e38f) || !(j.lse[row] < INFINITY)) latch_nonfinite(j.nonfinite);
+    }
   }
   // n_vis of window row p (shared by every query head): #{i : pos[i] <= qpos[p]},
   // one partial count per (row, token slice)
@@ -317,7 +319,7 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
     __syncthreads();
   }
   int target = gridDim.x;
-  if (!grid_barrier(j.ctrl, target, &s_ok)) {
+  if (!grid_barrier(j.ctrl, target, j.barrier_ticks, &s_ok)) {
     if (threadIdx.x == 0) *j.n_accepted = -1;
     return;
   }
@@ -332,7 +334,7 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
     for (int it = blockIdx.x; it < items; it += gridDim.x)
       joint_item(j, rs, it / n_rb, it % n_rb, cursor, pend, par, n_eff, &smax);
     target += gridDim.x;
-    if (!grid_barrier(j.ctrl, target, &s_ok)) {
+    if (!grid_barrier(j.ctrl, target, j.barrier_ticks, &s_ok)) {
       if (threadIdx.x == 0) *j.n_accepted = -1;
       return;
     }
@@ -352,14 +354,14 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
         else joint_fix_partial<64, false>(j, cursor, e0, np, parts, sacc);
       }
       target += gridDim.x;
-      if (!grid_barrier(j.ctrl, target, &s_ok)) {
+      if (!grid_barrier(j.ctrl, target, j.barrier_ticks, &s_ok)) {
         if (threadIdx.x == 0) *j.n_accepted = -1;
         return;
       }
       if (j.D == 128) joint_fix_final<128>(j, e0, np, parts);
       else joint_fix_final<64>(j, e0, np, parts);
       target += gridDim.x;
-      if (!grid_barrier(j.ctrl, target, &s_ok)) {
+      if (!grid_barrier(j.ctrl, target, j.barrier_ticks, &s_ok)) {
         if (threadIdx.x == 0) *j.n_accepted = -1;
         return;
       }
@@ -389,7 +391,7 @@ __global__ __launch_bounds__(256) void joint_persistent(JointArgs j, RowStats rs
       __hip_atomic_store(&j.ctrl[kParity], par ^ 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     target += gridDim.x;
-    if (!grid_barrier(j.ctrl, target, &s_ok)) {
+    if (!grid_barrier(j.ctrl, target, j.barrier_ticks, &s_ok)) {
       if (threadIdx.x == 0) *j.n_accepted = -1;
       return;
     }

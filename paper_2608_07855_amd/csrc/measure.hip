@@ -477,6 +477,9 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
     rs.onorm[rg] = sqrtf(n2);
     rs.nvis[rg] = nv;
     if (lse_out) lse_out[rg] = l2 * kLn2;
+    // a NaN or infinite key, query or value reaches the row's output or its
+    // log-sum-exp (a row that sees no token has lse -inf and o = 0)
+    if (!(n2 <= 3.4e38f) || (nv > 0 && !(l2 > -INFINITY && l2 < INFINITY))) latch_nonfinite(zl.nonfinite);
   }
 }
 

@@ -69,6 +69,8 @@ __global__ __launch_bounds__(256) void recorded_rows_kernel(AttnGeom a, const fl
     rs.lse2[rg] = l == -INFINITY ? -INFINITY : l * kLog2e;
     rs.onorm[rg] = sqrtf(n2);
     rs.nvis[rg] = nv;
+    // recorded o or lse NaN or infinite (lse -inf only for a row that sees nothing)
+    if (!(n2 <= 3.4e38f) || !(l < INFINITY) || (nv > 0 && !(l > -INFINITY))) latch_nonfinite(zl.nonfinite);
   }
 }
 

@@ -485,9 +485,8 @@ enum { qArrive = 0, qDone = 1, qNP = 2, qNF = 3, qNotLo = 4, qHi = 5, qError = 6
 // keys, they are listed (in the histogram rows of the later passes) and every
 // workgroup finishes the selection on the list in LDS: no further grid pass
 constexpr int kCandMax = kSelBins;
-constexpr long long kSelTimeoutTicks = 1ll << 27;   // ~1.3 s of the 100 MHz wall clock
 
-__device__ bool seq_barrier(int* ctrl, int target, int* s_ok) {
+__device__ bool seq_barrier(int* ctrl, int target, long long timeout, int* s_ok) {
   __syncthreads();
   if (threadIdx.x == 0) {
     __threadfence();
@@ -496,7 +495,7 @@ __device__ bool seq_barrier(int* ctrl, int target, int* s_ok) {
     int ok = 1;
     while (__hip_atomic_load(&ctrl[qArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
       if (__hip_atomic_load(&ctrl[qError], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
-          wall_clock64() - t0 > kSelTimeoutTicks) {
+          wall_clock64() - t0 >= timeout) {
         __hip_atomic_store(&ctrl[qError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         ok = 0;
         break;
@@ -652,7 +651,7 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
     }
   }
   int target = C;
-  bool ok = seq_barrier(ctrl, target, &s_ok);
+  bool ok = seq_barrier(ctrl, target, a.barrier_ticks, &s_ok);
   int32_t* kept = a.kept + (size_t)s * a.budget;
   if (ok) {
     const int NP = ld_agent(&ctrl[qNP]), NF = ld_agent(&ctrl[qNF]);
@@ -685,7 +684,7 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
         for (int i = tid; i < kSelBins; i += kQT)
           if (hist[i]) atomicAdd(&gh[pass * kSelBins + i], hist[i]);
         target += C;
-        if (!seq_barrier(ctrl, target, &s_ok)) { ok = false; break; }
+        if (!seq_barrier(ctrl, target, a.barrier_ticks, &s_ok)) { ok = false; break; }
         // thread g owns bins 8(kQT-1-g) .. 8(kQT-1-g)+7: an exclusive scan in
         // thread order counts the keys in higher bins
         const int g = kQT - 1 - tid;
@@ -750,7 +749,7 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
           ctrl[qCounts + 2 * cb] = tk;
         }
         target += C;
-        ok = seq_barrier(ctrl, target, &s_ok);
+        ok = seq_barrier(ctrl, target, a.barrier_ticks, &s_ok);
         if (ok) {
           const int M = min(ld_agent(&ctrl[qCand]), kCandMax);
           for (int i = tid; i < M; i += kQT) {
@@ -835,7 +834,7 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
           ctrl[qCounts + 2 * cb + 1] = te;
         }
         target += C;
-        ok = seq_barrier(ctrl, target, &s_ok);
+        ok = seq_barrier(ctrl, target, a.barrier_ticks, &s_ok);
         if (ok)
           for (int q = 0; q < cb; ++q) {
             k_before += ld_agent(&ctrl[qCounts + 2 * q]);
