@@ -491,3 +491,22 @@ def test_pool_identity_and_nan():
     np.testing.assert_array_equal(O.pool_scores(x[:3], 1, "max"), x[:3])
     np.testing.assert_array_equal(O.pool_scores(x, 3, "max"), [0.3, 2.0, 2.0, 2.0, 0.5])
     assert np.isnan(O.pool_scores(x, 3, "mean")[2]) and O.pool_scores(x, 3, "mean")[0] == (0.3 - 1.0) / 2
+
+
+def test_bf16_bits_decode_hand_patterns():
+    """The oracle's bf16 decoder on hand-written bit patterns (sign,
+    exponent, mantissa read off by hand): ones, a fraction, zeros of both
+    signs, infinities, NaN, the largest finite value and the smallest
+    subnormal."""
+    bits = np.array([0x3F80, 0xBF80, 0x4049, 0x3C00, 0x0000, 0x8000, 0x7F80, 0xFF80, 0x7F7F, 0x0001,
+                     0x4120, 0xC2F7], dtype=np.uint16)
+    want = [1.0, -1.0, 3.140625, 2.0 ** -7, 0.0, -0.0, np.inf, -np.inf, (2 - 2.0 ** -7) * 2.0 ** 127,
+            2.0 ** -133, 10.0, -123.5]
+    got = O.bf16_bits_to_f64(bits)
+    assert got.dtype == np.float64
+    np.testing.assert_array_equal(got, want)
+    assert np.signbit(got[5]) and not np.signbit(got[4])
+    assert np.isnan(O.bf16_bits_to_f64(np.array([0x7FC0], np.uint16)))[0]
+    # as_f64 takes the same path for uint16 input and leaves real arrays as they are
+    np.testing.assert_array_equal(O.as_f64(bits), got)
+    np.testing.assert_array_equal(O.as_f64(np.array([0.5, -2.0], np.float32)), [0.5, -2.0])
