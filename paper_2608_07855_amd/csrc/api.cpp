@@ -958,6 +958,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   if (!o || !lse || !cand || !n_cand || !accepted || !n_accepted)
     return fail(c, CKV_ERR_ARG, "NULL input or output array");
   if (max_cand < 1) return fail(c, CKV_ERR_SHAPE, "max_cand must be >= 1");
+  if (max_cand > (1 << 22)) return fail(c, CKV_ERR_UNSUPPORTED, "max_cand above 2^22 is not supported");
   if (!std::isfinite(tau_joint)) return fail(c, CKV_ERR_ARG, "tau_joint must be finite");
   DeviceGuard g(c->device);
   if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
@@ -1003,6 +1004,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   plan.add(&Cst, 2 * (size_t)total_rows);
   plan.add(&j.ctrl, 8);
   plan.add(&j.rbuf, kJointWindow);
+  plan.add(&j.bmax, (size_t)kTargetBlocks * kJointWindow);
   plan.add(&j.in_acc, std::max(pages->n_pages, 1));
   plan.add(&j.fix_list, 2 * (size_t)kJointWindow * total_rows);
   plan.add(&j.fpart, (size_t)ckv::kJointFixItems * (D + 1));

@@ -61,9 +61,9 @@ struct PageWork {
   int* fix_list;          // MODE 0: (page, global row, start, len) entries left to the fix-up kernel
   int* fix_count;         // MODE 0: entries in fix_list (zeroed before)
   int fix_cap;            // MODE 0: capacity of fix_list (window rows)
-  float* resid;           // MODE 1: [max_cand][total_rows][D]
-  float* resA;            // MODE 1: [max_cand][total_rows]
-  int* resC;              // MODE 1: [max_cand][total_rows]
+  float* resid;           // MODE 1: [total_rows][n_items][D] (a row's candidates together)
+  float* resA;            // MODE 1: [total_rows][n_items]
+  int* resC;              // MODE 1: [total_rows][n_items]
   int total_rows;         // Hq * W
   float lse_scale;        // rs.lse2 x lse_scale = log-sum-exp in log2 units (1, or log2 e
                           // when rs.lse2 holds natural-log values)
@@ -148,8 +148,8 @@ hipError_t launch_classify(const ClassifyArgs& c, hipStream_t s);
 struct JointArgs {
   int total_rows, D, max_cand, W;
   const int32_t* n_cand;
-  const float* resid;     // [max_cand][rows][D]
-  const float* resA;      // [max_cand][rows]
+  const float* resid;     // [rows][max_cand][D]
+  const float* resA;      // [rows][max_cand]
   const int* resC;
   float* onorm;           // [rows]: ||o_p|| (phase 0)
   int* nvis_part;         // [W][n_vis_slices]: visible tokens of window row p per slice (phase 0)
@@ -165,6 +165,7 @@ struct JointArgs {
   int* ctrl;              // [8]: cursor, pending accepted item, barrier arrivals, error, parity
                           //      (zero before the launch: the residual pass clears them)
   unsigned int* rbuf;     // [window] per-candidate max ratio bits
+  unsigned int* bmax;     // [workgroups][window] per-workgroup candidate maxima (owned-row form)
   int window;             // candidates evaluated per round
   int rows_per_block;
   float tau;

@@ -681,7 +681,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
 #pragma unroll
           for (int r = 0; r < 16; ++r) n2 = __builtin_fmaf(u[j][r], u[j][r], n2);
         if (MODE == 1 && ri.ok) {
-          float* rrow = pw.resid + ((size_t)item * pw.total_rows + ri.rg) * D;
+          float* rrow = pw.resid + ((size_t)ri.rg * pw.n_items + item) * D;
 #pragma unroll
           for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -732,7 +732,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
           atomicMax(rm, __float_as_uint(ratio));
         }
       } else if (ri.ok) {
-        const size_t base_i = (size_t)item * pw.total_rows + ri.rg;
+        const size_t base_i = (size_t)ri.rg * pw.n_items + item;
         if (half == 0) {
           pw.resA[base_i] = A;
           pw.resC[base_i] = c;
