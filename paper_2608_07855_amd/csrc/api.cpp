@@ -636,6 +636,7 @@ struct MeasureBufs {
   int* fix_list = nullptr;
   int* fix_count = nullptr;
   float* fpart = nullptr;
+  int* arrive = nullptr;      // per listed pair: fix-up parts finished
 };
 
 void plan_measure(const AttnGeom& a, int n_splits, float* o, Plan& plan, MeasureBufs& b) {
@@ -658,6 +659,7 @@ void plan_measure(const AttnGeom& a, int n_splits, float* o, Plan& plan, Measure
   plan.add(&b.fix_list, 4 * (size_t)total_rows);
   plan.add(&b.fix_count, 1);
   plan.add(&b.fpart, (size_t)total_rows * ckv::kFixParts * (D + 1));
+  plan.add(&b.arrive, total_rows);
 }
 
 // splits of the window pass: about one workgroup per compute unit, and at
@@ -687,7 +689,7 @@ int enqueue_measure(ckv_ctx* c, const AttnGeom& a, const MeasureBufs& b, const i
   const int n = pages->n_pages, total_rows = a.Hq * a.W;
   CKV_LAUNCH(c, "window_attention", launch_window_attention(a, b.sp, c->stream));
   ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
-              token_mass ? (size_t)a.S : 0, b.fix_count, nullptr, 0, c->nf_dev};
+              token_mass ? (size_t)a.S : 0, b.fix_count, b.arrive, (size_t)total_rows, c->nf_dev};
   CKV_LAUNCH(c, "combine", launch_combine(a, b.sp, b.rs, lse, zl, c->stream));
   if (n > 0) {
     PageWork pw{};
@@ -707,7 +709,7 @@ int enqueue_measure(ckv_ctx* c, const AttnGeom& a, const MeasureBufs& b, const i
     pw.fix_cap = total_rows;
     pw.fix_a = ckv::kFixA;
     CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, b.rs, 0, max_page_len(pages), c->stream));
-    CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, b.sp, b.rs, pw, b.fpart, ckv::kFixParts, 0, c->stream));
+    CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, b.sp, b.rs, pw, b.fpart, b.arrive, ckv::kFixParts, 0, c->stream));
   }
   if (token_mass) {
     const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kMassBlocks / a.Hkv)), 64);
@@ -857,7 +859,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
   const int items2 = std::max(ckv::kFixComplementItems, total_rows);
   int *list2 = nullptr, *count2 = nullptr;
   plan.add(&list2, 4 * (size_t)cap2);
-  plan.add(&count2, 1);
+  plan.add(&count2, 1 + (size_t)cap2);   // the count, then the pairs' arrival counts
   float* fpart = nullptr;
   plan.add(&fpart, (size_t)items2 * (a.D + 1));
   const int32_t *dstart = nullptr, *dlen = nullptr;
@@ -865,7 +867,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
   if ((rc = realize(c, plan))) return rc;
 
   ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
-              token_mass ? (size_t)a.S : 0, fix_count, count2, 1, c->nf_dev};
+              token_mass ? (size_t)a.S : 0, fix_count, count2, 1 + (size_t)cap2, c->nf_dev};
   CKV_LAUNCH(c, "recorded_rows", launch_recorded_rows(a, o, lse, rs, nvis_part, zl, c->stream));
   if (n > 0) {
     PageWork pw{};
@@ -895,7 +897,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
     pw2.fix_cap = cap2;
     AttnSplit whole{(int)round_up(a.S, 64), 1, 0, nullptr, nullptr, nullptr, nullptr};
     CKV_LAUNCH(c, "page_fixup_complement",
-               launch_page_fixup(a, whole, rs, pw2, fpart, ckv::kFixPartsRow, items2, c->stream));
+               launch_page_fixup(a, whole, rs, pw2, fpart, count2 + 1, ckv::kFixPartsRow, items2, c->stream));
   }
   if (token_mass) {
     const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kMassBlocks / a.Hkv)), 64);

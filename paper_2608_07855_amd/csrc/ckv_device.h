@@ -82,6 +82,21 @@ __device__ __forceinline__ int vt_col(int r, int s) {
   return (((s >> 3) ^ (r >> 4)) & 7) << 3 | (s & 7);
 }
 
+// Element offset of the 16-byte V^T fragment that lane (col, half) reads as
+// the A operand for width block db (< 4), 32-token slot tb and 16-token step
+// u: row r = 32 db + col, slots 32 tb + 16 u + 8 half .. + 7, i.e.
+// r * VP + vt_col(r, 32 tb + 16 u + 8 half).  The XOR of vt_col splits bit by
+// bit into a per-lane part (bit 0: half ^ (col >> 4)) and a part fixed by
+// (db, tb, u), so every fragment of a lane is one base register plus an
+// immediate offset.
+template <int VP>
+__device__ __forceinline__ int vt_frag_lane(int col, int half) {
+  return col * VP + 8 * (half ^ (col >> 4));
+}
+__device__ __forceinline__ constexpr int vt_frag_const(int VP, int db, int tb, int u) {
+  return 32 * db * VP + 8 * (((tb ^ (db >> 1)) << 2) | ((u ^ (db & 1)) << 1));
+}
+
 // loads through the global address space (pointers inside by-value argument
 // structs otherwise compile to flat accesses)
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));

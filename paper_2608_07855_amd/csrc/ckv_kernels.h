@@ -107,11 +107,14 @@ hipError_t launch_token_mass(const AttnGeom& a, const RowStats& rs, float* mass,
 // when item_budget > 0; each listed pair is spread over `parts` workgroups,
 // or, with an item budget, over min(parts, item_budget / pairs) of them (at
 // least 1, read from the device count), so every listed pair fits however
-// many there are (item_budget >= fix_cap)
+// many there are (item_budget >= fix_cap).  arrive: [fix_cap] ints, zero on
+// entry: the last part of a pair to finish (counted there) adds the parts up
+// and takes the ratio, so one launch does both steps.
 constexpr int kFixParts = 8;        // after the window pass: the page's own split(s)
 constexpr int kFixPartsRow = 32;    // recorded outputs: every other token of the row
 hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
-                             const PageWork& pw, float* fpart, int parts, int item_budget, hipStream_t s);
+                             const PageWork& pw, float* fpart, int* arrive, int parts, int item_budget,
+                             hipStream_t s);
 
 // recorded window outputs: row statistics from the caller's o and natural-log
 // lse (nvis_part: workspace [W][recorded_slices(S)] ints), and the fix-up of

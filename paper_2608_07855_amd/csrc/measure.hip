@@ -221,6 +221,27 @@ __device__ __forceinline__ f32x16 scores(const uint16_t* sK, int tb, int col, in
   return acc;
 }
 
+// the same with the K fragments read kPFS steps ahead of the products
+template <int D, int KP, int kPFS = 4>
+__device__ __forceinline__ f32x16 scores_pf(const uint16_t* sK, int tb, int col, int half,
+                                            const bf16x8 (&qf)[D / 16]) {
+  constexpr int KS = D / 16;
+  bf16x8 kf[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) kf[ks] = load_bf16x8(sK + (32 * tb + col) * KP + 16 * ks + 8 * half);
+  f32x16 acc = zero16();
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) acc = mfma_bf16(kf[ks], qf[ks], acc);
+  __builtin_amdgcn_sched_group_barrier(0x100, kPFS, 0);
+#pragma unroll
+  for (int i = 0; i < KS - kPFS; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, kPFS, 0);
+  return acc;
+}
+
 // Rounds the 16 weights of a score block to float16 (the B operands of the
 // two 16-token steps of O^T += V^T P^T) and adds the ROUNDED weights to sum.
 // Normalising by the sum of exactly the weights that multiply V keeps the
@@ -250,8 +271,8 @@ __device__ __forceinline__ void pv_slot(const _Float16* sV, int tb, int col, int
   for (int u = 0; u < 2; ++u) {
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
-      const int r = 32 * db + col;
-      const f16x8 af = *reinterpret_cast<const f16x8*>(sV + r * VP + vt_col(r, 32 * tb + 16 * u + 8 * half));
+      const f16x8 af =
+          *reinterpret_cast<const f16x8*>(sV + vt_frag_lane<VP>(col, half) + vt_frag_const(VP, db, tb, u));
       acc[db] = mfma_f16(af, h[u], acc[db]);
     }
   }
@@ -265,8 +286,8 @@ __device__ __forceinline__ void pv_half(const _Float16* sV, int tb, int col, int
   for (int u = 0; u < 2; ++u) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int r = 32 * (db0 + j) + col;
-      const f16x8 af = *reinterpret_cast<const f16x8*>(sV + r * VP + vt_col(r, 32 * tb + 16 * u + 8 * half));
+      const f16x8 af = *reinterpret_cast<const f16x8*>(sV + vt_frag_lane<VP>(col, half) +
+                                                        vt_frag_const(VP, db0 + j, tb, u));
       acc[j] = mfma_f16(af, h[u], acc[j]);
     }
   }
@@ -406,11 +427,20 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
     }
 }
 
-// one wave per window row: merge the splits, write o, lse, ||o||, n_vis
+// Merge of the splits: D/4 lanes per window row (16 bytes of the partial
+// output each), so a wave holds 256 / D rows.  Splits are read in batches of
+// kCombBatch with every load of a batch in flight; the running maximum is
+// updated once per batch (the weights of earlier batches are rescaled), and
+// the batch order is fixed, so the result does not depend on scheduling.
+// Writes o, lse, ||o|| and the visible count of every row.
+constexpr int kCombBatch = 16;
+
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, RowStats rs,
                                                       float* lse_out, ZeroList zl) {
-  const int lane = threadIdx.x & 63;
+  constexpr int TPR = D / 4;          // lanes per row
+  constexpr int RPW = 64 / TPR;       // rows per wave
+  const int lane = threadIdx.x & 63, c = lane % TPR;
   const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
   // zero the outputs that later kernels reduce into with atomic max
   const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -420,58 +450,57 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
   for (size_t i = gid; i < zl.n2; i += gsz) zl.p2[i] = 0.f;
   if (zl.i0 && gid == 0) *zl.i0 = 0;
   for (size_t i = gid; i < zl.n1i; i += gsz) zl.i1[i] = 0;
-  if (wid >= a.Hkv * a.rows) return;
-  const int g = wid / a.rows, row = wid % a.rows;
+  const int total = a.Hkv * a.rows;
+  const int rw = wid * RPW + lane / TPR;     // this lane's (KV head, row) pair
+  if (wid * RPW >= total) return;
+  const bool ok = rw < total;
+  const int g = ok ? rw / a.rows : 0, row = ok ? rw % a.rows : 0;
   const int rg = g * a.rows + row;
-  float M = -INFINITY;
+  const size_t base = (size_t)g * sp.n_splits * sp.rows_pad + row;
+  float M = -INFINITY, wsum = 0.f;
   int nv = 0;
-  for (int s = lane; s < sp.n_splits; s += 64) {
-    const size_t idx = (size_t)(g * sp.n_splits + s) * sp.rows_pad + row;
-    M = fmaxf(M, sp.part_m[idx]);
-    nv += sp.part_c[idx];
-  }
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < sp.n_splits; s0 += kCombBatch) {
+    float ms[kCombBatch], ls[kCombBatch];
+    int cs[kCombBatch];
+    f32x4 os[kCombBatch];
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    M = fmaxf(M, __shfl_xor(M, off, 64));
-    nv += __shfl_xor(nv, off, 64);
-  }
-  float wsum = 0.f;
-  float acc[D / 64];
+    for (int u = 0; u < kCombBatch; ++u) {
+      const bool in = s0 + u < sp.n_splits;
+      const size_t idx = base + (size_t)min(s0 + u, sp.n_splits - 1) * sp.rows_pad;
+      ms[u] = in ? sp.part_m[idx] : -INFINITY;
+      ls[u] = sp.part_l[idx];
+      cs[u] = in ? sp.part_c[idx] : 0;
+      os[u] = *reinterpret_cast<const f32x4*>(sp.part_o + idx * D + 4 * c);
+    }
+    float mb = M;
 #pragma unroll
-  for (int j = 0; j < D / 64; ++j) acc[j] = 0.f;
-  if (M != -INFINITY) {
-    // eight splits' loads in flight at a time
-    for (int s0 = 0; s0 < sp.n_splits; s0 += 8) {
-      float ms[8], ls[8], os[8][D / 64];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int s = min(s0 + u, sp.n_splits - 1);
-        const size_t idx = (size_t)(g * sp.n_splits + s) * sp.rows_pad + row;
-        ms[u] = s0 + u < sp.n_splits ? sp.part_m[idx] : -INFINITY;
-        ls[u] = sp.part_l[idx];
-#pragma unroll
-        for (int j = 0; j < D / 64; ++j) os[u][j] = sp.part_o[idx * D + lane + 64 * j];
+    for (int u = 0; u < kCombBatch; ++u) mb = fmaxf(mb, ms[u]);
+    if (mb != -INFINITY) {
+      if (mb > M) {
+        const float r = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - mb);
+        wsum *= r;
+        acc *= r;
+        M = mb;
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < kCombBatch; ++u) {
         const float w = ms[u] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms[u] - M);
         wsum += ls[u] * w;
-#pragma unroll
-        for (int j = 0; j < D / 64; ++j) acc[j] += os[u][j] * w;
+        acc += os[u] * w;
       }
     }
+#pragma unroll
+    for (int u = 0; u < kCombBatch; ++u) nv += cs[u];
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  float n2 = 0.f;
+  const f32x4 ov = acc * inv;
+  float n2 = ov[0] * ov[0] + ov[1] * ov[1] + ov[2] * ov[2] + ov[3] * ov[3];
 #pragma unroll
-  for (int j = 0; j < D / 64; ++j) {
-    const float ov = acc[j] * inv;
-    rs.o[(size_t)rg * D + lane + 64 * j] = ov;
-    n2 += ov * ov;
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) n2 += __shfl_xor(n2, off, 64);
-  if (lane == 0) {
+  for (int off = TPR / 2; off >= 1; off >>= 1) n2 += __shfl_xor(n2, off, 64);
+  if (!ok) return;
+  *reinterpret_cast<f32x4*>(rs.o + (size_t)rg * D + 4 * c) = ov;
+  if (c == 0) {
     const float l2 = wsum > 0.f ? M + __log2f(wsum) : -INFINITY;
     rs.lse2[rg] = l2;
     rs.onorm[rg] = sqrtf(n2);
@@ -794,10 +823,13 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
 // Each listed pair is spread over kFixParts workgroups: part j takes the
 // other splits s = j (mod kFixParts) and the j-th segment of the page's own
 // split(s), with every load of a 128-token round in flight at once, and
-// stores its partial sums (fixed order inside the part).  The final kernel
-// adds the parts in order (so the result does not depend on scheduling) and
-// takes the ratio.  Weights are taken relative to the row's log-sum-exp
-// (every weight <= 1).
+// stores its partial sums (fixed order inside the part).  The part that
+// finishes last (an arrival count per pair) adds the parts in order (so the
+// result does not depend on scheduling) and takes the ratio.  The sums cross
+// workgroups through agent-scope atomic stores and loads, which bypass the
+// per-XCD L2, so no cache-wide fence is needed; the workgroup barrier before
+// the arrival waits for the stores.  Weights are taken relative to the row's
+// log-sum-exp (every weight <= 1).
 // ---------------------------------------------------------------------------
 constexpr int kFixT = 256;        // threads of a fix-up workgroup
 constexpr int kFixGrid = 1024;    // (pair, part) items in flight
@@ -807,13 +839,56 @@ __device__ __forceinline__ int fix_parts(int parts, int item_budget, int n) {
   return item_budget > 0 ? max(1, min(parts, item_budget / max(n, 1))) : parts;
 }
 
+// ratio of listed pair e from its parts' sums (one wave)
+template <int D>
+__device__ void fixup_ratio(const AttnGeom& a, const RowStats& rs, const PageWork& pw, const float* fpart, int e,
+                            int parts, int lane) {
+  const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
+  const int page = ent.x, rg = ent.y, h = rg / a.W;
+  const float* fp = fpart + (size_t)e * parts * (D + 1);
+  auto ld = [](const float* p) {
+    return __uint_as_float(__hip_atomic_load(reinterpret_cast<const unsigned*>(p), __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT));
+  };
+  float num[D / 64], den = 0.f;
+#pragma unroll
+  for (int j = 0; j < D / 64; ++j) num[j] = 0.f;
+  for (int part = 0; part < parts; ++part) {
+#pragma unroll
+    for (int j = 0; j < D / 64; ++j) num[j] += ld(fp + part * (D + 1) + lane + 64 * j);
+    den += ld(fp + part * (D + 1) + D);
+  }
+  float dd = 0.f, oo = 0.f;
+#pragma unroll
+  for (int j = 0; j < D / 64; ++j) {
+    const float ov = rs.o[(size_t)rg * D + lane + 64 * j];
+    const float od = den > 0.f ? num[j] / den : 0.f;
+    dd += (ov - od) * (ov - od);
+    oo += ov * ov;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    dd += __shfl_xor(dd, off, 64);
+    oo += __shfl_xor(oo, off, 64);
+  }
+  if (lane == 0) {
+    float ratio;
+    if (!(den > 0.f)) ratio = INFINITY;
+    else if (oo > 0.f) ratio = sqrtf(dd) / sqrtf(oo);
+    else ratio = dd > 0.f ? INFINITY : 0.f;
+    if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], ratio);
+    atomic_max_nonneg(&pw.R[page], ratio);
+  }
+}
+
 template <int D, bool PG>
-__global__ __launch_bounds__(kFixT) void page_fixup_partial(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw,
-                                                            float* fpart, int parts, int item_budget) {
+__global__ __launch_bounds__(kFixT) void page_fixup_kernel(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw,
+                                                           float* fpart, int* arrive, int parts, int item_budget) {
   constexpr int TPR = D / 8;                  // threads per token row (16 bytes each)
   constexpr int RPR = kFixT / TPR;            // token rows per round
   constexpr int UNR = 128 / RPR;              // rounds whose loads are in flight together
   __shared__ float sacc[RPR][D + 1];
+  __shared__ int sLast;
   const int tid = threadIdx.x, c = tid % TPR, r = tid / TPR;
   const int n = min(*pw.fix_count, pw.fix_cap);
   parts = fix_parts(parts, item_budget, n);
@@ -900,52 +975,14 @@ __global__ __launch_bounds__(kFixT) void page_fixup_partial(AttnGeom a, AttnSpli
     for (int i = tid; i <= D; i += kFixT) {
       float v = 0.f;
       for (int k = 0; k < RPR; ++k) v += sacc[k][i];
-      out[i] = v;
+      __hip_atomic_store(reinterpret_cast<unsigned*>(out + i), __float_as_uint(v), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
-  }
-}
-
-// one wave per listed pair: parts added in order, ratio ||o - o'|| / ||o||
-template <int D>
-__global__ __launch_bounds__(256) void page_fixup_final(AttnGeom a, RowStats rs, PageWork pw, const float* fpart,
-                                                        int parts, int item_budget) {
-  const int lane = threadIdx.x & 63;
-  const int n = min(*pw.fix_count, pw.fix_cap);
-  parts = fix_parts(parts, item_budget, n);
-  for (int e = blockIdx.x * 4 + (threadIdx.x >> 6); e < n; e += gridDim.x * 4) {
-    const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
-    const int page = ent.x, rg = ent.y, h = rg / a.W;
-    const float* fp = fpart + (size_t)e * parts * (D + 1);
-    float num[D / 64], den = 0.f;
-#pragma unroll
-    for (int j = 0; j < D / 64; ++j) num[j] = 0.f;
-    for (int part = 0; part < parts; ++part) {
-#pragma unroll
-      for (int j = 0; j < D / 64; ++j) num[j] += fp[part * (D + 1) + lane + 64 * j];
-      den += fp[part * (D + 1) + D];
-    }
-    float dd = 0.f, oo = 0.f;
-#pragma unroll
-    for (int j = 0; j < D / 64; ++j) {
-      const float ov = rs.o[(size_t)rg * D + lane + 64 * j];
-      const float od = den > 0.f ? num[j] / den : 0.f;
-      dd += (ov - od) * (ov - od);
-      oo += ov * ov;
-    }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      dd += __shfl_xor(dd, off, 64);
-      oo += __shfl_xor(oo, off, 64);
-    }
-    if (lane == 0) {
-      float ratio;
-      if (!(den > 0.f)) ratio = INFINITY;
-      else if (oo > 0.f) ratio = sqrtf(dd) / sqrtf(oo);
-      else ratio = dd > 0.f ? INFINITY : 0.f;
-      if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], ratio);
-      atomic_max_nonneg(&pw.R[page], ratio);
-    }
+    if (tid == 0)
+      sLast = __hip_atomic_fetch_add(&arrive[e], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == parts - 1;
+    __syncthreads();
+    if (sLast && tid < 64) fixup_ratio<D>(a, rs, pw, fpart, e, parts, tid);
   }
 }
 
@@ -1245,7 +1282,7 @@ hipError_t launch_window_attention(const AttnGeom& a, const AttnSplit& sp, hipSt
 
 hipError_t launch_combine(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs, float* lse_out,
                           const ZeroList& zl, hipStream_t s) {
-  const int waves = a.Hkv * a.rows;
+  const int waves = (a.Hkv * a.rows * a.D + 255) / 256;   // 256 / D rows per wave
   dim3 grid((waves + 3) / 4), block(256);
   if (a.D == 128) hipLaunchKernelGGL((combine_kernel<128>), grid, block, 0, s, a, sp, rs, lse_out, zl);
   else hipLaunchKernelGGL((combine_kernel<64>), grid, block, 0, s, a, sp, rs, lse_out, zl);
@@ -1281,19 +1318,17 @@ hipError_t launch_page_kernel(const AttnGeom& a, const PageWork& pw, const RowSt
 }
 
 hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
-                             const PageWork& pw, float* fpart, int parts, int item_budget, hipStream_t s) {
+                             const PageWork& pw, float* fpart, int* arrive, int parts, int item_budget,
+                             hipStream_t s) {
   dim3 grid(std::max(1, std::min(pw.fix_cap * parts, kFixGrid))), block(kFixT);
-  dim3 grid2(std::max(1, std::min((pw.fix_cap + 3) / 4, 256))), block2(256);
   const bool pg = a.slot != nullptr;
   const int ib = item_budget;
   if (a.D == 128) {
-    if (pg) hipLaunchKernelGGL((page_fixup_partial<128, true>), grid, block, 0, s, a, sp, rs, pw, fpart, parts, ib);
-    else hipLaunchKernelGGL((page_fixup_partial<128, false>), grid, block, 0, s, a, sp, rs, pw, fpart, parts, ib);
-    hipLaunchKernelGGL((page_fixup_final<128>), grid2, block2, 0, s, a, rs, pw, fpart, parts, ib);
+    if (pg) hipLaunchKernelGGL((page_fixup_kernel<128, true>), grid, block, 0, s, a, sp, rs, pw, fpart, arrive, parts, ib);
+    else hipLaunchKernelGGL((page_fixup_kernel<128, false>), grid, block, 0, s, a, sp, rs, pw, fpart, arrive, parts, ib);
   } else {
-    if (pg) hipLaunchKernelGGL((page_fixup_partial<64, true>), grid, block, 0, s, a, sp, rs, pw, fpart, parts, ib);
-    else hipLaunchKernelGGL((page_fixup_partial<64, false>), grid, block, 0, s, a, sp, rs, pw, fpart, parts, ib);
-    hipLaunchKernelGGL((page_fixup_final<64>), grid2, block2, 0, s, a, rs, pw, fpart, parts, ib);
+    if (pg) hipLaunchKernelGGL((page_fixup_kernel<64, true>), grid, block, 0, s, a, sp, rs, pw, fpart, arrive, parts, ib);
+    else hipLaunchKernelGGL((page_fixup_kernel<64, false>), grid, block, 0, s, a, sp, rs, pw, fpart, arrive, parts, ib);
   }
   return hipGetLastError();
 }
