@@ -6,6 +6,7 @@
 // resident index ranges without reading the device.
 #include "commitkv_agent.h"
 #include "ckv_host.h"
+#include "ckv_trace.h"
 
 #include <hip/hip_runtime.h>
 
@@ -74,6 +75,7 @@ struct ckv_agent {
   std::vector<int32_t> freed;        // paged: rows released by the last checkpoint
   std::vector<int32_t> res;          // resident positions, ascending
   std::vector<Event> events;
+  bool events_ordered = true;   // every event starts after the previous one ends
   int64_t decoded = 0;
   bool pending = false;
   size_t commit_events = 0;          // events seen when the pending commit was made
@@ -143,21 +145,50 @@ struct ckv_agent {
   // E_c: pages of tool calls and observations, fully resident, not in D_c,
   // the max_scan_pages of largest start
   std::vector<Page> eligible() const {
+    CKV_RANGE("eligible pages");
+    const size_t cap = (size_t)max_pages();
     std::vector<Page> out;
-    for (const Event& e : events) {
-      if (!pageable(e.kind)) continue;
-      for (int off = 0; off < e.n; off += cfg.page_size) {
-        const Page p{e.start + off, std::min(cfg.page_size, e.n - off)};
-        if (std::binary_search(retired.begin(), retired.end(), p)) continue;
-        if (resident(p)) out.push_back(p);
+    if (events_ordered) {
+      // Events hold disjoint, increasing positions, so their pages come in
+      // increasing order and one forward walk over res (ascending, without
+      // repeats) and retired (sorted) settles every page: a page is wholly
+      // resident iff its first and last positions sit len - 1 entries apart.
+      size_t ir = 0, it = 0;
+      for (const Event& e : events) {
+        if (!pageable(e.kind) || e.n <= 0) continue;
+        ir = std::lower_bound(res.begin() + ir, res.end(), e.start) - res.begin();
+        if (ir == res.size()) break;
+        if (res[ir] >= e.start + e.n) continue;
+        for (int off = (res[ir] - e.start) / cfg.page_size * cfg.page_size; off < e.n; off += cfg.page_size) {
+          const Page p{e.start + off, std::min(cfg.page_size, e.n - off)};
+          if (ir < res.size() && res[ir] < p.start)
+            ir = std::lower_bound(res.begin() + ir, res.end(), p.start) - res.begin();
+          if (res.size() - ir < (size_t)p.len) break;
+          if (res[ir] != p.start || res[ir + p.len - 1] != p.start + p.len - 1) continue;
+          ir += p.len;   // the next page, if resident, starts right here
+          while (it < retired.size() && retired[it] < p) ++it;
+          if (it < retired.size() && retired[it] == p) continue;
+          out.push_back(p);
+        }
       }
+    } else {
+      for (const Event& e : events) {
+        if (!pageable(e.kind)) continue;
+        for (int off = 0; off < e.n; off += cfg.page_size) {
+          const Page p{e.start + off, std::min(cfg.page_size, e.n - off)};
+          if (std::binary_search(retired.begin(), retired.end(), p)) continue;
+          if (resident(p)) out.push_back(p);
+        }
+      }
+      std::sort(out.begin(), out.end());
     }
-    std::sort(out.begin(), out.end());
-    if ((int)out.size() > max_pages()) out.erase(out.begin(), out.end() - max_pages());
+    // the newest max_pages() pages are scored
+    if (out.size() > cap) out.erase(out.begin(), out.end() - cap);
     return out;
   }
 
   void ranges(const std::vector<Page>& pages, std::vector<int32_t>* st, std::vector<int32_t>* ln) const {
+    CKV_RANGE("page ranges");
     st->clear();
     ln->clear();
     for (const Page& p : pages) {
@@ -326,6 +357,7 @@ void free_agent(ckv_agent* a) {
 
 extern "C" int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* b0, const ckv_cache_view* b1,
                                 const ckv_agent_config* cfg, ckv_agent** out) {
+  CKV_RANGE("ckv_agent_create");
   if (!ctx) return CKV_ERR_ARG;
   if (!b0 || !b1 || !cfg || !out) return ctx_fail(ctx, CKV_ERR_ARG, "agent: NULL argument");
   *out = nullptr;
@@ -354,6 +386,7 @@ extern "C" int ckv_agent_create(ckv_ctx* ctx, const ckv_cache_view* b0, const ck
 
 extern "C" int ckv_agent_create_paged(ckv_ctx* ctx, const ckv_kv_view* pool, int32_t capacity,
                                       const ckv_agent_config* cfg, ckv_agent** out) {
+  CKV_RANGE("ckv_agent_create_paged");
   if (!ctx) return CKV_ERR_ARG;
   if (!pool || !cfg || !out) return ctx_fail(ctx, CKV_ERR_ARG, "agent: NULL argument");
   *out = nullptr;
@@ -391,6 +424,7 @@ extern "C" int ckv_agent_create_paged(ckv_ctx* ctx, const ckv_kv_view* pool, int
 }
 
 extern "C" int ckv_agent_destroy(ckv_agent* a) {
+  CKV_RANGE("ckv_agent_destroy");
   if (!a) return CKV_ERR_ARG;
   free_agent(a);
   return CKV_OK;
@@ -436,7 +470,11 @@ int record_tokens(ckv_agent* a, int32_t kind, const int32_t* pos, const int32_t*
     a->rows.insert(a->rows.end(), rows, rows + n);
   }
   if (n > 0 || fresh) {
-    if (fresh) a->events.push_back(Event{kind, n > 0 ? pos[0] : (a->res.empty() ? 0 : a->res.back() + 1), 0});
+    if (fresh) {
+      const int st = n > 0 ? pos[0] : (a->res.empty() ? 0 : a->res.back() + 1);
+      if (!a->events.empty() && st < a->events.back().start + a->events.back().n) a->events_ordered = false;
+      a->events.push_back(Event{kind, st, 0});
+    }
     a->events.back().n += n;
     a->res.insert(a->res.end(), pos, pos + n);
   }
@@ -458,6 +496,7 @@ int record_tokens(ckv_agent* a, int32_t kind, const int32_t* pos, const int32_t*
 
 extern "C" int ckv_agent_append(ckv_agent* a, int32_t kind, const int32_t* pos, int32_t n, int32_t decoded,
                                 int32_t begins_event, int32_t* due) {
+  CKV_RANGE("ckv_agent_append");
   if (!a) return CKV_ERR_ARG;
   if (a->paged) return ctx_fail(a->ctx, CKV_ERR_ARG, "append: a paged agent takes ckv_agent_append_rows");
   return record_tokens(a, kind, pos, nullptr, n, decoded, begins_event, due);
@@ -465,12 +504,14 @@ extern "C" int ckv_agent_append(ckv_agent* a, int32_t kind, const int32_t* pos, 
 
 extern "C" int ckv_agent_append_rows(ckv_agent* a, int32_t kind, const int32_t* pos, const int32_t* rows, int32_t n,
                                      int32_t decoded, int32_t begins_event, int32_t* due) {
+  CKV_RANGE("ckv_agent_append_rows");
   if (!a) return CKV_ERR_ARG;
   if (!a->paged) return ctx_fail(a->ctx, CKV_ERR_ARG, "append_rows: the agent owns cache buffers (ckv_agent_append)");
   return record_tokens(a, kind, pos, rows, n, decoded, begins_event, due);
 }
 
 extern "C" int ckv_agent_commit(ckv_agent* a, const ckv_window_view* q_pre) {
+  CKV_RANGE("ckv_agent_commit");
   if (!a) return CKV_ERR_ARG;
   int rc;
   if ((rc = a->check_window(q_pre, "commit"))) return rc;
@@ -484,6 +525,7 @@ extern "C" int ckv_agent_commit(ckv_agent* a, const ckv_window_view* q_pre) {
     const ckv_kv_view kv = a->layer_view();
     if ((rc = ckv_measure_page_effects(a->ctx, &kv, q_pre, &pl, a->d_r_pre, nullptr, nullptr, nullptr, nullptr)))
       return rc;
+    CKV_RANGE("copy back and sync");
     if ((rc = a->copy(a->dn_r, a->d_r_pre, E.size() * 4, hipMemcpyDeviceToHost)) || (rc = a->sync())) return rc;
     std::memcpy(r.data(), a->dn_r, E.size() * 4);
   }
@@ -496,6 +538,7 @@ extern "C" int ckv_agent_commit(ckv_agent* a, const ckv_window_view* q_pre) {
 }
 
 extern "C" int ckv_agent_post(ckv_agent* a, const ckv_window_view* q_post) {
+  CKV_RANGE("ckv_agent_post");
   if (!a) return CKV_ERR_ARG;
   int rc;
   if ((rc = a->check_window(q_post, "post"))) return rc;
@@ -563,6 +606,7 @@ extern "C" int ckv_agent_post(ckv_agent* a, const ckv_window_view* q_post) {
 }
 
 extern "C" int ckv_agent_checkpoint(ckv_agent* a, const ckv_window_view* q_score, int32_t* compacted) {
+  CKV_RANGE("ckv_agent_checkpoint");
   if (!a) return CKV_ERR_ARG;
   int rc;
   if ((rc = a->check_window(q_score, "checkpoint"))) return rc;

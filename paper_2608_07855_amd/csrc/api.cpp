@@ -6,6 +6,7 @@
 #include "commitkv.h"
 #include "ckv_host.h"
 #include "ckv_kernels.h"
+#include "ckv_trace.h"
 
 #include <hip/hip_runtime.h>
 
@@ -353,6 +354,7 @@ int cached_copy(ckv_ctx* c, std::vector<int32_t>&& key, const int32_t** dev) {
 
 // device copy of a (validated) page list: start[0..n) then len[0..n)
 int page_table(ckv_ctx* c, const ckv_page_list* pl, const int32_t** dstart, const int32_t** dlen) {
+  CKV_RANGE("page table");
   const int n = pl->n_pages;
   *dstart = *dlen = nullptr;
   if (n == 0) return CKV_OK;
@@ -457,6 +459,7 @@ int items_per_block(int n_items, int other_blocks) {
 // ----------------------------------------------------------------- context
 
 extern "C" int ckv_create(ckv_ctx** out, int device, void* hip_stream) {
+  CKV_RANGE("ckv_create");
   if (!out) return CKV_ERR_ARG;
   *out = nullptr;
   int n = 0;
@@ -511,6 +514,7 @@ extern "C" int ckv_create(ckv_ctx** out, int device, void* hip_stream) {
 }
 
 extern "C" int ckv_destroy(ckv_ctx* c) {
+  CKV_RANGE("ckv_destroy");
   if (!c) return CKV_ERR_ARG;
   {
     DeviceGuard g(c->device);   // best effort: the context is freed whatever happens
@@ -545,6 +549,7 @@ extern "C" int ckv_set_stream(ckv_ctx* c, void* hip_stream) {
 }
 
 extern "C" int ckv_sync(ckv_ctx* c) {
+  CKV_RANGE("ckv_sync");
   if (!c) return CKV_ERR_ARG;
   DeviceGuard g(c->device);
   if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
@@ -723,6 +728,7 @@ int enqueue_measure(ckv_ctx* c, const AttnGeom& a, const MeasureBufs& b, const i
 extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win,
                                         const ckv_page_list* pages, float* R, float* R_head, float* o,
                                         float* lse, float* token_mass) {
+  CKV_RANGE("ckv_measure_page_effects");
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
   if (int rc0 = latched_nonfinite(c)) return rc0;
@@ -744,6 +750,7 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
 extern "C" int ckv_measure_page_effects_noalloc(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win,
                                                 const ckv_page_list* pages, float* R, float* R_head, float* o,
                                                 float* lse, float* token_mass) {
+  CKV_RANGE("ckv_measure_page_effects_noalloc");
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
   if (int rc0 = latched_nonfinite(c)) return rc0;
@@ -794,6 +801,7 @@ extern "C" int ckv_measure_page_effects_batch(ckv_ctx* c, int32_t n, const ckv_k
                                               const ckv_window_view* win, const ckv_page_list* pages,
                                               float* const* R, float* const* R_head, float* const* o,
                                               float* const* lse, float* const* token_mass) {
+  CKV_RANGE("ckv_measure_page_effects_batch");
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
   if (int rc0 = latched_nonfinite(c)) return rc0;
@@ -825,6 +833,7 @@ extern "C" int ckv_measure_page_effects_batch(ckv_ctx* c, int32_t n, const ckv_k
 extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* win,
                                     const ckv_page_list* pages, const float* o, const float* lse, float* R,
                                     float* R_head, float* token_mass) {
+  CKV_RANGE("ckv_measure_recorded");
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
   if (int rc0 = latched_nonfinite(c)) return rc0;
@@ -910,6 +919,7 @@ extern "C" int ckv_classify_pages(ckv_ctx* c, int32_t n, const float* R_pre, con
                                   const ckv_thresholds* th, const uint8_t* force, int32_t max_cand,
                                   uint8_t* lambda, float* P_pre, float* P_post, int32_t* cand,
                                   int32_t* n_cand) {
+  CKV_RANGE("ckv_classify_pages");
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
   if (int rc0 = latched_nonfinite(c)) return rc0;
@@ -951,6 +961,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
                               const float* lse, const ckv_page_list* pages, const int32_t* cand,
                               const int32_t* n_cand, int32_t max_cand, float tau_joint, uint8_t* accepted,
                               float* union_R, int32_t* n_accepted) {
+  CKV_RANGE("ckv_joint_test");
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
   if (int rc0 = latched_nonfinite(c)) return rc0;
@@ -1052,6 +1063,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
 
 extern "C" int ckv_pool_scores(ckv_ctx* c, const float* score, float* out, int32_t n_seq, int64_t seq_stride,
                                const int32_t* n_tokens, int32_t kernel, int32_t mode) {
+  CKV_RANGE("ckv_pool_scores");
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
   if (int rc0 = latched_nonfinite(c)) return rc0;
@@ -1086,6 +1098,7 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
                                       const ckv_accepted_pages* accepted, const ckv_budget* budget,
                                       const ckv_cache_view* out, int32_t* kept_idx, int32_t* n_kept,
                                       uint8_t* token_state) {
+  CKV_RANGE("ckv_select_and_compact");
   if (!c) return CKV_ERR_ARG;
   begin_call(c);
   if (int rc0 = latched_nonfinite(c)) return rc0;
