@@ -195,6 +195,20 @@ def test_paper_operating_point_episode(ckv):
     assert s["compacted"] >= 1 and s["commit"] >= 5
 
 
+@pytest.mark.parametrize("budget,turns,obs_hi", [(4096, 9, 1024), (8192, 12, 1536)])
+def test_paper_operating_point_budgets(ckv, budget, turns, obs_hi):
+    """The paper's other two budgets (Sec. 4.1) at its operating point, each
+    episode long enough that checkpoints compact the cache past the budget."""
+    P, ctx = ckv
+    cfg = scaled_trajectory("paper_agent", n_layers=2, score_layer=1, budget=budget, obs_hi=obs_hi,
+                            reason_hi=384, prompt_hi=512, forced_frac=0.1, forced_pre=100.0,
+                            forced_post=0.005, heavy_frac=0.003)
+    traj = make_trajectory(cfg, seed=0, n_turns=turns)
+    assert traj.n_tokens > budget + 256
+    s = run_lockstep(P, ctx, traj)
+    assert s["compacted"] >= 1 and s["commit"] >= turns - 1
+
+
 @pytest.mark.parametrize("mode", ["max", "mean"])
 def test_pooled_score_episode(ckv, mode):
     """The SnapKV-style pooled base score (7 tokens) at every checkpoint."""
