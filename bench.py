@@ -504,6 +504,7 @@ def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped", paged=False, bud
         ag.close()
     ctx.close()
     total = sum(t.values())
+    kv_b = cfg.budget * Hkv * d * 2 * 2
     log(f"[bench] agent leg: {n_seq} episodes, {tokens} tokens, driver time {total:.3f}s")
     return dict(
         workload=f"{shape} stack, {L} layers (Hq {Hq}, Hkv {Hkv}, d {d}), {n_seq} agent episodes "
@@ -514,6 +515,12 @@ def agent_leg(n_seq, traj="q8b_agent", shape="qwen3-8b-shaped", paged=False, bud
         commits=n["commit"], posts=n["post"], checkpoints=n["checkpoint"], compactions=n["compacted"],
         ms_per_commit=1e3 * t["commit"] / max(n["commit"], 1), ms_per_post=1e3 * t["post"] / max(n["post"], 1),
         ms_per_checkpoint=1e3 * t["checkpoint"] / max(n["checkpoint"], 1),
+        # one read of the scored layer's keys and values at the budget, at
+        # 8 TB/s, against the host-timed call (commit: pre measurement; post:
+        # post measurement, classification and joint test)
+        layer_kv_bytes_at_budget=kv_b, kv_roofline_us=1e6 * kv_b / 8e12,
+        commit_kv_roofline_frac=(kv_b / 8e12) / (t["commit"] / n["commit"]) if n["commit"] else None,
+        post_kv_roofline_frac=(kv_b / 8e12) / (t["post"] / n["post"]) if n["post"] else None,
         compaction_GBps=moved / t["checkpoint"] / 1e9 if t["checkpoint"] > 0 and not paged else None)
 
 
