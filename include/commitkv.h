@@ -72,7 +72,8 @@ typedef enum ckv_status {
   CKV_ERR_UNSUPPORTED = -4, /* valid request outside what this build handles */
   CKV_ERR_NOMEM = -5,       /* workspace allocation failed or exceeds the limit */
   CKV_ERR_HIP = -6,         /* a HIP runtime call failed */
-  CKV_ERR_NONFINITE = -7    /* non-finite input detected on the device (latched) */
+  CKV_ERR_NONFINITE = -7,   /* non-finite input detected on the device (latched) */
+  CKV_ERR_DEVICE_CHECK = -8 /* a device bounds check failed (builds with device checks only; latched) */
 } ckv_status;
 
 /* Lifecycle states, Sec. 3.2 Eq. (10). */
@@ -115,6 +116,18 @@ const char* ckv_last_error(const ckv_ctx* ctx);
 
 /* (major << 16) | (minor << 8) | patch */
 uint32_t ckv_version(void);
+
+/* Build switches of this library.  CKV_BUILD_DEVICE_CHECKS: compiled with
+ * device bounds checks (-DCKV_DEBUG; libcommitkv_debug.so).  In such a build
+ * a kernel index outside its buffer is clamped into it and the check's site
+ * number latched in the context's pinned debug word; the next call on the
+ * context (or ckv_sync, after its wait) returns CKV_ERR_DEVICE_CHECK, names
+ * the site in ckv_last_error, and clears the word.  The sites cover the key
+ * and value rows of staged tiles, split partials, window-row outputs, page
+ * effects, residuals, fix-up entries, joint-test candidates and the
+ * compaction's kept indices.  Release builds return 0 and check nothing. */
+#define CKV_BUILD_DEVICE_CHECKS 1u
+uint32_t ckv_build_flags(void);
 
 /* Cap the workspace (bytes; 0 = no cap).  Calls that would need more fail
  * with CKV_ERR_NOMEM before enqueuing anything. */

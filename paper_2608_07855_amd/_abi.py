@@ -12,6 +12,9 @@ import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libcommitkv.so")
+# the same library built with device bounds checks (CKV_DEBUG)
+DEBUG_LIB_PATH = os.path.join(_HERE, "libcommitkv_debug.so")
+BUILD_DEVICE_CHECKS = 1
 
 CKV_OK = 0
 CKV_ERR_ARG = -1
@@ -21,9 +24,10 @@ CKV_ERR_UNSUPPORTED = -4
 CKV_ERR_NOMEM = -5
 CKV_ERR_HIP = -6
 CKV_ERR_NONFINITE = -7
+CKV_ERR_DEVICE_CHECK = -8
 STATUS_NAMES = {0: "CKV_OK", -1: "CKV_ERR_ARG", -2: "CKV_ERR_SHAPE", -3: "CKV_ERR_BUDGET",
                 -4: "CKV_ERR_UNSUPPORTED", -5: "CKV_ERR_NOMEM", -6: "CKV_ERR_HIP",
-                -7: "CKV_ERR_NONFINITE"}
+                -7: "CKV_ERR_NONFINITE", -8: "CKV_ERR_DEVICE_CHECK"}
 MAX_PAGE_LEN = 64
 # ckv_policy_flag: component switches of the Sec. 4.4 ablation variants
 POLICY_NO_PRECOMMIT = 1
@@ -120,6 +124,7 @@ SIGNATURES = {
     "ckv_sync": (ctypes.c_int, [ctypes.c_void_p]),
     "ckv_last_error": (ctypes.c_char_p, [ctypes.c_void_p]),
     "ckv_version": (ctypes.c_uint32, []),
+    "ckv_build_flags": (ctypes.c_uint32, []),
     "ckv_set_workspace_limit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t]),
     "ckv_workspace_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
     "ckv_set_policy": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_uint32]),

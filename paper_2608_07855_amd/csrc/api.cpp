@@ -101,6 +101,10 @@ struct ckv_ctx {
   // set; reported (and cleared) by the next call or by ckv_sync
   volatile uint32_t* nf_host = nullptr;
   uint32_t* nf_dev = nullptr;
+  // the next word of the same block: the site of a failed device bounds
+  // check (CKV_DEBUG builds only write it)
+  volatile uint32_t* dbg_host = nullptr;
+  uint32_t* dbg_dev = nullptr;
   void* scratch = nullptr;   // device address of the static scratch on this device
   std::string scratch_err;
   // kernel timing (events around every launch when enabled)
@@ -177,6 +181,11 @@ void begin_call(ckv_ctx* c) {
 // A non-finite value latched by an earlier call's kernels (visible once
 // those kernels have finished) is reported once, then cleared.
 int latched_nonfinite(ckv_ctx* c) {
+  if (c->dbg_host && *c->dbg_host != 0u) {
+    const uint32_t site = *c->dbg_host;
+    *c->dbg_host = 0u;
+    return fail(c, CKV_ERR_DEVICE_CHECK, "device bounds check %u failed in an earlier call on this context", site);
+  }
   if (!c->nf_host || *c->nf_host == 0u) return CKV_OK;
   *c->nf_host = 0u;
   return fail(c, CKV_ERR_NONFINITE,
@@ -418,8 +427,9 @@ int check_pages(ckv_ctx* c, const ckv_page_list* pl, int n_tokens, const char* w
   return CKV_OK;
 }
 
-AttnGeom make_geom(const ckv_kv_view* kv, const ckv_window_view* w) {
+AttnGeom make_geom(const ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* w) {
   AttnGeom a;
+  a.dbg = c->dbg_dev;
   a.k = kv->k;
   a.v = kv->v;
   a.kv_head_stride = kv->head_stride;
@@ -485,6 +495,8 @@ extern "C" int ckv_create(ckv_ctx** out, int device, void* hip_stream) {
     std::memset(h, 0, 256);
     c->nf_host = static_cast<volatile uint32_t*>(h);
     c->nf_dev = static_cast<uint32_t*>(d);
+    c->dbg_host = c->nf_host + 1;
+    c->dbg_dev = c->nf_dev + 1;
   }
   {
     // the static scratch's address on this device, looked up once per device
@@ -558,6 +570,14 @@ extern "C" int ckv_sync(ckv_ctx* c) {
 }
 
 extern "C" const char* ckv_last_error(const ckv_ctx* c) { return c ? c->err.c_str() : "NULL context"; }
+
+extern "C" uint32_t ckv_build_flags(void) {
+#ifdef CKV_DEBUG
+  return CKV_BUILD_DEVICE_CHECKS;
+#else
+  return 0u;
+#endif
+}
 
 extern "C" uint32_t ckv_version(void) {
   return (CKV_VERSION_MAJOR << 16) | (CKV_VERSION_MINOR << 8) | CKV_VERSION_PATCH;
@@ -737,7 +757,7 @@ extern "C" int ckv_measure_page_effects(ckv_ctx* c, const ckv_kv_view* kv, const
   DeviceGuard g(c->device);
   if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
 
-  const AttnGeom a = make_geom(kv, win);
+  const AttnGeom a = make_geom(c, kv, win);
   Plan plan;
   MeasureBufs b;
   plan_measure(a, default_splits(a), o, plan, b);
@@ -760,7 +780,7 @@ extern "C" int ckv_measure_page_effects_noalloc(ckv_ctx* c, const ckv_kv_view* k
   if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
   if (!c->scratch) return fail(c, CKV_ERR_HIP, "the device's static scratch is unavailable: %s", c->scratch_err.c_str());
 
-  const AttnGeom a = make_geom(kv, win);
+  const AttnGeom a = make_geom(c, kv, win);
   const int n = pages->n_pages;
   const size_t table = round_up(std::max<size_t>(2 * (size_t)n * sizeof(int32_t), 1), kAlign);
   // as many splits as the regular call uses, fewer if the split partials
@@ -849,7 +869,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
   DeviceGuard g(c->device);
   if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
 
-  const AttnGeom a = make_geom(kv, win);
+  const AttnGeom a = make_geom(c, kv, win);
   const int n = pages->n_pages, total_rows = a.Hq * a.W;
   RowStats rs{const_cast<float*>(o), nullptr, nullptr, nullptr};
   Plan plan;
@@ -975,7 +995,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   if (!std::isfinite(tau_joint)) return fail(c, CKV_ERR_ARG, "tau_joint must be finite");
   DeviceGuard g(c->device);
   if (!g.ok) return fail(c, CKV_ERR_HIP, "cannot select device %d", c->device);
-  const AttnGeom a = make_geom(kv, win);
+  const AttnGeom a = make_geom(c, kv, win);
   const int total_rows = a.Hq * a.W, D = a.D;
   // the residual pass reads the caller's o and natural-log lse directly
   RowStats rs{const_cast<float*>(o), const_cast<float*>(lse), nullptr, nullptr};
@@ -1325,6 +1345,8 @@ extern "C" int ckv_select_and_compact(ckv_ctx* c, const ckv_cache_view* in, cons
   ga.kept = kept_idx;
   ga.n_kept = n_kept;
   ga.budget = B;
+  ga.in_rows = in->capacity;
+  ga.dbg = c->dbg_dev;
   CKV_LAUNCH(c, "gather", launch_gather(ga, c->stream));
   return CKV_OK;
 }

@@ -97,6 +97,22 @@ __device__ __forceinline__ constexpr int vt_frag_const(int VP, int db, int tb, i
   return 32 * db * VP + 8 * (((tb ^ (db >> 1)) << 2) | ((u ^ (db & 1)) << 1));
 }
 
+// Device bounds checks (builds with -DCKV_DEBUG): an index outside [0, n)
+// stores the check's site number in the context's debug word (pinned host
+// memory, reported by the next call or ckv_sync as CKV_ERR_DEVICE_CHECK) and
+// is clamped into the range, so the access itself stays inside the buffer.
+// Other builds use the index as it is.
+#ifdef CKV_DEBUG
+__device__ __forceinline__ int64_t checked_index(int64_t i, int64_t n, uint32_t* word, uint32_t site) {
+  if (i >= 0 && i < n) return i;
+  if (word) __hip_atomic_store(word, site, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  return (i < 0 || n <= 0) ? 0 : n - 1;
+}
+#define CKV_IDX(i, n, word, site) ::ckv::checked_index((int64_t)(i), (int64_t)(n), (word), (site))
+#else
+#define CKV_IDX(i, n, word, site) (i)
+#endif
+
 // loads through the global address space (pointers inside by-value argument
 // structs otherwise compile to flat accesses)
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));

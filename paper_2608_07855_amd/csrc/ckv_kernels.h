@@ -24,6 +24,7 @@ struct AttnGeom {
   const int32_t* slot;                     // paged pool: token t is row slot[t] of each head
                                            // (clamped to pool_last), or null: row t
   uint32_t pool_last;                      // last row of the pool
+  uint32_t* dbg;                           // debug word of the context (CKV_DEBUG builds)
 };
 
 // split-sequence partials of pass A
@@ -268,6 +269,8 @@ struct GatherArgs {
   const int32_t* kept;           // [n_seq][budget]
   const int32_t* n_kept;
   int budget;
+  int64_t in_rows;               // token rows of an input sequence (capacity)
+  uint32_t* dbg;                 // debug word of the context (CKV_DEBUG builds)
 };
 hipError_t launch_gather(const GatherArgs& g, hipStream_t s);
 

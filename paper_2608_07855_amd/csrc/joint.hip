@@ -140,8 +140,14 @@ __device__ void joint_item(const JointArgs& j, const RowStats& rs, int jx, int r
       const int row = base + 4 * q;
       const bool ok = row < r1;
       const int rr = ok ? row : r0;
-      const float* rp = pend >= 0 ? j.resid + ((size_t)rr * j.max_cand + pend) * j.D : nullptr;
-      const float* rt = valid ? j.resid + ((size_t)rr * j.max_cand + t) * j.D : nullptr;
+      const float* rp =
+          pend >= 0 ? j.resid + (size_t)CKV_IDX((size_t)rr * j.max_cand + pend, (int64_t)j.total_rows * j.max_cand,
+                                                j.geo.dbg, 11) * j.D
+                    : nullptr;
+      const float* rt =
+          valid ? j.resid + (size_t)CKV_IDX((size_t)rr * j.max_cand + t, (int64_t)j.total_rows * j.max_cand,
+                                            j.geo.dbg, 11) * j.D
+                : nullptr;
 #pragma unroll
       for (int k = 0; k < KD; ++k) {
         const int d = lane + 64 * k;
@@ -277,8 +283,8 @@ __device__ void joint_fix_partial(const JointArgs& j, int cursor, int e0, int np
   for (int item = blockIdx.x; item < np * parts; item += gridDim.x) {
     const int e = e0 + item / parts, part = item % parts;
     const int2 ent = load_pair(j.fix_list + 2 * e);
-    const int rg = ent.y;
-    const int cp = j.cand[cursor + ent.x];   // the candidate's page
+    const int rg = (int)CKV_IDX(ent.y, j.total_rows, j.geo.dbg, 12);
+    const int cp = j.cand[CKV_IDX(cursor + ent.x, j.max_cand, j.geo.dbg, 13)];   // the candidate's page
     const int h = rg / a.W, p = rg % a.W, g = h / a.group;
     const int qp = a.qpos[p];
     const float ref = j.lse[rg] * kLog2e;

@@ -81,14 +81,15 @@ struct Stager {
   // segments read token 0.  r depends only on the thread, so the slot test
   // is a per-thread constant.
   __device__ __forceinline__ static uint32_t row_off(int r, int s0, int n0, int s1, int n1, uint32_t ts,
-                                                     const int32_t* slot, uint32_t last, bool& ok) {
+                                                     const int32_t* slot, uint32_t last, int S, uint32_t* dbg,
+                                                     bool& ok) {
     const bool hi = r >= 32;
     const int o = r & 31;
     ok = o < (hi ? n1 : n0);
     if constexpr (PG) {
-      return __umul24(min((uint32_t)slot[ok ? (hi ? s1 : s0) + o : 0], last), ts);
+      return __umul24(min((uint32_t)slot[ok ? CKV_IDX((hi ? s1 : s0) + o, S, dbg, 9) : 0], last), ts);
     } else {
-      return ok ? __umul24((uint32_t)((hi ? s1 : s0) + o), ts) : 0u;
+      return ok ? __umul24((uint32_t)CKV_IDX((hi ? s1 : s0) + o, S, dbg, 9), ts) : 0u;
     }
   }
 
@@ -98,12 +99,12 @@ struct Stager {
   // and its weight is exactly 0 (values are finite).
   __device__ __forceinline__ void issue(const uint16_t* kh, const uint16_t* vh, uint32_t ts,
                                         const int32_t* slot, uint32_t last, const int32_t* pos, int s0,
-                                        int n0, int s1, int n1, int tid) {
+                                        int n0, int s1, int n1, int tid, int S, uint32_t* dbg) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + i * NT;
       bool ok;
-      const uint32_t e = row_off((c / CPR) & (kTile - 1), s0, n0, s1, n1, ts, slot, last, ok);
+      const uint32_t e = row_off((c / CPR) & (kTile - 1), s0, n0, s1, n1, ts, slot, last, S, dbg, ok);
       kr[i] = ldg_u4(kh + ((c < KCH ? e : 0u) + (c % CPR) * 8));
     }
 #pragma unroll
@@ -113,14 +114,14 @@ struct Stager {
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         bool ok;
-        const uint32_t e = row_off(2 * tp + j, s0, n0, s1, n1, ts, slot, last, ok);
+        const uint32_t e = row_off(2 * tp + j, s0, n0, s1, n1, ts, slot, last, S, dbg, ok);
         vr[i][j] = ldg_u4(vh + ((u < VU ? e : 0u) + cg * 8));
       }
     }
     const int r = tid & 63;
     const int t = (r >= 32 ? s1 : s0) + (r & 31);
     const bool ok = (r & 31) < (r >= 32 ? n1 : n0) && tid < kTile;
-    pr = ldg_i32(pos + (ok ? t : 0));
+    pr = ldg_i32(pos + (ok ? CKV_IDX(t, S, dbg, 10) : 0));
     pok = ok;
   }
 
@@ -333,7 +334,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
     const int t0 = t_begin + it * kTile;
     const int n = it < n_tiles ? min(kTile, t_end - t0) : 0;
     st.issue(kh, vh, (uint32_t)a.kv_tok_stride, a.slot, a.pool_last, a.pos, t0, min(32, n), t0 + 32,
-             max(0, n - 32), tid);
+             max(0, n - 32), tid, a.S, a.dbg);
   };
   auto compute = [&](int b) {
     if (wave_on) {
@@ -409,7 +410,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
   const float lt = sum32(l);
   const int ct = sum32i(cnt);
   if (!ri.ok) return;
-  const size_t idx = ((size_t)(g * sp.n_splits + split) * sp.rows_pad + ri.row);
+  const size_t idx = CKV_IDX((size_t)(g * sp.n_splits + split) * sp.rows_pad + ri.row,
+                             (int64_t)a.Hkv * sp.n_splits * sp.rows_pad, a.dbg, 1);
   if (half == 0) {
     sp.part_m[idx] = mref;
     sp.part_l[idx] = lt;
@@ -467,7 +469,8 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
 #pragma unroll
     for (int u = 0; u < kCombBatch; ++u) {
       const bool in = s0 + u < sp.n_splits;
-      const size_t idx = base + (size_t)min(s0 + u, sp.n_splits - 1) * sp.rows_pad;
+      const size_t idx = CKV_IDX(base + (size_t)min(s0 + u, sp.n_splits - 1) * sp.rows_pad,
+                                 (int64_t)a.Hkv * sp.n_splits * sp.rows_pad, a.dbg, 2);
       ms[u] = in ? sp.part_m[idx] : -INFINITY;
       ls[u] = sp.part_l[idx];
       cs[u] = in ? sp.part_c[idx] : 0;
@@ -499,7 +502,7 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
 #pragma unroll
   for (int off = TPR / 2; off >= 1; off >>= 1) n2 += __shfl_xor(n2, off, 64);
   if (!ok) return;
-  *reinterpret_cast<f32x4*>(rs.o + (size_t)rg * D + 4 * c) = ov;
+  *reinterpret_cast<f32x4*>(rs.o + (size_t)CKV_IDX(rg, a.Hq * a.W, a.dbg, 3) * D + 4 * c) = ov;
   if (c == 0) {
     const float l2 = wsum > 0.f ? M + __log2f(wsum) : -INFINITY;
     rs.lse2[rg] = l2;
@@ -575,7 +578,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   // o_p in accumulator layout: register r of block db holds width 32db + 8(r/4) + 4h + r%4
   f32x16 of[DB];
   {
-    const float* orow = rs.o + (size_t)ri.rg * D;
+    const float* orow = rs.o + (size_t)CKV_IDX(ri.rg, a.Hq * a.W, a.dbg, 4) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -626,7 +629,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   // index past the end is an empty segment (its loads read token 0).
   auto issue_tile = [&](St& st, int k) {
     const int4 sg = k < n_tiles ? sTileSeg[k] : make_int4(0, 0, 0, 0);
-    st.issue(kh, vh, (uint32_t)a.kv_tok_stride, a.slot, a.pool_last, a.pos, sg.x, sg.y, sg.z, sg.w, tid);
+    st.issue(kh, vh, (uint32_t)a.kv_tok_stride, a.slot, a.pool_last, a.pos, sg.x, sg.y, sg.z, sg.w, tid, a.S,
+             a.dbg);
   };
   // A row sees at least nvis tokens; a page (at most kMaxPage tokens) can
   // hold all of them only if nvis <= kMaxPage, so most waves skip the count.
@@ -710,7 +714,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
 #pragma unroll
           for (int r = 0; r < 16; ++r) n2 = __builtin_fmaf(u[j][r], u[j][r], n2);
         if (MODE == 1 && ri.ok) {
-          float* rrow = pw.resid + ((size_t)ri.rg * pw.n_items + item) * D;
+          float* rrow = pw.resid + (size_t)CKV_IDX((size_t)ri.rg * pw.n_items + item,
+                                                   (int64_t)pw.total_rows * pw.n_items, a.dbg, 6) * D;
 #pragma unroll
           for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -798,10 +803,12 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
       for (int hl = 0; hl < n_heads_blk; ++hl) {
         const unsigned int v = sRm[i * n_heads_blk + hl];
         mx = max(mx, v);
-        if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + g * a.group + head0 + hl],
-                                         __uint_as_float(v));
+        if (pw.R_head)
+          atomic_max_nonneg(&pw.R_head[CKV_IDX((size_t)page * pw.Hq + g * a.group + head0 + hl,
+                                               (int64_t)pw.n_pages * pw.Hq, a.dbg, 5)],
+                            __uint_as_float(v));
       }
-      atomic_max_nonneg(&pw.R[page], __uint_as_float(mx));
+      atomic_max_nonneg(&pw.R[CKV_IDX(page, pw.n_pages, a.dbg, 5)], __uint_as_float(mx));
     }
     const int nf = min(sFixN, kRowsWG);
     if (nf > 0) {
@@ -844,7 +851,8 @@ template <int D>
 __device__ void fixup_ratio(const AttnGeom& a, const RowStats& rs, const PageWork& pw, const float* fpart, int e,
                             int parts, int lane) {
   const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
-  const int page = ent.x, rg = ent.y, h = rg / a.W;
+  const int page = (int)CKV_IDX(ent.x, pw.n_pages, a.dbg, 8), rg = (int)CKV_IDX(ent.y, a.Hq * a.W, a.dbg, 7);
+  const int h = rg / a.W;
   const float* fp = fpart + (size_t)e * parts * (D + 1);
   auto ld = [](const float* p) {
     return __uint_as_float(__hip_atomic_load(reinterpret_cast<const unsigned*>(p), __ATOMIC_RELAXED,
@@ -896,7 +904,7 @@ __global__ __launch_bounds__(kFixT) void page_fixup_kernel(AttnGeom a, AttnSplit
     const int e = item / parts, part = item % parts;
     // entry: page, global row, page start, page length
     const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
-    const int rg = ent.y, st = ent.z, ln = ent.w;
+    const int rg = (int)CKV_IDX(ent.y, a.Hq * a.W, a.dbg, 7), st = ent.z, ln = ent.w;
     const int h = rg / a.W, p = rg % a.W, g = h / a.group, row = rg - g * a.rows;
     const int qp = a.qpos[p];
     const float ref = rs.lse2[rg];

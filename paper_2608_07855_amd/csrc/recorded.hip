@@ -117,7 +117,7 @@ __global__ __launch_bounds__(256) void page_fixup_recorded(AttnGeom a, RowStats 
     }
     float ov[J];
 #pragma unroll
-    for (int j = 0; j < J; ++j) ov[j] = rs.o[(size_t)rg * D + lane + 64 * j];
+    for (int j = 0; j < J; ++j) ov[j] = rs.o[(size_t)CKV_IDX(rg, a.Hq * a.W, a.dbg, 4) * D + lane + 64 * j];
     // weights of the pass's tokens (0 for tokens the row does not see)
     float w[NP];
     float Al = 0.f;
@@ -194,8 +194,9 @@ __global__ __launch_bounds__(256) void page_fixup_recorded(AttnGeom a, RowStats 
       if (cnt >= rs.nvis[rg] || !(den > 0.f)) ratio = INFINITY;
       else if (oo > 0.f) ratio = sqrtf(rr) / (den * sqrtf(oo));
       else ratio = rr > 0.f ? INFINITY : 0.f;
-      if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], ratio);
-      atomic_max_nonneg(&pw.R[page], ratio);
+      if (pw.R_head)
+        atomic_max_nonneg(&pw.R_head[CKV_IDX((size_t)page * pw.Hq + h, (int64_t)pw.n_pages * pw.Hq, a.dbg, 5)], ratio);
+      atomic_max_nonneg(&pw.R[CKV_IDX(page, pw.n_pages, a.dbg, 5)], ratio);
     }
   }
 }

@@ -916,7 +916,8 @@ __global__ __launch_bounds__(kGT) void gather_kernel(GatherArgs g) {
   const int s = combo / (g.n_layers * g.Hkv);
   const int rem = combo % (g.n_layers * g.Hkv);
   const int l = rem / g.Hkv, h = rem % g.Hkv;
-  const int nk = g.n_kept[s];
+  const int nk0 = g.n_kept[s];   // -1: the selection gave up
+  const int nk = nk0 < 0 ? nk0 : (int)CKV_IDX(nk0, g.budget + 1, g.dbg, 15);
   const int j0 = blockIdx.x * kGRows;
   if (j0 >= nk) return;
   const int32_t* kept = g.kept + (size_t)s * g.budget;
@@ -928,7 +929,7 @@ __global__ __launch_bounds__(kGT) void gather_kernel(GatherArgs g) {
   const int j1 = min(nk, j0 + kGRows);
 #pragma unroll 4
   for (int j = j0 + threadIdx.x / CPR; j < j1; j += RPI) {
-    const int src = kept[j];
+    const int src = (int)CKV_IDX(kept[j], g.in_rows, g.dbg, 14);
     const uint4 kv = *reinterpret_cast<const uint4*>(kin + (int64_t)src * g.in_tok + cc * 8);
     const uint4 vv = *reinterpret_cast<const uint4*>(vin + (int64_t)src * g.in_tok + cc * 8);
     *reinterpret_cast<uint4*>(kout + (int64_t)j * g.out_tok + cc * 8) = kv;
@@ -936,7 +937,7 @@ __global__ __launch_bounds__(kGT) void gather_kernel(GatherArgs g) {
   }
   if (l == 0 && h == 0) {
     for (int j = j0 + threadIdx.x; j < j1; j += kGT)
-      g.pos_out[s * g.pos_out_seq + j] = g.pos_in[s * g.pos_in_seq + kept[j]];
+      g.pos_out[s * g.pos_out_seq + j] = g.pos_in[s * g.pos_in_seq + CKV_IDX(kept[j], g.in_rows, g.dbg, 14)];
   }
 }
 

@@ -123,3 +123,24 @@ def test_batch_null_handling(lib):
     L = _abi.load()
     assert L.ckv_measure_page_effects_batch(None, 0, None, None, None, None, None, None, None, None) \
         == _abi.CKV_ERR_ARG
+
+
+def test_device_check_build_exports_the_same_symbols(lib):
+    """libcommitkv_debug.so (-DCKV_DEBUG) exports the same entry points and
+    reports its device bounds checks; the release library reports none."""
+    if not os.path.exists(_abi.DEBUG_LIB_PATH):
+        from paper_2608_07855_amd import build
+        build.build(variant="debug")
+    dbg = _abi.load(_abi.DEBUG_LIB_PATH)
+    missing = [n for n in sorted(_declared()) if not hasattr(dbg, n)]
+    assert not missing, missing
+    assert dbg.ckv_build_flags() == _abi.BUILD_DEVICE_CHECKS
+    assert _abi.load().ckv_build_flags() == 0
+    assert dbg.ckv_sync(None) == _abi.CKV_ERR_ARG
+
+
+def test_device_check_status_in_header():
+    text = open(os.path.join(ROOT, "include", "commitkv.h")).read()
+    assert re.search(r"CKV_ERR_DEVICE_CHECK\s*=\s*-8", text)
+    assert re.search(r"#define CKV_BUILD_DEVICE_CHECKS 1u", text)
+    assert _abi.STATUS_NAMES[_abi.CKV_ERR_DEVICE_CHECK] == "CKV_ERR_DEVICE_CHECK"
