@@ -268,9 +268,9 @@ uint32_t ckv_get_policy(const ckv_ctx* ctx);
  * not hold, and a wait that passes the bound makes every workgroup of the
  * call leave, with *n_accepted = -1 or n_kept[s] = -1 as the result (the
  * outputs are then not valid; the lifecycle driver turns it into
- * CKV_ERR_UNSUPPORTED).  Default 1342177 us (about 1.3 s).  0 makes a wait
- * give up at once unless every workgroup has already arrived, which forces
- * the failure path (for tests of the caller's handling).  Returns
+ * CKV_ERR_UNSUPPORTED).  Default 1342177 us (about 1.3 s).  0 makes every
+ * wait give up at once, which forces the failure path (for tests of the
+ * caller's handling).  Returns
  * CKV_ERR_ARG for a negative or absurd value.
  */
 int ckv_set_barrier_timeout_us(ckv_ctx* ctx, int64_t us);

@@ -55,7 +55,11 @@ __device__ bool grid_barrier(int* ctrl, int target, long long timeout, int* s_ok
     atomicAdd(&ctrl[kBarrier], 1);
     const long long t0 = wall_clock64();
     int ok = 1;
-    while (__hip_atomic_load(&ctrl[kBarrier], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+    if (timeout <= 0) {   // a zero bound gives up at once: the failure path, forced
+      __hip_atomic_store(&ctrl[kError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ok = 0;
+    }
+    while (ok && __hip_atomic_load(&ctrl[kBarrier], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
       if (__hip_atomic_load(&ctrl[kError], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
           wall_clock64() - t0 >= timeout) {
         __hip_atomic_store(&ctrl[kError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -82,7 +86,11 @@ __device__ bool grid_barrier_nofence(int* ctrl, int target, long long timeout, i
     __hip_atomic_fetch_add(&ctrl[kBarrier], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const long long t0 = wall_clock64();
     int ok = 1;
-    while (__hip_atomic_load(&ctrl[kBarrier], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+    if (timeout <= 0) {   // a zero bound gives up at once: the failure path, forced
+      __hip_atomic_store(&ctrl[kError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ok = 0;
+    }
+    while (ok && __hip_atomic_load(&ctrl[kBarrier], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
       if (__hip_atomic_load(&ctrl[kError], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
           wall_clock64() - t0 >= timeout) {
         __hip_atomic_store(&ctrl[kError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -493,7 +493,11 @@ __device__ bool seq_barrier(int* ctrl, int target, long long timeout, int* s_ok)
     atomicAdd(&ctrl[qArrive], 1);
     const long long t0 = wall_clock64();
     int ok = 1;
-    while (__hip_atomic_load(&ctrl[qArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+    if (timeout <= 0) {   // a zero bound gives up at once: the failure path, forced
+      __hip_atomic_store(&ctrl[qError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ok = 0;
+    }
+    while (ok && __hip_atomic_load(&ctrl[qArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
       if (__hip_atomic_load(&ctrl[qError], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
           wall_clock64() - t0 >= timeout) {
         __hip_atomic_store(&ctrl[qError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
