@@ -671,7 +671,7 @@ void plan_measure(const AttnGeom& a, int n_splits, float* o, Plan& plan, Measure
   const int chunk = (int)round_up(ceil_div(a.S, n_splits), 64);
   n_splits = ceil_div(a.S, chunk);
   b.sp = AttnSplit{chunk, n_splits, nrb * rpb, nullptr, nullptr, nullptr, nullptr};
-  b.rs = RowStats{o, nullptr, nullptr, nullptr};
+  b.rs = RowStats{o, nullptr, nullptr, nullptr, nullptr};
   const size_t nsr = (size_t)a.Hkv * n_splits * b.sp.rows_pad;
   plan.add(&b.sp.part_o, nsr * D);
   plan.add(&b.sp.part_m, nsr);
@@ -681,6 +681,7 @@ void plan_measure(const AttnGeom& a, int n_splits, float* o, Plan& plan, Measure
   plan.add(&b.rs.lse2, total_rows);
   plan.add(&b.rs.onorm, total_rows);
   plan.add(&b.rs.nvis, total_rows);
+  plan.add(&b.rs.m2, total_rows);
   plan.add(&b.fix_list, 4 * (size_t)total_rows);
   plan.add(&b.fix_count, 1);
   plan.add(&b.fpart, (size_t)total_rows * ckv::kFixParts * (D + 1));
@@ -733,6 +734,7 @@ int enqueue_measure(ckv_ctx* c, const AttnGeom& a, const MeasureBufs& b, const i
     pw.fix_count = b.fix_count;
     pw.fix_cap = total_rows;
     pw.fix_a = ckv::kFixA;
+    pw.fix_a_hi = ckv::kFixAHi;
     CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, b.rs, 0, max_page_len(pages), c->stream));
     CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, b.sp, b.rs, pw, b.fpart, b.arrive, ckv::kFixParts, 0, c->stream));
   }
@@ -871,7 +873,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
 
   const AttnGeom a = make_geom(c, kv, win);
   const int n = pages->n_pages, total_rows = a.Hq * a.W;
-  RowStats rs{const_cast<float*>(o), nullptr, nullptr, nullptr};
+  RowStats rs{const_cast<float*>(o), nullptr, nullptr, nullptr, nullptr};
   Plan plan;
   plan.add(&rs.lse2, total_rows);
   plan.add(&rs.onorm, total_rows);
@@ -915,6 +917,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
     pw.fix_count = fix_count;
     pw.fix_cap = total_rows;
     pw.fix_a = ckv::kFixARecorded;
+    pw.fix_a_hi = ckv::kFixARecorded;
     CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, rs, 0, max_page_len(pages), c->stream));
     CKV_LAUNCH(c, "page_fixup_recorded", launch_page_fixup_recorded(a, rs, pw, list2, count2, cap2,
                                                                     ckv::kFixAComplement, c->stream));
@@ -998,7 +1001,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   const AttnGeom a = make_geom(c, kv, win);
   const int total_rows = a.Hq * a.W, D = a.D;
   // the residual pass reads the caller's o and natural-log lse directly
-  RowStats rs{const_cast<float*>(o), const_cast<float*>(lse), nullptr, nullptr};
+  RowStats rs{const_cast<float*>(o), const_cast<float*>(lse), nullptr, nullptr, nullptr};
   JointArgs j{};
   j.total_rows = total_rows;
   j.D = D;

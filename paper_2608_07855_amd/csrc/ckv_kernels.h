@@ -36,12 +36,16 @@ struct AttnSplit {
   int* part_c;     // visible-token counts
 };
 
-// per window row (global row h*W + p): o [rows][D], lse2 (log2 units), ||o||, n_vis
+// per window row (global row h*W + p): o [rows][D], lse2 (log2 units), ||o||, n_vis,
+// and m2, the largest scaled logit of the row (log2 units): the reference the
+// window pass's float16 weights were finally taken against (null when the
+// outputs were not computed by this library's window pass)
 struct RowStats {
   float* o;
   float* lse2;
   float* onorm;
   int* nvis;
+  float* m2;
 };
 
 // pages processed by pass B (MODE 0: item = page; MODE 1: item t = page cand[t])
@@ -70,11 +74,21 @@ struct PageWork {
                           // when rs.lse2 holds natural-log values)
   int* clear;             // MODE 1: words set to zero by workgroup (0, 0, 0) (or null)
   int n_clear;
-  float fix_a;            // MODE 0: pairs with A > fix_a (>= 0.5) go to the fix-up list
+  float fix_a;            // MODE 0: pairs with A > fix_a (>= 0.5) go to the fix-up list ...
+  float fix_a_hi;         // ... unless A <= fix_a_hi and the page holds its row's largest
+                          // logit (rs.m2 set): then the closed form is kept
 };
 
-constexpr float kFixA = 0.9f;           // fix-up threshold after this library's window pass
-constexpr float kFixARecorded = 0.5f;   // ... with recorded window outputs
+// Fix-up thresholds after this library's window pass.  A page that holds its
+// row's largest logit was weighted against the same reference (that logit)
+// in both passes, so its float16 weights are the very ones that formed o and
+// Eq. (6) loses only the float32 digits of the row's log-sum-exp, amplified
+// by 1/(1 - A): such pages keep the closed form up to kFixAHi.  Any other
+// page's weights round differently in the two passes, and the residual
+// u - A o inherits that rounding times 1/(1 - A): those go above kFixA.
+constexpr float kFixA = 0.9f;
+constexpr float kFixAHi = 0.99f;
+constexpr float kFixARecorded = 0.5f;   // with recorded window outputs (no shared weights)
 
 struct ZeroList {
   float* p0; size_t n0;

@@ -43,15 +43,24 @@ constexpr int kRowsWG = 32 * kNW;    // window rows per workgroup
 //
 // A page that holds nearly all of a row's mass (A -> 1) is ill-conditioned
 // for Eq. (6): o - u = (1 - A) o' keeps only the digits of o' that survive
-// float32 accumulation of o.  Rows where a page has A > kFixA are therefore
-// left out of the page kernel's maximum and listed; the fix-up kernel
-// recomputes the output without the page, o', directly (all other splits'
-// partial sums as they are, the page's own split again with the page
-// excluded) and takes ||o - o'|| / ||o|| by definition.  At most one page
-// per row can exceed kFixA, so the list never holds more than one entry per
-// window row.  With recorded outputs (computed without this pass's float16
-// weights) the threshold is kFixARecorded: the page pass's rounding is then
-// no longer shared by o, and 1/(1 - A) would amplify it past the tolerance.
+// float32 accumulation of o, and every error of u - A o is amplified by
+// 1/(1 - A).  How far the closed form holds depends on whether the page
+// holds its row's largest logit.  If it does, both passes weighted its
+// tokens against that same logit, so the page's float16 weights are the
+// very ones that formed o and cancel in u - A o; what is left is the
+// float32 rounding of the log-sum-exp (through 1 - A), a few 1e-7 times
+// 1/(1 - A), and such pairs keep the closed form up to A = kFixAHi.  Any
+// other page's weights were rounded against different references in the
+// two passes, and those roundings reach the residual amplified by
+// 1/(1 - A): such pairs are listed above A = kFixA.  Listed rows are left
+// out of the page kernel's maximum; the fix-up kernel recomputes the output
+// without the page, o', directly (all other splits' partial sums as they
+// are, the page's own split again with the page excluded) and takes
+// ||o - o'|| / ||o|| by definition.  At most one page per row can exceed
+// kFixA, so the list never holds more than one entry per window row.  With
+// recorded outputs (computed without this pass's float16 weights) every
+// pair above kFixARecorded is listed: the page pass's rounding is then no
+// longer shared by o, and 1/(1 - A) would amplify it past the tolerance.
 
 // ---------------------------------------------------------------------------
 // staging of a 64-token tile made of two 32-token segments (slot 0: offsets
@@ -508,6 +517,7 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
     rs.lse2[rg] = l2;
     rs.onorm[rg] = sqrtf(n2);
     rs.nvis[rg] = nv;
+    if (rs.m2) rs.m2[rg] = M;
     if (lse_out) lse_out[rg] = l2 * kLn2;
     // a NaN or infinite key, query or value reaches the row's output or its
     // log-sum-exp (a row that sees no token has lse -inf and o = 0)
@@ -593,6 +603,9 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   const float onorm = (MODE == 0 && ri.ok) ? rs.onorm[ri.rg] : 0.f;   // read by MODE 0 only
   const float inv_onorm = onorm > 0.f ? 1.f / onorm : 0.f;
   const int nvis = (MODE == 0 && ri.ok) ? rs.nvis[ri.rg] : 0;   // read by MODE 0 only
+  // the row's largest scaled logit, the window pass's final weight reference
+  // (NaN when unknown: no page then counts as holding it)
+  const float m2row = (MODE == 0 && rs.m2 && ri.ok) ? rs.m2[ri.rg] : __builtin_nanf("");
   const int row0 = rblk * kRowsWG;
   const int head0 = row0 / a.W;
   const int n_heads_blk = min(a.group, (min(a.rows, row0 + kRowsWG) - 1) / a.W + 1) - head0;
@@ -735,7 +748,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
           const float keep = 1.f - A;
           if (need_count && c >= nvis) {
             ratio = INFINITY;                 // the page holds every visible token
-          } else if (A > pw.fix_a || !(keep > 0.f)) {
+          } else if ((A > pw.fix_a && (A > pw.fix_a_hi || base != m2row)) || !(keep > 0.f)) {
             if (ri.ok && half == 0) {         // ill-conditioned: recomputed by the fix-up
               const int4 ent = make_int4(item, ri.rg, pstart(item), len);
               const int ls = atomicAdd(&sFixN, 1);

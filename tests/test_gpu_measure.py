@@ -172,6 +172,65 @@ def test_dominant_page(ckv, which):
     assert_scores_close(got["R_head"], Rh, "R_head")
 
 
+@pytest.mark.parametrize("which", ["max_inside", "max_outside"])
+def test_heavy_page_band(ckv, which):
+    """Pages carrying between 0.9 and 0.99 of a row's mass.  A page that holds
+    its row's largest logit keeps the closed form of Eq. (6) up to A = 0.99
+    (its float16 weights are the ones that formed o); a page whose tokens
+    share the mass while a token outside it holds the row's largest logit is
+    recomputed by definition above A = 0.9.  Both must meet the tolerance."""
+    P, ctx = ckv
+    import math
+    w = scaled("tiny", n_tokens=2048, n_q_heads=4, n_kv_heads=1)
+    L = make_layer(w, seed=11)
+    from synth import bf16_bits, bf16_bits_to_f32
+    k = bf16_bits_to_f32(L.k).copy()
+    q = bf16_bits_to_f32(L.q_post)
+    qdir = q.mean(axis=(0, 1))
+    qdir /= np.linalg.norm(qdir)
+    starts, lens = L.layout.page_start, L.layout.page_len
+    full = np.flatnonzero(lens == lens.max())
+    if which == "max_inside":
+        # one heavy token per page, at strengths that put A on both sides of
+        # 0.9 and 0.99 across the rows
+        strengths = np.geomspace(30.0, 200.0, 24)
+        picks = full[np.linspace(0, len(full) - 1, len(strengths)).astype(int)]
+        for j, c in zip(picks, strengths):
+            k[0, int(starts[j]) + 1] = qdir * c
+        probe = picks
+    else:
+        # every token of one page equally strong, one token elsewhere a little
+        # stronger: the page carries most of the mass without the largest logit
+        j = int(full[len(full) // 2])
+        st, ln = int(starts[j]), int(lens[j])
+        k[0, st:st + ln] = qdir * 80.0
+        k[0, int(starts[full[1]]) + 2] = qdir * 82.0
+        probe = [j]
+    L.k = bf16_bits(k)
+    dl = LayerOnDevice(L)
+    got = _measure(P, ctx, dl, "post")
+    R, Rh = O.page_effects(L.k, L.v, L.pos, L.q_post, L.qpos_post, L.pages, method="closed")
+    K, V, Q = O.as_f64(L.k), O.as_f64(L.v), O.as_f64(L.q_post)
+    vis = O.visibility(L.pos, L.qpos_post)
+    band = 0
+    for h in range(Q.shape[0]):
+        s = O.head_logits(Q[h], K[0], 1 / math.sqrt(K.shape[2]))
+        a, _ = O.attend(s, vis, V[0])
+        for j in probe:
+            st, ln = int(starts[j]), int(lens[j])
+            A = a[:, st:st + ln].sum(1)
+            sel = (A > 0.9) & (A < 0.99)
+            band += int(sel.sum())
+            if which == "max_outside" and sel.any():
+                # the row's largest logit lies outside the page
+                sm = np.where(vis, s, -np.inf)
+                assert (sm[sel, st:st + ln].max(1) < sm[sel].max(1)).all()
+    print(f"[measure] {which}: {band} (page, row) pairs with 0.9 < A < 0.99", flush=True)
+    assert band >= 20
+    assert_scores_close(got["R"], R, "R")
+    assert_scores_close(got["R_head"], Rh, "R_head")
+
+
 def test_batch_matches_single_calls(ckv):
     """ckv_measure_page_effects_batch over problems of different shapes (head
     width, grouping, window, prefix) gives, problem by problem, exactly what
