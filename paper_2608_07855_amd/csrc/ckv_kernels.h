@@ -75,17 +75,19 @@ struct PageWork {
   int* clear;             // MODE 1: words set to zero by workgroup (0, 0, 0) (or null)
   int n_clear;
   float fix_a;            // MODE 0: pairs with A > fix_a (>= 0.5) go to the fix-up list ...
-  float fix_a_hi;         // ... unless A <= fix_a_hi and the page holds its row's largest
-                          // logit (rs.m2 set): then the closed form is kept
+  float fix_a_hi;         // ... unless A <= fix_a_hi, the page holds its row's largest
+                          // logit (rs.m2 set) and lies inside one 64-token tile of the
+                          // window pass: then the closed form is kept
 };
 
 // Fix-up thresholds after this library's window pass.  A page that holds its
-// row's largest logit was weighted against the same reference (that logit)
-// in both passes, so its float16 weights are the very ones that formed o and
-// Eq. (6) loses only the float32 digits of the row's log-sum-exp, amplified
-// by 1/(1 - A): such pages keep the closed form up to kFixAHi.  Any other
-// page's weights round differently in the two passes, and the residual
-// u - A o inherits that rounding times 1/(1 - A): those go above kFixA.
+// row's largest logit and lies inside one 64-token tile of the window pass
+// was weighted against the same reference (that logit) in both passes, so
+// its float16 weights are the very ones that formed o and Eq. (6) loses only
+// the float32 digits of the row's log-sum-exp, amplified by 1/(1 - A): such
+// pages keep the closed form up to kFixAHi.  Any other page's weights round
+// differently in the two passes, and the residual u - A o inherits that
+// rounding times 1/(1 - A): those go above kFixA.
 constexpr float kFixA = 0.9f;
 constexpr float kFixAHi = 0.99f;
 constexpr float kFixARecorded = 0.5f;   // with recorded window outputs (no shared weights)

@@ -45,9 +45,12 @@ constexpr int kRowsWG = 32 * kNW;    // window rows per workgroup
 // for Eq. (6): o - u = (1 - A) o' keeps only the digits of o' that survive
 // float32 accumulation of o, and every error of u - A o is amplified by
 // 1/(1 - A).  How far the closed form holds depends on whether the page
-// holds its row's largest logit.  If it does, both passes weighted its
-// tokens against that same logit, so the page's float16 weights are the
-// very ones that formed o and cancel in u - A o; what is left is the
+// holds its row's largest logit and lies inside one 64-token tile of the
+// window pass (tiles start at multiples of 64 tokens).  If so, both passes
+// weighted its tokens against that same logit (the window pass takes a
+// tile's weights after the tile's own maximum has entered the reference),
+// so the page's float16 weights are the very ones that formed o and
+// cancel in u - A o; what is left is the
 // float32 rounding of the log-sum-exp (through 1 - A), a few 1e-7 times
 // 1/(1 - A), and such pairs keep the closed form up to A = kFixAHi.  Any
 // other page's weights were rounded against different references in the
@@ -748,7 +751,9 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
           const float keep = 1.f - A;
           if (need_count && c >= nvis) {
             ratio = INFINITY;                 // the page holds every visible token
-          } else if ((A > pw.fix_a && (A > pw.fix_a_hi || base != m2row)) || !(keep > 0.f)) {
+          } else if ((A > pw.fix_a && (A > pw.fix_a_hi || base != m2row ||
+                                        pstart(item) / kTile != (pstart(item) + len - 1) / kTile)) ||
+                     !(keep > 0.f)) {
             if (ri.ok && half == 0) {         // ill-conditioned: recomputed by the fix-up
               const int4 ent = make_int4(item, ri.rg, pstart(item), len);
               const int ls = atomicAdd(&sFixN, 1);

@@ -172,13 +172,16 @@ def test_dominant_page(ckv, which):
     assert_scores_close(got["R_head"], Rh, "R_head")
 
 
-@pytest.mark.parametrize("which", ["max_inside", "max_outside"])
+@pytest.mark.parametrize("which", ["max_inside", "max_outside", "max_second_tile"])
 def test_heavy_page_band(ckv, which):
     """Pages carrying between 0.9 and 0.99 of a row's mass.  A page that holds
-    its row's largest logit keeps the closed form of Eq. (6) up to A = 0.99
-    (its float16 weights are the ones that formed o); a page whose tokens
-    share the mass while a token outside it holds the row's largest logit is
-    recomputed by definition above A = 0.9.  Both must meet the tolerance."""
+    its row's largest logit inside one 64-token tile keeps the closed form of
+    Eq. (6) up to A = 0.99 (its float16 weights are the ones that formed o);
+    a page whose tokens share the mass while a token outside it holds the
+    row's largest logit, and a page that straddles a 64-token boundary with
+    its largest logit after it (the window pass weighted its first part
+    against an older reference), are recomputed by definition above A = 0.9.
+    All must meet the tolerance."""
     P, ctx = ckv
     import math
     w = scaled("tiny", n_tokens=2048, n_q_heads=4, n_kv_heads=1)
@@ -197,6 +200,14 @@ def test_heavy_page_band(ckv, which):
         picks = full[np.linspace(0, len(full) - 1, len(strengths)).astype(int)]
         for j, c in zip(picks, strengths):
             k[0, int(starts[j]) + 1] = qdir * c
+        probe = picks
+    elif which == "max_second_tile":
+        ends = starts + lens - 1
+        strad = np.flatnonzero(starts // 64 != ends // 64)
+        strengths = np.geomspace(30.0, 200.0, min(24, len(strad)))
+        picks = strad[np.linspace(0, len(strad) - 1, len(strengths)).astype(int)]
+        for j, c in zip(picks, strengths):
+            k[0, (int(starts[j]) // 64 + 1) * 64] = qdir * c    # first token after the boundary
         probe = picks
     else:
         # every token of one page equally strong, one token elsewhere a little
