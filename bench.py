@@ -624,7 +624,7 @@ def kernel_work(w, L, name, launches_per_step):
         note = (f"re-reads the {n_elig} eligible tokens' keys and values "
                 f"({n_elig * (Hkv * d * 2 * 2 + 4) / 1e6:.1f} MB per launch) after the window pass: "
                 "implementation traffic, not counted as algorithmic")
-    elif name == "token_mass":
+    elif name in ("token_mass", "token_mass_fixup"):   # the latter also carries the post pass's fix-up
         byt = S * (Hkv * d * 2 + 4 + 4) + rows * d * 2
         flop = 2.0 * rows * S * d
     elif name == "gather":

@@ -459,6 +459,11 @@ int max_page_len(const ckv_page_list* pl) {
   return m;
 }
 
+// tokens per token-mass workgroup
+int mass_chunk(const AttnGeom& a) {
+  return (int)round_up(ceil_div(a.S, std::max(1, kMassBlocks / a.Hkv)), 64);
+}
+
 int items_per_block(int n_items, int other_blocks) {
   const int per = ceil_div(n_items * std::max(other_blocks, 1), kTargetBlocks);
   return std::min(ckv::kPageItemsMax, std::max(1, per));
@@ -736,12 +741,15 @@ int enqueue_measure(ckv_ctx* c, const AttnGeom& a, const MeasureBufs& b, const i
     pw.fix_a = ckv::kFixA;
     pw.fix_a_hi = ckv::kFixAHi;
     CKV_LAUNCH(c, "page_effect", launch_page_kernel(a, pw, b.rs, 0, max_page_len(pages), c->stream));
+    if (token_mass && mass_fixup_applies(a)) {
+      // the fix-up runs in the shadow of the token mass, in one launch
+      CKV_LAUNCH(c, "token_mass_fixup", launch_mass_fixup(a, b.sp, b.rs, pw, b.fpart, b.arrive, ckv::kFixParts,
+                                                          token_mass, mass_chunk(a), c->stream));
+      return CKV_OK;
+    }
     CKV_LAUNCH(c, "page_fixup", launch_page_fixup(a, b.sp, b.rs, pw, b.fpart, b.arrive, ckv::kFixParts, 0, c->stream));
   }
-  if (token_mass) {
-    const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kMassBlocks / a.Hkv)), 64);
-    CKV_LAUNCH(c, "token_mass", launch_token_mass(a, b.rs, token_mass, mchunk, c->stream));
-  }
+  if (token_mass) CKV_LAUNCH(c, "token_mass", launch_token_mass(a, b.rs, token_mass, mass_chunk(a), c->stream));
   return CKV_OK;
 }
 
@@ -932,8 +940,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
                launch_page_fixup(a, whole, rs, pw2, fpart, count2 + 1, ckv::kFixPartsRow, items2, c->stream));
   }
   if (token_mass) {
-    const int mchunk = (int)round_up(ceil_div(a.S, std::max(1, kMassBlocks / a.Hkv)), 64);
-    CKV_LAUNCH(c, "token_mass", launch_token_mass(a, rs, token_mass, mchunk, c->stream));
+    CKV_LAUNCH(c, "token_mass", launch_token_mass(a, rs, token_mass, mass_chunk(a), c->stream));
   }
   return CKV_OK;
 }

@@ -133,6 +133,16 @@ hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowSt
                              const PageWork& pw, float* fpart, int* arrive, int parts, int item_budget,
                              hipStream_t s);
 
+// The same fix-up fused with the token mass of the same pass (one launch):
+// kMassFixBlocks blocks of 512 threads serve the listed pairs (grid-stride
+// over (pair, part) items), the rest of the grid is launch_token_mass's.
+// Applies unless the token mass needs its general kernel (window rows per KV
+// head that do not fill whole workgroups); otherwise the launcher refuses.
+constexpr int kMassFixBlocks = 256;
+bool mass_fixup_applies(const AttnGeom& a);
+hipError_t launch_mass_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs, const PageWork& pw,
+                             float* fpart, int* arrive, int parts, float* mass, int chunk, hipStream_t s);
+
 // recorded window outputs: row statistics from the caller's o and natural-log
 // lse (nvis_part: workspace [W][recorded_slices(S)] ints), and the fix-up of
 // the listed pairs from the page's own tokens

@@ -39,7 +39,11 @@ constexpr int kRowsWG = 32 * kNW;    // window rows per workgroup
 // enters o and its own sum with the same weight, which keeps the residual
 // u - A o of Eq. (6) free of that token's rounding; a reference that lags
 // the max (weights above 1) was measured to cost ~10x in score error on
-// such pages.
+// such pages.  It also keeps o itself exact in the weight of a row's
+// dominant token, which recorded-output callers rely on: a reference
+// allowed to lag the max by up to 15 (log2 units, which skipped most
+// rescales) put a rounding of 2^-12 on that weight and about 4e-3 on the
+// effects of dominant pages computed from such an o.
 //
 // A page that holds nearly all of a row's mass (A -> 1) is ill-conditioned
 // for Eq. (6): o - u = (1 - A) o' keeps only the digits of o' that survive
@@ -446,7 +450,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
 // kCombBatch with every load of a batch in flight; the running maximum is
 // updated once per batch (the weights of earlier batches are rescaled), and
 // the batch order is fixed, so the result does not depend on scheduling.
-// Writes o, lse, ||o|| and the visible count of every row.
+// Writes o, lse, ||o||, the visible count and the row's largest logit.
 constexpr int kCombBatch = 16;
 
 template <int D>
@@ -702,6 +706,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
       mx = max32(mx);
       const bool touched = mx != -INFINITY;
       const float base = touched ? mx * a.sl2 : 0.f;
+      const bool holds_max = base == m2row;   // the row's largest logit is in the page
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[0][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0][r], a.sl2, -base));
       float ls = 0.f;
@@ -751,7 +756,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
           const float keep = 1.f - A;
           if (need_count && c >= nvis) {
             ratio = INFINITY;                 // the page holds every visible token
-          } else if ((A > pw.fix_a && (A > pw.fix_a_hi || base != m2row ||
+          } else if ((A > pw.fix_a && (A > pw.fix_a_hi || !holds_max ||
                                         pstart(item) / kTile != (pstart(item) + len - 1) / kTile)) ||
                      !(keep > 0.f)) {
             if (ri.ok && half == 0) {         // ill-conditioned: recomputed by the fix-up
@@ -907,18 +912,20 @@ __device__ void fixup_ratio(const AttnGeom& a, const RowStats& rs, const PageWor
   }
 }
 
-template <int D, bool PG>
-__global__ __launch_bounds__(kFixT) void page_fixup_kernel(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw,
-                                                           float* fpart, int* arrive, int parts, int item_budget) {
+// the fix-up of block bx of nb fix-up blocks, each of T threads
+template <int D, bool PG, int T>
+__device__ __forceinline__ void page_fixup_body(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
+                                                const PageWork& pw, float* fpart, int* arrive, int parts,
+                                                int item_budget, int bx, int nb) {
   constexpr int TPR = D / 8;                  // threads per token row (16 bytes each)
-  constexpr int RPR = kFixT / TPR;            // token rows per round
+  constexpr int RPR = T / TPR;                // token rows per round
   constexpr int UNR = 128 / RPR;              // rounds whose loads are in flight together
   __shared__ float sacc[RPR][D + 1];
   __shared__ int sLast;
   const int tid = threadIdx.x, c = tid % TPR, r = tid / TPR;
   const int n = min(*pw.fix_count, pw.fix_cap);
   parts = fix_parts(parts, item_budget, n);
-  for (int item = blockIdx.x; item < n * parts; item += gridDim.x) {
+  for (int item = bx; item < n * parts; item += nb) {
     const int e = item / parts, part = item % parts;
     // entry: page, global row, page start, page length
     const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
@@ -998,7 +1005,7 @@ __global__ __launch_bounds__(kFixT) void page_fixup_kernel(AttnGeom a, AttnSplit
     __syncthreads();
     // the part's sums: row groups added in order
     float* out = fpart + ((size_t)e * parts + part) * (D + 1);
-    for (int i = tid; i <= D; i += kFixT) {
+    for (int i = tid; i <= D; i += T) {
       float v = 0.f;
       for (int k = 0; k < RPR; ++k) v += sacc[k][i];
       __hip_atomic_store(reinterpret_cast<unsigned*>(out + i), __float_as_uint(v), __ATOMIC_RELAXED,
@@ -1010,6 +1017,12 @@ __global__ __launch_bounds__(kFixT) void page_fixup_kernel(AttnGeom a, AttnSplit
     __syncthreads();
     if (sLast && tid < 64) fixup_ratio<D>(a, rs, pw, fpart, e, parts, tid);
   }
+}
+
+template <int D, bool PG>
+__global__ __launch_bounds__(kFixT) void page_fixup_kernel(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw,
+                                                           float* fpart, int* arrive, int parts, int item_budget) {
+  page_fixup_body<D, PG, kFixT>(a, sp, rs, pw, fpart, arrive, parts, item_budget, blockIdx.x, gridDim.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -1134,7 +1147,8 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_kernel(AttnGeom a, RowSta
 // [8 PPW z, 8 PPW (z+1)), whole heads only (8 PPW is a multiple of the row
 // blocks per head); heads of other z-slices meet in the atomic max.
 template <int D, int PPW, bool PG>
-__global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats rs, float* mass, int chunk) {
+__device__ __forceinline__ void token_mass_body(const AttnGeom& a, const RowStats& rs, float* mass, int chunk,
+                                                int bx, int by, int bz) {
   constexpr int NT = kNW * 64, KS = D / 16;
   constexpr int KP = D + 8, CPR = D / 8, KCH = kTile * CPR, KPT = (KCH + NT - 1) / NT;
   constexpr int NP = kNW * PPW;                 // pairs per workgroup
@@ -1143,16 +1157,16 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats
   __shared__ int sFull[2];
   __shared__ float sPart[2][NP][kTile];
   __shared__ int sMin;
-  const int g = blockIdx.y;
+  const int g = by;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
-  const int t_begin = blockIdx.x * chunk;
+  const int t_begin = bx * chunk;
   const int t_end = min(a.S, t_begin + chunk);
   if (t_begin >= t_end) return;
   const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
   const int nrb = (a.W + 31) / 32;
   const int n_pairs = a.group * nrb;
-  const int p0 = blockIdx.z * NP;
+  const int p0 = bz * NP;
   const int np_blk = min(NP, n_pairs - p0);
   // smallest window position (every head has the same window rows)
   if (tid == 0) sMin = INT_MAX;
@@ -1284,6 +1298,29 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats
   }
 }
 
+template <int D, int PPW, bool PG>
+__global__ __launch_bounds__(kNW * 64) void token_mass_fast(AttnGeom a, RowStats rs, float* mass, int chunk) {
+  token_mass_body<D, PPW, PG>(a, rs, mass, chunk, blockIdx.x, blockIdx.y, blockIdx.z);
+}
+
+// The fix-up of the listed pairs and the token mass in one launch (the post
+// pass runs both after the page kernel): blocks [0, nfix) are fix-up
+// blocks, the rest the token-mass grid (mx x my x mz) in x-fastest order.
+// The fix-up is a short chain of dependent latencies; here it runs in the
+// shadow of the token mass instead of taking a launch of its own.
+template <int D, int PPW, bool PG>
+__global__ __launch_bounds__(kNW * 64) void mass_fixup_kernel(AttnGeom a, AttnSplit sp, RowStats rs, PageWork pw,
+                                                              float* fpart, int* arrive, int parts, float* mass,
+                                                              int chunk, int nfix, int mx, int my) {
+  if ((int)blockIdx.x < nfix) {
+    page_fixup_body<D, PG, kNW * 64>(a, sp, rs, pw, fpart, arrive, parts, 0, blockIdx.x, nfix);
+    return;
+  }
+  const int b = blockIdx.x - nfix;
+  token_mass_body<D, PPW, PG>(a, rs, mass, chunk, b % mx, (b / mx) % my, b / (mx * my));
+}
+
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
@@ -1356,6 +1393,40 @@ hipError_t launch_page_fixup(const AttnGeom& a, const AttnSplit& sp, const RowSt
     if (pg) hipLaunchKernelGGL((page_fixup_kernel<64, true>), grid, block, 0, s, a, sp, rs, pw, fpart, arrive, parts, ib);
     else hipLaunchKernelGGL((page_fixup_kernel<64, false>), grid, block, 0, s, a, sp, rs, pw, fpart, arrive, parts, ib);
   }
+  return hipGetLastError();
+}
+
+bool mass_fixup_applies(const AttnGeom& a) {
+  const int nrb = (a.W + 31) / 32, n_pairs = a.group * nrb;
+  const int ppw = n_pairs <= kNW ? 1 : 2;
+  return (kNW * ppw) % nrb == 0;
+}
+
+hipError_t launch_mass_fixup(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs, const PageWork& pw,
+                             float* fpart, int* arrive, int parts, float* mass, int chunk, hipStream_t s) {
+  if (!mass_fixup_applies(a)) return hipErrorInvalidValue;
+  const int nrb = (a.W + 31) / 32, n_pairs = a.group * nrb;
+  const int ppw = n_pairs <= kNW ? 1 : 2;
+  const int nz = (n_pairs + kNW * ppw - 1) / (kNW * ppw);
+  const int mx = (a.S + chunk - 1) / chunk, my = a.Hkv;
+  const int nfix = kMassFixBlocks;
+  dim3 grid(nfix + mx * my * nz), block(kNW * 64);
+  const bool pg = a.slot != nullptr;
+#define CKV_MF_LAUNCH(DD, PP)                                                                             \
+  do {                                                                                                    \
+    if (pg) hipLaunchKernelGGL((mass_fixup_kernel<DD, PP, true>), grid, block, 0, s, a, sp, rs, pw, fpart,  \
+                               arrive, parts, mass, chunk, nfix, mx, my);                                 \
+    else hipLaunchKernelGGL((mass_fixup_kernel<DD, PP, false>), grid, block, 0, s, a, sp, rs, pw, fpart,    \
+                            arrive, parts, mass, chunk, nfix, mx, my);                                    \
+  } while (0)
+  if (a.D == 128) {
+    if (ppw == 1) CKV_MF_LAUNCH(128, 1);
+    else CKV_MF_LAUNCH(128, 2);
+  } else {
+    if (ppw == 1) CKV_MF_LAUNCH(64, 1);
+    else CKV_MF_LAUNCH(64, 2);
+  }
+#undef CKV_MF_LAUNCH
   return hipGetLastError();
 }
 

@@ -93,6 +93,9 @@ def test_token_mass(ckv, case):
     got = _measure(P, ctx, dl, "post", want=("R", "token_mass"))
     want = O.token_mass(L.k, L.v, L.pos, L.q_post, L.qpos_post)
     np.testing.assert_allclose(got["token_mass"], want, rtol=3e-3, atol=1e-6)
+    # with token mass requested the fix-up shares its launch: R still holds
+    R, _ = oracle_pass(L, "post")
+    assert_scores_close(got["R"], R, "R")
 
 
 def test_edge_pages(ckv):
@@ -134,11 +137,13 @@ def test_deterministic(ckv):
     assert np.array_equal(a["R"], b["R"]) and np.array_equal(a["o"], b["o"])
 
 
+@pytest.mark.parametrize("mass", [False, True])
 @pytest.mark.parametrize("which", ["single_heavy", "two_heavy_straddling"])
-def test_dominant_page(ckv, which):
+def test_dominant_page(ckv, which, mass):
     """Pages that hold nearly all of a row's attention mass (A -> 1): the
     closed form of Eq. (6) cancels there; the library recomputes such rows
-    without the page and must still meet the score tolerance."""
+    without the page and must still meet the score tolerance.  With token
+    mass requested the recomputation runs inside the token-mass launch."""
     P, ctx = ckv
     w = scaled("tiny", n_tokens=2048, n_q_heads=4, n_kv_heads=1)
     L = make_layer(w, seed=7)
@@ -158,8 +163,11 @@ def test_dominant_page(ckv, which):
         k[0, st + 9] = qdir * 52.0
     L.k = bf16_bits(k)
     dl = LayerOnDevice(L)
-    got = _measure(P, ctx, dl, "post")
+    got = _measure(P, ctx, dl, "post", want=("R", "R_head") + (("token_mass",) if mass else ()))
     R, Rh = O.page_effects(L.k, L.v, L.pos, L.q_post, L.qpos_post, L.pages, method="closed")
+    if mass:
+        np.testing.assert_allclose(got["token_mass"], O.token_mass(L.k, L.v, L.pos, L.q_post, L.qpos_post),
+                                   rtol=3e-3, atol=1e-6)
     # the oracle confirms the page is dominant for some rows
     import math
     K, V, Q = O.as_f64(L.k), O.as_f64(L.v), O.as_f64(L.q_post)
