@@ -430,6 +430,7 @@ int check_pages(ckv_ctx* c, const ckv_page_list* pl, int n_tokens, const char* w
 AttnGeom make_geom(const ckv_ctx* c, const ckv_kv_view* kv, const ckv_window_view* w) {
   AttnGeom a;
   a.dbg = c->dbg_dev;
+  a.nonfinite = c->nf_dev;
   a.k = kv->k;
   a.v = kv->v;
   a.kv_head_stride = kv->head_stride;
@@ -907,7 +908,9 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
 
   ZeroList zl{R, R ? (size_t)n : 0, R_head, R_head ? (size_t)n * a.Hq : 0, token_mass,
               token_mass ? (size_t)a.S : 0, fix_count, count2, 1 + (size_t)cap2, c->nf_dev};
-  CKV_LAUNCH(c, "recorded_rows", launch_recorded_rows(a, o, lse, rs, nvis_part, zl, c->stream));
+  // without pages the visible counts have no reader (the token mass latches
+  // a non-finite sum itself), so the counting pass is skipped
+  CKV_LAUNCH(c, "recorded_rows", launch_recorded_rows(a, o, lse, rs, n > 0 ? nvis_part : nullptr, zl, c->stream));
   if (n > 0) {
     PageWork pw{};
     pw.start = dstart;

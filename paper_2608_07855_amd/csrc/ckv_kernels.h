@@ -25,6 +25,7 @@ struct AttnGeom {
                                            // (clamped to pool_last), or null: row t
   uint32_t pool_last;                      // last row of the pool
   uint32_t* dbg;                           // debug word of the context (CKV_DEBUG builds)
+  uint32_t* nonfinite;                     // the context's latched non-finite flag (or null)
 };
 
 // split-sequence partials of pass A
@@ -144,7 +145,8 @@ hipError_t launch_mass_fixup(const AttnGeom& a, const AttnSplit& sp, const RowSt
                              float* fpart, int* arrive, int parts, float* mass, int chunk, hipStream_t s);
 
 // recorded window outputs: row statistics from the caller's o and natural-log
-// lse (nvis_part: workspace [W][recorded_slices(S)] ints), and the fix-up of
+// lse (nvis_part: workspace [W][recorded_slices(S)] ints, or null to skip the
+// visible counts, which then read 0), and the fix-up of
 // the listed pairs from the page's own tokens
 int recorded_slices(int S);
 hipError_t launch_recorded_rows(const AttnGeom& a, const float* o, const float* lse, const RowStats& rs,

@@ -1128,11 +1128,14 @@ __global__ __launch_bounds__(kNW * 64) void token_mass_kernel(AttnGeom a, RowSta
     __syncthreads();
     if (tid < kTile && t0 + tid < t_end) {
       float best = 0.f;
+      bool bad = false;
       for (int hl = 0; hl < a.group; ++hl) {
         float sum = 0.f;
         for (int rb = 0; rb < nrb; ++rb) sum += sPart[hl * nrb + rb][tid];
+        bad |= !(sum <= 3.4e38f);   // a NaN or infinite weight (e.g. a row's lse of -inf)
         best = fmaxf(best, sum);
       }
+      if (bad) latch_nonfinite(a.nonfinite);
       atomic_max_nonneg(&mass[t0 + tid], best);
     }
     __syncthreads();
@@ -1271,11 +1274,14 @@ __device__ __forceinline__ void token_mass_body(const AttnGeom& a, const RowStat
     const int t0 = t_begin + it * kTile;
     if (tid < kTile && t0 + tid < t_end) {
       float best = 0.f;
+      bool bad = false;
       for (int hp = 0; hp < np_blk; hp += nrb) {
         float sum = 0.f;
         for (int rb = 0; rb < nrb; ++rb) sum += sPart[it & 1][hp + rb][tid];
+        bad |= !(sum <= 3.4e38f);   // a NaN or infinite weight (e.g. a row's lse of -inf)
         best = fmaxf(best, sum);
       }
+      if (bad) latch_nonfinite(a.nonfinite);
       atomic_max_nonneg(&mass[t0 + tid], best);
     }
   };

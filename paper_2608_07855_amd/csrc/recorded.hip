@@ -205,10 +205,12 @@ int recorded_slices(int S) { return std::max(1, std::min(kVisSlices, (S + 1023) 
 
 hipError_t launch_recorded_rows(const AttnGeom& a, const float* o, const float* lse, const RowStats& rs,
                                 int* nvis_part, const ZeroList& zl, hipStream_t s) {
-  const int ns = recorded_slices(a.S);
-  hipLaunchKernelGGL(recorded_count_kernel, dim3(a.W * ns), dim3(256), 0, s, a, nvis_part, ns);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  const int ns = nvis_part ? recorded_slices(a.S) : 0;   // no counts: every row's count reads 0
+  if (ns > 0) {
+    hipLaunchKernelGGL(recorded_count_kernel, dim3(a.W * ns), dim3(256), 0, s, a, nvis_part, ns);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   dim3 grid((a.Hq * a.W + 3) / 4), block(256);
   if (a.D == 128)
     hipLaunchKernelGGL((recorded_rows_kernel<128>), grid, block, 0, s, a, o, lse, rs, nvis_part, ns, zl);

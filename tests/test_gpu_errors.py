@@ -31,7 +31,7 @@ def _views(P, dl, k=None, v=None):
     return kv, win, pages
 
 
-@pytest.mark.parametrize("which", ["key", "value", "recorded"])
+@pytest.mark.parametrize("which", ["key", "value", "recorded", "recorded_lse_no_pages"])
 def test_nonfinite_input_is_latched(ckv, which):
     P, ctx = ckv
     L = make_layer(WORKLOADS["tiny"], seed=2)
@@ -44,6 +44,14 @@ def test_nonfinite_input_is_latched(ckv, which):
         o = m["o"].reshape(-1).clone()
         o[5] = float("nan")
         P.ckv_measure_recorded(ctx, kv, win, pages, o, m["lse"].reshape(-1).contiguous())
+    elif which == "recorded_lse_no_pages":
+        # a recorded log-sum-exp of -inf for a row that sees tokens, in a call
+        # without pages (token mass only): the mass of its tokens is infinite
+        m = P.ckv_measure_page_effects(ctx, kv, win, pages, want=("R", "o", "lse"))
+        lse = m["lse"].reshape(-1).clone()
+        lse[3] = float("-inf")
+        P.ckv_measure_recorded(ctx, kv, win, P.Pages(np.zeros(0, np.int32), np.zeros(0, np.int32)),
+                               m["o"].reshape(-1).contiguous(), lse, want=("token_mass",))
     else:
         k, v = dl.k.clone(), dl.v.clone()
         t = int(L.layout.page_start[3])          # a token every post-window row sees
