@@ -47,6 +47,11 @@ CASES = {
                      event_hi=90),
     "w40_d128": scaled("q8b", n_tokens=1500, n_q_heads=6, n_kv_heads=2, window=40, page_size=24,
                        event_lo=41, event_hi=200),
+    # 80-row windows: three 32-row blocks per query head, which the fast
+    # token-mass kernel's whole-head workgroups do not take (general kernel,
+    # separate fix-up launch)
+    "w80_general": scaled("tiny", n_tokens=1700, n_q_heads=2, n_kv_heads=1, window=80, event_lo=81,
+                          event_hi=300),
 }
 
 
@@ -82,7 +87,7 @@ def test_bruteforce_subsample_tiny(ckv):
     assert_scores_close(got["R"][sub], R, "R (brute force)")
 
 
-@pytest.mark.parametrize("case", ["d128_ragged", "g64_w128", "w8_mha", "w40_d128", "tiny_gapped"])
+@pytest.mark.parametrize("case", ["d128_ragged", "g64_w128", "w8_mha", "w40_d128", "tiny_gapped", "w80_general"])
 def test_token_mass(ckv, case):
     """Window mass max_h sum_p a_hpi of every token (the base score that
     fills the budget), over several head groupings and window sizes."""
