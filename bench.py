@@ -842,6 +842,9 @@ def main():
         measure_kernels_tokens_per_s=tokens / (meas / 1e3) if meas > 0 else None,
         compaction_GBps=comp_bytes / (sel_ms / 1e3) / 1e9 if sel_ms > 0 else None,
         gather_GBps=comp_bytes / (g_ms / 1e3) / 1e9 if g_ms > 0 else None,
+        compaction_note="the step compacts the copy the post pass has just streamed, so its kept rows may "
+                        "still be in the 256 MB Infinity Cache; the stack leg's checkpoint (19.3 GB in one "
+                        "call) is the figure no cache can hold",
         kernels=per_kernel,
         kernels_note="per-kernel times from separate profiling steps with events around every kernel",
         n_candidates=int(st.last["cl"]["n_cand"].item()),
