@@ -35,18 +35,24 @@ struct AttnSplit {
   float* part_m;   // [Hkv][n_splits][rows_pad]  (log2 units)
   float* part_l;
   int* part_c;     // visible-token counts
+  int* part_t;     // start of the first tile of the split whose largest scaled logit
+                   // equals the split's (the tile where the split's weight reference
+                   // took its final value); -1 when the split shows the row no token
 };
 
 // per window row (global row h*W + p): o [rows][D], lse2 (log2 units), ||o||, n_vis,
 // and m2, the largest scaled logit of the row (log2 units): the reference the
-// window pass's float16 weights were finally taken against (null when the
-// outputs were not computed by this library's window pass)
+// window pass's float16 weights were finally taken against, with m2t, the
+// start of the tile where it entered that reference in the first split that
+// holds it (both null when the outputs were not computed by this library's
+// window pass)
 struct RowStats {
   float* o;
   float* lse2;
   float* onorm;
   int* nvis;
   float* m2;
+  int* m2t;
 };
 
 // pages processed by pass B (MODE 0: item = page; MODE 1: item t = page cand[t])
@@ -77,13 +83,18 @@ struct PageWork {
   int n_clear;
   float fix_a;            // MODE 0: pairs with A > fix_a (>= 0.5) go to the fix-up list ...
   float fix_a_hi;         // ... unless A <= fix_a_hi, the page holds its row's largest
-                          // logit (rs.m2 set) and lies inside one 64-token tile of the
-                          // window pass: then the closed form is kept
+                          // logit (rs.m2 set) and the window pass weighted all of it
+                          // against that logit: then the closed form is kept
+  int split_tokens;       // MODE 0: split length of the window pass (a multiple of 64;
+                          // 0: unknown, and no page across a tile boundary keeps the
+                          // closed form above fix_a; nor does one without rs.m2)
 };
 
 // Fix-up thresholds after this library's window pass.  A page that holds its
-// row's largest logit and lies inside one 64-token tile of the window pass
-// was weighted against the same reference (that logit) in both passes, so
+// row's largest logit and lies inside one 64-token tile of the window pass,
+// or crosses into the next tile of the same split after that logit entered
+// the split's reference (by the tile of the page's first part), was weighted
+// against the same reference (that logit) in both passes, so
 // its float16 weights are the very ones that formed o and Eq. (6) loses only
 // the float32 digits of the row's log-sum-exp, amplified by 1/(1 - A): such
 // pages keep the closed form up to kFixAHi.  Any other page's weights round

@@ -48,13 +48,18 @@ constexpr int kRowsWG = 32 * kNW;    // window rows per workgroup
 // A page that holds nearly all of a row's mass (A -> 1) is ill-conditioned
 // for Eq. (6): o - u = (1 - A) o' keeps only the digits of o' that survive
 // float32 accumulation of o, and every error of u - A o is amplified by
-// 1/(1 - A).  How far the closed form holds depends on whether the page
-// holds its row's largest logit and lies inside one 64-token tile of the
-// window pass (tiles start at multiples of 64 tokens).  If so, both passes
-// weighted its tokens against that same logit (the window pass takes a
-// tile's weights after the tile's own maximum has entered the reference),
-// so the page's float16 weights are the very ones that formed o and
-// cancel in u - A o; what is left is the
+// 1/(1 - A).  How far the closed form holds depends on whether the window
+// pass weighted all of the page against its row's largest logit, the
+// reference the page kernel uses when the page holds that logit.  The
+// window pass takes a tile's weights after the tile's own maximum has
+// entered the reference (tiles start at multiples of 64 tokens, splits at
+// multiples of the split length), so that holds for a page that holds the
+// logit and lies inside one tile, and for a page that crosses into the next
+// tile of the same split once the logit has entered that split's reference
+// by the tile of the page's first part (the window pass records, per row,
+// the tile where it did; the next tile keeps the reference).  Then the
+// page's float16 weights are the very ones that formed o and cancel in
+// u - A o; what is left is the
 // float32 rounding of the log-sum-exp (through 1 - A), a few 1e-7 times
 // 1/(1 - A), and such pairs keep the closed form up to A = kFixAHi.  Any
 // other page's weights were rounded against different references in the
@@ -342,6 +347,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
   for (int db = 0; db < DB; ++db) oacc[db] = zero16();
   float mref = -INFINITY, l = 0.f;
   int cnt = 0;
+  int mt = -1;   // start of the tile where mref last grew
 
   const int n_tiles = t_end > t_begin ? (t_end - t_begin + kTile - 1) / kTile : 0;
   // Loads run two tiles ahead of the math: stager A holds even tiles, B odd
@@ -352,7 +358,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
     st.issue(kh, vh, (uint32_t)a.kv_tok_stride, a.slot, a.pool_last, a.pos, t0, min(32, n), t0 + 32,
              max(0, n - 32), tid, a.S, a.dbg);
   };
-  auto compute = [&](int b) {
+  auto compute = [&](int b, int it) {
     if (wave_on) {
       f32x16 s[2];
       s[0] = scores<D, St::KP>(sK[b], 0, col, half, qf);
@@ -392,6 +398,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
 #pragma unroll
         for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
         mref = nref;
+        if (need) mt = t_begin + it * kTile;
       }
       const float base = mref == -INFINITY ? 0.f : mref;
 #pragma unroll
@@ -412,12 +419,12 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
   __syncthreads();
   for (int it = 0; it < n_tiles; it += 2) {
     issue(stA, it + 2);
-    compute(0);
+    compute(0, it);
     if (it + 1 < n_tiles) stB.commit(sK[1], sV[1], sP[1], sFull[1], minq, tid);
     __syncthreads();
     if (it + 1 >= n_tiles) break;
     issue(stB, it + 3);
-    compute(1);
+    compute(1, it + 1);
     if (it + 2 < n_tiles) stA.commit(sK[0], sV[0], sP[0], sFull[0], minq, tid);
     __syncthreads();
   }
@@ -432,6 +439,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
     sp.part_m[idx] = mref;
     sp.part_l[idx] = lt;
     sp.part_c[idx] = ct;
+    sp.part_t[idx] = mt;
   }
   float* po = sp.part_o + idx * D;
 #pragma unroll
@@ -476,11 +484,11 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
   const int rg = g * a.rows + row;
   const size_t base = (size_t)g * sp.n_splits * sp.rows_pad + row;
   float M = -INFINITY, wsum = 0.f;
-  int nv = 0;
+  int nv = 0, mt = -1;   // mt: tile where M entered the first split that holds it
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < sp.n_splits; s0 += kCombBatch) {
     float ms[kCombBatch], ls[kCombBatch];
-    int cs[kCombBatch];
+    int cs[kCombBatch], ts[kCombBatch];
     f32x4 os[kCombBatch];
 #pragma unroll
     for (int u = 0; u < kCombBatch; ++u) {
@@ -490,11 +498,15 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
       ms[u] = in ? sp.part_m[idx] : -INFINITY;
       ls[u] = sp.part_l[idx];
       cs[u] = in ? sp.part_c[idx] : 0;
+      ts[u] = sp.part_t[idx];
       os[u] = *reinterpret_cast<const f32x4*>(sp.part_o + idx * D + 4 * c);
     }
     float mb = M;
 #pragma unroll
-    for (int u = 0; u < kCombBatch; ++u) mb = fmaxf(mb, ms[u]);
+    for (int u = 0; u < kCombBatch; ++u) {
+      mt = ms[u] > mb ? ts[u] : mt;   // the first split wins a tie
+      mb = fmaxf(mb, ms[u]);
+    }
     if (mb != -INFINITY) {
       if (mb > M) {
         const float r = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - mb);
@@ -525,6 +537,7 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
     rs.onorm[rg] = sqrtf(n2);
     rs.nvis[rg] = nv;
     if (rs.m2) rs.m2[rg] = M;
+    if (rs.m2t) rs.m2t[rg] = mt;
     if (lse_out) lse_out[rg] = l2 * kLn2;
     // a NaN or infinite key, query or value reaches the row's output or its
     // log-sum-exp (a row that sees no token has lse -inf and o = 0)
@@ -540,6 +553,7 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
 // derives the same tile sequence from the page lengths.
 // ---------------------------------------------------------------------------
 // NB: 32-token slots a page may span (1 when every page has <= 32 tokens).
+constexpr int kAcrossSplit = 0x7f;   // page class: across a split boundary of the window pass
 template <int D, int MODE, int NB, bool PG>
 __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork pw, RowStats rs) {
   constexpr int NT = kNW * 64, KS = D / 16, DB = D / 32;
@@ -560,6 +574,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   __shared__ int sFixN, sFixBase;
   __shared__ int sMin;
   __shared__ int sItStart[kPageItemsMax], sItLen[kPageItemsMax];   // this block's pages
+  __shared__ int sItLo[MODE == 0 ? kPageItemsMax : 1];   // start of the split of a page's first part
   __shared__ int4 sTileSeg[kPageItemsMax];    // per tile: segments (s0, n0, s1, n1)
   __shared__ int sTileIt[kPageItemsMax + 1];  // per tile: first item; entry n_tiles = i_end
   __shared__ int sNTiles;
@@ -585,7 +600,17 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
     const int pg = MODE == 0 ? item : pw.cand[item];
     const bool ok = pg >= 0 && pg < pw.n_pages;
     sItStart[i] = ok ? pw.start[pg] : 0;
-    sItLen[i] = ok ? pw.len[pg] : 0;
+    // the length, and above bit 8 (MODE 0) where the page meets the window
+    // pass's tiles: 0 inside one tile, n < 64 across a tile boundary after
+    // n tokens inside one split, kAcrossSplit across a split boundary (or
+    // with the split length unknown)
+    int lw = ok ? pw.len[pg] : 0;
+    if (MODE == 0 && ok) {
+      const int s0 = pw.start[pg], nf = (s0 / kTile + 1) * kTile - s0;
+      if (nf < lw) lw |= (pw.split_tokens > 0 && (s0 + nf) % pw.split_tokens != 0 ? nf : kAcrossSplit) << 8;
+      if (pw.split_tokens > 0) sItLo[i] = s0 - s0 % pw.split_tokens;
+    }
+    sItLen[i] = lw;
   }
   const RowInfo ri = row_info(a, g, rblk * kRowsWG + wave * 32 + col);
   const bool wave_on = __ballot(ri.ok) != 0ull;
@@ -613,6 +638,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   // the row's largest scaled logit, the window pass's final weight reference
   // (NaN when unknown: no page then counts as holding it)
   const float m2row = (MODE == 0 && rs.m2 && ri.ok) ? rs.m2[ri.rg] : __builtin_nanf("");
+  // where that logit entered the window pass's reference (first split holding it)
+  const int m2trow = (MODE == 0 && rs.m2t && ri.ok) ? rs.m2t[ri.rg] : -1;
   const int row0 = rblk * kRowsWG;
   const int head0 = row0 / a.W;
   const int n_heads_blk = min(a.group, (min(a.rows, row0 + kRowsWG) - 1) / a.W + 1) - head0;
@@ -624,7 +651,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   }
 
   auto pstart = [&](int item) { return sItStart[item - i_begin]; };
-  auto plen = [&](int item) { return sItLen[item - i_begin]; };
+  auto plen = [&](int item) { return sItLen[item - i_begin] & 0xff; };
   // pages in the tile that starts at item `it`: two short pages share a tile
   auto tile_items = [&](int it) {
     return (it + 1 < i_end && plen(it) <= 32 && plen(it + 1) <= 32) ? 2 : 1;
@@ -661,7 +688,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
   // so the slot's LDS offsets fold into the instructions)
   auto page = [&](int b, int item, int m, const int ps) {
     {
-      const int len = plen(item);
+      const int lw = sItLen[item - i_begin];
+      const int len = lw & 0xff, cross = lw >> 8;
       // a short page occupies slot ps; a long one both slots from slot 0
       const int nblk = (NB == 1 || m == 2) ? 1 : (len > 32 ? 2 : 1);
       const int slot0 = ps;
@@ -749,6 +777,20 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
         }
       }
       n2 = sum32(n2);
+      // Past fix_a the closed form is kept only where the window pass
+      // weighted all of the page against the row's largest logit.  For a
+      // page across a tile boundary inside one split, that logit must have
+      // entered the split's reference by the tile of the page's first part
+      // (lanes without a row have m2row NaN, so holds_max is false there).
+      bool form_ok = MODE == 0 && holds_max && A <= pw.fix_a_hi;
+      if (MODE == 0 && cross != 0) {
+        if (cross == kAcrossSplit) {
+          form_ok = false;
+        } else {
+          const int hi = pstart(item) + cross - kTile, lo = sItLo[item - i_begin];
+          form_ok = form_ok && m2trow >= lo && m2trow <= hi;
+        }
+      }
       // the ratio of Eq. (6)-(7)
       if (MODE == 0) {
         float ratio = 0.f;
@@ -756,9 +798,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
           const float keep = 1.f - A;
           if (need_count && c >= nvis) {
             ratio = INFINITY;                 // the page holds every visible token
-          } else if ((A > pw.fix_a && (A > pw.fix_a_hi || !holds_max ||
-                                        pstart(item) / kTile != (pstart(item) + len - 1) / kTile)) ||
-                     !(keep > 0.f)) {
+          } else if ((A > pw.fix_a && !form_ok) || !(keep > 0.f)) {
             if (ri.ok && half == 0) {         // ill-conditioned: recomputed by the fix-up
               const int4 ent = make_int4(item, ri.rg, pstart(item), len);
               const int ls = atomicAdd(&sFixN, 1);

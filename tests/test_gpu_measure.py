@@ -185,19 +185,30 @@ def test_dominant_page(ckv, which, mass):
     assert_scores_close(got["R_head"], Rh, "R_head")
 
 
-@pytest.mark.parametrize("which", ["max_inside", "max_outside", "max_second_tile"])
+@pytest.mark.parametrize("which", ["max_inside", "max_outside", "max_second_tile", "max_first_part_g32",
+                                   "max_first_part_g64", "max_second_part_g64"])
 def test_heavy_page_band(ckv, which):
     """Pages carrying between 0.9 and 0.99 of a row's mass.  A page that holds
     its row's largest logit inside one 64-token tile keeps the closed form of
-    Eq. (6) up to A = 0.99 (its float16 weights are the ones that formed o);
-    a page whose tokens share the mass while a token outside it holds the
-    row's largest logit, and a page that straddles a 64-token boundary with
-    its largest logit after it (the window pass weighted its first part
-    against an older reference), are recomputed by definition above A = 0.9.
-    All must meet the tolerance."""
+    Eq. (6) up to A = 0.99 (its float16 weights are the ones that formed o),
+    and so does one that crosses into the next tile of the same window-pass
+    split with that logit before the crossing (max_first_part: 32- and
+    64-token pages over 128-token splits, so every other tile boundary is
+    also a split boundary, where the page is recomputed).  A page whose
+    tokens share the mass while a token outside it holds the row's largest
+    logit, and a page that straddles a 64-token boundary with its largest
+    logit after it (the window pass weighted its first part against an older
+    reference; max_second_tile over one-tile splits, max_second_part over
+    128-token splits), are recomputed by definition above A = 0.9.  All must
+    meet the tolerance."""
     P, ctx = ckv
     import math
-    w = scaled("tiny", n_tokens=2048, n_q_heads=4, n_kv_heads=1)
+    split128 = which[:-4] in ("max_first_part", "max_second_part")
+    if split128:
+        # 8 KV heads over 4096 tokens: 32 splits of 128 tokens
+        w = scaled("tiny", n_tokens=4096, n_q_heads=16, n_kv_heads=8, page_size=int(which[-2:]))
+    else:
+        w = scaled("tiny", n_tokens=2048, n_q_heads=4, n_kv_heads=1)
     L = make_layer(w, seed=11)
     from synth import bf16_bits, bf16_bits_to_f32
     k = bf16_bits_to_f32(L.k).copy()
@@ -206,7 +217,22 @@ def test_heavy_page_band(ckv, which):
     qdir /= np.linalg.norm(qdir)
     starts, lens = L.layout.page_start, L.layout.page_len
     full = np.flatnonzero(lens == lens.max())
-    if which == "max_inside":
+    ends = starts + lens - 1
+    if split128:
+        # every page across a tile boundary gets a heavy token in each KV
+        # head, its first one (before the boundary) or the first after the
+        # boundary, aimed at one row of the group's first query head with a
+        # logit from a ladder that puts A on both sides of 0.9 and 0.99
+        strad = np.flatnonzero(starts // 64 != ends // 64)
+        logit = np.linspace(9.0, 16.0, len(strad))
+        group = w.n_q_heads // w.n_kv_heads
+        for n, j in enumerate(strad):
+            for g in range(w.n_kv_heads):
+                qr = q[g * group, (n + 7 * g) % w.window]
+                at = int(starts[j]) if which.startswith("max_first") else (int(starts[j]) // 64 + 1) * 64
+                k[g, at] = qr * (logit[(n + 5 * g) % len(strad)] * math.sqrt(w.head_dim) / float(qr @ qr))
+        probe = strad
+    elif which == "max_inside":
         # one heavy token per page, at strengths that put A on both sides of
         # 0.9 and 0.99 across the rows
         strengths = np.geomspace(30.0, 200.0, 24)
@@ -215,7 +241,6 @@ def test_heavy_page_band(ckv, which):
             k[0, int(starts[j]) + 1] = qdir * c
         probe = picks
     elif which == "max_second_tile":
-        ends = starts + lens - 1
         strad = np.flatnonzero(starts // 64 != ends // 64)
         strengths = np.geomspace(30.0, 200.0, min(24, len(strad)))
         picks = strad[np.linspace(0, len(strad) - 1, len(strengths)).astype(int)]
@@ -236,21 +261,29 @@ def test_heavy_page_band(ckv, which):
     R, Rh = O.page_effects(L.k, L.v, L.pos, L.q_post, L.qpos_post, L.pages, method="closed")
     K, V, Q = O.as_f64(L.k), O.as_f64(L.v), O.as_f64(L.q_post)
     vis = O.visibility(L.pos, L.qpos_post)
-    band = 0
+    band = inside = 0
+    group = Q.shape[0] // K.shape[0]
     for h in range(Q.shape[0]):
-        s = O.head_logits(Q[h], K[0], 1 / math.sqrt(K.shape[2]))
-        a, _ = O.attend(s, vis, V[0])
+        s = O.head_logits(Q[h], K[h // group], 1 / math.sqrt(K.shape[2]))
+        a, _ = O.attend(s, vis, V[h // group])
         for j in probe:
             st, ln = int(starts[j]), int(lens[j])
             A = a[:, st:st + ln].sum(1)
             sel = (A > 0.9) & (A < 0.99)
             band += int(sel.sum())
+            if split128 and (st // 64 + 1) % 2 == 1:
+                # a tile boundary inside a split (max_first_part: the closed
+                # form is kept)
+                inside += int(sel.sum())
             if which == "max_outside" and sel.any():
                 # the row's largest logit lies outside the page
                 sm = np.where(vis, s, -np.inf)
                 assert (sm[sel, st:st + ln].max(1) < sm[sel].max(1)).all()
-    print(f"[measure] {which}: {band} (page, row) pairs with 0.9 < A < 0.99", flush=True)
+    print(f"[measure] {which}: {band} (page, row) pairs with 0.9 < A < 0.99, {inside} of them across a "
+          f"tile boundary inside a split", flush=True)
     assert band >= 20
+    if split128:
+        assert inside >= 10 and band - inside >= 10
     assert_scores_close(got["R"], R, "R")
     assert_scores_close(got["R_head"], Rh, "R_head")
 
