@@ -474,12 +474,18 @@ __device__ __forceinline__ void hist_add1(unsigned int* hist, uint32_t bin, bool
 //      the ordered write at the chunk's offset.
 // The control words and histograms start at zero (allocated zeroed); the
 // last workgroup of a sequence to finish clears them again for the next
-// call, and marks a call whose barrier timed out with n_kept = -1.
+// call, and marks a call whose barrier timed out with n_kept = -1.  Every
+// word that crosses workgroups (control words, histograms, the candidate
+// list, chunk counts, n_kept) moves through agent-scope atomics, so the
+// barrier needs no fence (one writes back and invalidates the whole L2 of
+// the workgroup's XCD); the workgroup barrier before an arrival waits for
+// the workgroup's own memory operations.
 // ---------------------------------------------------------------------------
 namespace {
 constexpr int kQT = 256;
 constexpr int kQW = kQT / 64;
 constexpr int kQKPT = kSelGridChunk / kQT;   // keys per thread
+static_assert(kSelGridPendMax <= kQT, "one pending page per thread");
 enum { qArrive = 0, qDone = 1, qNP = 2, qNF = 3, qNotLo = 4, qHi = 5, qError = 6, qCand = 7, qCounts = 8 };
 // when the threshold bin of the first pass holds at most this many free
 // keys, they are listed (in the histogram rows of the later passes) and every
@@ -489,8 +495,7 @@ constexpr int kCandMax = kSelBins;
 __device__ bool seq_barrier(int* ctrl, int target, long long timeout, int* s_ok) {
   __syncthreads();
   if (threadIdx.x == 0) {
-    __threadfence();
-    atomicAdd(&ctrl[qArrive], 1);
+    __hip_atomic_fetch_add(&ctrl[qArrive], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const long long t0 = wall_clock64();
     int ok = 1;
     if (timeout <= 0) {   // a zero bound gives up at once: the failure path, forced
@@ -506,7 +511,6 @@ __device__ bool seq_barrier(int* ctrl, int target, long long timeout, int* s_ok)
       }
       __builtin_amdgcn_s_sleep(1);
     }
-    __threadfence();
     *s_ok = ok;
   }
   __syncthreads();
@@ -515,6 +519,16 @@ __device__ bool seq_barrier(int* ctrl, int target, long long timeout, int* s_ok)
 
 __device__ __forceinline__ int ld_agent(const int* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ void st_agent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// sum of the chunk counts (which = 0: kept, 1: ties) of the chunks before
+// chunk cb (< 64): lane q reads chunk q, the same sum in every wave
+__device__ __forceinline__ int counts_before(const int* ctrl, int cb, int which) {
+  const int q = threadIdx.x & 63;
+  return wave_sum(q < cb ? ld_agent(&ctrl[qCounts + 2 * q + which]) : 0);
 }
 }  // namespace
 
@@ -527,7 +541,7 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
   __shared__ int tmp[kQW], wa[kQW], wb[kQW];
   __shared__ uint32_t wlo[kQW], whi[kQW];
   __shared__ uint32_t s_lo, s_hi;
-  __shared__ int s_need, s_ok, s_m, s_cnt[3];
+  __shared__ int s_need, s_ok, s_m;
   __shared__ uint32_t sCk[kCandMax];
   __shared__ int sCi[kCandMax];
   const int s = blockIdx.y, cb = blockIdx.x, C = gridDim.x;
@@ -549,6 +563,34 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
   const int poff = a.pend_off[s], n = a.pend_off[s + 1] - poff;   // n <= kSelGridPendMax
   const int roff = a.ret_off[s], nr = a.ret_off[s + 1] - roff;
   const float* R = reinterpret_cast<const float*>(a.pend_r[s]);
+  const AccPages ap = a.acc ? a.acc[s] : AccPages{};
+  // The loads of each thread's first pending page, retired page and accepted
+  // candidate (with its page span) are issued before the LDS is cleared, so
+  // their latencies overlap one another and the barrier; a candidate's flag
+  // and page index do not wait for the candidate count.
+  float pr = 0.f;
+  int pln = 0, pst = 0, rst = 0, rln = 0, ast = 0, aln = 0;
+  if (tid < n) {
+    pr = pend_key(R[tid]);
+    pln = a.pend_len[poff + tid];
+    pst = a.pend_start[poff + tid];
+  }
+  if (tid < nr) {
+    rst = a.ret_start[roff + tid];
+    rln = a.ret_len[roff + tid];
+  }
+  int nc = 0;
+  if (ap.cand) {
+    nc = min(*ap.n_cand, ap.max_cand);
+    if (tid < ap.max_cand) {
+      const uint8_t acc = ap.accepted[tid];
+      const int pg = ap.cand[tid];
+      if (acc && pg >= 0 && pg < ap.n_pages) {
+        ast = ap.start[pg];
+        aln = ap.len[pg];
+      }
+    }
+  }
   for (int i = tid; i < kSelGridChunk / 4; i += kQT) {
     reinterpret_cast<uint32_t*>(sRet)[i] = 0u;
     reinterpret_cast<uint32_t*>(sPro)[i] = 0u;
@@ -556,26 +598,26 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
   __syncthreads();
   // pending pages to LDS; retired and accepted pages that overlap the chunk
   // marked meanwhile
-  for (int i = tid; i < n; i += kQT) {
-    sR[i] = pend_key(R[i]);
-    sLen[i] = a.pend_len[poff + i];
-    sStart[i] = a.pend_start[poff + i];
-    sProt[i] = 0;
+  if (tid < n) {
+    sR[tid] = pr;
+    sLen[tid] = pln;
+    sStart[tid] = pst;
+    sProt[tid] = 0;
   }
-  for (int i = tid; i < nr; i += kQT) {
+  if (tid < nr)
+    for (int t = max(rst, c0); t < min(rst + rln, c1); ++t) sRet[t - c0] = 1;
+  for (int i = tid + kQT; i < nr; i += kQT) {
     const int st = a.ret_start[roff + i], ln = a.ret_len[roff + i];
     for (int t = max(st, c0); t < min(st + ln, c1); ++t) sRet[t - c0] = 1;
   }
-  if (a.acc && a.acc[s].cand) {
-    const AccPages ap = a.acc[s];
-    const int nc = min(*ap.n_cand, ap.max_cand);
-    for (int i = tid; i < nc; i += kQT) {
-      if (!ap.accepted[i]) continue;
-      const int pg = ap.cand[i];
-      if (pg < 0 || pg >= ap.n_pages) continue;
-      const int st = ap.start[pg], ln = ap.len[pg];
-      for (int t = max(st, c0); t < min(st + ln, c1); ++t) sRet[t - c0] = 1;
-    }
+  if (tid < nc)
+    for (int t = max(ast, c0); t < min(ast + aln, c1); ++t) sRet[t - c0] = 1;
+  for (int i = tid + kQT; i < nc; i += kQT) {
+    if (!ap.accepted[i]) continue;
+    const int pg = ap.cand[i];
+    if (pg < 0 || pg >= ap.n_pages) continue;
+    const int st = ap.start[pg], ln = ap.len[pg];
+    for (int t = max(st, c0); t < min(st + ln, c1); ++t) sRet[t - c0] = 1;
   }
   __syncthreads();
   // Eq. (12): pending pages ranked by (R- descending, page order), protected
@@ -595,15 +637,14 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
     }
   }
   __syncthreads();
-  if (tid == 0) {
-    int taken = 0, tok = 0;
-    for (int r = 0; r < n; ++r) {
-      const int i = sOrd[r];
-      if (taken >= a.max_pages || tok + sLen[i] > a.bn) break;
-      sProt[i] = 1;
-      ++taken;
-      tok += sLen[i];
-    }
+  {
+    // thread r takes rank r (n <= kQT): protected while r < max_pages and
+    // the running token total in rank order, this page included, fits B_N;
+    // the total only grows, so this is the prefix the rule above takes
+    const int li = tid < n ? sLen[sOrd[tid]] : 0;
+    int total;
+    const int before = block_scan<kQT>(li, tmp, total);
+    if (tid < n && tid < a.max_pages && before + li <= a.bn) sProt[sOrd[tid]] = 1;
   }
   __syncthreads();
   for (int i = tid; i < n; i += kQT) {
@@ -727,20 +768,26 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
         // (the histogram rows of the later passes, unused on this path);
         // the chunk publishes how many of its tokens are kept outright
         uint32_t* gc = gh + kSelBins;
-        int nk = 0;
+        int nk = 0, nin = 0;
+        unsigned long long inm[kQKPT];
 #pragma unroll
         for (int u = 0; u < kQKPT; ++u) {
           const uint32_t kk = key[u];
           nk += (kk == kKeyProt || (key_free(kk) && kk > hi)) ? 1 : 0;
-          const bool inb = key_free(kk) && kk >= lo && kk <= hi;
-          const unsigned long long m = __ballot(inb);
-          int base = 0;
-          if (m && lane == 0) base = atomicAdd(&ctrl[qCand], __popcll(m));
-          base = __shfl(base, 0, 64);
-          const int slot = base + lanes_below(m);
-          if (inb && slot < kCandMax) {
-            gc[2 * slot] = kk;
-            gc[2 * slot + 1] = (uint32_t)(t_base + 64 * u);
+          inm[u] = __ballot(key_free(kk) && kk >= lo && kk <= hi);
+          nin += __popcll(inm[u]);
+        }
+        // one slot reservation per wave for all of its keys in the bin
+        int base = 0;
+        if (nin && lane == 0) base = atomicAdd(&ctrl[qCand], nin);
+        base = __shfl(base, 0, 64);
+#pragma unroll
+        for (int u = 0; u < kQKPT; ++u) {
+          const int slot = base + lanes_below(inm[u]);
+          base += __popcll(inm[u]);
+          if (((inm[u] >> lane) & 1ull) && slot < kCandMax) {
+            st_agent(&gc[2 * slot], key[u]);
+            st_agent(&gc[2 * slot + 1], (uint32_t)(t_base + 64 * u));
           }
         }
         nk = wave_sum(nk);
@@ -750,17 +797,31 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
         if (tid == 0) {
           int tk = 0;
           for (int w = 0; w < kQW; ++w) tk += wa[w];
-          ctrl[qCounts + 2 * cb] = tk;
+          st_agent(&ctrl[qCounts + 2 * cb], tk);
         }
         target += C;
         ok = seq_barrier(ctrl, target, a.barrier_ticks, &s_ok);
         if (ok) {
           const int M = min(ld_agent(&ctrl[qCand]), kCandMax);
-          for (int i = tid; i < M; i += kQT) {
-            sCk[i] = __hip_atomic_load(&gc[2 * i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            sCi[i] = (int)__hip_atomic_load(&gc[2 * i + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          {
+            // every load of the list in flight before the first LDS store
+            constexpr int kCPT = kCandMax / kQT;
+            uint32_t ck[kCPT], ci[kCPT];
+#pragma unroll
+            for (int j = 0; j < kCPT; ++j) {
+              const int i = tid + j * kQT;
+              ck[j] = i < M ? __hip_atomic_load(&gc[2 * i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+              ci[j] = i < M ? __hip_atomic_load(&gc[2 * i + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+            }
+#pragma unroll
+            for (int j = 0; j < kCPT; ++j) {
+              const int i = tid + j * kQT;
+              if (i < M) {
+                sCk[i] = ck[j];
+                sCi[i] = (int)ci[j];
+              }
+            }
           }
-          if (tid < 3) s_cnt[tid] = 0;
           // the same narrowing as the grid passes, on the list in LDS
           while (lo != hi) {
             const uint32_t range = hi - lo;
@@ -799,16 +860,23 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
           }
           T = lo;                        // the need-th largest key; need ties at T are kept
           need_eq = need;
-          // what the chunks before this one hold of the listed keys
+          // what the chunks before this one hold of the listed keys: counted
+          // per thread, then added over the block (LDS atomics on two words
+          // would serialise over the whole list)
+          int gt = 0, eq = 0;
           for (int i = tid; i < M; i += kQT) {
             if (sCi[i] >= c0) continue;
-            if (sCk[i] > T) atomicAdd(&s_cnt[1], 1);
-            else if (sCk[i] == T) atomicAdd(&s_cnt[2], 1);
+            gt += sCk[i] > T ? 1 : 0;
+            eq += sCk[i] == T ? 1 : 0;
           }
+          gt = wave_sum(gt);
+          eq = wave_sum(eq);
+          if (lane == 0) { wa[wave] = gt; wb[wave] = eq; }
           __syncthreads();
-          k_before = s_cnt[1];
-          e_before = s_cnt[2];
-          for (int q = 0; q < cb; ++q) k_before += ld_agent(&ctrl[qCounts + 2 * q]);
+#pragma unroll
+          for (int w = 0; w < kQW; ++w) { k_before += wa[w]; e_before += wb[w]; }
+          __syncthreads();
+          k_before += counts_before(ctrl, cb, 0);
         }
       } else {
         T = lo;                          // lo == hi: the need-th largest key
@@ -834,15 +902,15 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
         if (tid == 0) {
           int tk = 0, te = 0;
           for (int w = 0; w < kQW; ++w) { tk += wa[w]; te += wb[w]; }
-          ctrl[qCounts + 2 * cb] = tk;
-          ctrl[qCounts + 2 * cb + 1] = te;
+          st_agent(&ctrl[qCounts + 2 * cb], tk);
+          st_agent(&ctrl[qCounts + 2 * cb + 1], te);
         }
         target += C;
         ok = seq_barrier(ctrl, target, a.barrier_ticks, &s_ok);
         if (ok)
-          for (int q = 0; q < cb; ++q) {
-            k_before += ld_agent(&ctrl[qCounts + 2 * q]);
-            e_before += ld_agent(&ctrl[qCounts + 2 * q + 1]);
+          {
+            k_before += counts_before(ctrl, cb, 0);
+            e_before += counts_before(ctrl, cb, 1);
           }
       }
     }
@@ -866,22 +934,18 @@ __global__ __launch_bounds__(kQT) void select_grid(SelectArgs a) {
       }
       const int n_kept = min(a.budget, NP + k);
       for (int j = n_kept + cb * kQT + tid; j < a.budget; j += C * kQT) kept[j] = -1;
-      if (cb == 0 && tid == 0) a.n_kept[s] = n_kept;
+      if (cb == 0 && tid == 0) st_agent(&a.n_kept[s], n_kept);   // ordered before a give-up's -1
     }
   }
   // the last workgroup of the sequence clears the control words and the
   // histograms for the next call (every other workgroup is done with them)
   __syncthreads();
-  if (tid == 0) {
-    __threadfence();
-    s_ok = atomicAdd(&ctrl[qDone], 1) == C - 1;
-  }
+  if (tid == 0) s_ok = __hip_atomic_fetch_add(&ctrl[qDone], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == C - 1;
   __syncthreads();
   if (s_ok) {
-    __threadfence();
-    if (tid == 0 && ld_agent(&ctrl[qError]) != 0) a.n_kept[s] = -1;
-    for (int i = tid; i < 3 * kSelBins; i += kQT) gh[i] = 0u;
-    for (int i = tid; i < kSelGridCtrl; i += kQT) ctrl[i] = 0;
+    if (tid == 0 && ld_agent(&ctrl[qError]) != 0) st_agent(&a.n_kept[s], -1);
+    for (int i = tid; i < 3 * kSelBins; i += kQT) st_agent(&gh[i], 0u);
+    for (int i = tid; i < kSelGridCtrl; i += kQT) st_agent(&ctrl[i], 0);
   }
 }
 
