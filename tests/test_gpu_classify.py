@@ -74,6 +74,27 @@ def test_random_effects_identical(ckv, n):
     assert np.all(raw[nc:] == -1)
 
 
+@pytest.mark.parametrize("n", [300, 1500])
+def test_infinite_effects(ckv, n):
+    """Pages that hold every visible token have R = +inf (Eq. (6)-(7)):
+    they rank above every finite page and tie with each other; zero
+    effects tie at the bottom."""
+    P, ctx = ckv
+    r = np.random.default_rng(n + 1)
+    Rm = np.exp(r.uniform(np.log(1e-4), np.log(2.0), n)).astype(np.float32)
+    Rp = np.exp(r.uniform(np.log(1e-4), np.log(2.0), n)).astype(np.float32)
+    Rm[::37] = np.inf
+    Rp[::41] = np.inf
+    Rp[5::53] = 0.0
+    lam, Pm, Pp, cand, nc, raw = _gpu_classify(P, ctx, Rm, Rp)
+    lam_o, Pm_o, Pp_o, cand_o = _oracle(Rm, Rp)
+    np.testing.assert_array_equal(lam, lam_o)
+    np.testing.assert_allclose(Pm, Pm_o, rtol=1e-7)
+    np.testing.assert_allclose(Pp, Pp_o, rtol=1e-7)
+    np.testing.assert_array_equal(cand, cand_o)
+    assert np.all(raw[nc:] == -1)
+
+
 def test_force_and_cap(ckv):
     P, ctx = ckv
     r = np.random.default_rng(0)
