@@ -676,20 +676,22 @@ void plan_measure(const AttnGeom& a, int n_splits, float* o, Plan& plan, Measure
   const int nrb = ceil_div(a.rows, rpb);
   const int chunk = (int)round_up(ceil_div(a.S, n_splits), 64);
   n_splits = ceil_div(a.S, chunk);
-  b.sp = AttnSplit{chunk, n_splits, nrb * rpb, nullptr, nullptr, nullptr, nullptr, nullptr};
-  b.rs = RowStats{o, nullptr, nullptr, nullptr, nullptr, nullptr};
+  b.sp = AttnSplit{chunk, n_splits, nrb * rpb, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  b.rs = RowStats{o, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   const size_t nsr = (size_t)a.Hkv * n_splits * b.sp.rows_pad;
   plan.add(&b.sp.part_o, nsr * D);
   plan.add(&b.sp.part_m, nsr);
   plan.add(&b.sp.part_l, nsr);
   plan.add(&b.sp.part_c, nsr);
   plan.add(&b.sp.part_t, nsr);
+  plan.add(&b.sp.part_p, nsr);
   if (!o) plan.add(&b.rs.o, (size_t)total_rows * D);
   plan.add(&b.rs.lse2, total_rows);
   plan.add(&b.rs.onorm, total_rows);
   plan.add(&b.rs.nvis, total_rows);
   plan.add(&b.rs.m2, total_rows);
   plan.add(&b.rs.m2t, total_rows);
+  plan.add(&b.rs.m2p, total_rows);
   plan.add(&b.fix_list, 4 * (size_t)total_rows);
   plan.add(&b.fix_count, 1);
   plan.add(&b.fpart, (size_t)total_rows * ckv::kFixParts * (D + 1));
@@ -885,7 +887,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
 
   const AttnGeom a = make_geom(c, kv, win);
   const int n = pages->n_pages, total_rows = a.Hq * a.W;
-  RowStats rs{const_cast<float*>(o), nullptr, nullptr, nullptr, nullptr, nullptr};
+  RowStats rs{const_cast<float*>(o), nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   Plan plan;
   plan.add(&rs.lse2, total_rows);
   plan.add(&rs.onorm, total_rows);
@@ -941,7 +943,7 @@ extern "C" int ckv_measure_recorded(ckv_ctx* c, const ckv_kv_view* kv, const ckv
     pw2.fix_list = list2;
     pw2.fix_count = count2;
     pw2.fix_cap = cap2;
-    AttnSplit whole{(int)round_up(a.S, 64), 1, 0, nullptr, nullptr, nullptr, nullptr, nullptr};
+    AttnSplit whole{(int)round_up(a.S, 64), 1, 0, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
     CKV_LAUNCH(c, "page_fixup_complement",
                launch_page_fixup(a, whole, rs, pw2, fpart, count2 + 1, ckv::kFixPartsRow, items2, c->stream));
   }
@@ -1014,7 +1016,7 @@ extern "C" int ckv_joint_test(ckv_ctx* c, const ckv_kv_view* kv, const ckv_windo
   const AttnGeom a = make_geom(c, kv, win);
   const int total_rows = a.Hq * a.W, D = a.D;
   // the residual pass reads the caller's o and natural-log lse directly
-  RowStats rs{const_cast<float*>(o), const_cast<float*>(lse), nullptr, nullptr, nullptr, nullptr};
+  RowStats rs{const_cast<float*>(o), const_cast<float*>(lse), nullptr, nullptr, nullptr, nullptr, nullptr};
   JointArgs j{};
   j.total_rows = total_rows;
   j.D = D;

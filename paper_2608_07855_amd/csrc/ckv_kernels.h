@@ -38,14 +38,16 @@ struct AttnSplit {
   int* part_t;     // start of the first tile of the split whose largest scaled logit
                    // equals the split's (the tile where the split's weight reference
                    // took its final value); -1 when the split shows the row no token
+  float* part_p;   // the split's weight reference before that tile (log2 units; -inf
+                   // when the reference grew only once)
 };
 
 // per window row (global row h*W + p): o [rows][D], lse2 (log2 units), ||o||, n_vis,
 // and m2, the largest scaled logit of the row (log2 units): the reference the
 // window pass's float16 weights were finally taken against, with m2t, the
 // start of the tile where it entered that reference in the first split that
-// holds it (both null when the outputs were not computed by this library's
-// window pass)
+// holds it, and m2p, that split's reference before that tile (all null when
+// the outputs were not computed by this library's window pass)
 struct RowStats {
   float* o;
   float* lse2;
@@ -53,6 +55,7 @@ struct RowStats {
   int* nvis;
   float* m2;
   int* m2t;
+  float* m2p;
 };
 
 // pages processed by pass B (MODE 0: item = page; MODE 1: item t = page cand[t])
@@ -100,6 +103,13 @@ struct PageWork {
 // pages keep the closed form up to kFixAHi.  Any other page's weights round
 // differently in the two passes, and the residual u - A o inherits that
 // rounding times 1/(1 - A): those go above kFixA.
+// A fix-up entry (page, row, start, length) whose length carries this flag
+// has A <= kFixAHi after this library's window pass.  If its page crosses a
+// tile boundary inside one split and the row's largest logit entered the
+// reference with the page's second tile, the fix-up evaluates Eq. (6) with
+// the window pass's own weights (first part against the older reference,
+// rescaled) instead of recomputing the split.  The length is the low byte.
+constexpr int kFixRescaled = 1 << 16;
 constexpr float kFixA = 0.9f;
 constexpr float kFixAHi = 0.99f;
 constexpr float kFixARecorded = 0.5f;   // with recorded window outputs (no shared weights)

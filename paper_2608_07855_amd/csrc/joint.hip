@@ -781,7 +781,7 @@ __global__ __launch_bounds__(256) void joint_owned(JointArgs j, RowStats rs) {
 int joint_vis_slices(int S) { return (S + kVisSlice - 1) / kVisSlice; }
 
 hipError_t launch_joint_persistent(const JointArgs& j, int max_blocks, hipStream_t s) {
-  RowStats rs{nullptr, nullptr, const_cast<float*>(j.onorm), nullptr, nullptr, nullptr};
+  RowStats rs{nullptr, nullptr, const_cast<float*>(j.onorm), nullptr, nullptr, nullptr, nullptr};
   const int n_rb = (j.total_rows + j.rows_per_block - 1) / j.rows_per_block;
   // workgroups of each form that fit on the device at once (queried once per device)
   static int resident[64][2];

@@ -68,7 +68,11 @@ constexpr int kRowsWG = 32 * kNW;    // window rows per workgroup
 // out of the page kernel's maximum; the fix-up kernel recomputes the output
 // without the page, o', directly (all other splits' partial sums as they
 // are, the page's own split again with the page excluded) and takes
-// ||o - o'|| / ||o|| by definition.  At most one page per row can exceed
+// ||o - o'|| / ||o|| by definition; a listed page across a tile boundary
+// inside one split whose row maximum entered the reference with its second
+// tile is instead evaluated with the window pass's own weights (older
+// reference for the first part, then rescaled), which the window kernel's
+// recorded references make known.  At most one page per row can exceed
 // kFixA, so the list never holds more than one entry per window row.  With
 // recorded outputs (computed without this pass's float16 weights) every
 // pair above kFixARecorded is listed: the page pass's rounding is then no
@@ -347,7 +351,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
   for (int db = 0; db < DB; ++db) oacc[db] = zero16();
   float mref = -INFINITY, l = 0.f;
   int cnt = 0;
-  int mt = -1;   // start of the tile where mref last grew
+  int mt = -1;          // start of the tile where mref last grew
+  float mp = -INFINITY;  // mref before that tile
 
   const int n_tiles = t_end > t_begin ? (t_end - t_begin + kTile - 1) / kTile : 0;
   // Loads run two tiles ahead of the math: stager A holds even tiles, B odd
@@ -397,8 +402,11 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
         l *= alpha;
 #pragma unroll
         for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+        if (need) {
+          mp = mref;
+          mt = t_begin + it * kTile;
+        }
         mref = nref;
-        if (need) mt = t_begin + it * kTile;
       }
       const float base = mref == -INFINITY ? 0.f : mref;
 #pragma unroll
@@ -440,6 +448,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void window_attention_kernel(AttnGeom 
     sp.part_l[idx] = lt;
     sp.part_c[idx] = ct;
     sp.part_t[idx] = mt;
+    sp.part_p[idx] = mp;
   }
   float* po = sp.part_o + idx * D;
 #pragma unroll
@@ -485,10 +494,12 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
   const size_t base = (size_t)g * sp.n_splits * sp.rows_pad + row;
   float M = -INFINITY, wsum = 0.f;
   int nv = 0, mt = -1;   // mt: tile where M entered the first split that holds it
+  float mp = -INFINITY;  // that split's reference before the tile
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < sp.n_splits; s0 += kCombBatch) {
     float ms[kCombBatch], ls[kCombBatch];
     int cs[kCombBatch], ts[kCombBatch];
+    float ps[kCombBatch];
     f32x4 os[kCombBatch];
 #pragma unroll
     for (int u = 0; u < kCombBatch; ++u) {
@@ -499,12 +510,14 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
       ls[u] = sp.part_l[idx];
       cs[u] = in ? sp.part_c[idx] : 0;
       ts[u] = sp.part_t[idx];
+      ps[u] = sp.part_p[idx];
       os[u] = *reinterpret_cast<const f32x4*>(sp.part_o + idx * D + 4 * c);
     }
     float mb = M;
 #pragma unroll
     for (int u = 0; u < kCombBatch; ++u) {
       mt = ms[u] > mb ? ts[u] : mt;   // the first split wins a tie
+      mp = ms[u] > mb ? ps[u] : mp;
       mb = fmaxf(mb, ms[u]);
     }
     if (mb != -INFINITY) {
@@ -538,6 +551,7 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnGeom a, AttnSplit sp, 
     rs.nvis[rg] = nv;
     if (rs.m2) rs.m2[rg] = M;
     if (rs.m2t) rs.m2t[rg] = mt;
+    if (rs.m2p) rs.m2p[rg] = mp;
     if (lse_out) lse_out[rg] = l2 * kLn2;
     // a NaN or infinite key, query or value reaches the row's output or its
     // log-sum-exp (a row that sees no token has lse -inf and o = 0)
@@ -783,6 +797,8 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
       // entered the split's reference by the tile of the page's first part
       // (lanes without a row have m2row NaN, so holds_max is false there).
       bool form_ok = MODE == 0 && holds_max && A <= pw.fix_a_hi;
+      // the fix-up may evaluate a listed pair with the window pass's own weights
+      const bool cand = MODE == 0 && rs.m2t != nullptr && A <= pw.fix_a_hi;
       if (MODE == 0 && cross != 0) {
         if (cross == kAcrossSplit) {
           form_ok = false;
@@ -800,7 +816,7 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
             ratio = INFINITY;                 // the page holds every visible token
           } else if ((A > pw.fix_a && !form_ok) || !(keep > 0.f)) {
             if (ri.ok && half == 0) {         // ill-conditioned: recomputed by the fix-up
-              const int4 ent = make_int4(item, ri.rg, pstart(item), len);
+              const int4 ent = make_int4(item, ri.rg, pstart(item), len | (cand ? kFixRescaled : 0));
               const int ls = atomicAdd(&sFixN, 1);
               if (ls < kRowsWG) {
                 sFix[ls] = ent;
@@ -904,9 +920,18 @@ __global__ __launch_bounds__(kNW * 64, 1) void page_kernel(AttnGeom a, PageWork 
 constexpr int kFixT = 256;        // threads of a fix-up workgroup
 constexpr int kFixGrid = 1024;    // (pair, part) items in flight
 
-// parts per listed pair: fixed, or within an item budget for n pairs
-__device__ __forceinline__ int fix_parts(int parts, int item_budget, int n) {
-  return item_budget > 0 ? max(1, min(parts, item_budget / max(n, 1))) : parts;
+constexpr int kFixMinSeg = 256;   // tokens of the page's split per part, at least, when parts grow
+constexpr int kFixPartsMax = 32;
+
+// parts per listed pair: within an item budget for n pairs; or, without one,
+// at least `parts`, and more while the n pairs leave fix-up blocks idle and
+// each part still takes kFixMinSeg tokens of a split of `chunk` (the partial
+// sums buffer holds cap x parts entries)
+__device__ __forceinline__ int fix_parts(int parts, int item_budget, int n, int nb, int chunk, int cap) {
+  const int m = max(n, 1);
+  if (item_budget > 0) return max(1, min(parts, item_budget / m));
+  const int grow = min(min(nb / m, chunk / kFixMinSeg), kFixPartsMax);
+  return max(parts, min(grow, cap * parts / m));
 }
 
 // ratio of listed pair e from its parts' sums (one wave)
@@ -924,6 +949,7 @@ __device__ void fixup_ratio(const AttnGeom& a, const RowStats& rs, const PageWor
   float num[D / 64], den = 0.f;
 #pragma unroll
   for (int j = 0; j < D / 64; ++j) num[j] = 0.f;
+#pragma unroll 8
   for (int part = 0; part < parts; ++part) {
 #pragma unroll
     for (int j = 0; j < D / 64; ++j) num[j] += ld(fp + part * (D + 1) + lane + 64 * j);
@@ -952,6 +978,119 @@ __device__ void fixup_ratio(const AttnGeom& a, const RowStats& rs, const PageWor
   }
 }
 
+// Eq. (6)-(7) for a listed pair whose page crosses a tile boundary inside
+// one split while the row's largest logit entered the window pass's
+// reference with the page's second tile: the first part's float16 weights
+// were taken against the split's older reference and the running output was
+// rescaled by 2^(older - largest) when the largest arrived.  One wave takes
+// the same weights (the key fragments and the query in the layout and product
+// chain of the window pass, so the scores are bit-identical), rescales the
+// first part's sums the same way and evaluates the closed form; the
+// cancellation in u - A o then loses only float32 digits.
+template <int D, bool PG>
+__device__ void rescaled_pair(const AttnGeom& a, const RowStats& rs, const PageWork& pw, const int4 ent,
+                              int lane) {
+  constexpr int KS = D / 16, DL = D / 64;
+  const int half = lane >> 5, col = lane & 31;
+  const int page = (int)CKV_IDX(ent.x, pw.n_pages, a.dbg, 8), rg = (int)CKV_IDX(ent.y, a.Hq * a.W, a.dbg, 7);
+  const int st = ent.z, ln = ent.w & 0xFF;
+  const int h = rg / a.W, p = rg % a.W, g = h / a.group;
+  const int qp = a.qpos[p];
+  const int nf = (st / kTile + 1) * kTile - st;          // tokens before the boundary
+  const float M = rs.m2[rg], mprev = rs.m2p[rg];
+  const float alpha = __builtin_amdgcn_exp2f(mprev - M);
+  __shared__ float sW[32];   // one block's weights
+  const uint16_t* qrow = a.q + (int64_t)h * a.q_head_stride + (int64_t)p * a.q_row_stride;
+  const uint16_t* kh = a.k + (int64_t)g * a.kv_head_stride;
+  const uint16_t* vh = a.v + (int64_t)g * a.kv_head_stride;
+  auto krow = [&](int t) -> int64_t { return PG ? (int64_t)min((uint32_t)a.slot[t], a.pool_last) : t; };
+  bf16x8 qf[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qrow + 16 * ks + 8 * half);
+  float l1 = 0.f, l2 = 0.f;   // weight sums of the first and the second part
+  float u1[DL], u2[DL];       // U over each part; lane d takes widths d, d + 64
+#pragma unroll
+  for (int j = 0; j < DL; ++j) u1[j] = u2[j] = 0.f;
+  // one 32-token block at a time (every column of the product is the same row)
+#pragma unroll 1
+  for (int tb = 0; tb < 2 && 32 * tb < ln; ++tb) {
+    const int ok_tok = 32 * tb + col < ln;
+    const uint16_t* kr = kh + krow(ok_tok ? st + 32 * tb + col : st) * a.kv_tok_stride;
+    f32x16 acc = zero16();
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      acc = mfma_bf16(ok_tok ? load_bf16x8(kr + 16 * ks + 8 * half) : zero_bf16x8(), qf[ks], acc);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int o = 32 * tb + 8 * (r >> 2) + 4 * half + (r & 3);
+      const bool vis = o < ln && a.pos[st + min(o, ln - 1)] <= qp;
+      const float ref = o < nf ? mprev : M;
+      const float x = vis ? __builtin_amdgcn_exp2f(__builtin_fmaf(acc[r], a.sl2, -ref)) : 0.f;
+      acc[r] = (float)(_Float16)x;
+      if (o < nf) l1 += acc[r];
+      else l2 += acc[r];
+    }
+    // the block's weights through LDS (lanes 0 and 32 hold the two halves)
+    if (col == 0) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sW[8 * (r >> 2) + 4 * half + (r & 3)] = acc[r];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int nb = min(32, ln - 32 * tb);
+#pragma unroll 8
+    for (int i = 0; i < nb; ++i) {
+      const int o = 32 * tb + i;
+      const float wt = sW[i];
+      const uint16_t* vr = vh + krow(st + o) * a.kv_tok_stride;
+#pragma unroll
+      for (int j = 0; j < DL; ++j) {
+        const float v = (float)(_Float16)bf16_bits_to_float(vr[lane + 64 * j]);   // as the window pass
+        if (o < nf) u1[j] = __builtin_fmaf(wt, v, u1[j]);
+        else u2[j] = __builtin_fmaf(wt, v, u2[j]);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+  }
+  // token sums over both halves (lanes l and l ^ 32 hold the two halves)
+  l1 += __shfl_xor(l1, 32, 64);
+  l2 += __shfl_xor(l2, 32, 64);
+  const float lhat = alpha * l1 + l2;
+  float n2 = 0.f;
+#pragma unroll
+  for (int j = 0; j < DL; ++j) {
+    const float ov = rs.o[(size_t)rg * D + lane + 64 * j];
+    const float uj = __builtin_fmaf(alpha, u1[j], u2[j]) - lhat * ov;
+    n2 = __builtin_fmaf(uj, uj, n2);
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) n2 += __shfl_xor(n2, off, 64);
+  if (lane == 0) {
+    const float f = __builtin_amdgcn_exp2f(M - rs.lse2[rg] * pw.lse_scale);
+    const float keep = 1.f - f * lhat;
+    const float onorm = rs.onorm[rg];
+    float ratio;
+    if (onorm > 0.f) ratio = keep > 0.f ? f * sqrtf(n2) / (onorm * keep) : INFINITY;
+    else ratio = n2 > 0.f ? INFINITY : 0.f;
+    if (pw.R_head) atomic_max_nonneg(&pw.R_head[(size_t)page * pw.Hq + h], ratio);
+    atomic_max_nonneg(&pw.R[page], ratio);
+  }
+}
+
+// A listed pair with A <= fix_a_hi (flagged by the page kernel) whose page
+// crosses a tile boundary inside one split, where the row's largest logit
+// entered the window pass's reference with the page's second tile: the
+// references of both tiles are then known (the same decision in every part
+// of the pair)
+__device__ __forceinline__ bool rescaled_entry(const AttnSplit& sp, const RowStats& rs, const int4 ent) {
+  if (!(ent.w & kFixRescaled) || !rs.m2t || !rs.m2p) return false;
+  const int st = ent.z, ln = ent.w & 0xFF;
+  const int t1 = (st / kTile + 1) * kTile;   // start of the page's second tile
+  return t1 < st + ln && t1 % sp.chunk != 0 && rs.m2t[ent.y] == t1;
+}
+
 // the fix-up of block bx of nb fix-up blocks, each of T threads
 template <int D, bool PG, int T>
 __device__ __forceinline__ void page_fixup_body(const AttnGeom& a, const AttnSplit& sp, const RowStats& rs,
@@ -964,12 +1103,16 @@ __device__ __forceinline__ void page_fixup_body(const AttnGeom& a, const AttnSpl
   __shared__ int sLast;
   const int tid = threadIdx.x, c = tid % TPR, r = tid / TPR;
   const int n = min(*pw.fix_count, pw.fix_cap);
-  parts = fix_parts(parts, item_budget, n);
+  parts = fix_parts(parts, item_budget, n, nb, sp.chunk, pw.fix_cap);
   for (int item = bx; item < n * parts; item += nb) {
     const int e = item / parts, part = item % parts;
     // entry: page, global row, page start, page length
     const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
-    const int rg = (int)CKV_IDX(ent.y, a.Hq * a.W, a.dbg, 7), st = ent.z, ln = ent.w;
+    if (rescaled_entry(sp, rs, ent)) {   // evaluated with the window pass's own weights, by one wave
+      if (part == 0 && tid < 64) rescaled_pair<D, PG>(a, rs, pw, ent, tid);
+      continue;
+    }
+    const int rg = (int)CKV_IDX(ent.y, a.Hq * a.W, a.dbg, 7), st = ent.z, ln = ent.w & 0xFF;
     const int h = rg / a.W, p = rg % a.W, g = h / a.group, row = rg - g * a.rows;
     const int qp = a.qpos[p];
     const float ref = rs.lse2[rg];

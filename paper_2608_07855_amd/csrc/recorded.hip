@@ -95,7 +95,7 @@ __global__ __launch_bounds__(256) void page_fixup_recorded(AttnGeom a, RowStats 
   const int n = min(*pw.fix_count, pw.fix_cap);
   for (int e = blockIdx.x * 4 + (threadIdx.x >> 6); e < n; e += gridDim.x * 4) {
     const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
-    const int page = ent.x, rg = ent.y, st = ent.z, ln = ent.w;
+    const int page = ent.x, rg = ent.y, st = ent.z, ln = ent.w & 0xFF;
     const int h = rg / a.W, p = rg % a.W, g = h / a.group;
     const int qp = a.qpos[p];
     const float ref = rs.lse2[rg];
