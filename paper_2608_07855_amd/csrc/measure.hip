@@ -990,7 +990,7 @@ __device__ void fixup_ratio(const AttnGeom& a, const RowStats& rs, const PageWor
 template <int D, bool PG>
 __device__ void rescaled_pair(const AttnGeom& a, const RowStats& rs, const PageWork& pw, const int4 ent,
                               int lane) {
-  constexpr int KS = D / 16, DL = D / 64;
+  constexpr int KS = D / 16;
   const int half = lane >> 5, col = lane & 31;
   const int page = (int)CKV_IDX(ent.x, pw.n_pages, a.dbg, 8), rg = (int)CKV_IDX(ent.y, a.Hq * a.W, a.dbg, 7);
   const int st = ent.z, ln = ent.w & 0xFF;
@@ -1007,13 +1007,22 @@ __device__ void rescaled_pair(const AttnGeom& a, const RowStats& rs, const PageW
   bf16x8 qf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) qf[ks] = load_bf16x8(qrow + 16 * ks + 8 * half);
-  float l1 = 0.f, l2 = 0.f;   // weight sums of the first and the second part
-  float u1[DL], u2[DL];       // U over each part; lane d takes widths d, d + 64
+  constexpr int DPL = D / 64;   // widths per lane: lane * DPL .. lane * DPL + DPL - 1
+  float l1 = 0.f, l2 = 0.f;      // weight sums of the first and the second part
+  float u1[DPL], u2[DPL];        // U over each part, at this lane's widths
 #pragma unroll
-  for (int j = 0; j < DL; ++j) u1[j] = u2[j] = 0.f;
+  for (int j = 0; j < DPL; ++j) u1[j] = u2[j] = 0.f;
   // one 32-token block at a time (every column of the product is the same row)
 #pragma unroll 1
   for (int tb = 0; tb < 2 && 32 * tb < ln; ++tb) {
+    const int nb = min(32, ln - 32 * tb);
+    // the block's value rows, loaded before its products (this lane's widths)
+    uint32_t vraw[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const uint16_t* vr = vh + krow(st + min(32 * tb + i, ln - 1)) * a.kv_tok_stride + lane * DPL;
+      vraw[i] = DPL == 2 ? *reinterpret_cast<const uint32_t*>(vr) : (uint32_t)vr[0];
+    }
     const int ok_tok = 32 * tb + col < ln;
     const uint16_t* kr = kh + krow(ok_tok ? st + 32 * tb + col : st) * a.kv_tok_stride;
     f32x16 acc = zero16();
@@ -1038,17 +1047,18 @@ __device__ void rescaled_pair(const AttnGeom& a, const RowStats& rs, const PageW
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const int nb = min(32, ln - 32 * tb);
-#pragma unroll 8
-    for (int i = 0; i < nb; ++i) {
-      const int o = 32 * tb + i;
-      const float wt = sW[i];
-      const uint16_t* vr = vh + krow(st + o) * a.kv_tok_stride;
 #pragma unroll
-      for (int j = 0; j < DL; ++j) {
-        const float v = (float)(_Float16)bf16_bits_to_float(vr[lane + 64 * j]);   // as the window pass
-        if (o < nf) u1[j] = __builtin_fmaf(wt, v, u1[j]);
-        else u2[j] = __builtin_fmaf(wt, v, u2[j]);
+    for (int i = 0; i < 32; ++i) {
+      if (i < nb) {
+        const int o = 32 * tb + i;
+        const float wt = sW[i];
+#pragma unroll
+        for (int j = 0; j < DPL; ++j) {
+          // through float16, as the window pass converted the values
+          const float v = (float)(_Float16)bf16_bits_to_float((vraw[i] >> (16 * j)) & 0xFFFFu);
+          if (o < nf) u1[j] = __builtin_fmaf(wt, v, u1[j]);
+          else u2[j] = __builtin_fmaf(wt, v, u2[j]);
+        }
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -1060,8 +1070,8 @@ __device__ void rescaled_pair(const AttnGeom& a, const RowStats& rs, const PageW
   const float lhat = alpha * l1 + l2;
   float n2 = 0.f;
 #pragma unroll
-  for (int j = 0; j < DL; ++j) {
-    const float ov = rs.o[(size_t)rg * D + lane + 64 * j];
+  for (int j = 0; j < DPL; ++j) {
+    const float ov = rs.o[(size_t)rg * D + lane * DPL + j];
     const float uj = __builtin_fmaf(alpha, u1[j], u2[j]) - lhat * ov;
     n2 = __builtin_fmaf(uj, uj, n2);
   }
