@@ -101,8 +101,10 @@ struct PageWork {
 // its float16 weights are the very ones that formed o and Eq. (6) loses only
 // the float32 digits of the row's log-sum-exp, amplified by 1/(1 - A): such
 // pages keep the closed form up to kFixAHi.  Any other page's weights round
-// differently in the two passes, and the residual u - A o inherits that
-// rounding times 1/(1 - A): those go above kFixA.
+// differently in the two passes (by up to one float16 ulp, 2^-11 relative),
+// and the residual u - A o inherits that rounding times A/(1 - A): 2e-3 of
+// the effect at A = 0.8 if every token's rounding falls the same way, so
+// those go above kFixA.
 // A fix-up entry (page, row, start, length) whose length carries this flag
 // has A <= kFixAHi after this library's window pass.  If its page crosses a
 // tile boundary inside one split and the row's largest logit entered the
@@ -110,7 +112,7 @@ struct PageWork {
 // the window pass's own weights (first part against the older reference,
 // rescaled) instead of recomputing the split.  The length is the low byte.
 constexpr int kFixRescaled = 1 << 16;
-constexpr float kFixA = 0.9f;
+constexpr float kFixA = 0.8f;
 constexpr float kFixAHi = 0.99f;
 constexpr float kFixARecorded = 0.5f;   // with recorded window outputs (no shared weights)
 
@@ -240,7 +242,7 @@ struct JointArgs {
   int* fix_list;          // [window * rows] (slot, row) pairs flagged in a round
   float* fpart;           // [kJointFixItems][D + 1] partial sums of the fix-up
 };
-constexpr float kJointFixA = 0.9f;      // union mass above which a pair is recomputed
+constexpr float kJointFixA = 0.8f;      // union mass above which a pair is recomputed
 constexpr int kJointFixItems = 32768;   // (pair, part) items of the fix-up workspace
 constexpr int kJointFixParts = 16;      // parts a pair's row is split into at most
 int joint_vis_slices(int S);

@@ -186,7 +186,7 @@ def test_dominant_page(ckv, which, mass):
 
 
 @pytest.mark.parametrize("which", ["max_inside", "max_outside", "max_second_tile", "max_first_part_g32",
-                                   "max_first_part_g64", "max_second_part_g64"])
+                                   "max_first_part_g64", "max_second_part_g64", "max_after_page_g64"])
 def test_heavy_page_band(ckv, which):
     """Pages carrying between 0.9 and 0.99 of a row's mass.  A page that holds
     its row's largest logit inside one 64-token tile keeps the closed form of
@@ -199,11 +199,14 @@ def test_heavy_page_band(ckv, which):
     logit, and a page that straddles a 64-token boundary with its largest
     logit after it (the window pass weighted its first part against an older
     reference; max_second_tile over one-tile splits, max_second_part over
-    128-token splits), are recomputed by definition above A = 0.9.  All must
-    meet the tolerance."""
+    128-token splits), are listed above A = 0.9: recomputed by definition,
+    or, where the logit entered the reference with the page's second tile
+    inside one split (max_second_part, and max_after_page, whose largest
+    logit is the token just after a page that carries the mass), evaluated
+    with the window pass's own weights.  All must meet the tolerance."""
     P, ctx = ckv
     import math
-    split128 = which[:-4] in ("max_first_part", "max_second_part")
+    split128 = which[:-4] in ("max_first_part", "max_second_part", "max_after_page")
     if split128:
         # 8 KV heads over 4096 tokens: 32 splits of 128 tokens
         w = scaled("tiny", n_tokens=4096, n_q_heads=16, n_kv_heads=8, page_size=int(which[-2:]))
@@ -218,7 +221,21 @@ def test_heavy_page_band(ckv, which):
     starts, lens = L.layout.page_start, L.layout.page_len
     full = np.flatnonzero(lens == lens.max())
     ends = starts + lens - 1
-    if split128:
+    if which == "max_after_page_g64":
+        # every token of a page across a tile boundary at one logit for one
+        # row of the group's first query head (a ladder over the pages), the
+        # token just after the page (in the page's second tile) one higher
+        strad = np.flatnonzero((starts // 64 != ends // 64) & (ends + 1 < w.n_tokens))[::2]   # apart
+        logit = np.linspace(8.0, 16.0, len(strad))
+        group = w.n_q_heads // w.n_kv_heads
+        for n, j in enumerate(strad):
+            for g in range(w.n_kv_heads):
+                qr = q[g * group, (n + 7 * g) % w.window]
+                c = logit[(n + 5 * g) % len(strad)] * math.sqrt(w.head_dim) / float(qr @ qr)
+                k[g, int(starts[j]):int(ends[j]) + 1] = qr * c
+                k[g, int(ends[j]) + 1] = qr * (c * (1.0 + 1.0 / logit[(n + 5 * g) % len(strad)]))
+        probe = strad
+    elif split128:
         # every page across a tile boundary gets a heavy token in each KV
         # head, its first one (before the boundary) or the first after the
         # boundary, aimed at one row of the group's first query head with a
