@@ -106,11 +106,12 @@ struct PageWork {
 // the effect at A = 0.8 if every token's rounding falls the same way, so
 // those go above kFixA.
 // A fix-up entry (page, row, start, length) whose length carries this flag
-// has A <= kFixAHi after this library's window pass.  If its page crosses a
-// tile boundary inside one split and the row's largest logit entered the
-// reference with the page's second tile, the fix-up evaluates Eq. (6) with
-// the window pass's own weights (first part against the older reference,
-// rescaled) instead of recomputing the split.  The length is the low byte.
+// has A <= kFixAHi after this library's window pass.  If its page lies in
+// the first split holding the row's largest logit, from the tile before the
+// one where that logit entered the split's reference on, the fix-up
+// evaluates Eq. (6) with the window pass's own weights (tokens before that
+// tile against the older reference, rescaled) instead of recomputing the
+// split.  The length is the low byte.
 constexpr int kFixRescaled = 1 << 16;
 constexpr float kFixA = 0.8f;
 constexpr float kFixAHi = 0.99f;

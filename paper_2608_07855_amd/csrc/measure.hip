@@ -978,25 +978,24 @@ __device__ void fixup_ratio(const AttnGeom& a, const RowStats& rs, const PageWor
   }
 }
 
-// Eq. (6)-(7) for a listed pair whose page crosses a tile boundary inside
-// one split while the row's largest logit entered the window pass's
-// reference with the page's second tile: the first part's float16 weights
-// were taken against the split's older reference and the running output was
-// rescaled by 2^(older - largest) when the largest arrived.  One wave takes
-// the same weights (the key fragments and the query in the layout and product
-// chain of the window pass, so the scores are bit-identical), rescales the
-// first part's sums the same way and evaluates the closed form; the
-// cancellation in u - A o then loses only float32 digits.
+// Eq. (6)-(7) for a listed pair whose page lies in tiles with known window
+// references (see rescaled_entry): its first nf tokens were weighted in
+// float16 against the split's older reference, and the running output was
+// rescaled by 2^(older - largest) when the largest logit arrived; the rest
+// against the largest.  One wave takes the same weights (the key fragments
+// and the query in the layout and product chain of the window pass, so the
+// scores are bit-identical), rescales the first part's sums the same way and
+// evaluates the closed form; the cancellation in u - A o then loses only
+// float32 digits.
 template <int D, bool PG>
 __device__ void rescaled_pair(const AttnGeom& a, const RowStats& rs, const PageWork& pw, const int4 ent,
-                              int lane) {
+                              int nf, int lane) {
   constexpr int KS = D / 16;
   const int half = lane >> 5, col = lane & 31;
   const int page = (int)CKV_IDX(ent.x, pw.n_pages, a.dbg, 8), rg = (int)CKV_IDX(ent.y, a.Hq * a.W, a.dbg, 7);
   const int st = ent.z, ln = ent.w & 0xFF;
   const int h = rg / a.W, p = rg % a.W, g = h / a.group;
   const int qp = a.qpos[p];
-  const int nf = (st / kTile + 1) * kTile - st;          // tokens before the boundary
   const float M = rs.m2[rg], mprev = rs.m2p[rg];
   const float alpha = __builtin_amdgcn_exp2f(mprev - M);
   __shared__ float sW[32];   // one block's weights
@@ -1090,15 +1089,20 @@ __device__ void rescaled_pair(const AttnGeom& a, const RowStats& rs, const PageW
 }
 
 // A listed pair with A <= fix_a_hi (flagged by the page kernel) whose page
-// crosses a tile boundary inside one split, where the row's largest logit
-// entered the window pass's reference with the page's second tile: the
-// references of both tiles are then known (the same decision in every part
-// of the pair)
-__device__ __forceinline__ bool rescaled_entry(const AttnSplit& sp, const RowStats& rs, const int4 ent) {
-  if (!(ent.w & kFixRescaled) || !rs.m2t || !rs.m2p) return false;
-  const int st = ent.z, ln = ent.w & 0xFF;
-  const int t1 = (st / kTile + 1) * kTile;   // start of the page's second tile
-  return t1 < st + ln && t1 % sp.chunk != 0 && rs.m2t[ent.y] == t1;
+// lies in tiles whose window-pass references are known: in the first split
+// that holds the row's largest logit, the tile before the one where it
+// entered (reference m2p, rescaled when it entered) and every tile from that
+// one on (reference m2).  Returns the page's tokens before that tile (the
+// ones weighted against m2p), or -1 if the pair is not such a pair; every
+// part of the pair takes the same decision.
+__device__ __forceinline__ int rescaled_entry(const AttnSplit& sp, const RowStats& rs, const int4 ent) {
+  if (!(ent.w & kFixRescaled) || !rs.m2t || !rs.m2p) return -1;
+  const int st = ent.z, ln = ent.w & 0xFF, mt = rs.m2t[ent.y];
+  if (mt < 0) return -1;
+  const int first = st / kTile * kTile, last = (st + ln - 1) / kTile * kTile;
+  const int s_lo = mt / sp.chunk * sp.chunk, s_hi = s_lo + sp.chunk;
+  if (first < mt - kTile || first < s_lo || last >= s_hi) return -1;
+  return min(max(mt - st, 0), ln);
 }
 
 // the fix-up of block bx of nb fix-up blocks, each of T threads
@@ -1118,8 +1122,9 @@ __device__ __forceinline__ void page_fixup_body(const AttnGeom& a, const AttnSpl
     const int e = item / parts, part = item % parts;
     // entry: page, global row, page start, page length
     const int4 ent = reinterpret_cast<const int4*>(pw.fix_list)[e];
-    if (rescaled_entry(sp, rs, ent)) {   // evaluated with the window pass's own weights, by one wave
-      if (part == 0 && tid < 64) rescaled_pair<D, PG>(a, rs, pw, ent, tid);
+    const int nf_resc = rescaled_entry(sp, rs, ent);
+    if (nf_resc >= 0) {   // evaluated with the window pass's own weights, by one wave
+      if (part == 0 && tid < 64) rescaled_pair<D, PG>(a, rs, pw, ent, nf_resc, tid);
       continue;
     }
     const int rg = (int)CKV_IDX(ent.y, a.Hq * a.W, a.dbg, 7), st = ent.z, ln = ent.w & 0xFF;

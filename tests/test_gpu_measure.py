@@ -186,7 +186,8 @@ def test_dominant_page(ckv, which, mass):
 
 
 @pytest.mark.parametrize("which", ["max_inside", "max_outside", "max_second_tile", "max_first_part_g32",
-                                   "max_first_part_g64", "max_second_part_g64", "max_after_page_g64"])
+                                   "max_first_part_g64", "max_second_part_g64", "max_after_page_g64",
+                                   "max_near_page_g32"])
 def test_heavy_page_band(ckv, which):
     """Pages carrying between 0.9 and 0.99 of a row's mass.  A page that holds
     its row's largest logit inside one 64-token tile keeps the closed form of
@@ -199,14 +200,16 @@ def test_heavy_page_band(ckv, which):
     logit, and a page that straddles a 64-token boundary with its largest
     logit after it (the window pass weighted its first part against an older
     reference; max_second_tile over one-tile splits, max_second_part over
-    128-token splits), are listed above A = 0.9: recomputed by definition,
-    or, where the logit entered the reference with the page's second tile
-    inside one split (max_second_part, and max_after_page, whose largest
-    logit is the token just after a page that carries the mass), evaluated
-    with the window pass's own weights.  All must meet the tolerance."""
+    128-token splits), are listed above A = 0.8: recomputed by definition,
+    or, where the page lies in the tile before the one where the logit
+    entered the split's reference or in a later tile of that split, evaluated
+    with the window pass's own weights (max_second_part; max_after_page,
+    whose largest logit is the token just after a page that carries the
+    mass; max_near_page, a page inside one tile with the largest logit in
+    the split's other tile).  All must meet the tolerance."""
     P, ctx = ckv
     import math
-    split128 = which[:-4] in ("max_first_part", "max_second_part", "max_after_page")
+    split128 = which[:-4] in ("max_first_part", "max_second_part", "max_after_page", "max_near_page")
     if split128:
         # 8 KV heads over 4096 tokens: 32 splits of 128 tokens
         w = scaled("tiny", n_tokens=4096, n_q_heads=16, n_kv_heads=8, page_size=int(which[-2:]))
@@ -235,6 +238,28 @@ def test_heavy_page_band(ckv, which):
                 k[g, int(starts[j]):int(ends[j]) + 1] = qr * c
                 k[g, int(ends[j]) + 1] = qr * (c * (1.0 + 1.0 / logit[(n + 5 * g) % len(strad)]))
         probe = strad
+    elif which == "max_near_page_g32":
+        # one page inside one tile per 128-token split (the split's first
+        # tile in even splits, its second in odd ones), every token at one
+        # logit for one row of the group's first query head (a ladder over
+        # the pages), and the first token of the split's other tile one higher
+        inner = np.flatnonzero(starts // 64 == ends // 64)
+        probe = []
+        for sp in range(w.n_tokens // 128):
+            pick = [j for j in inner if starts[j] // 128 == sp and (starts[j] // 64) % 2 == sp % 2]
+            if pick and ends[pick[0]] < w.n_tokens - 1:
+                probe.append(pick[0])
+        logit = np.linspace(8.0, 16.0, len(probe))
+        group = w.n_q_heads // w.n_kv_heads
+        for n, j in enumerate(probe):
+            t = int(starts[j]) // 64
+            other = (t + 1) * 64 if t % 2 == 0 else (t - 1) * 64
+            for g in range(w.n_kv_heads):
+                qr = q[g * group, (n + 7 * g) % w.window]
+                lg = logit[(n + 5 * g) % len(probe)]
+                c = lg * math.sqrt(w.head_dim) / float(qr @ qr)
+                k[g, int(starts[j]):int(ends[j]) + 1] = qr * c
+                k[g, other] = qr * (c * (1.0 + 1.0 / lg))
     elif split128:
         # every page across a tile boundary gets a heavy token in each KV
         # head, its first one (before the boundary) or the first after the
@@ -290,7 +315,8 @@ def test_heavy_page_band(ckv, which):
             band += int(sel.sum())
             if split128 and (st // 64 + 1) % 2 == 1:
                 # a tile boundary inside a split (max_first_part: the closed
-                # form is kept)
+                # form is kept), or a page in the split's first tile
+                # (max_near_page: weighted against the older reference)
                 inside += int(sel.sum())
             if which == "max_outside" and sel.any():
                 # the row's largest logit lies outside the page
