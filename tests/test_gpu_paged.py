@@ -117,6 +117,46 @@ def test_dominant_page_fixups_bit_identical(ckv):
         _same(ra[k_], rb[k_], "recorded " + k_)
 
 
+def test_window_weight_fixups_bit_identical(ckv):
+    """Pages inside one tile of a 128-token window-pass split carrying most of
+    a row's mass while the row's largest logit lies in the split's other
+    tile: the fix-up evaluates them with the window pass's own weights, and
+    through the pool it must give the same bits."""
+    P, ctx = ckv
+    import math
+    from synth import bf16_bits_to_f32
+    w = scaled("tiny", n_tokens=4096, n_q_heads=16, n_kv_heads=8, page_size=32)
+    L = make_layer(w, seed=11)
+    k = bf16_bits_to_f32(L.k).copy()
+    q = bf16_bits_to_f32(L.q_post)
+    starts, ends = L.layout.page_start, L.layout.page_start + L.layout.page_len - 1
+    inner = [j for j in np.flatnonzero(starts // 64 == ends // 64) if ends[j] < w.n_tokens - 1]
+    probe = [next(j for j in inner if starts[j] // 128 == sp and (starts[j] // 64) % 2 == sp % 2)
+             for sp in range(w.n_tokens // 128)
+             if any(starts[j] // 128 == sp and (starts[j] // 64) % 2 == sp % 2 for j in inner)]
+    group = w.n_q_heads // w.n_kv_heads
+    for n, j in enumerate(probe):
+        t = int(starts[j]) // 64
+        other = (t + 1) * 64 if t % 2 == 0 else (t - 1) * 64
+        for g in range(w.n_kv_heads):
+            qr = q[g * group, (n + 7 * g) % w.window]
+            lg = 8.0 + 8.0 * ((n + 5 * g) % len(probe)) / max(len(probe) - 1, 1)
+            c = lg * math.sqrt(w.head_dim) / float(qr @ qr)
+            k[g, int(starts[j]):int(ends[j]) + 1] = qr * c
+            k[g, other] = qr * (c * (1.0 + 1.0 / lg))
+    L.k = bf16_bits(k)
+    dl = LayerOnDevice(L)
+    kp, vp, slot = _pool(L, seed=5)
+    pages = P.Pages(L.layout.page_start, L.layout.page_len)
+    for which in ("pre", "post"):
+        dense, paged, win = _both(P, dl, kp, vp, slot, which)
+        a = P.ckv_measure_page_effects(ctx, dense, win, pages, want=("R", "R_head"))
+        b = P.ckv_measure_page_effects(ctx, paged, win, pages, want=("R", "R_head"))
+        torch.cuda.synchronize()
+        for k_ in ("R", "R_head"):
+            _same(a[k_], b[k_], which + " " + k_)
+
+
 def test_joint_bit_identical(ckv):
     P, ctx = ckv
     w = scaled("stress", n_tokens=4096, n_q_heads=8, n_kv_heads=2, max_cand=64)
